@@ -1,0 +1,587 @@
+/*
+ * kgq_oracle.c -- CPU oracle for batched complex-logical-query answering.
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the slow, plain reference against
+ * which the GPU library is checked. It is called from the test suite, from
+ * the smoke check and from the benchmark's CPU-baseline leg, never from the
+ * product path. It shares no code, header, table or constant with the GPU
+ * library.
+ *
+ * Arithmetic: every operator is evaluated one node at a time in double
+ * precision from the float32 (or bfloat16-decoded) inputs, with no fusion
+ * and no algebraic regrouping. The paper's operator fusion is stated to
+ * leave the output unchanged (Methodology, Operator Fuser), so the fused GPU
+ * result must equal this node-by-node evaluation.
+ *
+ * What the paper fixes and what it leaves open:
+ *  - Query computation graph and its mapping from a first-order query
+ *    (Preliminaries, Query Computation Graph; Methodology, Graph Capturer,
+ *    Eq. 2): entities become value nodes, each relation becomes a projection
+ *    operator node, and conjunction / disjunction / negation become
+ *    intersection / union / negation functions.
+ *  - Disjunctive normal form (Preliminaries, Eq. 1): a union is evaluated as
+ *    separate conjunctive branches whose entity scores are combined by max.
+ *  - Beta embeddings (Methodology, Pattern Recognizer, Eq. 3) and the BetaE
+ *    projection as three matmul+bias layers with ReLU between them (Eq. 4).
+ *    Eq. 4 prints a softmax as the last operator; here the last operator is
+ *    the regulariser clamp(y + 1, 0.05, 1e9), because a softmax would force
+ *    the shape parameters of each query to sum to one.
+ *  - Reasoning time is operator execution plus the entity-similarity query,
+ *    i.e. scoring every entity (Experiments, Metrics).
+ *  - GQE and Query2Box are named (Related Work; Experiments, Baselines) but
+ *    their operators are not written out in the paper. The forms used here:
+ *      GQE:   anchor q = E[a]; projection q + Rel[r]; intersection by
+ *             attention over branches; score gamma - ||q - e||_1.
+ *      Q2B:   anchor box (E[a], 0); projection (c + C[r], o + softplus(O[r]));
+ *             intersection: attention over centers, offset
+ *             min_j(o_j) * sigmoid(W4 mean_j ReLU(W3 o_j + b3) + b4);
+ *             score gamma - (dist_out + center_reg * dist_in).
+ *      BetaE: negation (alpha, beta) -> (1/alpha, 1/beta), no clamp after;
+ *             intersection: attention over branches on [alpha; beta];
+ *             score gamma - sum_i KL(Beta(entity_i) || Beta(query_i)).
+ *  - The 14 query shapes are named in the paper (Introduction; Experiments,
+ *    Datasets & Tasks) but drawn only in a figure that is not available;
+ *    the shapes below are the standard ones of the BetaE benchmark that the
+ *    paper adopts. pin negates the one-hop branch, pni the two-hop branch.
+ *
+ * Parity pins: every function below is checked in the CPU test suite against
+ * closed forms, identities, worked examples, special cases that reduce to a
+ * library routine, or brute force (see the tests named test_oracle_*).
+ */
+
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define KGO_GQE 0
+#define KGO_Q2B 1
+#define KGO_BETAE 2
+
+typedef struct {
+    int32_t model;
+    int32_t dim;
+    int64_t n_entities;
+    int32_t n_relations;
+    int32_t pad_;
+    double gamma;
+    double center_reg;
+    const float* entity;     /* GQE/Q2B [N x d]; BetaE [N x 2d], alpha then beta */
+    const float* relation;   /* GQE [R x d]; Q2B centers [R x d]; BetaE [R x 2d] */
+    const float* offset_raw; /* Q2B [R x d], offsets before softplus */
+    const float* att_w1;     /* intersection attention layer 1 [h x in] */
+    const float* att_b1;
+    const float* att_w2;     /* intersection attention layer 2 [d x h] */
+    const float* att_b2;
+    const float* off_w1;     /* Q2B offset set-function layers [d x d] */
+    const float* off_b1;
+    const float* off_w2;
+    const float* off_b2;
+    const float* proj_w1;    /* BetaE projection [4d x 2d], [4d x 4d], [2d x 4d] */
+    const float* proj_b1;
+    const float* proj_w2;
+    const float* proj_b2;
+    const float* proj_w3;
+    const float* proj_b3;
+} kgo_model;
+
+/* A query state: GQE uses x[0..d); Q2B holds center x[0..d) and offset
+ * x[d..2d); BetaE holds alpha x[0..d) and beta x[d..2d). */
+#define KGO_MAX_DIM 4096
+
+/* ------------------------------------------------------------------ */
+/* Special functions                                                   */
+/* ------------------------------------------------------------------ */
+
+/* Digamma psi(x) for x > 0: raise the argument with psi(x) = psi(x+1) - 1/x
+ * until it is at least 10, then apply the asymptotic expansion
+ * psi(x) ~ ln x - 1/(2x) - sum_n B_2n / (2n x^(2n)) through B_12
+ * (Abramowitz & Stegun 6.3.18). The first omitted term is below 1e-16 at
+ * x >= 10. */
+double kgo_digamma(double x)
+{
+    double acc = 0.0;
+    while (x < 10.0) {
+        acc -= 1.0 / x;
+        x += 1.0;
+    }
+    double r = 1.0 / x;
+    double r2 = r * r;
+    /* B2 = 1/6, B4 = -1/30, B6 = 1/42, B8 = -1/30, B10 = 5/66, B12 = -691/2730 */
+    double series = r2 * (1.0 / 12.0
+                  - r2 * (1.0 / 120.0
+                  - r2 * (1.0 / 252.0
+                  - r2 * (1.0 / 240.0
+                  - r2 * (1.0 / 132.0
+                  - r2 * (691.0 / 32760.0))))));
+    return acc + log(x) - 0.5 * r - series;
+}
+
+double kgo_lgamma(double x)
+{
+    int sign;
+    return lgamma_r(x, &sign);
+}
+
+/* ln B(a, b) with B the Beta function of Eq. 3. */
+double kgo_lnbeta(double a, double b)
+{
+    return kgo_lgamma(a) + kgo_lgamma(b) - kgo_lgamma(a + b);
+}
+
+/* KL( Beta(a1, b1) || Beta(a2, b2) ) for the densities of Eq. 3. */
+double kgo_kl_beta(double a1, double b1, double a2, double b2)
+{
+    return kgo_lnbeta(a2, b2) - kgo_lnbeta(a1, b1)
+         + (a1 - a2) * kgo_digamma(a1)
+         + (b1 - b2) * kgo_digamma(b1)
+         + (a2 - a1 + b2 - b1) * kgo_digamma(a1 + b1);
+}
+
+double kgo_softplus(double x)
+{
+    return (x > 0.0 ? x : 0.0) + log1p(exp(-fabs(x)));
+}
+
+static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+/* y = W x + b for W stored [out x in] row-major (one dense layer of Eq. 4). */
+static void dense(const float* W, const float* b, int out, int in, const double* x, double* y)
+{
+    for (int i = 0; i < out; ++i) {
+        double s = (double)b[i];
+        const float* w = W + (size_t)i * in;
+        for (int j = 0; j < in; ++j) s += (double)w[j] * x[j];
+        y[i] = s;
+    }
+}
+
+static void relu_inplace(double* x, int n)
+{
+    for (int i = 0; i < n; ++i) if (x[i] < 0.0) x[i] = 0.0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Operators                                                           */
+/* ------------------------------------------------------------------ */
+
+int kgo_state_width(const kgo_model* m)
+{
+    return m->model == KGO_GQE ? m->dim : 2 * m->dim;
+}
+
+/* Anchor entity -> value node (Eq. 2, first rule). */
+void kgo_anchor(const kgo_model* m, int64_t e, double* st)
+{
+    int d = m->dim;
+    if (m->model == KGO_GQE) {
+        for (int i = 0; i < d; ++i) st[i] = m->entity[(size_t)e * d + i];
+    } else if (m->model == KGO_Q2B) {
+        for (int i = 0; i < d; ++i) { st[i] = m->entity[(size_t)e * d + i]; st[d + i] = 0.0; }
+    } else {
+        for (int i = 0; i < 2 * d; ++i) st[i] = m->entity[(size_t)e * 2 * d + i];
+    }
+}
+
+/* Relation projection (Eq. 2, relation rule; BetaE: Eq. 4). in and out may alias. */
+void kgo_project(const kgo_model* m, const double* in, int32_t r, double* out)
+{
+    int d = m->dim;
+    if (m->model == KGO_GQE) {
+        for (int i = 0; i < d; ++i) out[i] = in[i] + (double)m->relation[(size_t)r * d + i];
+        return;
+    }
+    if (m->model == KGO_Q2B) {
+        for (int i = 0; i < d; ++i) {
+            out[i] = in[i] + (double)m->relation[(size_t)r * d + i];
+            out[d + i] = in[d + i] + kgo_softplus((double)m->offset_raw[(size_t)r * d + i]);
+        }
+        return;
+    }
+    /* BetaE: x = [alpha; beta] + Rel[r]; three dense layers; regulariser. */
+    int w = 2 * d, h = 4 * d;
+    double* x = (double*)malloc(sizeof(double) * (size_t)(w + h + h + w));
+    double* h1 = x + w;
+    double* h2 = h1 + h;
+    double* y = h2 + h;
+    for (int i = 0; i < w; ++i) x[i] = in[i] + (double)m->relation[(size_t)r * w + i];
+    dense(m->proj_w1, m->proj_b1, h, w, x, h1);
+    relu_inplace(h1, h);
+    dense(m->proj_w2, m->proj_b2, h, h, h1, h2);
+    relu_inplace(h2, h);
+    dense(m->proj_w3, m->proj_b3, w, h, h2, y);
+    for (int i = 0; i < w; ++i) {
+        double v = y[i] + 1.0;
+        if (v < 0.05) v = 0.05;
+        if (v > 1e9) v = 1e9;
+        out[i] = v;
+    }
+    free(x);
+}
+
+/* Negation (f_not of Eq. 2), defined for BetaE only: reciprocal of both
+ * shape parameters. */
+void kgo_negate(const kgo_model* m, const double* in, double* out)
+{
+    int w = 2 * m->dim;
+    for (int i = 0; i < w; ++i) out[i] = 1.0 / in[i];
+}
+
+/* Intersection (f_and of Eq. 2) of n branch states. */
+void kgo_intersect(const kgo_model* m, int n, const double* const* br, double* out)
+{
+    int d = m->dim;
+    int in_w = (m->model == KGO_BETAE) ? 2 * d : d;   /* attention input width */
+    int hid = in_w;                                    /* attention hidden width */
+    double* hbuf = (double*)malloc(sizeof(double) * (size_t)hid);
+    double* logits = (double*)malloc(sizeof(double) * (size_t)n * d);
+    for (int j = 0; j < n; ++j) {
+        /* GQE: the query vector; Q2B: the center; BetaE: [alpha; beta]. */
+        dense(m->att_w1, m->att_b1, hid, in_w, br[j], hbuf);
+        relu_inplace(hbuf, hid);
+        dense(m->att_w2, m->att_b2, d, hid, hbuf, logits + (size_t)j * d);
+    }
+    for (int i = 0; i < d; ++i) {
+        double mx = logits[i];
+        for (int j = 1; j < n; ++j) if (logits[(size_t)j * d + i] > mx) mx = logits[(size_t)j * d + i];
+        double z = 0.0;
+        double wts[3];
+        for (int j = 0; j < n; ++j) { wts[j] = exp(logits[(size_t)j * d + i] - mx); z += wts[j]; }
+        for (int j = 0; j < n; ++j) wts[j] /= z;
+        if (m->model == KGO_BETAE) {
+            double a = 0.0, b = 0.0;
+            for (int j = 0; j < n; ++j) { a += wts[j] * br[j][i]; b += wts[j] * br[j][d + i]; }
+            out[i] = a;
+            out[d + i] = b;
+        } else {
+            double c = 0.0;
+            for (int j = 0; j < n; ++j) c += wts[j] * br[j][i];
+            out[i] = c;
+        }
+    }
+    if (m->model == KGO_Q2B) {
+        /* Offset: elementwise minimum over branches, shrunk by a sigmoid gate
+         * computed from the mean of per-branch set-function features. */
+        double* z = (double*)malloc(sizeof(double) * (size_t)d);
+        double* mean = (double*)calloc((size_t)d, sizeof(double));
+        double* g = (double*)malloc(sizeof(double) * (size_t)d);
+        for (int j = 0; j < n; ++j) {
+            dense(m->off_w1, m->off_b1, d, d, br[j] + d, z);
+            relu_inplace(z, d);
+            for (int i = 0; i < d; ++i) mean[i] += z[i];
+        }
+        for (int i = 0; i < d; ++i) mean[i] /= (double)n;
+        dense(m->off_w2, m->off_b2, d, d, mean, g);
+        for (int i = 0; i < d; ++i) {
+            double mn = br[0][d + i];
+            for (int j = 1; j < n; ++j) if (br[j][d + i] < mn) mn = br[j][d + i];
+            out[d + i] = mn * sigmoid(g[i]);
+        }
+        free(z); free(mean); free(g);
+    }
+    free(hbuf);
+    free(logits);
+}
+
+/* Score of one entity against one query state (entity-similarity query). */
+double kgo_score(const kgo_model* m, const double* st, int64_t e)
+{
+    int d = m->dim;
+    if (m->model == KGO_GQE) {
+        double s = 0.0;
+        for (int i = 0; i < d; ++i) s += fabs(st[i] - (double)m->entity[(size_t)e * d + i]);
+        return m->gamma - s;
+    }
+    if (m->model == KGO_Q2B) {
+        double out = 0.0, in = 0.0;
+        for (int i = 0; i < d; ++i) {
+            double v = m->entity[(size_t)e * d + i];
+            double c = st[i], o = st[d + i];
+            double lo = c - o, hi = c + o;
+            double mm = v > lo ? v : lo;       /* max(c - o, v) */
+            if (mm > hi) mm = hi;              /* min(c + o, .) */
+            out += fabs(v - mm);
+            in += fabs(c - mm);
+        }
+        return m->gamma - (out + m->center_reg * in);
+    }
+    double kl = 0.0;
+    for (int i = 0; i < d; ++i) {
+        double ae = m->entity[(size_t)e * 2 * d + i], be = m->entity[(size_t)e * 2 * d + d + i];
+        kl += kgo_kl_beta(ae, be, st[i], st[d + i]);
+    }
+    return m->gamma - kl;
+}
+
+/* ------------------------------------------------------------------ */
+/* Query structures                                                    */
+/* ------------------------------------------------------------------ */
+
+enum { S_1P, S_2P, S_3P, S_2I, S_3I, S_PI, S_IP, S_2U, S_UP,
+       S_2IN, S_3IN, S_INP, S_PIN, S_PNI, S_COUNT };
+
+static const int ARITY_A[S_COUNT] = {1, 1, 1, 2, 3, 2, 2, 2, 2, 2, 3, 2, 2, 2};
+static const int ARITY_R[S_COUNT] = {1, 2, 3, 2, 3, 3, 3, 2, 3, 2, 3, 3, 3, 3};
+
+int kgo_arity(int s, int* na, int* nr)
+{
+    if (s < 0 || s >= S_COUNT) return -1;
+    *na = ARITY_A[s];
+    *nr = ARITY_R[s];
+    return 0;
+}
+
+/* a0..a2 / r0..r2 refer to the query's anchor and relation slots in order. */
+#define ANCHOR(st, k) kgo_anchor(m, a[k], st)
+#define PROJ(st, k) kgo_project(m, st, r[k], st)
+
+/* Evaluate one query; writes 1 or 2 final states (2 for a union, whose
+ * entity score is the max over the two conjunctive branches of its DNF).
+ * Returns the number of states, or -1 for an unknown or unsupported shape. */
+int kgo_query_states(const kgo_model* m, int s, const int32_t* a, const int32_t* r, double* out)
+{
+    int w = kgo_state_width(m);
+    if (s < 0 || s >= S_COUNT) return -1;
+    if (s >= S_2IN && m->model != KGO_BETAE) return -1;
+    double* b0 = (double*)malloc(sizeof(double) * (size_t)w * 3);
+    double* b1 = b0 + w;
+    double* b2 = b1 + w;
+    const double* br[3] = {b0, b1, b2};
+    int nout = 1;
+    switch (s) {
+    case S_1P: ANCHOR(b0, 0); PROJ(b0, 0); memcpy(out, b0, sizeof(double) * w); break;
+    case S_2P: ANCHOR(b0, 0); PROJ(b0, 0); PROJ(b0, 1); memcpy(out, b0, sizeof(double) * w); break;
+    case S_3P: ANCHOR(b0, 0); PROJ(b0, 0); PROJ(b0, 1); PROJ(b0, 2);
+               memcpy(out, b0, sizeof(double) * w); break;
+    case S_2I: ANCHOR(b0, 0); PROJ(b0, 0); ANCHOR(b1, 1); PROJ(b1, 1);
+               kgo_intersect(m, 2, br, out); break;
+    case S_3I: ANCHOR(b0, 0); PROJ(b0, 0); ANCHOR(b1, 1); PROJ(b1, 1); ANCHOR(b2, 2); PROJ(b2, 2);
+               kgo_intersect(m, 3, br, out); break;
+    case S_PI: ANCHOR(b0, 0); PROJ(b0, 0); PROJ(b0, 1); ANCHOR(b1, 1); PROJ(b1, 2);
+               kgo_intersect(m, 2, br, out); break;
+    case S_IP: ANCHOR(b0, 0); PROJ(b0, 0); ANCHOR(b1, 1); PROJ(b1, 1);
+               kgo_intersect(m, 2, br, out); kgo_project(m, out, r[2], out); break;
+    case S_2U: ANCHOR(b0, 0); PROJ(b0, 0); ANCHOR(b1, 1); PROJ(b1, 1);
+               memcpy(out, b0, sizeof(double) * w); memcpy(out + w, b1, sizeof(double) * w);
+               nout = 2; break;
+    case S_UP: /* DNF: (a0.r0 v a1.r1).r2 = (a0.r0.r2) v (a1.r1.r2) */
+               ANCHOR(b0, 0); PROJ(b0, 0); PROJ(b0, 2); ANCHOR(b1, 1); PROJ(b1, 1); PROJ(b1, 2);
+               memcpy(out, b0, sizeof(double) * w); memcpy(out + w, b1, sizeof(double) * w);
+               nout = 2; break;
+    case S_2IN: ANCHOR(b0, 0); PROJ(b0, 0); ANCHOR(b1, 1); PROJ(b1, 1); kgo_negate(m, b1, b1);
+                kgo_intersect(m, 2, br, out); break;
+    case S_3IN: ANCHOR(b0, 0); PROJ(b0, 0); ANCHOR(b1, 1); PROJ(b1, 1); ANCHOR(b2, 2); PROJ(b2, 2);
+                kgo_negate(m, b2, b2); kgo_intersect(m, 3, br, out); break;
+    case S_INP: ANCHOR(b0, 0); PROJ(b0, 0); ANCHOR(b1, 1); PROJ(b1, 1); kgo_negate(m, b1, b1);
+                kgo_intersect(m, 2, br, out); kgo_project(m, out, r[2], out); break;
+    case S_PIN: ANCHOR(b0, 0); PROJ(b0, 0); PROJ(b0, 1); ANCHOR(b1, 1); PROJ(b1, 2);
+                kgo_negate(m, b1, b1); kgo_intersect(m, 2, br, out); break;
+    case S_PNI: ANCHOR(b0, 0); PROJ(b0, 0); PROJ(b0, 1); kgo_negate(m, b0, b0);
+                ANCHOR(b1, 1); PROJ(b1, 2); kgo_intersect(m, 2, br, out); break;
+    }
+    free(b0);
+    return nout;
+}
+
+#undef ANCHOR
+#undef PROJ
+
+/* ------------------------------------------------------------------ */
+/* Batched scoring and top-k                                           */
+/* ------------------------------------------------------------------ */
+
+static int set_threads(int nthreads)
+{
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+    return omp_get_max_threads();
+#else
+    (void)nthreads;
+    return 1;
+#endif
+}
+
+int kgo_max_threads(int nthreads) { return set_threads(nthreads); }
+
+/* Scores of every entity for B queries. Query q has structure sid[q], anchors
+ * anchors[q*astride ..] and relations rels[q*rstride ..]. scores is [B x N].
+ * Returns 0, or -1 if any query has an unknown/unsupported structure or an
+ * id outside the tables. */
+int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t* anchors,
+               int32_t astride, const int32_t* rels, int32_t rstride, double* scores,
+               int nthreads)
+{
+    int w = kgo_state_width(m);
+    int64_t N = m->n_entities;
+    int d = m->dim;
+    if (d > KGO_MAX_DIM) return -1;
+    for (int32_t q = 0; q < B; ++q) {
+        int na, nr;
+        if (kgo_arity(sid[q], &na, &nr)) return -1;
+        if (sid[q] >= S_2IN && m->model != KGO_BETAE) return -1;
+        for (int k = 0; k < na; ++k) {
+            int32_t e = anchors[(size_t)q * astride + k];
+            if (e < 0 || e >= N) return -1;
+        }
+        for (int k = 0; k < nr; ++k) {
+            int32_t r = rels[(size_t)q * rstride + k];
+            if (r < 0 || r >= m->n_relations) return -1;
+        }
+    }
+    set_threads(nthreads);
+    double* states = (double*)malloc(sizeof(double) * (size_t)B * 2 * w);
+    int* nst = (int*)malloc(sizeof(int) * (size_t)B);
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t q = 0; q < B; ++q) {
+        nst[q] = kgo_query_states(m, sid[q], anchors + (size_t)q * astride,
+                                  rels + (size_t)q * rstride, states + (size_t)q * 2 * w);
+        if (nst[q] < 0) bad = 1;
+    }
+    if (bad) { free(states); free(nst); return -1; }
+
+    /* Entity-similarity query over all N entities. Entities are processed in
+     * chunks so that BetaE's per-entity function values (psi, ln B) are
+     * computed once per chunk and then reused for every query; the KL
+     * formula itself is unchanged. */
+    const int64_t CH = 256;
+    int64_t nch = (N + CH - 1) / CH;
+#pragma omp parallel
+    {
+        double* memo = NULL;
+        if (m->model == KGO_BETAE) memo = (double*)malloc(sizeof(double) * (size_t)CH * d * 4);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t c = 0; c < nch; ++c) {
+            int64_t e0 = c * CH, e1 = e0 + CH < N ? e0 + CH : N;
+            if (m->model != KGO_BETAE) {
+                for (int32_t q = 0; q < B; ++q) {
+                    for (int64_t e = e0; e < e1; ++e) {
+                        double best = kgo_score(m, states + (size_t)q * 2 * w, e);
+                        if (nst[q] == 2) {
+                            double s2 = kgo_score(m, states + (size_t)q * 2 * w + w, e);
+                            if (s2 > best) best = s2;
+                        }
+                        scores[(size_t)q * N + e] = best;
+                    }
+                }
+                continue;
+            }
+            /* BetaE: memo[(e-e0)*d + i] slots: lnB(a,b), psi(a), psi(b), psi(a+b). */
+            for (int64_t e = e0; e < e1; ++e) {
+                const float* ab = m->entity + (size_t)e * 2 * d;
+                double* mm = memo + (size_t)(e - e0) * d * 4;
+                for (int i = 0; i < d; ++i) {
+                    double a1 = ab[i], b1 = ab[d + i];
+                    mm[4 * i + 0] = kgo_lnbeta(a1, b1);
+                    mm[4 * i + 1] = kgo_digamma(a1);
+                    mm[4 * i + 2] = kgo_digamma(b1);
+                    mm[4 * i + 3] = kgo_digamma(a1 + b1);
+                }
+            }
+            double* lnbq = (double*)malloc(sizeof(double) * (size_t)d * 2);
+            for (int32_t q = 0; q < B; ++q) {
+                for (int t = 0; t < nst[q]; ++t) {
+                    const double* st = states + (size_t)q * 2 * w + (size_t)t * w;
+                    for (int i = 0; i < d; ++i) lnbq[i] = kgo_lnbeta(st[i], st[d + i]);
+                    for (int64_t e = e0; e < e1; ++e) {
+                        const float* ab = m->entity + (size_t)e * 2 * d;
+                        const double* mm = memo + (size_t)(e - e0) * d * 4;
+                        double kl = 0.0;
+                        for (int i = 0; i < d; ++i) {
+                            double a1 = ab[i], b1 = ab[d + i], a2 = st[i], b2 = st[d + i];
+                            /* KL(Beta(a1,b1) || Beta(a2,b2)) with memoised
+                             * values of lnB and psi. */
+                            kl += lnbq[i] - mm[4 * i + 0]
+                                + (a1 - a2) * mm[4 * i + 1]
+                                + (b1 - b2) * mm[4 * i + 2]
+                                + (a2 - a1 + b2 - b1) * mm[4 * i + 3];
+                        }
+                        double s = m->gamma - kl;
+                        if (t == 0 || s > scores[(size_t)q * N + e]) scores[(size_t)q * N + e] = s;
+                    }
+                }
+            }
+            free(lnbq);
+        }
+        free(memo);
+    }
+    free(states);
+    free(nst);
+    return 0;
+}
+
+/* Ranking order: higher score first; equal scores by lower entity index. */
+static int ranks_before(double sa, int64_t ia, double sb, int64_t ib)
+{
+    return sa > sb || (sa == sb && ia < ib);
+}
+
+/* Top-k of each row of scores [B x N]: a size-k heap whose root is the
+ * weakest kept entry, then the kept entries in ranking order. */
+int kgo_topk(const double* scores, int32_t B, int64_t N, int32_t k, int32_t* idx, double* val,
+             int nthreads)
+{
+    if (k < 1 || k > N) return -1;
+    set_threads(nthreads);
+#pragma omp parallel
+    {
+        int64_t* hi = (int64_t*)malloc(sizeof(int64_t) * (size_t)k);
+        double* hs = (double*)malloc(sizeof(double) * (size_t)k);
+#pragma omp for schedule(dynamic, 1)
+        for (int32_t q = 0; q < B; ++q) {
+            const double* row = scores + (size_t)q * N;
+            int n = 0;
+            for (int64_t e = 0; e < N; ++e) {
+                double s = row[e];
+                if (n < k) {
+                    /* sift up: the root holds the entry that ranks last */
+                    int c = n++;
+                    while (c > 0) {
+                        int p = (c - 1) / 2;
+                        if (!ranks_before(hs[p], hi[p], s, e)) break;
+                        hs[c] = hs[p]; hi[c] = hi[p];
+                        c = p;
+                    }
+                    hs[c] = s; hi[c] = e;
+                } else if (ranks_before(s, e, hs[0], hi[0])) {
+                    int c = 0;
+                    for (;;) {
+                        int l = 2 * c + 1, r = l + 1, worst = -1;
+                        double ws = s; int64_t wi = e;
+                        if (l < k && ranks_before(ws, wi, hs[l], hi[l])) { worst = l; ws = hs[l]; wi = hi[l]; }
+                        if (r < k && ranks_before(ws, wi, hs[r], hi[r])) { worst = r; ws = hs[r]; wi = hi[r]; }
+                        if (worst < 0) break;
+                        hs[c] = hs[worst]; hi[c] = hi[worst];
+                        c = worst;
+                    }
+                    hs[c] = s; hi[c] = e;
+                }
+            }
+            /* pop the weakest into the last slot until empty */
+            for (int t = k - 1; t >= 0; --t) {
+                idx[(size_t)q * k + t] = (int32_t)hi[0];
+                val[(size_t)q * k + t] = hs[0];
+                double s = hs[t]; int64_t e = hi[t];
+                int m2 = t, c = 0;
+                if (m2 > 0) {
+                    for (;;) {
+                        int l = 2 * c + 1, r = l + 1, worst = -1;
+                        double ws = s; int64_t wi = e;
+                        if (l < m2 && ranks_before(ws, wi, hs[l], hi[l])) { worst = l; ws = hs[l]; wi = hi[l]; }
+                        if (r < m2 && ranks_before(ws, wi, hs[r], hi[r])) { worst = r; ws = hs[r]; wi = hi[r]; }
+                        if (worst < 0) break;
+                        hs[c] = hs[worst]; hi[c] = hi[worst];
+                        c = worst;
+                    }
+                    hs[c] = s; hi[c] = e;
+                }
+            }
+        }
+        free(hi);
+        free(hs);
+    }
+    return 0;
+}

@@ -1,0 +1,252 @@
+"""ctypes wrapper for the CPU oracle (liboracle.so).
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's CPU-baseline leg. The product path never imports it.
+
+The oracle evaluates every operator node by node in double precision; see
+kgq_oracle.c for the definitions it follows.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboracle.so")
+
+GQE, Q2B, BETAE = 0, 1, 2
+
+_fp = ctypes.POINTER(ctypes.c_float)
+
+
+class _Model(ctypes.Structure):
+    _fields_ = [
+        ("model", ctypes.c_int32), ("dim", ctypes.c_int32),
+        ("n_entities", ctypes.c_int64), ("n_relations", ctypes.c_int32), ("pad_", ctypes.c_int32),
+        ("gamma", ctypes.c_double), ("center_reg", ctypes.c_double),
+        ("entity", _fp), ("relation", _fp), ("offset_raw", _fp),
+        ("att_w1", _fp), ("att_b1", _fp), ("att_w2", _fp), ("att_b2", _fp),
+        ("off_w1", _fp), ("off_b1", _fp), ("off_w2", _fp), ("off_b2", _fp),
+        ("proj_w1", _fp), ("proj_b1", _fp), ("proj_w2", _fp), ("proj_b2", _fp),
+        ("proj_w3", _fp), ("proj_b3", _fp),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            from . import build as _b  # type: ignore
+            _b.build()
+        L = ctypes.CDLL(LIB_PATH)
+        dp = ctypes.POINTER(ctypes.c_double)
+        ip = ctypes.POINTER(ctypes.c_int32)
+        mp = ctypes.POINTER(_Model)
+        for name in ("kgo_digamma", "kgo_lgamma", "kgo_softplus"):
+            getattr(L, name).restype = ctypes.c_double
+            getattr(L, name).argtypes = [ctypes.c_double]
+        L.kgo_lnbeta.restype = ctypes.c_double
+        L.kgo_lnbeta.argtypes = [ctypes.c_double] * 2
+        L.kgo_kl_beta.restype = ctypes.c_double
+        L.kgo_kl_beta.argtypes = [ctypes.c_double] * 4
+        L.kgo_state_width.restype = ctypes.c_int
+        L.kgo_state_width.argtypes = [mp]
+        L.kgo_anchor.restype = None
+        L.kgo_anchor.argtypes = [mp, ctypes.c_int64, dp]
+        L.kgo_project.restype = None
+        L.kgo_project.argtypes = [mp, dp, ctypes.c_int32, dp]
+        L.kgo_negate.restype = None
+        L.kgo_negate.argtypes = [mp, dp, dp]
+        L.kgo_intersect.restype = None
+        L.kgo_intersect.argtypes = [mp, ctypes.c_int, ctypes.POINTER(dp), dp]
+        L.kgo_score.restype = ctypes.c_double
+        L.kgo_score.argtypes = [mp, dp, ctypes.c_int64]
+        L.kgo_arity.restype = ctypes.c_int
+        L.kgo_arity.argtypes = [ctypes.c_int, ip, ip]
+        L.kgo_query_states.restype = ctypes.c_int
+        L.kgo_query_states.argtypes = [mp, ctypes.c_int, ip, ip, dp]
+        L.kgo_scores.restype = ctypes.c_int
+        L.kgo_scores.argtypes = [mp, ctypes.c_int32, ip, ip, ctypes.c_int32, ip, ctypes.c_int32,
+                                 dp, ctypes.c_int]
+        L.kgo_topk.restype = ctypes.c_int
+        L.kgo_topk.argtypes = [dp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ip, dp,
+                               ctypes.c_int]
+        L.kgo_max_threads.restype = ctypes.c_int
+        L.kgo_max_threads.argtypes = [ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def _f32(a: Optional[np.ndarray]):
+    if a is None:
+        return None
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _ptr(a):
+    if a is None:
+        return ctypes.cast(None, _fp)
+    return a.ctypes.data_as(_fp)
+
+
+def _dp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _ip(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+class Model:
+    """One model's parameters, held as float32 arrays for the oracle.
+
+    ``params`` uses the library's parameter names: ``entity``, ``relation``
+    (GQE) / ``relation.center`` + ``relation.offset_raw`` (Q2B);
+    ``inter.w1`` ... (GQE, BetaE) / ``inter.center.*`` + ``inter.offset.*``
+    (Q2B); ``entity.alpha_beta``, ``relation``, ``proj.*`` (BetaE).
+    """
+
+    def __init__(self, model: int, params: Dict[str, np.ndarray], gamma: float,
+                 center_reg: float = 0.02, entity_override: Optional[np.ndarray] = None):
+        self.model = model
+        keep = {}
+        if model == BETAE:
+            ent = params["entity.alpha_beta"] if entity_override is None else entity_override
+            keep["entity"] = _f32(ent)
+            keep["relation"] = _f32(params["relation"])
+            for k in ("w1", "b1", "w2", "b2"):
+                keep["att_" + k] = _f32(params["inter." + k])
+            for k in ("w1", "b1", "w2", "b2", "w3", "b3"):
+                keep["proj_" + k] = _f32(params["proj." + k])
+            dim = keep["entity"].shape[1] // 2
+        elif model == Q2B:
+            keep["entity"] = _f32(params["entity"] if entity_override is None else entity_override)
+            keep["relation"] = _f32(params["relation.center"])
+            keep["offset_raw"] = _f32(params["relation.offset_raw"])
+            for k in ("w1", "b1", "w2", "b2"):
+                keep["att_" + k] = _f32(params["inter.center." + k])
+                keep["off_" + k] = _f32(params["inter.offset." + k])
+            dim = keep["entity"].shape[1]
+        else:
+            keep["entity"] = _f32(params["entity"] if entity_override is None else entity_override)
+            keep["relation"] = _f32(params["relation"])
+            for k in ("w1", "b1", "w2", "b2"):
+                keep["att_" + k] = _f32(params["inter." + k])
+            dim = keep["entity"].shape[1]
+        self._keep = keep
+        s = _Model()
+        s.model = model
+        s.dim = dim
+        s.n_entities = keep["entity"].shape[0]
+        s.n_relations = keep["relation"].shape[0]
+        s.gamma = gamma
+        s.center_reg = center_reg
+        for name, _ in _Model._fields_:
+            if name in keep:
+                setattr(s, name, _ptr(keep[name]))
+        self.s = s
+        self.dim = dim
+        self.n_entities = int(s.n_entities)
+        self.width = dim if model == GQE else 2 * dim
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.s)
+
+    # -- single operators -------------------------------------------------
+    def anchor(self, e: int) -> np.ndarray:
+        out = np.zeros(self.width, np.float64)
+        lib().kgo_anchor(self.ref, e, _dp(out))
+        return out
+
+    def project(self, state: np.ndarray, r: int) -> np.ndarray:
+        x = np.ascontiguousarray(state, np.float64)
+        out = np.zeros(self.width, np.float64)
+        lib().kgo_project(self.ref, _dp(x), r, _dp(out))
+        return out
+
+    def negate(self, state: np.ndarray) -> np.ndarray:
+        x = np.ascontiguousarray(state, np.float64)
+        out = np.zeros(self.width, np.float64)
+        lib().kgo_negate(self.ref, _dp(x), _dp(out))
+        return out
+
+    def intersect(self, states: Sequence[np.ndarray]) -> np.ndarray:
+        xs = [np.ascontiguousarray(s, np.float64) for s in states]
+        arr = (ctypes.POINTER(ctypes.c_double) * len(xs))(*[_dp(x) for x in xs])
+        out = np.zeros(self.width, np.float64)
+        lib().kgo_intersect(self.ref, len(xs), arr, _dp(out))
+        return out
+
+    def score(self, state: np.ndarray, e: int) -> float:
+        x = np.ascontiguousarray(state, np.float64)
+        return float(lib().kgo_score(self.ref, _dp(x), e))
+
+    def query_states(self, structure: int, anchors, rels) -> np.ndarray:
+        a = np.ascontiguousarray(anchors, np.int32)
+        r = np.ascontiguousarray(rels, np.int32)
+        out = np.zeros(2 * self.width, np.float64)
+        n = lib().kgo_query_states(self.ref, structure, _ip(a), _ip(r), _dp(out))
+        if n < 0:
+            raise ValueError("unsupported structure")
+        return out[: n * self.width].reshape(n, self.width)
+
+    # -- batched ------------------------------------------------------------
+    def scores(self, structure_ids, anchors: np.ndarray, rels: np.ndarray,
+               nthreads: int = 0) -> np.ndarray:
+        """[B x N] float64 scores. structure_ids: int or int array [B]."""
+        a = np.ascontiguousarray(anchors, np.int32)
+        r = np.ascontiguousarray(rels, np.int32)
+        B = a.shape[0]
+        if np.isscalar(structure_ids):
+            sid = np.full(B, int(structure_ids), np.int32)
+        else:
+            sid = np.ascontiguousarray(structure_ids, np.int32)
+        out = np.empty((B, self.n_entities), np.float64)
+        rc = lib().kgo_scores(self.ref, B, _ip(sid), _ip(a), a.shape[1], _ip(r), r.shape[1],
+                              _dp(out), nthreads)
+        if rc != 0:
+            raise ValueError("oracle rejected the batch (structure, arity or id out of range)")
+        return out
+
+
+def topk(scores: np.ndarray, k: int, nthreads: int = 0):
+    s = np.ascontiguousarray(scores, np.float64)
+    B, N = s.shape
+    idx = np.empty((B, k), np.int32)
+    val = np.empty((B, k), np.float64)
+    rc = lib().kgo_topk(_dp(s), B, N, k, _ip(idx), _dp(val), nthreads)
+    if rc != 0:
+        raise ValueError("bad k")
+    return idx, val
+
+
+def digamma(x: float) -> float:
+    return float(lib().kgo_digamma(x))
+
+
+def lgamma(x: float) -> float:
+    return float(lib().kgo_lgamma(x))
+
+
+def lnbeta(a: float, b: float) -> float:
+    return float(lib().kgo_lnbeta(a, b))
+
+
+def kl_beta(a1: float, b1: float, a2: float, b2: float) -> float:
+    return float(lib().kgo_kl_beta(a1, b1, a2, b2))
+
+
+def softplus(x: float) -> float:
+    return float(lib().kgo_softplus(x))
+
+
+def max_threads(n: int = 0) -> int:
+    return int(lib().kgo_max_threads(n))
