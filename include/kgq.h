@@ -1,0 +1,214 @@
+/*
+ * kgq.h -- C ABI of libkgq: batched complex logical query answering (CLQA)
+ * over knowledge-graph embeddings on one AMD Instinct MI355X (gfx950).
+ *
+ * The calls follow the paper's query-plan formulation (Methodology, Fig. 2
+ * and Eq. 2): a first-order query is identified by its structure, the
+ * structure fixes a computation graph of projection, intersection, union
+ * and negation operators over anchor entities and relations, and the
+ * library executes that graph for a batch of queries, then scores every
+ * entity against each query embedding (the "entity similarity query" of
+ * the Experiments section) and selects the top k.
+ *
+ * Three embedding models are supported: GQE, Query2Box and BetaE (the paper
+ * names them in Related Work and Experiments/Baselines; BetaE's Beta
+ * embedding is its Eq. 3 and BetaE's projection the MLP of its Eq. 4).
+ *
+ * Conventions
+ *  - Every function returns a kgq_status; no C++ exception crosses the ABI.
+ *  - Pointers marked "device" must point to memory of the handle's GPU (for
+ *    example torch.Tensor.data_ptr() of a CUDA tensor). Pointers marked
+ *    "host" point to ordinary host memory.
+ *  - The caller owns every buffer it passes in. The handle owns device
+ *    copies of all parameters, the derived tables, and its scratch space,
+ *    all freed by kgq_destroy.
+ *  - kgq_execute / kgq_execute_mixed are asynchronous: work is enqueued on
+ *    the caller's stream and the call returns. Outputs are valid after the
+ *    caller synchronises that stream; inputs must stay alive until then.
+ *    Calls on one handle must be issued from one host thread at a time.
+ *  - Host-checkable errors are reported before anything is enqueued.
+ */
+#ifndef KGQ_H
+#define KGQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct kgq_handle kgq_handle;
+
+typedef enum {
+    KGQ_OK = 0,
+    KGQ_E_INVALID_ARG = -1,   /* null pointer, bad id/size/shape/dtype, k or batch out of range */
+    KGQ_E_OUT_OF_RANGE = -2,  /* checked mode: an anchor or relation id in device memory is out of range */
+    KGQ_E_NOT_LOADED = -3,    /* execute before every parameter of the model was loaded */
+    KGQ_E_UNSUPPORTED = -4,   /* structure with negation on GQE or Query2Box */
+    KGQ_E_NO_DEVICE = -5,     /* no usable GPU (or a validation-only handle, device = -1) */
+    KGQ_E_OOM = -6,           /* device or pinned host allocation failed */
+    KGQ_E_DEVICE = -7         /* a HIP runtime call failed */
+} kgq_status;
+
+typedef enum { KGQ_GQE = 0, KGQ_Q2B = 1, KGQ_BETAE = 2 } kgq_model;
+typedef enum { KGQ_F32 = 0, KGQ_BF16 = 1 } kgq_dtype;
+
+/* Query structures, in the column order of the paper's Table 1. The shapes
+ * (the paper shows them only in its Fig. 1): "p" chains projections, "i"
+ * intersects branches, "u" takes a union (evaluated in disjunctive normal
+ * form, Eq. 1: the entity score is the max over the branch scores), "n"
+ * negates one branch before the intersection. Anchor slots a0..a2 and
+ * relation slots r0..r2 are consumed in the order written:
+ *   1p  a0.r0                      2p  a0.r0.r1          3p  a0.r0.r1.r2
+ *   2i  a0.r0 & a1.r1              3i  a0.r0 & a1.r1 & a2.r2
+ *   pi  a0.r0.r1 & a1.r2           ip  (a0.r0 & a1.r1).r2
+ *   2u  a0.r0 | a1.r1              up  (a0.r0 | a1.r1).r2 = a0.r0.r2 | a1.r1.r2
+ *   2in a0.r0 & !a1.r1             3in a0.r0 & a1.r1 & !a2.r2
+ *   inp (a0.r0 & !a1.r1).r2        pin a0.r0.r1 & !a1.r2      pni !(a0.r0.r1) & a1.r2
+ * The five structures with negation (ids 9..13) exist for BetaE only. */
+typedef enum {
+    KGQ_1P = 0, KGQ_2P, KGQ_3P, KGQ_2I, KGQ_3I, KGQ_PI, KGQ_IP, KGQ_2U, KGQ_UP,
+    KGQ_2IN, KGQ_3IN, KGQ_INP, KGQ_PIN, KGQ_PNI, KGQ_NUM_STRUCTURES
+} kgq_structure;
+
+#define KGQ_MAX_K 1024
+
+typedef struct {
+    int32_t model;        /* kgq_model */
+    int32_t dim;          /* embedding dimension d; a multiple of 4, at most 4096 */
+    int64_t n_entities;   /* N >= 1, at most 2^31 - 1 */
+    int32_t n_relations;  /* R >= 1 */
+    int32_t entity_dtype; /* kgq_dtype of the entity table as passed to kgq_load_params */
+    float gamma;          /* score margin: score = gamma - distance */
+    float center_reg;     /* Query2Box weight of the inside distance (0.02 in the standard model); ignored otherwise */
+    int32_t max_batch;    /* largest batch any execute call will pass; sizes the scratch space */
+    int32_t device;       /* HIP device ordinal, or -1 for a validation-only handle with no GPU */
+} kgq_config;
+
+/* Create a handle. Validates cfg, selects the device, and allocates all
+ * scratch space for max_batch queries (execute allocates nothing).
+ * Errors: INVALID_ARG (cfg or out null, bad field), NO_DEVICE, OOM, DEVICE.
+ * A handle with device = -1 validates arguments exactly like a real one;
+ * its execute calls return NO_DEVICE once every argument has passed. */
+kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out);
+
+/* Load one named parameter array (row-major; dense layers W are [out x in]
+ * and compute y = W x + b).
+ *   GQE:   "entity" [N x d], "relation" [R x d],
+ *          "inter.w1" [d x d], "inter.b1" [d], "inter.w2" [d x d], "inter.b2" [d]
+ *   Q2B:   "entity" [N x d], "relation.center" [R x d],
+ *          "relation.offset_raw" [R x d] (the library applies softplus),
+ *          "inter.center.{w1,b1,w2,b2}" and "inter.offset.{w1,b1,w2,b2}" ([d x d], [d])
+ *   BetaE: "entity.alpha_beta" [N x 2d] (alpha in columns 0..d-1, beta in d..2d-1, all > 0),
+ *          "relation" [R x 2d],
+ *          "proj.w1" [4d x 2d], "proj.b1" [4d], "proj.w2" [4d x 4d], "proj.b2" [4d],
+ *          "proj.w3" [2d x 4d], "proj.b3" [2d],
+ *          "inter.w1" [2d x 2d], "inter.b1" [2d], "inter.w2" [d x 2d], "inter.b2" [d]
+ * dtype is KGQ_F32 for every array except the entity table, which takes
+ * cfg.entity_dtype (KGQ_BF16: bfloat16 bit patterns, decoded to float32 on
+ * the device). nbytes must equal the array's size. src is a host pointer,
+ * or a device pointer if src_is_device is non-zero; it is read before the
+ * call returns (the call synchronises). Loading a name again replaces it.
+ * Derived tables are rebuilt here, not in execute: the blocked entity
+ * layout for scoring, Query2Box's softplus offsets, and BetaE's per-entity
+ * digamma / log-Beta tables.
+ * Errors: INVALID_ARG (unknown name, wrong nbytes or dtype, null src), OOM, DEVICE. */
+kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, size_t nbytes,
+                           int32_t dtype, int32_t src_is_device);
+
+/* Number of anchor entities and relations a query of this structure takes.
+ * Errors: INVALID_ARG (unknown structure id or null outputs). */
+kgq_status kgq_structure_arity(int32_t structure_id, int32_t* n_anchors, int32_t* n_relations);
+
+/* Execute a batch of queries that all have the same structure.
+ *   anchors   device int32 [batch x n_anchors(structure)]
+ *   relations device int32 [batch x n_relations(structure)]
+ *   k         1 <= k <= min(N, KGQ_MAX_K) when top-k outputs are requested
+ *   out_scores      device float [batch x N] or NULL: score of every entity
+ *   out_topk_idx    device int32 [batch x k] or NULL
+ *   out_topk_score  device float [batch x k] or NULL
+ *   stream          hipStream_t, or NULL for the null stream
+ * At least one output must be requested; the two top-k outputs go together.
+ * Top-k lists are ordered by score descending, equal scores by entity index
+ * ascending.
+ * Ids out of range never cause an out-of-bounds access: the device replaces
+ * them and raises a flag. In checked mode (environment KGQ_CHECKED=1 at
+ * create, or kgq_set_checked) execute then synchronises the stream and
+ * returns OUT_OF_RANGE; otherwise the affected outputs are unspecified.
+ * Errors: INVALID_ARG, UNSUPPORTED, NOT_LOADED, OUT_OF_RANGE (checked),
+ * NO_DEVICE, DEVICE. */
+kgq_status kgq_execute(kgq_handle* h, int32_t structure_id, int32_t batch,
+                       const int32_t* anchors, const int32_t* relations, int32_t k,
+                       float* out_scores, int32_t* out_topk_idx, float* out_topk_score,
+                       void* stream);
+
+/* Execute a batch whose queries have different structures, in one plan.
+ *   structure_ids  HOST int32 [batch]: the plan is lowered on the host.
+ *   anchors        device int32 [batch x 3], unused slots -1
+ *   relations      device int32 [batch x 3], unused slots -1
+ * Results are written in input order, with the same output rules as
+ * kgq_execute. The plan reads only the slots a query's structure uses; in
+ * checked mode a device-side check also requires every unused slot to be -1
+ * and returns INVALID_ARG otherwise.
+ * Errors: as kgq_execute. */
+kgq_status kgq_execute_mixed(kgq_handle* h, int32_t batch, const int32_t* structure_ids,
+                             const int32_t* anchors, const int32_t* relations, int32_t k,
+                             float* out_scores, int32_t* out_topk_idx, float* out_topk_score,
+                             void* stream);
+
+/* Turn checked mode on (non-zero) or off for this handle. */
+kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
+
+/* Describe the lowered plan of a batch (host structure ids) without running
+ * it. counts receives KGQ_PLAN_NCOUNTS values, in this order:
+ *   0 chain rows (branch states), 1 intersection groups, 2 intersection inputs,
+ *   3..6 BetaE projection rows at hop levels 1, 2, 3 and after the
+ *   intersection, 7 scored rows, 8 union pairs, 9 kernel launches per execute.
+ * Errors: INVALID_ARG, UNSUPPORTED. */
+#define KGQ_PLAN_NCOUNTS 10
+kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* structure_ids,
+                             int32_t* counts);
+
+/* Per-stage timing. While profiling is on, execute records a pair of HIP
+ * events around every kernel it launches, on the caller's stream.
+ * kgq_profile_read synchronises on those events and returns the summed
+ * milliseconds and launch count of one stage since profiling was turned
+ * on (or last reset), then keeps accumulating. Stages:
+ *   0 anchor gather and translation chains, 1 dense layers (MFMA),
+ *   2 intersection / negation combines, 3 query packing,
+ *   4 entity scoring, 5 top-k selection. */
+#define KGQ_NUM_STAGES 6
+kgq_status kgq_profile_enable(kgq_handle* h, int32_t on);
+kgq_status kgq_profile_read(kgq_handle* h, int32_t stage, double* total_ms, int64_t* launches);
+kgq_status kgq_profile_reset(kgq_handle* h);
+
+/* One dense layer on the device with the library's FP32 matrix-core GEMM:
+ * y[m][n] = act(sum_k x[m][k] * w[n][k] + b[n]) (the matmul + add (+ ReLU)
+ * pattern of the paper's Eq. 4).
+ *   x  device float [M x K], w device float [N x K], b device float [N] or NULL,
+ *   y  device float [M x N]; K a multiple of 4, rows 16-byte aligned.
+ *   act 0 = none, 1 = ReLU, 2 = BetaE regulariser clamp(v + 1, 0.05, 1e9).
+ * Asynchronous on `stream`. Errors: INVALID_ARG, NO_DEVICE, DEVICE. */
+kgq_status kgq_dense(kgq_handle* h, const float* x, int32_t M, int32_t K, const float* w, const float* b,
+                     int32_t N, int32_t act, float* y, void* stream);
+
+/* Free the handle and everything it owns (waits for its work first).
+ * NULL is accepted. */
+kgq_status kgq_destroy(kgq_handle* h);
+
+/* Static description of a status code. */
+const char* kgq_status_string(kgq_status s);
+
+/* Message of the last failing call on this handle ("" if none). The string
+ * stays valid until the next call on the handle. */
+const char* kgq_last_error(const kgq_handle* h);
+
+/* Message of the last failing kgq_create in this thread. */
+const char* kgq_create_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KGQ_H */

@@ -1,0 +1,440 @@
+// Query-plan operator kernels other than the dense layers and the scorer:
+// parameter re-layout at load time, anchor gathers, translation chains,
+// intersection / negation combines, query packing and id validation.
+//
+// Operators (the paper's Eq. 2 maps a query's relations, conjunctions and
+// negations to projection, intersection and negation functions):
+//   GQE   projection q + Rel[r]; intersection sum_j softmax_j(s_j) q_j with
+//         s_j = W2 ReLU(W1 q_j + b1) + b2 (softmax across branches, per dim).
+//   Q2B   projection (c + C[r], o + softplus(O[r])); intersection: attention
+//         as above on the centers; offset min_j(o_j) * sigmoid(W4 mean_j
+//         ReLU(W3 o_j + b3) + b4).
+//   BetaE negation (alpha, beta) -> (1/alpha, 1/beta); intersection:
+//         attention weights from [alpha; beta] (W1: 2d -> 2d, W2: 2d -> d),
+//         applied to alpha and beta; projection MLP (Eq. 4) runs on the MFMA
+//         GEMM, with x = [alpha; beta] + Rel[r] built here.
+// Ids read from device memory are range-checked in every kernel that reads
+// them: an out-of-range id raises a flag bit and is replaced by 0, so no
+// access ever leaves a table.
+#include "kgq_internal.hpp"
+
+namespace kgq {
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h)
+{
+    return __uint_as_float(((uint32_t)h) << 16);
+}
+
+__device__ __forceinline__ float load_param(const void* src, int bf16, int64_t i)
+{
+    return bf16 ? bf16_to_f32(reinterpret_cast<const uint16_t*>(src)[i])
+                : reinterpret_cast<const float*>(src)[i];
+}
+
+// ---------------------------------------------------------------------------
+// Load-time kernels
+// ---------------------------------------------------------------------------
+
+// One thread per entity slot of the padded table; writes the blocked
+// dimension-major layout (coalesced across threads) and a row-major copy.
+__global__ void k_relayout_points(const void* src, int bf16, int64_t N, int d, int64_t n_pad,
+                                  float* rowmajor, float* blocked)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n_pad) return;
+    const int64_t blk = e / kEntBlock;
+    const int lo = (int)(e % kEntBlock);
+    float* dst = blocked + blk * (int64_t)d * kEntBlock + lo;
+    for (int k = 0; k < d; ++k) {
+        float v = 0.f;
+        if (e < N) {
+            v = load_param(src, bf16, e * d + k);
+            rowmajor[e * d + k] = v;
+        }
+        dst[(int64_t)k * kEntBlock] = v;
+    }
+}
+
+void launch_relayout_points(const void* src, int src_bf16, int64_t N, int d, int64_t n_blocks,
+                            float* rowmajor, float* blocked, hipStream_t s)
+{
+    const int64_t n_pad = n_blocks * kEntBlock;
+    hipLaunchKernelGGL(k_relayout_points, dim3((unsigned)((n_pad + 255) / 256)), dim3(256), 0, s,
+                       src, src_bf16, N, d, n_pad, rowmajor, blocked);
+}
+
+// Digamma for x > 0 in double precision: shift the argument up with
+// psi(x) = psi(x + 1) - 1/x until x >= 8, then the asymptotic series
+// psi(x) = ln x - 1/(2x) - sum_{n>=1} B_2n / (2n x^2n), kept through B_12
+// (Abramowitz & Stegun 6.3.18); the first dropped term is below 2e-14 at x = 8.
+__device__ double digamma_d(double x)
+{
+    double shift = 0.0;
+    while (x < 8.0) {
+        shift -= 1.0 / x;
+        x += 1.0;
+    }
+    const double f = 1.0 / (x * x);
+    const double tail = f * (-1.0 / 12.0 + f * (1.0 / 120.0 + f * (-1.0 / 252.0 + f * (1.0 / 240.0
+                      + f * (-1.0 / 132.0 + f * (691.0 / 32760.0))))));
+    return shift + log(x) - 0.5 / x + tail;
+}
+
+// BetaE entity tables: alpha|beta decoded to fp32 (row-major, for anchor
+// gathers), U/V blocked for the scorer, and E_e, all from the stored values.
+__global__ __launch_bounds__(128) void k_betae_entity_prep(const void* src, int bf16, int64_t N, int d, int64_t n_pad,
+                                    float* ab_rowmajor, float* uv_blocked, double* e_const)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n_pad) return;
+    const int64_t blk = e / kEntBlock;
+    const int lo = (int)(e % kEntBlock);
+    float* dst = uv_blocked + blk * (int64_t)d * 2 * kEntBlock + lo;
+    double acc = 0.0;
+    for (int k = 0; k < d; ++k) {
+        float u = 0.f, v = 0.f;
+        if (e < N) {
+            const float af = load_param(src, bf16, e * 2 * d + k);
+            const float bf = load_param(src, bf16, e * 2 * d + d + k);
+            ab_rowmajor[e * 2 * d + k] = af;
+            ab_rowmajor[e * 2 * d + d + k] = bf;
+            const double a = af, b = bf;
+            const double pa = digamma_d(a), pb = digamma_d(b), pab = digamma_d(a + b);
+            u = (float)(pab - pa);
+            v = (float)(pab - pb);
+            const double lnb = lgamma(a) + lgamma(b) - lgamma(a + b);
+            acc += -lnb + a * pa + b * pb - (a + b) * pab;
+        }
+        dst[(int64_t)k * 2 * kEntBlock] = u;
+        dst[(int64_t)k * 2 * kEntBlock + kEntBlock] = v;
+    }
+    e_const[e] = acc;
+}
+
+void launch_betae_entity_prep(const void* src, int src_bf16, int64_t N, int d, int64_t n_blocks,
+                              float* ab_rowmajor, float* uv_blocked, double* e_const, hipStream_t s)
+{
+    const int64_t n_pad = n_blocks * kEntBlock;
+    hipLaunchKernelGGL(k_betae_entity_prep, dim3((unsigned)((n_pad + 127) / 128)), dim3(128), 0, s,
+                       src, src_bf16, N, d, n_pad, ab_rowmajor, uv_blocked, e_const);
+}
+
+__global__ void k_softplus(const float* src, float* dst, int64_t n)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const double x = src[i];
+    dst[i] = (float)((x > 0.0 ? x : 0.0) + log1p(exp(-fabs(x))));
+}
+
+void launch_softplus(const float* src, float* dst, int64_t n, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_softplus, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst, n);
+}
+
+// ---------------------------------------------------------------------------
+// Validation
+// ---------------------------------------------------------------------------
+
+__global__ void k_clear_flag(int* flag) { *flag = 0; }
+
+void launch_clear_flag(int* flag, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, flag);
+}
+
+__device__ __forceinline__ int32_t checked_id(int32_t id, int64_t n, int* flag)
+{
+    if (id < 0 || (int64_t)id >= n) {
+        atomicOr(flag, kErrRange);
+        return 0;
+    }
+    return id;
+}
+
+// arity: one thread per query. For a mixed batch na_q / nr_q hold the
+// per-query arity (from the plan) and unused slots must be -1.
+__global__ void k_validate(const int32_t* anchors, const int32_t* rels, const int32_t* arity_q,
+                           int B, int sa, int sr, int fixed_na, int fixed_nr,
+                           int64_t n_ent, int n_rel, int* flag)
+{
+    const int q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= B) return;
+    const int na = arity_q ? arity_q[2 * q] : fixed_na;
+    const int nr = arity_q ? arity_q[2 * q + 1] : fixed_nr;
+    int bits = 0;
+    for (int s = 0; s < sa; ++s) {
+        const int32_t v = anchors[(int64_t)q * sa + s];
+        if (s < na) { if (v < 0 || (int64_t)v >= n_ent) bits |= kErrRange; }
+        else if (v != -1) bits |= kErrPadding;
+    }
+    for (int s = 0; s < sr; ++s) {
+        const int32_t v = rels[(int64_t)q * sr + s];
+        if (s < nr) { if (v < 0 || v >= n_rel) bits |= kErrRange; }
+        else if (v != -1) bits |= kErrPadding;
+    }
+    if (bits) atomicOr(flag, bits);
+}
+
+void launch_validate(const int32_t* anchors, const int32_t* rels, const int32_t* arity_q,
+                     int B, int sa, int sr, int fixed_na, int fixed_nr,
+                     int64_t n_ent, int n_rel, int* flag, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_validate, dim3((B + 255) / 256), dim3(256), 0, s, anchors, rels, arity_q,
+                       B, sa, sr, fixed_na, fixed_nr, n_ent, n_rel, flag);
+}
+
+// ---------------------------------------------------------------------------
+// GQE / Query2Box translation chains (horizontal fusion of consecutive
+// projections: the whole chain is one pass over the row)
+// ---------------------------------------------------------------------------
+
+__global__ void k_chain(int model, const int32_t* anchor_ref, const int32_t* rel_ref,
+                        const int32_t* anchors, const int32_t* rels, const float* ent_rm,
+                        const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
+                        float* states, int* flag)
+{
+    const int c = blockIdx.x;
+    const int64_t a = checked_id(anchors[anchor_ref[c]], n_ent, flag);
+    int32_t r[3];
+    int nh = 0;
+    for (int h = 0; h < 3; ++h) {
+        const int32_t ref = rel_ref[3 * c + h];
+        if (ref >= 0) r[nh++] = checked_id(rels[ref], n_rel, flag);
+    }
+    const int W = model == 0 ? d : 2 * d;
+    float* out = states + (int64_t)c * W;
+    for (int k = threadIdx.x; k < d; k += blockDim.x) {
+        float x = ent_rm[a * d + k];
+        for (int h = 0; h < nh; ++h) x += rel_c[(int64_t)r[h] * d + k];
+        out[k] = x;
+        if (model == 1) {
+            float o = 0.f;
+            for (int h = 0; h < nh; ++h) o += rel_o[(int64_t)r[h] * d + k];
+            out[d + k] = o;
+        }
+    }
+}
+
+void launch_chain(int model, const int32_t* anchor_ref, const int32_t* rel_ref, int n_chain,
+                  const int32_t* anchors, const int32_t* rels, const float* ent_rm,
+                  const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
+                  float* states, int* flag, hipStream_t s)
+{
+    if (n_chain <= 0) return;
+    hipLaunchKernelGGL(k_chain, dim3(n_chain), dim3(128), 0, s, model, anchor_ref, rel_ref, anchors, rels,
+                       ent_rm, rel_c, rel_o, n_ent, n_rel, d, states, flag);
+}
+
+// ---------------------------------------------------------------------------
+// Intersections (vertical fusion: all branches of a group in one pass)
+// ---------------------------------------------------------------------------
+
+// Attention weights across the n (<= 3) branches of one dimension.
+__device__ __forceinline__ void softmax_branches(const float* logits, int64_t ld, int n, int k, float* w)
+{
+    float mx = logits[k];
+    for (int j = 1; j < n; ++j) mx = fmaxf(mx, logits[j * ld + k]);
+    float z = 0.f;
+    for (int j = 0; j < n; ++j) { w[j] = expf(logits[j * ld + k] - mx); z += w[j]; }
+    const float inv = 1.0f / z;
+    for (int j = 0; j < n; ++j) w[j] *= inv;
+}
+
+__global__ void k_combine_center(int model, GroupArgs g, const float* states, int W,
+                                 const float* logits, const float* zfeat, float* zmean,
+                                 const int32_t* rels, const float* rel_c, int n_rel, int d,
+                                 float* out_states, int* flag)
+{
+    const int gi = blockIdx.x;
+    const int i0 = g.in_start[gi];
+    const int n = g.n_in[gi];
+    const int64_t orow = g.out_row[gi];
+    const int32_t pref = g.post_ref[gi];
+    const int32_t pr = pref >= 0 ? checked_id(rels[pref], n_rel, flag) : -1;
+    for (int k = threadIdx.x; k < d; k += blockDim.x) {
+        float w[3];
+        softmax_branches(logits + (int64_t)i0 * d, d, n, k, w);
+        float c = 0.f;
+        for (int j = 0; j < n; ++j) c += w[j] * states[(int64_t)(i0 + j) * W + k];
+        if (pr >= 0) c += rel_c[(int64_t)pr * d + k];
+        out_states[orow * W + k] = c;
+        if (model == 1) {
+            float z = 0.f;
+            for (int j = 0; j < n; ++j) z += zfeat[(int64_t)(i0 + j) * d + k];
+            zmean[(int64_t)gi * d + k] = z / (float)n;
+        }
+    }
+}
+
+void launch_combine_center(int model, const GroupArgs& g, const float* states, int W,
+                           const float* logits, const float* zfeat, float* zmean,
+                           const int32_t* rels, const float* rel_c, int n_rel, int d,
+                           float* out_states, int* flag, hipStream_t s)
+{
+    if (g.n_groups <= 0) return;
+    hipLaunchKernelGGL(k_combine_center, dim3(g.n_groups), dim3(128), 0, s, model, g, states, W, logits,
+                       zfeat, zmean, rels, rel_c, n_rel, d, out_states, flag);
+}
+
+__global__ void k_combine_offset(GroupArgs g, const float* states, int W, const float* gate,
+                                 const int32_t* rels, const float* rel_o, int n_rel, int d,
+                                 float* out_states, int* flag)
+{
+    const int gi = blockIdx.x;
+    const int i0 = g.in_start[gi];
+    const int n = g.n_in[gi];
+    const int64_t orow = g.out_row[gi];
+    const int32_t pref = g.post_ref[gi];
+    const int32_t pr = pref >= 0 ? checked_id(rels[pref], n_rel, flag) : -1;
+    for (int k = threadIdx.x; k < d; k += blockDim.x) {
+        float m = states[(int64_t)i0 * W + d + k];
+        for (int j = 1; j < n; ++j) m = fminf(m, states[(int64_t)(i0 + j) * W + d + k]);
+        const float gv = gate[(int64_t)gi * d + k];
+        float o = m * (1.0f / (1.0f + expf(-gv)));
+        if (pr >= 0) o += rel_o[(int64_t)pr * d + k];
+        out_states[orow * W + d + k] = o;
+    }
+}
+
+void launch_combine_offset(const GroupArgs& g, const float* states, int W, const float* gate,
+                           const int32_t* rels, const float* rel_o, int n_rel, int d,
+                           float* out_states, int* flag, hipStream_t s)
+{
+    if (g.n_groups <= 0) return;
+    hipLaunchKernelGGL(k_combine_offset, dim3(g.n_groups), dim3(128), 0, s, g, states, W, gate, rels,
+                       rel_o, n_rel, d, out_states, flag);
+}
+
+// BetaE: copy each intersection input row, inverting both shape parameters
+// of negated branches (negation), into the attention MLP input buffer.
+__global__ void k_betae_int_prep(GroupArgs g, const float* states, int d, float* x_int)
+{
+    const int gi = blockIdx.x;
+    const int i0 = g.in_start[gi];
+    const int n = g.n_in[gi];
+    const int neg = g.neg_mask[gi];
+    const int W = 2 * d;
+    for (int j = 0; j < n; ++j) {
+        const bool inv = (neg >> j) & 1;
+        const float* src = states + (int64_t)(i0 + j) * W;
+        float* dst = x_int + (int64_t)(i0 + j) * W;
+        for (int k = threadIdx.x; k < W; k += blockDim.x) {
+            const float v = src[k];
+            dst[k] = inv ? 1.0f / v : v;
+        }
+    }
+}
+
+void launch_betae_int_prep(const GroupArgs& g, const float* states, int d, float* x_int, hipStream_t s)
+{
+    if (g.n_groups <= 0) return;
+    hipLaunchKernelGGL(k_betae_int_prep, dim3(g.n_groups), dim3(256), 0, s, g, states, d, x_int);
+}
+
+__global__ void k_betae_combine(GroupArgs g, const float* x_int, const float* logits, int d, float* states)
+{
+    const int gi = blockIdx.x;
+    const int i0 = g.in_start[gi];
+    const int n = g.n_in[gi];
+    const int64_t orow = g.out_row[gi];
+    const int W = 2 * d;
+    for (int k = threadIdx.x; k < d; k += blockDim.x) {
+        float w[3];
+        softmax_branches(logits + (int64_t)i0 * d, d, n, k, w);
+        float al = 0.f, be = 0.f;
+        for (int j = 0; j < n; ++j) {
+            al += w[j] * x_int[(int64_t)(i0 + j) * W + k];
+            be += w[j] * x_int[(int64_t)(i0 + j) * W + d + k];
+        }
+        states[orow * W + k] = al;
+        states[orow * W + d + k] = be;
+    }
+}
+
+void launch_betae_combine(const GroupArgs& g, const float* x_int, const float* logits, int d,
+                          float* states, hipStream_t s)
+{
+    if (g.n_groups <= 0) return;
+    hipLaunchKernelGGL(k_betae_combine, dim3(g.n_groups), dim3(128), 0, s, g, x_int, logits, d, states);
+}
+
+__global__ void k_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
+                                  const int32_t* anchors, const int32_t* rels, const float* states,
+                                  const float* ent_ab, const float* rel, int64_t n_ent, int n_rel, int d,
+                                  float* x, int* flag)
+{
+    const int m = blockIdx.x;
+    const int W = 2 * d;
+    const int32_t sr = src_row[m];
+    const float* base;
+    if (sr >= 0) {
+        base = states + (int64_t)sr * W;
+    } else {
+        const int64_t a = checked_id(anchors[anchor_ref[m]], n_ent, flag);
+        base = ent_ab + a * W;
+    }
+    const int64_t r = checked_id(rels[rel_ref[m]], n_rel, flag);
+    const float* rr = rel + r * W;
+    float* dst = x + (int64_t)m * W;
+    for (int k = threadIdx.x; k < W; k += blockDim.x) dst[k] = base[k] + rr[k];
+}
+
+void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
+                            int M, const int32_t* anchors, const int32_t* rels,
+                            const float* states, const float* ent_ab, const float* rel,
+                            int64_t n_ent, int n_rel, int d, float* x, int* flag, hipStream_t s)
+{
+    if (M <= 0) return;
+    hipLaunchKernelGGL(k_betae_proj_prep, dim3(M), dim3(256), 0, s, src_row, anchor_ref, rel_ref, anchors,
+                       rels, states, ent_ab, rel, n_ent, n_rel, d, x, flag);
+}
+
+// ---------------------------------------------------------------------------
+// Query packing for the scorer: [row_block][k][field][TQ]; BetaE also C_q.
+// ---------------------------------------------------------------------------
+
+template <int TQ, int F>
+__global__ __launch_bounds__(64) void k_pack(int model, const int32_t* src_row, int n_rows, const float* states, int W, int d,
+                       float* qpack, double* cq)
+{
+    const int j = blockIdx.x;           // padded row index
+    const int qb = j / TQ, i = j % TQ;
+    const int32_t src = j < n_rows ? src_row[j] : -1;
+    double lnb = 0.0;
+    for (int k = threadIdx.x; k < d; k += blockDim.x) {
+        float* dst = qpack + (((int64_t)qb * d + k) * F) * TQ + i;
+        if (src >= 0) {
+            const float* st = states + (int64_t)src * W;
+            for (int f = 0; f < F; ++f) dst[f * TQ] = st[f * d + k];
+            if (model == 2) {
+                const double a = st[k], b = st[d + k];
+                lnb += lgamma(a) + lgamma(b) - lgamma(a + b);
+            }
+        } else {
+            for (int f = 0; f < F; ++f) dst[f * TQ] = 0.f;
+        }
+    }
+    if (model == 2) {
+        // wavefront reduction (blockDim == 64)
+        for (int off = 32; off > 0; off >>= 1) lnb += __shfl_down(lnb, off, 64);
+        if (threadIdx.x == 0) cq[j] = lnb;
+    }
+}
+
+void launch_pack(int model, const int32_t* src_row, int n_rows, int n_rows_pad, const float* states,
+                 int W, int d, float* qpack, double* cq, hipStream_t s)
+{
+    if (n_rows_pad <= 0) return;
+    if (model == 0)
+        hipLaunchKernelGGL((k_pack<kTqGqe, 1>), dim3(n_rows_pad), dim3(64), 0, s, model, src_row, n_rows,
+                           states, W, d, qpack, cq);
+    else if (model == 1)
+        hipLaunchKernelGGL((k_pack<kTqQ2b, 2>), dim3(n_rows_pad), dim3(64), 0, s, model, src_row, n_rows,
+                           states, W, d, qpack, cq);
+    else
+        hipLaunchKernelGGL((k_pack<kTqBetae, 2>), dim3(n_rows_pad), dim3(64), 0, s, model, src_row, n_rows,
+                           states, W, d, qpack, cq);
+}
+
+}  // namespace kgq

@@ -1,0 +1,169 @@
+// Entity scoring: the "entity similarity query" that the paper times
+// together with operator execution (Experiments, Metrics): every query
+// embedding is scored against every entity.
+//
+// This is VALU work, not a dense contraction: per (query, entity, dim)
+// triple GQE needs |q - e| accumulated, Query2Box a box distance, BetaE a KL
+// divergence. The kernel is organised like a register-blocked GEMM without
+// the multiply-add:
+//   - a lane owns 4 consecutive entities (one 128-bit load per dimension
+//     from the blocked, dimension-major entity table);
+//   - a wavefront owns kTq query rows that are uniform across its lanes, so
+//     the query values come through the scalar cache into SGPRs and feed the
+//     VALU as scalar operands: no LDS traffic and no cross-lane reduction;
+//   - the 4 wavefronts of a workgroup share one entity block (L1 reuse), and
+//     workgroups are assigned so that each XCD sweeps a contiguous range of
+//     entity blocks with all query groups, keeping its share of the table in
+//     that XCD's L2.
+//
+// Per-triple work (one non-packed VALU op each):
+//   GQE     d = e - q;  acc += |d|                                       (2)
+//   Q2B     t = |e - c|: acc1 += t; acc2 += min(t, o)                    (4)
+//           score = gamma - acc1 + (1 - center_reg) * acc2, the exact
+//           regrouping of dist_out + center_reg * dist_in
+//           (t <= o: center_reg * t; t > o: (t - o) + center_reg * o)
+//   BetaE   acc += alpha_q * U_e + beta_q * V_e                          (2 FMA)
+//           score = gamma - (C_q + E_e + acc), the exact regrouping of
+//           sum_i KL(Beta(entity_i) || Beta(query_i)) with
+//           U = psi(a + b) - psi(a), V = psi(a + b) - psi(b),
+//           E_e = sum_i [-lnB(a,b) + a psi(a) + b psi(b) - (a+b) psi(a+b)],
+//           C_q = sum_i lnB(alpha_q, beta_q)  (entity a, b; query alpha_q, beta_q).
+// Union (disjunctive normal form, Eq. 1 of the paper): a union query has two
+// adjacent rows; its score is the max of the two rows' scores.
+#include "kgq_internal.hpp"
+
+namespace kgq {
+
+template <int MODEL, int TQ>
+__global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int total_wg, int wg_per_xcd)
+{
+    // XCD-aware mapping: workgroup b runs on XCD b % 8 (round-robin dispatch).
+    const int b = blockIdx.x;
+    const int L = (b & 7) * wg_per_xcd + (b >> 3);
+    if (L >= total_wg) return;
+    const int eb = L / nqg;
+    const int qg = L - eb * nqg;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int qb = qg * 4 + wave;
+    if (qb * TQ >= a.n_rows) return;
+
+    constexpr int F = (MODEL == 0) ? 1 : 2;      // query fields per row
+    constexpr int EF = (MODEL == 2) ? 2 : 1;     // entity fields per dim
+    const int d = a.d;
+    const float* __restrict__ qp = a.qpack + (int64_t)qb * d * F * TQ;
+    const float* __restrict__ ep = a.ent + (int64_t)eb * d * EF * kEntBlock + lane * 4;
+
+    float acc[TQ][4];
+    float acc2[(MODEL == 1) ? TQ : 1][4];
+#pragma unroll
+    for (int i = 0; i < TQ; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+#pragma unroll
+    for (int i = 0; i < ((MODEL == 1) ? TQ : 1); ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc2[i][j] = 0.f;
+
+#pragma unroll 2
+    for (int k = 0; k < d; ++k) {
+        const float* q = qp + k * F * TQ;
+        if (MODEL == 2) {
+            const float4 u = *reinterpret_cast<const float4*>(ep + (int64_t)k * 2 * kEntBlock);
+            const float4 v = *reinterpret_cast<const float4*>(ep + (int64_t)k * 2 * kEntBlock + kEntBlock);
+#pragma unroll
+            for (int i = 0; i < TQ; ++i) {
+                const float al = q[i], be = q[TQ + i];
+                acc[i][0] = fmaf(be, v.x, fmaf(al, u.x, acc[i][0]));
+                acc[i][1] = fmaf(be, v.y, fmaf(al, u.y, acc[i][1]));
+                acc[i][2] = fmaf(be, v.z, fmaf(al, u.z, acc[i][2]));
+                acc[i][3] = fmaf(be, v.w, fmaf(al, u.w, acc[i][3]));
+            }
+        } else {
+            const float4 e = *reinterpret_cast<const float4*>(ep + (int64_t)k * kEntBlock);
+            const float ev[4] = {e.x, e.y, e.z, e.w};
+#pragma unroll
+            for (int i = 0; i < TQ; ++i) {
+                const float c = q[i];
+                if (MODEL == 0) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[i][j] += fabsf(ev[j] - c);
+                } else {
+                    const float o = q[TQ + i];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float t = fabsf(ev[j] - c);
+                        acc[i][j] += t;
+                        acc2[i][j] += __builtin_fminf(t, o);
+                    }
+                }
+            }
+        }
+    }
+
+    // Epilogue: finish the scores, merge union pairs, store.
+    const int64_t e0 = (int64_t)eb * kEntBlock + lane * 4;
+    double ee[4] = {0.0, 0.0, 0.0, 0.0};
+    if (MODEL == 2) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ee[j] = (e0 + j < a.N) ? a.ee[e0 + j] : 0.0;
+    }
+    const int nu_pairs = a.n_union_rows >> 1;
+#pragma unroll
+    for (int i = 0; i < TQ; i += 2) {
+        const int row = qb * TQ + i;
+        if (row >= a.n_rows) break;
+        float s0[4], s1[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (MODEL == 0) {
+                s0[j] = a.gamma - acc[i][j];
+                s1[j] = a.gamma - acc[i + 1][j];
+            } else if (MODEL == 1) {
+                const float w = 1.0f - a.center_reg;
+                s0[j] = a.gamma - acc[i][j] + w * acc2[i][j];
+                s1[j] = a.gamma - acc[i + 1][j] + w * acc2[i + 1][j];
+            } else {
+                s0[j] = (float)((double)a.gamma - (a.cq[row] + ee[j] + (double)acc[i][j]));
+                s1[j] = (float)((double)a.gamma - (a.cq[row + 1] + ee[j] + (double)acc[i + 1][j]));
+            }
+        }
+        if (row < a.n_union_rows) {
+            float* dst = a.scores + (int64_t)a.out_dest[row >> 1] * a.ld;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (e0 + j < a.N) dst[e0 + j] = fmaxf(s0[j], s1[j]);
+        } else {
+            const int o0 = nu_pairs + (row - a.n_union_rows);
+            float* dst0 = a.scores + (int64_t)a.out_dest[o0] * a.ld;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (e0 + j < a.N) dst0[e0 + j] = s0[j];
+            if (row + 1 < a.n_rows) {
+                float* dst1 = a.scores + (int64_t)a.out_dest[o0 + 1] * a.ld;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (e0 + j < a.N) dst1[e0 + j] = s1[j];
+            }
+        }
+    }
+}
+
+void launch_score(const ScoreArgs& a, hipStream_t s)
+{
+    if (a.n_rows <= 0) return;
+    const int tq = score_tq(a.model);
+    const int nqb = (a.n_rows + tq - 1) / tq;
+    const int nqg = (nqb + 3) / 4;
+    const int total = (int)(a.n_blocks * nqg);
+    const int per_xcd = (total + 7) / 8;
+    dim3 grid(per_xcd * 8);
+    if (a.model == 0)
+        hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, a, nqg, total, per_xcd);
+    else if (a.model == 1)
+        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, a, nqg, total, per_xcd);
+    else
+        hipLaunchKernelGGL((k_score<2, kTqBetae>), grid, dim3(256), 0, s, a, nqg, total, per_xcd);
+}
+
+}  // namespace kgq

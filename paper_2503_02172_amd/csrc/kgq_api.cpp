@@ -1,0 +1,765 @@
+// C ABI of libkgq (declared in include/kgq.h): handle, parameter loading,
+// argument validation, plan upload and the per-model stage sequence.
+#include <hip/hip_runtime.h>
+
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "../../include/kgq.h"
+#include "kgq_internal.hpp"
+#include "plan.hpp"
+
+using namespace kgq;
+
+namespace {
+
+struct ParamSpec {
+    int64_t rows, cols;     // element count = rows * cols
+    bool entity;            // takes cfg.entity_dtype
+};
+
+struct DevBuf {
+    void* p = nullptr;
+    size_t bytes = 0;
+};
+
+struct ProfPair {
+    int stage;
+    hipEvent_t start, stop;
+};
+
+thread_local std::string g_create_error;
+
+}  // namespace
+
+struct kgq_handle {
+    kgq_config cfg{};
+    bool dry = false;
+    bool checked = false;
+    std::string err;
+
+    std::map<std::string, ParamSpec> specs;
+    std::map<std::string, bool> loaded;
+    std::map<std::string, float*> dparam;   // device fp32 parameters (weights, relations)
+
+    // derived entity tables
+    int64_t n_blocks = 0;
+    float* ent_rm = nullptr;      // GQE/Q2B [N x d]; BetaE alpha|beta [N x 2d]
+    float* ent_blk = nullptr;     // GQE/Q2B blocked points; BetaE blocked U|V
+    double* ent_const = nullptr;  // BetaE E_e [n_pad]
+    float* rel_o_sp = nullptr;    // Q2B softplus(offset_raw) [R x d]
+
+    // scratch (sized for max_batch at create)
+    float* states = nullptr;
+    float* xbuf = nullptr;        // BetaE MLP input / intersection input
+    float* h1 = nullptr;
+    float* h2 = nullptr;
+    float* logits = nullptr;
+    float* zfeat = nullptr;
+    float* zmean = nullptr;
+    float* gate = nullptr;
+    float* qpack = nullptr;
+    double* cq = nullptr;
+    float* scores = nullptr;
+    int* dflag = nullptr;
+    int* hflag = nullptr;         // pinned
+
+    // plan images: per-structure cache slots + a ring for mixed batches
+    int64_t plan_words = 0;
+    int32_t* plan_dev = nullptr;  // (kNumStructures + 2) slots
+    int32_t* plan_host = nullptr; // pinned staging, same slot layout
+    hipEvent_t slot_event[kNumStructures + 2]{};
+    bool slot_event_live[kNumStructures + 2]{};
+    int cached_B[kNumStructures];
+    std::unique_ptr<Plan> cached_plan[kNumStructures];
+    int ring_next = 0;
+    Plan mixed_plan;
+
+    std::vector<void*> allocations;
+
+    // profiling
+    bool prof = false;
+    std::vector<ProfPair> prof_pending;
+    std::vector<hipEvent_t> prof_pool;
+    double prof_ms[KGQ_NUM_STAGES]{};
+    int64_t prof_n[KGQ_NUM_STAGES]{};
+};
+
+namespace {
+
+kgq_status fail(kgq_handle* h, kgq_status s, const std::string& msg)
+{
+    if (h) h->err = msg;
+    return s;
+}
+
+#define HIP_TRY(h, call)                                                                   \
+    do {                                                                                   \
+        hipError_t e_ = (call);                                                            \
+        if (e_ != hipSuccess)                                                              \
+            return fail((h), e_ == hipErrorOutOfMemory ? KGQ_E_OOM : KGQ_E_DEVICE,         \
+                        std::string(#call) + ": " + hipGetErrorString(e_));                 \
+    } while (0)
+
+void build_specs(kgq_handle* h)
+{
+    const int64_t N = h->cfg.n_entities, R = h->cfg.n_relations, d = h->cfg.dim;
+    auto& s = h->specs;
+    switch (h->cfg.model) {
+    case KGQ_GQE:
+        s["entity"] = {N, d, true};
+        s["relation"] = {R, d, false};
+        s["inter.w1"] = {d, d, false};
+        s["inter.b1"] = {1, d, false};
+        s["inter.w2"] = {d, d, false};
+        s["inter.b2"] = {1, d, false};
+        break;
+    case KGQ_Q2B:
+        s["entity"] = {N, d, true};
+        s["relation.center"] = {R, d, false};
+        s["relation.offset_raw"] = {R, d, false};
+        for (const char* grp : {"inter.center.", "inter.offset."}) {
+            s[std::string(grp) + "w1"] = {d, d, false};
+            s[std::string(grp) + "b1"] = {1, d, false};
+            s[std::string(grp) + "w2"] = {d, d, false};
+            s[std::string(grp) + "b2"] = {1, d, false};
+        }
+        break;
+    default:
+        s["entity.alpha_beta"] = {N, 2 * d, true};
+        s["relation"] = {R, 2 * d, false};
+        s["proj.w1"] = {4 * d, 2 * d, false};
+        s["proj.b1"] = {1, 4 * d, false};
+        s["proj.w2"] = {4 * d, 4 * d, false};
+        s["proj.b2"] = {1, 4 * d, false};
+        s["proj.w3"] = {2 * d, 4 * d, false};
+        s["proj.b3"] = {1, 2 * d, false};
+        s["inter.w1"] = {2 * d, 2 * d, false};
+        s["inter.b1"] = {1, 2 * d, false};
+        s["inter.w2"] = {d, 2 * d, false};
+        s["inter.b2"] = {1, d, false};
+        break;
+    }
+    for (auto& kv : s) h->loaded[kv.first] = false;
+}
+
+kgq_status dev_alloc(kgq_handle* h, void** p, size_t bytes)
+{
+    *p = nullptr;
+    if (bytes == 0) bytes = 16;
+    hipError_t e = hipMalloc(p, bytes);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        return fail(h, e == hipErrorOutOfMemory ? KGQ_E_OOM : KGQ_E_DEVICE,
+                    std::string("hipMalloc(") + std::to_string(bytes) + "): " + hipGetErrorString(e));
+    }
+    h->allocations.push_back(*p);
+    return KGQ_OK;
+}
+
+template <typename T>
+kgq_status dev_alloc_t(kgq_handle* h, T** p, size_t count)
+{
+    void* v = nullptr;
+    kgq_status s = dev_alloc(h, &v, count * sizeof(T));
+    *p = reinterpret_cast<T*>(v);
+    return s;
+}
+
+void free_all(kgq_handle* h)
+{
+    if (h->dry) return;
+    // Teardown: errors are ignored, every resource is released regardless.
+    (void)hipSetDevice(h->cfg.device);
+    (void)hipDeviceSynchronize();
+    for (void* p : h->allocations) (void)hipFree(p);
+    h->allocations.clear();
+    if (h->hflag) (void)hipHostFree(h->hflag);
+    if (h->plan_host) (void)hipHostFree(h->plan_host);
+    for (int i = 0; i < kNumStructures + 2; ++i)
+        if (h->slot_event[i]) (void)hipEventDestroy(h->slot_event[i]);
+    for (auto& pp : h->prof_pending) {
+        (void)hipEventDestroy(pp.start);
+        (void)hipEventDestroy(pp.stop);
+    }
+    for (hipEvent_t e : h->prof_pool) (void)hipEventDestroy(e);
+}
+
+kgq_status allocate_all(kgq_handle* h)
+{
+    const kgq_config& c = h->cfg;
+    const int64_t N = c.n_entities, d = c.dim, Bm = c.max_batch;
+    const int W = (c.model == KGQ_GQE) ? (int)d : (int)(2 * d);
+    h->n_blocks = (N + kEntBlock - 1) / kEntBlock;
+    const int64_t n_pad = h->n_blocks * kEntBlock;
+    kgq_status s;
+#define ALLOC(ptr, count) if ((s = dev_alloc_t(h, &(ptr), (size_t)(count))) != KGQ_OK) return s
+    // parameters other than the entity table
+    for (auto& kv : h->specs) {
+        if (kv.second.entity) continue;
+        float* p = nullptr;
+        ALLOC(p, kv.second.rows * kv.second.cols);
+        h->dparam[kv.first] = p;
+    }
+    if (c.model == KGQ_BETAE) {
+        ALLOC(h->ent_rm, N * 2 * d);
+        ALLOC(h->ent_blk, n_pad * 2 * d);
+        ALLOC(h->ent_const, n_pad);
+    } else {
+        ALLOC(h->ent_rm, N * d);
+        ALLOC(h->ent_blk, n_pad * d);
+        if (c.model == KGQ_Q2B) ALLOC(h->rel_o_sp, (int64_t)c.n_relations * d);
+    }
+    const int64_t rows = Bm * kStateRowsPerQuery;
+    ALLOC(h->states, rows * W);
+    const int64_t m_max = 3 * Bm;   // rows of one MLP level / intersection inputs
+    if (c.model == KGQ_BETAE) {
+        ALLOC(h->xbuf, m_max * 2 * d);
+        ALLOC(h->h1, m_max * 4 * d);
+        ALLOC(h->h2, m_max * 4 * d);
+    } else {
+        ALLOC(h->h1, m_max * d);
+        if (c.model == KGQ_Q2B) {
+            ALLOC(h->zfeat, m_max * d);
+            ALLOC(h->zmean, Bm * d);
+            ALLOC(h->gate, Bm * d);
+        }
+    }
+    ALLOC(h->logits, m_max * d);
+    const int tq = score_tq(c.model);
+    const int64_t prow = ((2 * Bm + tq - 1) / tq) * tq;
+    ALLOC(h->qpack, prow * 2 * d);
+    ALLOC(h->cq, prow);
+    ALLOC(h->scores, Bm * N);
+    ALLOC(h->dflag, 1);
+    h->plan_words = plan_image_words((int)Bm);
+    ALLOC(h->plan_dev, (int64_t)(kNumStructures + 2) * h->plan_words);
+#undef ALLOC
+    hipError_t e = hipHostMalloc((void**)&h->hflag, sizeof(int), hipHostMallocDefault);
+    if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(flag)");
+    e = hipHostMalloc((void**)&h->plan_host, sizeof(int32_t) * (kNumStructures + 2) * h->plan_words,
+                      hipHostMallocDefault);
+    if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(plan staging)");
+    for (int i = 0; i < kNumStructures + 2; ++i) HIP_TRY(h, hipEventCreateWithFlags(&h->slot_event[i], hipEventDisableTiming));
+    HIP_TRY(h, hipMemset(h->dflag, 0, sizeof(int)));
+    return KGQ_OK;
+}
+
+// --- profiling -------------------------------------------------------------
+
+hipEvent_t prof_event(kgq_handle* h)
+{
+    if (!h->prof_pool.empty()) {
+        hipEvent_t e = h->prof_pool.back();
+        h->prof_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+struct StageTimer {
+    kgq_handle* h;
+    int stage;
+    hipStream_t s;
+    hipEvent_t a = nullptr, b = nullptr;
+    StageTimer(kgq_handle* h_, int st, hipStream_t s_) : h(h_), stage(st), s(s_)
+    {
+        if (h->prof) {
+            a = prof_event(h);
+            b = prof_event(h);
+            if (hipEventRecord(a, s) != hipSuccess) a = nullptr;
+        }
+    }
+    ~StageTimer()
+    {
+        if (h->prof && a && b && hipEventRecord(b, s) == hipSuccess) h->prof_pending.push_back({stage, a, b});
+    }
+};
+
+void prof_collect(kgq_handle* h)
+{
+    for (auto& pp : h->prof_pending) {
+        float ms = 0.f;
+        if (hipEventSynchronize(pp.stop) == hipSuccess && hipEventElapsedTime(&ms, pp.start, pp.stop) == hipSuccess) {
+            h->prof_ms[pp.stage] += ms;
+            h->prof_n[pp.stage] += 1;
+        }
+        h->prof_pool.push_back(pp.start);
+        h->prof_pool.push_back(pp.stop);
+    }
+    h->prof_pending.clear();
+}
+
+// --- execute helpers ----------------------------------------------------------
+
+bool all_loaded(const kgq_handle* h, std::string& missing)
+{
+    for (auto& kv : h->loaded)
+        if (!kv.second) {
+            missing = kv.first;
+            return false;
+        }
+    return true;
+}
+
+kgq_status check_outputs(kgq_handle* h, int32_t batch, const void* anchors, const void* rels, int32_t k,
+                         const float* out_scores, const int32_t* out_idx, const float* out_score)
+{
+    if (batch < 1 || batch > h->cfg.max_batch)
+        return fail(h, KGQ_E_INVALID_ARG, "batch " + std::to_string(batch) + " outside [1, max_batch=" +
+                                              std::to_string(h->cfg.max_batch) + "]");
+    if (!anchors || !rels) return fail(h, KGQ_E_INVALID_ARG, "anchors and relations must not be NULL");
+    if ((out_idx == nullptr) != (out_score == nullptr))
+        return fail(h, KGQ_E_INVALID_ARG, "out_topk_idx and out_topk_score must both be set or both be NULL");
+    if (!out_scores && !out_idx) return fail(h, KGQ_E_INVALID_ARG, "no output requested");
+    if (out_idx) {
+        const int64_t kmax = h->cfg.n_entities < kMaxK ? h->cfg.n_entities : kMaxK;
+        if (k < 1 || k > kmax)
+            return fail(h, KGQ_E_INVALID_ARG, "k=" + std::to_string(k) + " outside [1, " + std::to_string(kmax) + "]");
+    }
+    std::string missing;
+    if (!all_loaded(h, missing)) return fail(h, KGQ_E_NOT_LOADED, "parameter '" + missing + "' not loaded");
+    return KGQ_OK;
+}
+
+// Upload a plan image into device slot `slot` (after the slot's last use).
+kgq_status upload_plan(kgq_handle* h, const Plan& p, int slot, hipStream_t s)
+{
+    if ((int64_t)p.image.size() > h->plan_words) return fail(h, KGQ_E_DEVICE, "plan image exceeds its slot");
+    if (h->slot_event_live[slot]) HIP_TRY(h, hipEventSynchronize(h->slot_event[slot]));
+    int32_t* host = h->plan_host + (int64_t)slot * h->plan_words;
+    std::memcpy(host, p.image.data(), p.image.size() * sizeof(int32_t));
+    HIP_TRY(h, hipMemcpyAsync(h->plan_dev + (int64_t)slot * h->plan_words, host,
+                              p.image.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+    return KGQ_OK;
+}
+
+kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_t* anchors,
+                    const int32_t* rels, int sa, int sr, int fixed_na, int fixed_nr, bool mixed, int32_t k,
+                    float* out_scores, int32_t* out_idx, float* out_score, hipStream_t s)
+{
+    const kgq_config& c = h->cfg;
+    const int d = c.dim;
+    const int W = (c.model == KGQ_GQE) ? d : 2 * d;
+    const int64_t N = c.n_entities;
+    const int n_rel = c.n_relations;
+    auto param = [&](const char* n) { return h->dparam.at(n); };
+
+    if (h->checked) {
+        launch_clear_flag(h->dflag, s);
+        launch_validate(anchors, rels, mixed ? P + p.off.arity : nullptr, p.B, sa, sr, fixed_na, fixed_nr,
+                        N, n_rel, h->dflag, s);
+    }
+    GroupArgs g{P + p.off.g_in_start, P + p.off.g_n, P + p.off.g_out, P + p.off.g_post, P + p.off.g_neg,
+                p.n_groups};
+
+    if (c.model == KGQ_GQE || c.model == KGQ_Q2B) {
+        const bool q2b = c.model == KGQ_Q2B;
+        const float* rel_c = q2b ? param("relation.center") : param("relation");
+        {
+            StageTimer t(h, 0, s);
+            launch_chain(c.model, P + p.off.chain_anchor, P + p.off.chain_rel, p.n_chain, anchors, rels,
+                         h->ent_rm, rel_c, h->rel_o_sp, N, n_rel, d, h->states, h->dflag, s);
+        }
+        if (p.n_groups) {
+            const std::string pre = q2b ? "inter.center." : "inter.";
+            {
+                StageTimer t(h, 1, s);
+                launch_gemm({h->states, W, param((pre + "w1").c_str()), d, param((pre + "b1").c_str()), h->h1, d,
+                             nullptr, p.n_int_in, d, d, EPI_RELU}, s);
+            }
+            {
+                StageTimer t(h, 1, s);
+                launch_gemm({h->h1, d, param((pre + "w2").c_str()), d, param((pre + "b2").c_str()), h->logits, d,
+                             nullptr, p.n_int_in, d, d, EPI_NONE}, s);
+            }
+            if (q2b) {
+                StageTimer t(h, 1, s);
+                launch_gemm({h->states + d, W, param("inter.offset.w1"), d, param("inter.offset.b1"), h->zfeat, d,
+                             nullptr, p.n_int_in, d, d, EPI_RELU}, s);
+            }
+            {
+                StageTimer t(h, 2, s);
+                launch_combine_center(c.model, g, h->states, W, h->logits, h->zfeat, h->zmean, rels, rel_c, n_rel,
+                                      d, h->states, h->dflag, s);
+            }
+            if (q2b) {
+                {
+                    StageTimer t(h, 1, s);
+                    launch_gemm({h->zmean, d, param("inter.offset.w2"), d, param("inter.offset.b2"), h->gate, d,
+                                 nullptr, p.n_groups, d, d, EPI_NONE}, s);
+                }
+                StageTimer t(h, 2, s);
+                launch_combine_offset(g, h->states, W, h->gate, rels, h->rel_o_sp, n_rel, d, h->states, h->dflag, s);
+            }
+        }
+    } else {
+        const float* rel = param("relation");
+        auto mlp_level = [&](int l) {
+            const int M = (int)p.lv_dst[l].size();
+            if (!M) return;
+            {
+                StageTimer t(h, 0, s);
+                launch_betae_proj_prep(P + p.off.lv_src[l], P + p.off.lv_anchor[l], P + p.off.lv_rel[l], M, anchors,
+                                       rels, h->states, h->ent_rm, rel, N, n_rel, d, h->xbuf, h->dflag, s);
+            }
+            {
+                StageTimer t(h, 1, s);
+                launch_gemm({h->xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), h->h1, 4 * d, nullptr, M,
+                             4 * d, 2 * d, EPI_RELU}, s);
+            }
+            {
+                StageTimer t(h, 1, s);
+                launch_gemm({h->h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), h->h2, 4 * d, nullptr, M,
+                             4 * d, 4 * d, EPI_RELU}, s);
+            }
+            StageTimer t(h, 1, s);
+            launch_gemm({h->h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), h->states, 2 * d,
+                         P + p.off.lv_dst[l], M, 2 * d, 4 * d, EPI_BETA_REG}, s);
+        };
+        for (int l = 0; l < 3; ++l) mlp_level(l);
+        if (p.n_groups) {
+            {
+                StageTimer t(h, 2, s);
+                launch_betae_int_prep(g, h->states, d, h->xbuf, s);
+            }
+            {
+                StageTimer t(h, 1, s);
+                launch_gemm({h->xbuf, 2 * d, param("inter.w1"), 2 * d, param("inter.b1"), h->h1, 2 * d, nullptr,
+                             p.n_int_in, 2 * d, 2 * d, EPI_RELU}, s);
+            }
+            {
+                StageTimer t(h, 1, s);
+                launch_gemm({h->h1, 2 * d, param("inter.w2"), 2 * d, param("inter.b2"), h->logits, d, nullptr,
+                             p.n_int_in, d, 2 * d, EPI_NONE}, s);
+            }
+            StageTimer t(h, 2, s);
+            launch_betae_combine(g, h->xbuf, h->logits, d, h->states, s);
+        }
+        mlp_level(3);
+    }
+
+    const int tq = score_tq(c.model);
+    const int n_rows_pad = ((p.n_score_rows + tq - 1) / tq) * tq;
+    {
+        StageTimer t(h, 3, s);
+        launch_pack(c.model, P + p.off.score_src, p.n_score_rows, n_rows_pad, h->states, W, d, h->qpack, h->cq, s);
+    }
+    float* dst = out_scores ? out_scores : h->scores;
+    {
+        StageTimer t(h, 4, s);
+        ScoreArgs a{c.model, h->qpack, h->ent_blk, h->cq, h->ent_const, P + p.off.out_dest, p.n_score_rows,
+                    p.n_union_rows, d, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
+        launch_score(a, s);
+    }
+    if (out_idx) {
+        StageTimer t(h, 5, s);
+        launch_topk({dst, N, N, p.B, k, out_idx, out_score}, s);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(h, KGQ_E_DEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
+    if (h->checked) {
+        HIP_TRY(h, hipMemcpyAsync(h->hflag, h->dflag, sizeof(int), hipMemcpyDeviceToHost, s));
+        HIP_TRY(h, hipStreamSynchronize(s));
+        if (*h->hflag & kErrPadding)
+            return fail(h, KGQ_E_INVALID_ARG, "a mixed-batch unused anchor/relation slot is not -1");
+        if (*h->hflag & kErrRange) return fail(h, KGQ_E_OUT_OF_RANGE, "an anchor or relation id is out of range");
+    }
+    return KGQ_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// Exported API
+// ===========================================================================
+
+extern "C" {
+
+const char* kgq_status_string(kgq_status s)
+{
+    switch (s) {
+    case KGQ_OK: return "ok";
+    case KGQ_E_INVALID_ARG: return "invalid argument";
+    case KGQ_E_OUT_OF_RANGE: return "id out of range";
+    case KGQ_E_NOT_LOADED: return "parameters not loaded";
+    case KGQ_E_UNSUPPORTED: return "unsupported structure for this model";
+    case KGQ_E_NO_DEVICE: return "no device";
+    case KGQ_E_OOM: return "out of memory";
+    case KGQ_E_DEVICE: return "device error";
+    }
+    return "unknown status";
+}
+
+const char* kgq_last_error(const kgq_handle* h) { return h ? h->err.c_str() : ""; }
+
+const char* kgq_create_error(void) { return g_create_error.c_str(); }
+
+kgq_status kgq_structure_arity(int32_t structure_id, int32_t* n_anchors, int32_t* n_relations)
+{
+    const StructureDef* d = structure_def(structure_id);
+    if (!d || !n_anchors || !n_relations) return KGQ_E_INVALID_ARG;
+    *n_anchors = d->n_anchors;
+    *n_relations = d->n_relations;
+    return KGQ_OK;
+}
+
+kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out)
+{
+    g_create_error.clear();
+    auto bad = [](const std::string& m) {
+        g_create_error = m;
+        return KGQ_E_INVALID_ARG;
+    };
+    if (!cfg || !out) return bad("cfg and out must not be NULL");
+    *out = nullptr;
+    const kgq_config& c = *cfg;
+    if (c.model < KGQ_GQE || c.model > KGQ_BETAE) return bad("unknown model " + std::to_string(c.model));
+    if (c.dim < 4 || c.dim > 4096 || c.dim % 4) return bad("dim must be a multiple of 4 in [4, 4096]");
+    if (c.n_entities < 1 || c.n_entities > 0x7fffffffLL) return bad("n_entities outside [1, 2^31-1]");
+    if (c.n_relations < 1) return bad("n_relations must be >= 1");
+    if (c.entity_dtype != KGQ_F32 && c.entity_dtype != KGQ_BF16) return bad("unknown entity_dtype");
+    if (c.max_batch < 1 || c.max_batch > (1 << 20)) return bad("max_batch outside [1, 2^20]");
+    if (!(c.gamma == c.gamma)) return bad("gamma is NaN");
+    if (c.model == KGQ_Q2B && !(c.center_reg >= 0.f && c.center_reg <= 1.f)) return bad("center_reg outside [0, 1]");
+    if (c.device < -1) return bad("device must be >= -1");
+
+    std::unique_ptr<kgq_handle> h(new kgq_handle());
+    h->cfg = c;
+    h->dry = c.device < 0;
+    const char* env = std::getenv("KGQ_CHECKED");
+    h->checked = env && env[0] == '1';
+    for (int i = 0; i < kNumStructures; ++i) h->cached_B[i] = -1;
+    build_specs(h.get());
+    if (h->dry) {
+        *out = h.release();
+        return KGQ_OK;
+    }
+    int n_dev = 0;
+    if (hipGetDeviceCount(&n_dev) != hipSuccess || n_dev <= c.device) {
+        g_create_error = "no HIP device " + std::to_string(c.device);
+        return KGQ_E_NO_DEVICE;
+    }
+    if (hipSetDevice(c.device) != hipSuccess) {
+        g_create_error = "hipSetDevice failed";
+        return KGQ_E_NO_DEVICE;
+    }
+    kgq_status s = allocate_all(h.get());
+    if (s != KGQ_OK) {
+        g_create_error = h->err;
+        free_all(h.get());
+        return s;
+    }
+    *out = h.release();
+    return KGQ_OK;
+}
+
+kgq_status kgq_destroy(kgq_handle* h)
+{
+    if (!h) return KGQ_OK;
+    free_all(h);
+    delete h;
+    return KGQ_OK;
+}
+
+kgq_status kgq_set_checked(kgq_handle* h, int32_t on)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    h->checked = on != 0;
+    return KGQ_OK;
+}
+
+kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, size_t nbytes, int32_t dtype,
+                           int32_t src_is_device)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (!name) return fail(h, KGQ_E_INVALID_ARG, "name must not be NULL");
+    auto it = h->specs.find(name);
+    if (it == h->specs.end()) return fail(h, KGQ_E_INVALID_ARG, std::string("unknown parameter '") + name + "'");
+    const ParamSpec& ps = it->second;
+    const int want_dtype = ps.entity ? h->cfg.entity_dtype : KGQ_F32;
+    if (dtype != want_dtype)
+        return fail(h, KGQ_E_INVALID_ARG, std::string("parameter '") + name + "' expects dtype " +
+                                              (want_dtype == KGQ_BF16 ? "bf16" : "f32"));
+    const size_t elem = dtype == KGQ_BF16 ? 2 : 4;
+    const size_t want = (size_t)(ps.rows * ps.cols) * elem;
+    if (nbytes != want)
+        return fail(h, KGQ_E_INVALID_ARG, std::string("parameter '") + name + "' needs " + std::to_string(want) +
+                                              " bytes, got " + std::to_string(nbytes));
+    if (!src) return fail(h, KGQ_E_INVALID_ARG, "src must not be NULL");
+    if (h->dry) {
+        h->loaded[name] = true;
+        return KGQ_OK;
+    }
+    HIP_TRY(h, hipSetDevice(h->cfg.device));
+    const hipMemcpyKind kind = src_is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    const kgq_config& c = h->cfg;
+    if (!ps.entity) {
+        float* dst = h->dparam.at(name);
+        HIP_TRY(h, hipMemcpy(dst, src, nbytes, kind));
+        if (c.model == KGQ_Q2B && std::strcmp(name, "relation.offset_raw") == 0) {
+            launch_softplus(dst, h->rel_o_sp, ps.rows * ps.cols, nullptr);
+            HIP_TRY(h, hipGetLastError());
+            HIP_TRY(h, hipStreamSynchronize(nullptr));
+        }
+        h->loaded[name] = true;
+        return KGQ_OK;
+    }
+    // entity table: stage, then build the derived layouts
+    void* stage = nullptr;
+    hipError_t e = hipMalloc(&stage, nbytes);
+    if (e != hipSuccess) return fail(h, KGQ_E_OOM, "staging buffer for the entity table");
+    e = hipMemcpy(stage, src, nbytes, kind);
+    if (e == hipSuccess) {
+        const int bf16 = dtype == KGQ_BF16;
+        if (c.model == KGQ_BETAE)
+            launch_betae_entity_prep(stage, bf16, c.n_entities, c.dim, h->n_blocks, h->ent_rm, h->ent_blk,
+                                     h->ent_const, nullptr);
+        else
+            launch_relayout_points(stage, bf16, c.n_entities, c.dim, h->n_blocks, h->ent_rm, h->ent_blk, nullptr);
+        e = hipGetLastError();
+        if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+    }
+    (void)hipFree(stage);
+    if (e != hipSuccess) return fail(h, KGQ_E_DEVICE, std::string("entity table load: ") + hipGetErrorString(e));
+    h->loaded[name] = true;
+    return KGQ_OK;
+}
+
+kgq_status kgq_execute(kgq_handle* h, int32_t structure_id, int32_t batch, const int32_t* anchors,
+                       const int32_t* relations, int32_t k, float* out_scores, int32_t* out_topk_idx,
+                       float* out_topk_score, void* stream)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    const StructureDef* sd = structure_def(structure_id);
+    if (!sd) return fail(h, KGQ_E_INVALID_ARG, "unknown structure id " + std::to_string(structure_id));
+    if (sd->negation && h->cfg.model != KGQ_BETAE)
+        return fail(h, KGQ_E_UNSUPPORTED, std::string("structure ") + sd->name + " needs negation (BetaE only)");
+    kgq_status st = check_outputs(h, batch, anchors, relations, k, out_scores, out_topk_idx, out_topk_score);
+    if (st != KGQ_OK) return st;
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    HIP_TRY(h, hipSetDevice(h->cfg.device));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int slot = structure_id;
+    if (h->cached_B[slot] != batch || !h->cached_plan[slot]) {
+        std::unique_ptr<Plan> p(new Plan());
+        std::string err;
+        int es = 0;
+        if (!lower(h->cfg.model, batch, nullptr, structure_id, sd->n_anchors, sd->n_relations, false, *p, err, es))
+            return fail(h, (kgq_status)es, err);
+        st = upload_plan(h, *p, slot, s);
+        if (st != KGQ_OK) return st;
+        h->cached_plan[slot] = std::move(p);
+        h->cached_B[slot] = batch;
+    }
+    const int32_t* P = h->plan_dev + (int64_t)slot * h->plan_words;
+    st = run_plan(h, *h->cached_plan[slot], P, anchors, relations, sd->n_anchors, sd->n_relations, sd->n_anchors,
+                  sd->n_relations, false, k, out_scores, out_topk_idx, out_topk_score, s);
+    h->slot_event_live[slot] = hipEventRecord(h->slot_event[slot], s) == hipSuccess;
+    return st;
+}
+
+kgq_status kgq_execute_mixed(kgq_handle* h, int32_t batch, const int32_t* structure_ids, const int32_t* anchors,
+                             const int32_t* relations, int32_t k, float* out_scores, int32_t* out_topk_idx,
+                             float* out_topk_score, void* stream)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (!structure_ids) return fail(h, KGQ_E_INVALID_ARG, "structure_ids must not be NULL");
+    kgq_status st = check_outputs(h, batch, anchors, relations, k, out_scores, out_topk_idx, out_topk_score);
+    if (st != KGQ_OK) return st;
+    std::string err;
+    int es = 0;
+    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, h->mixed_plan, err, es))
+        return fail(h, (kgq_status)es, err);
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    HIP_TRY(h, hipSetDevice(h->cfg.device));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int slot = kNumStructures + h->ring_next;
+    h->ring_next ^= 1;
+    st = upload_plan(h, h->mixed_plan, slot, s);
+    if (st != KGQ_OK) return st;
+    const int32_t* P = h->plan_dev + (int64_t)slot * h->plan_words;
+    st = run_plan(h, h->mixed_plan, P, anchors, relations, 3, 3, 0, 0, true, k, out_scores, out_topk_idx,
+                  out_topk_score, s);
+    h->slot_event_live[slot] = hipEventRecord(h->slot_event[slot], s) == hipSuccess;
+    return st;
+}
+
+kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* structure_ids, int32_t* counts)
+{
+    if (!h || !structure_ids || !counts || batch < 1) return KGQ_E_INVALID_ARG;
+    Plan p;
+    std::string err;
+    int es = 0;
+    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, p, err, es)) {
+        const_cast<kgq_handle*>(h)->err = err;
+        return (kgq_status)es;
+    }
+    counts[0] = p.n_chain;
+    counts[1] = p.n_groups;
+    counts[2] = p.n_int_in;
+    for (int l = 0; l < 4; ++l) counts[3 + l] = (int32_t)p.lv_dst[l].size();
+    counts[7] = p.n_score_rows;
+    counts[8] = p.n_union_rows / 2;
+    counts[9] = plan_launches(p, true);
+    return KGQ_OK;
+}
+
+kgq_status kgq_dense(kgq_handle* h, const float* x, int32_t M, int32_t K, const float* w, const float* b, int32_t N,
+                     int32_t act, float* y, void* stream)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (!x || !w || !y) return fail(h, KGQ_E_INVALID_ARG, "x, w and y must not be NULL");
+    if (M < 1 || N < 1 || K < 4 || K % 4) return fail(h, KGQ_E_INVALID_ARG, "need M, N >= 1 and K a multiple of 4");
+    if (act < EPI_NONE || act > EPI_BETA_REG) return fail(h, KGQ_E_INVALID_ARG, "unknown activation");
+    if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w)) & 15)
+        return fail(h, KGQ_E_INVALID_ARG, "x and w must be 16-byte aligned");
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    HIP_TRY(h, hipSetDevice(h->cfg.device));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    {
+        StageTimer t(h, 1, s);
+        launch_gemm({x, K, w, K, b, y, N, nullptr, M, N, K, act}, s);
+    }
+    HIP_TRY(h, hipGetLastError());
+    return KGQ_OK;
+}
+
+kgq_status kgq_profile_enable(kgq_handle* h, int32_t on)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    if (!on && h->prof) prof_collect(h);
+    h->prof = on != 0;
+    return KGQ_OK;
+}
+
+kgq_status kgq_profile_read(kgq_handle* h, int32_t stage, double* total_ms, int64_t* launches)
+{
+    if (!h || stage < 0 || stage >= KGQ_NUM_STAGES || !total_ms || !launches) return KGQ_E_INVALID_ARG;
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    prof_collect(h);
+    *total_ms = h->prof_ms[stage];
+    *launches = h->prof_n[stage];
+    return KGQ_OK;
+}
+
+kgq_status kgq_profile_reset(kgq_handle* h)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (h->dry) return KGQ_OK;
+    prof_collect(h);
+    for (int i = 0; i < KGQ_NUM_STAGES; ++i) {
+        h->prof_ms[i] = 0.0;
+        h->prof_n[i] = 0;
+    }
+    return KGQ_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,127 @@
+// Internal declarations shared by the host library and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kgq {
+
+// ---- data layout constants -------------------------------------------------
+
+// Entities are scored in blocks of 256: 64 lanes of one wavefront, each lane
+// owning 4 consecutive entities. The entity table is stored block by block,
+// dimension-major inside a block: element (e, k) lives at
+//   [e / 256][k][e % 256]            (GQE, Query2Box points)
+//   [e / 256][k][f][e % 256], f=0,1  (BetaE: f=0 U, f=1 V)
+// so that a wavefront reads 1 KiB contiguous per dimension.
+constexpr int kEntBlock = 256;
+
+// Largest k of a top-k request (the selection buffer lives in LDS).
+constexpr int kMaxK = 1024;
+
+// Query rows per wavefront in the scorer (rows are wave-uniform and read
+// through the scalar cache). Packed layout [row_block][k][field][kTq].
+constexpr int kTqGqe = 16;
+constexpr int kTqQ2b = 8;
+constexpr int kTqBetae = 16;
+
+inline int score_tq(int model) { return model == 0 ? kTqGqe : (model == 1 ? kTqQ2b : kTqBetae); }
+
+// Device error flag bits.
+constexpr int kErrRange = 1;    // an anchor or relation id outside its table
+constexpr int kErrPadding = 2;  // a mixed-batch unused slot that is not -1
+
+enum Epilogue { EPI_NONE = 0, EPI_RELU = 1, EPI_BETA_REG = 2 };
+
+// ---- launchers (each enqueues on `s` and returns) ---------------------------
+
+struct GemmArgs {
+    const float* A; int64_t lda;       // [M x K] row-major
+    const float* W; int64_t ldw;       // [N x K] row-major (y = W x + b)
+    const float* bias;                 // [N] or nullptr
+    float* C; int64_t ldc;             // [M x N] (row m stored at C + map(m) * ldc)
+    const int32_t* c_rowmap;           // nullptr = identity
+    int M, N, K;                       // K % 4 == 0, A/W 16-byte aligned rows
+    int epi;
+};
+void launch_gemm(const GemmArgs& g, hipStream_t s);
+
+// Relayout a row-major [N x d] table (fp32 or bf16 bits) into the blocked
+// scorer layout (fp32), padding with zeros; also writes a row-major fp32 copy.
+void launch_relayout_points(const void* src, int src_bf16, int64_t N, int d, int64_t n_blocks,
+                            float* rowmajor, float* blocked, hipStream_t s);
+
+// BetaE: decode alpha|beta [N x 2d] to fp32 row-major, and build U, V
+// (blocked) and the per-entity constant E_e (double).
+void launch_betae_entity_prep(const void* src, int src_bf16, int64_t N, int d, int64_t n_blocks,
+                              float* ab_rowmajor, float* uv_blocked, double* e_const, hipStream_t s);
+
+void launch_softplus(const float* src, float* dst, int64_t n, hipStream_t s);
+
+void launch_clear_flag(int* flag, hipStream_t s);
+
+// Checked-mode validation of a batch's ids (and mixed padding).
+void launch_validate(const int32_t* anchors, const int32_t* rels, const int32_t* sid_dev,
+                     int B, int sa, int sr, int fixed_na, int fixed_nr,
+                     int64_t n_ent, int n_rel, int* flag, hipStream_t s);
+
+// GQE / Query2Box translation chains: row c = E[a] + sum_h C[r_h]
+// (Q2B also offset = sum_h softplus(O[r_h])). Width W = d (GQE) or 2d (Q2B).
+void launch_chain(int model, const int32_t* anchor_ref, const int32_t* rel_ref, int n_chain,
+                  const int32_t* anchors, const int32_t* rels, const float* ent_rm,
+                  const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
+                  float* states, int* flag, hipStream_t s);
+
+// Intersection combine, GQE / Q2B centers: softmax over branches of logits,
+// weighted center sum; Q2B also the mean of the offset features. Optional
+// post-projection (center part; Q2B offset part is added in combine2).
+struct GroupArgs {
+    const int32_t* in_start; const int32_t* n_in; const int32_t* out_row;
+    const int32_t* post_ref; const int32_t* neg_mask; int n_groups;
+};
+void launch_combine_center(int model, const GroupArgs& g, const float* states, int W,
+                           const float* logits, const float* zfeat, float* zmean,
+                           const int32_t* rels, const float* rel_c, int n_rel, int d,
+                           float* out_states, int* flag, hipStream_t s);
+// Query2Box offsets: min over branches times sigmoid(gate) (+ post offset).
+void launch_combine_offset(const GroupArgs& g, const float* states, int W, const float* gate,
+                           const int32_t* rels, const float* rel_o, int n_rel, int d,
+                           float* out_states, int* flag, hipStream_t s);
+
+// BetaE: intersection inputs (reciprocal where the branch is negated).
+void launch_betae_int_prep(const GroupArgs& g, const float* states, int d, float* x_int,
+                           hipStream_t s);
+// BetaE: attention-weighted alpha/beta over branches.
+void launch_betae_combine(const GroupArgs& g, const float* x_int, const float* logits, int d,
+                          float* states, hipStream_t s);
+// BetaE projection input rows x = base + Rel[r] (base = a state row, or an
+// anchor entity when src_row < 0).
+void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
+                            int M, const int32_t* anchors, const int32_t* rels,
+                            const float* states, const float* ent_ab, const float* rel,
+                            int64_t n_ent, int n_rel, int d, float* x, int* flag, hipStream_t s);
+
+// Pack scored rows into the scorer's layout; BetaE also C_q = sum lnB(a, b).
+void launch_pack(int model, const int32_t* src_row, int n_rows, int n_rows_pad, const float* states,
+                 int W, int d, float* qpack, double* cq, hipStream_t s);
+
+struct ScoreArgs {
+    int model;
+    const float* qpack; const float* ent; const double* cq; const double* ee;
+    const int32_t* out_dest;
+    int n_rows, n_union_rows, d;
+    int64_t N, n_blocks;
+    float gamma, center_reg;
+    float* scores; int64_t ld;
+};
+void launch_score(const ScoreArgs& a, hipStream_t s);
+
+struct TopkArgs {
+    const float* scores; int64_t ld; int64_t N;
+    int n_rows;                        // rows 0 .. n_rows-1 of the score buffer
+    int k;
+    int32_t* out_idx; float* out_score;
+};
+void launch_topk(const TopkArgs& a, hipStream_t s);
+
+}  // namespace kgq

@@ -1,0 +1,253 @@
+"""ctypes binding of libkgq (include/kgq.h).
+
+Argument marshalling only: every step of query execution runs in the HIP
+library. PyTorch supplies device memory and the current stream. If the
+library has not been built this module raises instead of falling back to
+anything else.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkgq.so")
+
+GQE, Q2B, BETAE = 0, 1, 2
+F32, BF16 = 0, 1
+NUM_STRUCTURES = 14
+MAX_K = 1024
+PLAN_FIELDS = ["chains", "groups", "intersection_inputs", "level1", "level2", "level3", "post",
+               "scored_rows", "union_pairs", "launches"]
+STAGES = ["chain", "dense", "combine", "pack", "score", "topk"]
+
+OK = 0
+STATUS = {0: "OK", -1: "INVALID_ARG", -2: "OUT_OF_RANGE", -3: "NOT_LOADED", -4: "UNSUPPORTED",
+          -5: "NO_DEVICE", -6: "OOM", -7: "DEVICE"}
+
+
+class KgqError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("model", ctypes.c_int32), ("dim", ctypes.c_int32), ("n_entities", ctypes.c_int64),
+                ("n_relations", ctypes.c_int32), ("entity_dtype", ctypes.c_int32), ("gamma", ctypes.c_float),
+                ("center_reg", ctypes.c_float), ("max_batch", ctypes.c_int32), ("device", ctypes.c_int32)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    """Open libkgq.so (built in-tree by paper_2503_02172_amd/build.py)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: run `python paper_2503_02172_amd/build.py` "
+                          "(or __graft_entry__.build()) first")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    i32p, i64p, dp = ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)
+    sig = {
+        "kgq_create": ([ctypes.POINTER(Config), ctypes.POINTER(vp)], i32),
+        "kgq_load_params": ([vp, ctypes.c_char_p, vp, ctypes.c_size_t, i32, i32], i32),
+        "kgq_structure_arity": ([i32, i32p, i32p], i32),
+        "kgq_execute": ([vp, i32, i32, vp, vp, i32, vp, vp, vp, vp], i32),
+        "kgq_execute_mixed": ([vp, i32, i32p, vp, vp, i32, vp, vp, vp, vp], i32),
+        "kgq_set_checked": ([vp, i32], i32),
+        "kgq_describe_plan": ([vp, i32, i32p, i32p], i32),
+        "kgq_dense": ([vp, vp, i32, i32, vp, vp, i32, i32, vp, vp], i32),
+        "kgq_profile_enable": ([vp, i32], i32),
+        "kgq_profile_read": ([vp, i32, dp, i64p], i32),
+        "kgq_profile_reset": ([vp], i32),
+        "kgq_destroy": ([vp], i32),
+        "kgq_status_string": ([i32], ctypes.c_char_p),
+        "kgq_last_error": ([vp], ctypes.c_char_p),
+        "kgq_create_error": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def arity(structure: int):
+    a, r = ctypes.c_int32(), ctypes.c_int32()
+    rc = lib().kgq_structure_arity(structure, ctypes.byref(a), ctypes.byref(r))
+    if rc != OK:
+        raise KgqError(rc, f"structure {structure}")
+    return a.value, r.value
+
+
+def _ptr(t) -> int:
+    """Address of a torch tensor or numpy array (None -> 0)."""
+    if t is None:
+        return 0
+    if hasattr(t, "data_ptr"):
+        return int(t.data_ptr())
+    return int(t.ctypes.data)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+class Engine:
+    """One kgq handle: a model's parameters on one GPU plus scratch space."""
+
+    def __init__(self, model: int, n_entities: int, n_relations: int, dim: int, gamma: float,
+                 max_batch: int, center_reg: float = 0.02, entity_dtype: int = F32, device: int = 0):
+        self.cfg = Config(model, dim, n_entities, n_relations, entity_dtype, gamma, center_reg,
+                          max_batch, device)
+        h = ctypes.c_void_p()
+        rc = lib().kgq_create(ctypes.byref(self.cfg), ctypes.byref(h))
+        if rc != OK:
+            raise KgqError(rc, lib().kgq_create_error().decode())
+        self.h = h
+        self.model, self.n_entities, self.dim = model, n_entities, dim
+        self.device = device
+
+    # -- lifecycle ------------------------------------------------------------
+    def close(self):
+        if getattr(self, "h", None):
+            lib().kgq_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def _check(self, rc: int):
+        if rc != OK:
+            raise KgqError(rc, lib().kgq_last_error(self.h).decode())
+
+    # -- parameters -----------------------------------------------------------
+    def load(self, name: str, arr, dtype: int = F32):
+        """Load one parameter from a numpy array (host) or a torch tensor."""
+        if hasattr(arr, "data_ptr"):
+            t = arr.contiguous()
+            self._check(lib().kgq_load_params(self.h, name.encode(), t.data_ptr(),
+                                              t.numel() * t.element_size(), dtype, int(t.is_cuda)))
+            return
+        a = np.ascontiguousarray(arr)
+        self._check(lib().kgq_load_params(self.h, name.encode(), a.ctypes.data, a.nbytes, dtype, 0))
+
+    def load_all(self, params: Dict[str, np.ndarray], entity_bf16: Optional[np.ndarray] = None):
+        for name, arr in params.items():
+            if entity_bf16 is not None and name.startswith("entity"):
+                self.load(name, np.ascontiguousarray(entity_bf16, np.uint16), BF16)
+            else:
+                self.load(name, np.ascontiguousarray(arr, np.float32), F32)
+
+    def set_checked(self, on: bool):
+        self._check(lib().kgq_set_checked(self.h, int(bool(on))))
+
+    # -- execution ------------------------------------------------------------
+    def execute_into(self, structure: int, batch: int, anchors, relations, k: int,
+                     out_scores=None, out_idx=None, out_score=None, stream=None):
+        """Enqueue one single-structure batch with caller-owned outputs."""
+        self._check(lib().kgq_execute(self.h, structure, batch, _ptr(anchors), _ptr(relations), k,
+                                      _ptr(out_scores), _ptr(out_idx), _ptr(out_score),
+                                      _stream(stream)))
+
+    def execute_mixed_into(self, structure_ids: np.ndarray, anchors, relations, k: int,
+                           out_scores=None, out_idx=None, out_score=None, stream=None):
+        sid = np.ascontiguousarray(structure_ids, np.int32)
+        self._check(lib().kgq_execute_mixed(self.h, sid.shape[0],
+                                            sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                            _ptr(anchors), _ptr(relations), k, _ptr(out_scores),
+                                            _ptr(out_idx), _ptr(out_score), _stream(stream)))
+
+    def execute(self, structure, anchors, relations, k: Optional[int] = None, scores: bool = False,
+                stream=None):
+        """Run a batch on the current stream and return torch tensors.
+
+        structure: an id (all queries alike; anchors [B x nA], relations
+        [B x nR]) or a host int array [B] (mixed; anchors/relations [B x 3]
+        padded with -1). Returns dict(scores=[B x N] or None, idx, score).
+        """
+        import torch
+        dev = torch.device("cuda", self.device)
+        a = torch.as_tensor(anchors, dtype=torch.int32, device=dev).contiguous()
+        r = torch.as_tensor(relations, dtype=torch.int32, device=dev).contiguous()
+        B = a.shape[0]
+        out_s = torch.empty((B, self.n_entities), dtype=torch.float32, device=dev) if scores else None
+        out_i = out_v = None
+        if k is not None:
+            out_i = torch.empty((B, k), dtype=torch.int32, device=dev)
+            out_v = torch.empty((B, k), dtype=torch.float32, device=dev)
+        kk = k if k is not None else 0
+        if np.ndim(structure) == 0:
+            self.execute_into(int(structure), B, a, r, kk, out_s, out_i, out_v, stream)
+        else:
+            self.execute_mixed_into(np.asarray(structure), a, r, kk, out_s, out_i, out_v, stream)
+        return {"scores": out_s, "idx": out_i, "score": out_v}
+
+    def describe_plan(self, structure_ids: Sequence[int]) -> Dict[str, int]:
+        sid = np.ascontiguousarray(structure_ids, np.int32)
+        counts = (ctypes.c_int32 * 10)()
+        self._check(lib().kgq_describe_plan(self.h, sid.shape[0],
+                                            sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), counts))
+        return dict(zip(PLAN_FIELDS, list(counts)))
+
+    def dense(self, x, w, b=None, act: int = 0, out=None, stream=None):
+        """y = act(x @ w.T + b) with the library's MFMA kernel (torch tensors)."""
+        import torch
+        M, K = x.shape
+        N = w.shape[0]
+        y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=x.device)
+        self._check(lib().kgq_dense(self.h, _ptr(x), M, K, _ptr(w), _ptr(b), N, act, _ptr(y),
+                                    _stream(stream)))
+        return y
+
+    # -- profiling ------------------------------------------------------------
+    def profile(self, on: bool):
+        self._check(lib().kgq_profile_enable(self.h, int(bool(on))))
+
+    def profile_reset(self):
+        self._check(lib().kgq_profile_reset(self.h))
+
+    def profile_read(self) -> Dict[str, tuple]:
+        out = {}
+        for i, name in enumerate(STAGES):
+            ms, n = ctypes.c_double(), ctypes.c_int64()
+            self._check(lib().kgq_profile_read(self.h, i, ctypes.byref(ms), ctypes.byref(n)))
+            out[name] = (ms.value, n.value)
+        return out
+
+
+def engine_for(workload, max_batch: Optional[int] = None, device: int = 0, model: Optional[int] = None,
+               params: Optional[Dict[str, np.ndarray]] = None) -> Engine:
+    """Create an Engine for a synthetic workload and load its parameters."""
+    m = workload.model if model is None else model
+    p = workload.params if params is None else params
+    bmax = max_batch or max(b.batch for b in workload.batches)
+    bf16 = workload.entity_bf16 if (m == BETAE and workload.entity_bf16 is not None) else None
+    eng = Engine(m, workload.n_entities, workload.n_relations, workload.dim, workload.gamma, bmax,
+                 workload.center_reg, BF16 if bf16 is not None else F32, device)
+    eng.load_all(p, entity_bf16=bf16)
+    return eng
