@@ -1,0 +1,274 @@
+"""Benchmark: batched query answering (score every entity + top-k) on one MI355X.
+
+One step = one pass of the whole hot path over one batch of the headline
+workload: Query2Box at 14,505 entities x 474 relations, d = 400, 512 queries
+for each of the 9 structures without negation (4,608 queries, nine
+single-structure execute calls), every query scored against all entities,
+top-100. Inputs are resident in HBM before the timed region starts.
+
+Prints one JSON line. `value` is queries/s over the timed steps.
+`roofline` describes the dominant kernel (the entity scorer): algorithmic
+VALU operations per launch divided by its average launch time, measured
+with HIP events on the execute stream during the timed region, against the
+FP32 VALU lane-operation peak of the chip. `cpu_baseline` times the CPU
+oracle on a bounded sample of the same workload. `others` reports the other
+four workloads (throughput only).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X FP32 VALU peak in lane-operations per second: 256 CUs x 4 SIMDs x
+# 32 lanes per clock x 2.4 GHz = 78.64e12, the published 157.3 TFLOP/s FP32
+# vector peak counted at 2 flops per lane-operation. Each sub / add / min /
+# max / fma of the scorers counts as one lane-operation (packed FP32 is
+# disabled in this build, so every instruction does one operation per lane).
+PEAK_VALU_OPS = 256 * 4 * 32 * 2.4e9
+HBM_PEAK = 8.0e12
+# algorithmic VALU operations per (query row, entity, dimension) triple
+OPS_PER_TRIPLE = {0: 2, 1: 4, 2: 2}
+K_TOP = 100
+
+WORKLOAD_DESC = {
+    "C1": "GQE, 1,000 entities x 20 relations, d=32, fp32; 16 x 1p + 16 x 2i; top-10",
+    "C2": "Query2Box, 14,505 entities x 474 relations, d=400, fp32; 512 queries per structure over "
+          "1p,2p,3p,2i,3i,pi,ip,2u,up (4,608 queries, 9 execute calls); top-100",
+    "C3": "BetaE, 14,505 entities x 474 relations, d=400, fp32; 512 queries per structure over "
+          "1p,2in,3in,inp,pin,pni; top-100",
+    "C4-q2b": "Query2Box, 63,361 entities x 400 relations, d=400, fp32; 1,024 mixed 3p/ip/pi/up/3i; top-100",
+    "C4-gqe": "GQE, 63,361 entities x 400 relations, d=400, fp32; 1,024 mixed 3p/ip/pi/up/3i; top-100",
+    "C5": "BetaE, 63,361 entities x 400 relations, d=400, bf16 entity table; 2,048 mixed over all 14 "
+          "structures; top-100",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Prepared:
+    """A workload on the device: engine, resident inputs and outputs."""
+
+    def __init__(self, name: str):
+        import torch
+        from paper_2503_02172_amd import kgq, synth
+
+        self.name = name
+        w = synth.make_workload(name)
+        self.w = w
+        model = w.model
+        params = w.params
+        if name == "C4-gqe":
+            model = kgq.GQE
+        self.model = model
+        self.eng = kgq.engine_for(w, model=model, params=params)
+        dev = torch.device("cuda", 0)
+        self.calls = []
+        for b in w.batches:
+            a = torch.as_tensor(b.anchors, dtype=torch.int32, device=dev).contiguous()
+            r = torch.as_tensor(b.relations, dtype=torch.int32, device=dev).contiguous()
+            idx = torch.empty((b.batch, w.k), dtype=torch.int32, device=dev)
+            val = torch.empty((b.batch, w.k), dtype=torch.float32, device=dev)
+            sid = synth.STRUCTURE_ID[b.structure] if b.structure else b.structure_ids
+            self.calls.append((sid, b.batch, a, r, idx, val))
+        self.n_queries = sum(c[1] for c in self.calls)
+        # scored rows (union queries score two rows) -> triples per step
+        rows = 0
+        for c in self.calls:
+            ids = np.full(c[1], c[0]) if np.ndim(c[0]) == 0 else c[0]
+            rows += self.eng.describe_plan(ids)["scored_rows"]
+        self.rows = rows
+        self.triples = rows * w.n_entities * w.dim
+        torch.cuda.synchronize()
+
+    def step(self, stream):
+        for sid, B, a, r, idx, val in self.calls:
+            if np.ndim(sid) == 0:
+                self.eng.execute_into(int(sid), B, a, r, self.w.k, None, idx, val, stream)
+            else:
+                self.eng.execute_mixed_into(sid, a, r, self.w.k, None, idx, val, stream)
+
+
+def time_steps(p: Prepared, steps: int, warmup: int, stream, profile_score: bool):
+    import torch
+    for _ in range(warmup):
+        p.step(stream)
+    torch.cuda.synchronize()
+    if profile_score:
+        p.eng.profile_reset()
+        p.eng.profile(["score"])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        p.step(stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prof = None
+    if profile_score:
+        prof = p.eng.profile_read()
+        p.eng.profile(None)
+    return dt, prof
+
+
+def stage_breakdown(p: Prepared, stream, reps: int = 3):
+    """Per-stage device time of one step (separate, fully instrumented pass)."""
+    import torch
+    p.eng.profile_reset()
+    p.eng.profile("all")
+    for _ in range(reps):
+        p.step(stream)
+    torch.cuda.synchronize()
+    r = p.eng.profile_read()
+    p.eng.profile(None)
+    p.eng.profile_reset()
+    return {k: round(v[0] / reps, 4) for k, v in r.items()}
+
+
+def traffic_for(kernel_src: str, name: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(name)
+    except Exception:
+        return None
+    if not rec:
+        return None
+    h = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+    if rec.get("kernel_sha256") != h:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(name: str, per_structure: int):
+    from oracle import oracle as O
+    from paper_2503_02172_amd import synth
+
+    w = synth.make_workload(name)
+    m = O.Model(w.model, w.params, w.gamma)
+    threads = O.max_threads(0)
+    nq = 0
+    t0 = time.perf_counter()
+    for b in w.batches:
+        n = min(per_structure, b.batch)
+        sid = synth.STRUCTURE_ID[b.structure] if b.structure else b.structure_ids[:n]
+        sc = m.scores(sid, b.anchors[:n], b.relations[:n])
+        O.topk(sc, w.k)
+        nq += n
+    dt = time.perf_counter() - t0
+    return {"value": nq / dt, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nq} of the {sum(b.batch for b in w.batches)} queries ({per_structure} per "
+                      f"structure), fp64 node-by-node evaluation, full scoring + top-{w.k}",
+            "seconds": round(dt, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="C2")
+    ap.add_argument("--no-others", action="store_true", help="skip the other four workloads")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-per-structure", type=int, default=512)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
+              "multi-GPU path; see the sharding notes in DESIGN.md.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    stream = torch.cuda.current_stream()
+
+    log(f"[bench] preparing {args.workload}")
+    p = Prepared(args.workload)
+    log(f"[bench] warmup {args.warmup}, timing {args.steps} steps")
+    dt, prof = time_steps(p, args.steps, args.warmup, stream, profile_score=True)
+    ms_step = dt / args.steps * 1e3
+    qps = p.n_queries * args.steps / dt
+    score_ms, score_n = prof["score"]
+    launches_per_step = len(p.calls)
+    avg_launch_ms = score_ms / max(score_n, 1)
+    ops_per_launch = OPS_PER_TRIPLE[p.model] * p.triples / launches_per_step
+    achieved = ops_per_launch / (avg_launch_ms * 1e-3)
+    src = os.path.join(ROOT, "paper_2503_02172_amd", "csrc", "k_score.hip")
+    traffic = traffic_for(src, f"score:{args.workload}")
+    roofline = {"bound": "alu", "kernel": "k_score (entity scorer)",
+                "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
+                "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4), "traffic": traffic,
+                "ops_per_launch": ops_per_launch, "avg_launch_ms": round(avg_launch_ms, 5),
+                "launches": score_n}
+    log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {qps:.0f} q/s, scorer {avg_launch_ms:.4f} ms/launch, "
+        f"{roofline['frac']*100:.1f}% of VALU peak")
+    stages = stage_breakdown(p, stream)
+    log(f"[bench] stage ms per step: {stages}")
+
+    others = {}
+    if not args.no_others:
+        for name in ["C1", "C3", "C4-q2b", "C4-gqe", "C5"]:
+            if name == args.workload:
+                continue
+            log(f"[bench] other workload {name}")
+            q = Prepared(name)
+            steps = max(3, min(args.steps, 10))
+            d2, pr = time_steps(q, steps, 2, stream, profile_score=True)
+            sm, sn = pr["score"]
+            ops = OPS_PER_TRIPLE[q.model] * q.triples / len(q.calls)
+            others[name] = {"workload": WORKLOAD_DESC[name], "queries_per_s": round(q.n_queries * steps / d2, 1),
+                            "ms_per_step": round(d2 / steps * 1e3, 4),
+                            "entity_scores_per_s": round(q.n_queries * q.w.n_entities * steps / d2, 1),
+                            "scorer_ms_per_launch": round(sm / max(sn, 1), 5),
+                            "scorer_valu_frac": round(ops / (sm / max(sn, 1) * 1e-3) / PEAK_VALU_OPS, 4),
+                            "stage_ms": stage_breakdown(q, stream, reps=2)}
+            log(f"[bench]   {name}: {others[name]['queries_per_s']} q/s, scorer frac "
+                f"{others[name]['scorer_valu_frac']}")
+            q.eng.close()
+            del q
+            torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu:
+        log("[bench] CPU oracle baseline")
+        cpu = cpu_baseline(args.workload, args.cpu_per_structure)
+        log(f"[bench]   oracle {cpu['value']:.1f} q/s on {cpu['cores']} threads ({cpu['seconds']} s)")
+
+    out = {
+        "metric": "queries/sec (score all entities + top-k) and achieved VALU/HBM roofline %",
+        "value": round(qps, 2),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded random tables and queries of the workload's shapes)",
+        "config": {"workload": WORKLOAD_DESC[args.workload], "name": args.workload,
+                   "queries_per_step": p.n_queries, "scored_rows_per_step": p.rows, "k": p.w.k},
+        "entity_scores_per_s": round(qps * p.w.n_entities, 1),
+        "roofline": roofline,
+        "stage_ms_per_step": stages,
+        "cpu_baseline": cpu,
+        "others": others,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

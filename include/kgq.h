@@ -170,8 +170,10 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
 kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* structure_ids,
                              int32_t* counts);
 
-/* Per-stage timing. While profiling is on, execute records a pair of HIP
- * events around every kernel it launches, on the caller's stream.
+/* Per-stage timing. kgq_profile_enable takes a bitmask of stages (bit i =
+ * stage i; 0 turns profiling off). While a stage's bit is set, execute
+ * records a pair of HIP events around every kernel of that stage it
+ * launches, on the caller's stream.
  * kgq_profile_read synchronises on those events and returns the summed
  * milliseconds and launch count of one stage since profiling was turned
  * on (or last reset), then keeps accumulating. Stages:

@@ -74,6 +74,20 @@ def check_no_packed_fp32(lib: str) -> None:
         raise RuntimeError("packed FP32 instructions in device code: " + ", ".join(bad))
 
 
+def build_microbench(verbose: bool = False) -> str:
+    """The VALU issue-rate microbenchmark (a standalone executable)."""
+    src = os.path.join(HERE, "microbench", "valu_peak.hip")
+    out = os.path.join(HERE, "microbench", "valu_peak")
+    cmd = [HIPCC] + [f for f in COMMON if f != "-fPIC"] + ["-fno-honor-nans", "-o", out + ".tmp", src]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed on valu_peak.hip:\n" + r.stdout + r.stderr)
+    os.replace(out + ".tmp", out)
+    return out
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(6, os.cpu_count() or 1)) as ex:
@@ -87,6 +101,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
     check_no_packed_fp32(tmp)
     os.replace(tmp, OUT)
+    build_microbench(verbose)
     return OUT
 
 

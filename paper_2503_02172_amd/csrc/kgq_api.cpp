@@ -82,7 +82,7 @@ struct kgq_handle {
     std::vector<void*> allocations;
 
     // profiling
-    bool prof = false;
+    int prof = 0;                 // bitmask of stages being timed
     std::vector<ProfPair> prof_pending;
     std::vector<hipEvent_t> prof_pool;
     double prof_ms[KGQ_NUM_STAGES]{};
@@ -270,7 +270,7 @@ struct StageTimer {
     hipEvent_t a = nullptr, b = nullptr;
     StageTimer(kgq_handle* h_, int st, hipStream_t s_) : h(h_), stage(st), s(s_)
     {
-        if (h->prof) {
+        if ((h->prof >> stage) & 1) {
             a = prof_event(h);
             b = prof_event(h);
             if (hipEventRecord(a, s) != hipSuccess) a = nullptr;
@@ -278,7 +278,7 @@ struct StageTimer {
     }
     ~StageTimer()
     {
-        if (h->prof && a && b && hipEventRecord(b, s) == hipSuccess) h->prof_pending.push_back({stage, a, b});
+        if (a && b && hipEventRecord(b, s) == hipSuccess) h->prof_pending.push_back({stage, a, b});
     }
 };
 
@@ -735,8 +735,9 @@ kgq_status kgq_profile_enable(kgq_handle* h, int32_t on)
 {
     if (!h) return KGQ_E_INVALID_ARG;
     if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    if (on < 0 || on >= (1 << KGQ_NUM_STAGES)) return fail(h, KGQ_E_INVALID_ARG, "stage mask out of range");
     if (!on && h->prof) prof_collect(h);
-    h->prof = on != 0;
+    h->prof = on;
     return KGQ_OK;
 }
 

@@ -54,6 +54,10 @@ def lib() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: run `python paper_2503_02172_amd/build.py` "
                           "(or __graft_entry__.build()) first")
+    # PyTorch ships its own HIP runtime with the same SONAME as ROCm's. Loading
+    # torch first makes libkgq bind to that one copy, so device pointers and
+    # streams from torch are native to the runtime libkgq calls.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     i32p, i64p, dp = ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)
@@ -217,16 +221,32 @@ class Engine:
     def dense(self, x, w, b=None, act: int = 0, out=None, stream=None):
         """y = act(x @ w.T + b) with the library's MFMA kernel (torch tensors)."""
         import torch
+        for name, t in (("x", x), ("w", w), ("b", b), ("out", out)):
+            if t is not None and (t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous()):
+                raise TypeError(f"dense: {name} must be a contiguous float32 CUDA tensor")
         M, K = x.shape
         N = w.shape[0]
+        if w.shape[1] != K or (b is not None and b.numel() != N):
+            raise ValueError("dense: shapes do not match")
         y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=x.device)
+        if y.shape != (M, N):
+            raise ValueError("dense: out has the wrong shape")
         self._check(lib().kgq_dense(self.h, _ptr(x), M, K, _ptr(w), _ptr(b), N, act, _ptr(y),
                                     _stream(stream)))
         return y
 
     # -- profiling ------------------------------------------------------------
-    def profile(self, on: bool):
-        self._check(lib().kgq_profile_enable(self.h, int(bool(on))))
+    def profile(self, stages=None):
+        """Time the given stages (names or ids; None = off, "all" = every stage)."""
+        if stages is None:
+            mask = 0
+        elif stages == "all":
+            mask = (1 << len(STAGES)) - 1
+        else:
+            mask = 0
+            for s_ in stages:
+                mask |= 1 << (STAGES.index(s_) if isinstance(s_, str) else int(s_))
+        self._check(lib().kgq_profile_enable(self.h, mask))
 
     def profile_reset(self):
         self._check(lib().kgq_profile_reset(self.h))
