@@ -65,6 +65,8 @@ struct kgq_handle {
     float* qpack = nullptr;
     double* cq = nullptr;
     float* scores = nullptr;
+    int32_t* cand_idx[2] = {nullptr, nullptr};   // top-k candidates of long rows
+    float* cand_score[2] = {nullptr, nullptr};
     int* dflag = nullptr;
     int* hflag = nullptr;         // pinned
 
@@ -235,6 +237,11 @@ kgq_status allocate_all(kgq_handle* h)
     ALLOC(h->qpack, prow * 2 * d);
     ALLOC(h->cq, prow);
     ALLOC(h->scores, Bm * N);
+    const int64_t ncand = topk_scratch_elems(Bm, N, kMaxK);
+    for (int i = 0; i < 2; ++i) {
+        ALLOC(h->cand_idx[i], ncand);
+        ALLOC(h->cand_score[i], ncand);
+    }
     ALLOC(h->dflag, 1);
     h->plan_words = plan_image_words((int)Bm);
     ALLOC(h->plan_dev, (int64_t)(kNumStructures + 2) * h->plan_words);
@@ -460,7 +467,19 @@ kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_
     }
     if (out_idx) {
         StageTimer t(h, 5, s);
-        launch_topk({dst, N, N, p.B, k, out_idx, out_score}, s);
+        TopkArgs ta{};
+        ta.scores = dst;
+        ta.ld = N;
+        ta.N = N;
+        ta.n_rows = p.B;
+        ta.k = k;
+        ta.out_idx = out_idx;
+        ta.out_score = out_score;
+        for (int i = 0; i < 2; ++i) {
+            ta.cand_idx[i] = h->cand_idx[i];
+            ta.cand_score[i] = h->cand_score[i];
+        }
+        launch_topk(ta, s);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(h, KGQ_E_DEVICE, std::string("kernel launch: ") + hipGetErrorString(e));

@@ -116,12 +116,23 @@ struct ScoreArgs {
 };
 void launch_score(const ScoreArgs& a, hipStream_t s);
 
+// Top-k works on segments of at most kTopkSegment scores per workgroup;
+// longer rows take extra rounds over per-segment candidates.
+constexpr int kTopkSegment = 16384;
+
 struct TopkArgs {
     const float* scores; int64_t ld; int64_t N;
     int n_rows;                        // rows 0 .. n_rows-1 of the score buffer
     int k;
-    int32_t* out_idx; float* out_score;
+    int32_t* out_idx; float* out_score;        // [n_rows x k]
+    int32_t* cand_idx[2]; float* cand_score[2]; // scratch for long rows (topk_scratch_elems each)
+    // set by launch_topk for each round
+    const int32_t* in_idx;             // index of each element (nullptr: its position)
+    int64_t seg_len;
+    int64_t out_ld;
+    int out_rows_per_row;
 };
 void launch_topk(const TopkArgs& a, hipStream_t s);
+int64_t topk_scratch_elems(int64_t n_rows, int64_t N, int k);
 
 }  // namespace kgq

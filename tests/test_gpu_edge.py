@@ -56,7 +56,8 @@ def test_gpu_exact_ties_order_by_index():
         eng.close()
 
 
-@pytest.mark.parametrize("N,k", [(37, 1), (37, 37), (1500, 1024), (1500, 1), (5000, 100)])
+@pytest.mark.parametrize("N,k", [(37, 1), (37, 37), (1500, 1024), (1500, 1), (5000, 100), (16384, 7),
+                                 (16385, 300), (40000, 1024), (40000, 100)])
 def test_gpu_k_limits(N, k):
     import torch
     w = synth.make_tiny(O.Q2B, n_ent=N, n_rel=5, dim=8, seed=50)
@@ -67,6 +68,34 @@ def test_gpu_k_limits(N, k):
     torch.cuda.synchronize()
     ora = m.scores(S["2u"], qb.anchors, qb.relations)
     check_topk(out["idx"].cpu().numpy(), out["score"].cpu().numpy(), ora, k, w.rtol, w.gamma, f"N={N} k={k}")
+    eng.close()
+
+
+def test_gpu_ties_across_topk_segments():
+    """Rows longer than one top-k segment are reduced in rounds; exact ties in
+    different segments must still come out lowest index first."""
+    import torch
+    w = synth.make_tiny(O.GQE, n_ent=40000, n_rel=3, dim=8, seed=90)
+    rel = w.params["relation"].copy()
+    rel[0] = 0.0
+    w.params["relation"] = rel
+    ent = w.params["entity"].copy()
+    dup = [5, 16383, 16384, 32768, 39999]
+    ent[dup] = ent[20000]
+    w.params["entity"] = ent
+    eng = _eng(w, max_batch=4)
+    a = np.full((2, 1), 20000, np.int32)
+    r = np.zeros((2, 1), np.int32)
+    for k, want in ((3, [5, 16383, 16384]), (6, [5, 16383, 16384, 20000, 32768, 39999]), (100, None)):
+        out = eng.execute(S["1p"], a, r, k=k)
+        torch.cuda.synchronize()
+        got = out["idx"].cpu().numpy()
+        if want is not None:
+            assert got[0].tolist() == want and got[1].tolist() == want
+        else:
+            assert got[0, :6].tolist() == sorted(dup + [20000])
+            m = O.Model(O.GQE, w.params, w.gamma)
+            check_topk(got, out["score"].cpu().numpy(), m.scores(S["1p"], a, r), k, w.rtol, w.gamma)
     eng.close()
 
 
