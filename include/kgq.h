@@ -26,6 +26,11 @@
  *    the caller's stream and the call returns. Outputs are valid after the
  *    caller synchronises that stream; inputs must stay alive until then.
  *    Calls on one handle must be issued from one host thread at a time.
+ *  - A handle owns cfg.concurrency sets of scratch space, used round-robin
+ *    by successive execute calls. Before a call reuses a set, its stream
+ *    waits on the device for the set's previous call to finish, so calls on
+ *    different streams may overlap (up to cfg.concurrency at once) and calls
+ *    on one stream stay in order. The host never blocks for this.
  *  - Host-checkable errors are reported before anything is enqueued.
  */
 #ifndef KGQ_H
@@ -84,6 +89,8 @@ typedef struct {
     float center_reg;     /* Query2Box weight of the inside distance (0.02 in the standard model); ignored otherwise */
     int32_t max_batch;    /* largest batch any execute call will pass; sizes the scratch space */
     int32_t device;       /* HIP device ordinal, or -1 for a validation-only handle with no GPU */
+    int32_t concurrency;  /* scratch sets (1 if 0): executes issued on different streams can run
+                             concurrently, up to this many at once */
 } kgq_config;
 
 /* Create a handle. Validates cfg, selects the device, and allocates all
@@ -184,6 +191,12 @@ kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* 
 kgq_status kgq_profile_enable(kgq_handle* h, int32_t on);
 kgq_status kgq_profile_read(kgq_handle* h, int32_t stage, double* total_ms, int64_t* launches);
 kgq_status kgq_profile_reset(kgq_handle* h);
+/* Start and end (milliseconds from a time origin recorded when profiling
+ * was first enabled on the handle) of every timed launch of a stage since
+ * the last reset: out receives min(cap, *n) (start, end) pairs; *n is the
+ * total count. Launches on different streams may overlap in time; the
+ * union of the intervals is the time the stage had work on the GPU. */
+kgq_status kgq_profile_intervals(kgq_handle* h, int32_t stage, double* out, int64_t cap, int64_t* n);
 
 /* One dense layer on the device with the library's FP32 matrix-core GEMM:
  * y[m][n] = act(sum_k x[m][k] * w[n][k] + b[n]) (the matmul + add (+ ReLU)

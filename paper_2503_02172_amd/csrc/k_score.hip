@@ -30,6 +30,8 @@
 //           C_q = sum_i lnB(alpha_q, beta_q)  (entity a, b; query alpha_q, beta_q).
 // Union (disjunctive normal form, Eq. 1 of the paper): a union query has two
 // adjacent rows; its score is the max of the two rows' scores.
+#include <type_traits>
+
 #include "kgq_internal.hpp"
 
 namespace kgq {
@@ -65,40 +67,77 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int total_w
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc2[i][j] = 0.f;
 
-#pragma unroll 2
-    for (int k = 0; k < d; ++k) {
-        const float* q = qp + k * F * TQ;
+    // Software pipeline, two steps per trip with named buffers A and B: a
+    // step's entity vector(s) are requested a step ahead, and its query
+    // scalars half a step ahead, after the previous wait (scalar loads may
+    // return out of order, so each wait on them covers every one
+    // outstanding). d is even (a multiple of 4).
+    constexpr int QN = F * TQ;
+    // The packed queries are read-only for the whole kernel; reading them
+    // through the constant address space keeps them on scalar loads.
+    const __attribute__((address_space(4))) float* qc = (const __attribute__((address_space(4))) float*)qp;
+    auto load_e = [&](int k, float4& u, float4& v) {
+        u = *reinterpret_cast<const float4*>(ep + (int64_t)k * EF * kEntBlock);
+        if (MODEL == 2) v = *reinterpret_cast<const float4*>(ep + (int64_t)k * 2 * kEntBlock + kEntBlock);
+    };
+    // rows [R0, R1) of one step
+    auto compute = [&](const float4& eu, const float4& ev, const float* qv, auto R0c, auto R1c) {
+        constexpr int R0 = decltype(R0c)::value, R1 = decltype(R1c)::value;
         if (MODEL == 2) {
-            const float4 u = *reinterpret_cast<const float4*>(ep + (int64_t)k * 2 * kEntBlock);
-            const float4 v = *reinterpret_cast<const float4*>(ep + (int64_t)k * 2 * kEntBlock + kEntBlock);
 #pragma unroll
-            for (int i = 0; i < TQ; ++i) {
-                const float al = q[i], be = q[TQ + i];
-                acc[i][0] = fmaf(be, v.x, fmaf(al, u.x, acc[i][0]));
-                acc[i][1] = fmaf(be, v.y, fmaf(al, u.y, acc[i][1]));
-                acc[i][2] = fmaf(be, v.z, fmaf(al, u.z, acc[i][2]));
-                acc[i][3] = fmaf(be, v.w, fmaf(al, u.w, acc[i][3]));
+            for (int i = R0; i < R1; ++i) {
+                const float al = qv[i], be = qv[TQ + i];
+                acc[i][0] = fmaf(be, ev.x, fmaf(al, eu.x, acc[i][0]));
+                acc[i][1] = fmaf(be, ev.y, fmaf(al, eu.y, acc[i][1]));
+                acc[i][2] = fmaf(be, ev.z, fmaf(al, eu.z, acc[i][2]));
+                acc[i][3] = fmaf(be, ev.w, fmaf(al, eu.w, acc[i][3]));
             }
         } else {
-            const float4 e = *reinterpret_cast<const float4*>(ep + (int64_t)k * kEntBlock);
-            const float ev[4] = {e.x, e.y, e.z, e.w};
+            const float e4[4] = {eu.x, eu.y, eu.z, eu.w};
 #pragma unroll
-            for (int i = 0; i < TQ; ++i) {
-                const float c = q[i];
+            for (int i = R0; i < R1; ++i) {
+                const float c = qv[i];
                 if (MODEL == 0) {
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[i][j] += fabsf(ev[j] - c);
+                    for (int j = 0; j < 4; ++j) acc[i][j] += fabsf(e4[j] - c);
                 } else {
-                    const float o = q[TQ + i];
+                    const float o = qv[TQ + i];
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const float t = fabsf(ev[j] - c);
+                        const float t = fabsf(e4[j] - c);
                         acc[i][j] += t;
                         acc2[i][j] += __builtin_fminf(t, o);
                     }
                 }
             }
         }
+    };
+    using H0 = std::integral_constant<int, 0>;
+    using H1 = std::integral_constant<int, TQ / 2>;
+    using H2 = std::integral_constant<int, TQ>;
+    float4 ua, va, ub, vb;
+    float qa[QN], qb2[QN];
+    load_e(0, ua, va);
+#pragma unroll
+    for (int t = 0; t < QN; ++t) qa[t] = qc[t];
+    for (int k = 0; k < d; k += 2) {
+        load_e(k + 1, ub, vb);                              // B <- step k + 1
+        __builtin_amdgcn_sched_barrier(0);
+        compute(ua, va, qa, H0{}, H1{});
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < QN; ++t) qb2[t] = qc[(k + 1) * QN + t];
+        __builtin_amdgcn_sched_barrier(0);
+        compute(ua, va, qa, H1{}, H2{});
+        const int k2 = (k + 2 < d) ? k + 2 : k + 1;         // A <- step k + 2 (last trip: in bounds, unused)
+        load_e(k2, ua, va);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(ub, vb, qb2, H0{}, H1{});
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < QN; ++t) qa[t] = qc[k2 * QN + t];
+        __builtin_amdgcn_sched_barrier(0);
+        compute(ub, vb, qb2, H1{}, H2{});
     }
 
     // Epilogue: finish the scores, merge union pairs, store.

@@ -32,6 +32,38 @@ struct ProfPair {
     hipEvent_t start, stop;
 };
 
+// Scratch of one execute in flight. A handle owns cfg.concurrency lanes;
+// consecutive executes use them round-robin, and an execute's stream first
+// waits (on the device) for the lane's previous use to finish.
+struct Lane {
+    float* states = nullptr;
+    float* xbuf = nullptr;        // BetaE MLP input / intersection input
+    float* h1 = nullptr;
+    float* h2 = nullptr;
+    float* logits = nullptr;
+    float* zfeat = nullptr;
+    float* zmean = nullptr;
+    float* gate = nullptr;
+    float* qpack = nullptr;
+    double* cq = nullptr;
+    float* scores = nullptr;
+    int32_t* cand_idx[2] = {nullptr, nullptr};   // top-k candidates of long rows
+    float* cand_score[2] = {nullptr, nullptr};
+    int* dflag = nullptr;
+    int* hflag = nullptr;         // pinned
+    // plan images: per-structure cache slots + a ring of two for mixed batches
+    int32_t* plan_dev = nullptr;  // (kNumStructures + 2) slots
+    int32_t* plan_host = nullptr; // pinned staging, same slot layout
+    hipEvent_t slot_event[kNumStructures + 2]{};
+    bool slot_event_live[kNumStructures + 2]{};
+    int cached_B[kNumStructures];
+    std::unique_ptr<Plan> cached_plan[kNumStructures];
+    int ring_next = 0;
+    hipEvent_t done = nullptr;    // recorded after the lane's last execute
+    bool done_live = false;
+    Lane() { for (int i = 0; i < kNumStructures; ++i) cached_B[i] = -1; }
+};
+
 thread_local std::string g_create_error;
 
 }  // namespace
@@ -53,33 +85,11 @@ struct kgq_handle {
     double* ent_const = nullptr;  // BetaE E_e [n_pad]
     float* rel_o_sp = nullptr;    // Q2B softplus(offset_raw) [R x d]
 
-    // scratch (sized for max_batch at create)
-    float* states = nullptr;
-    float* xbuf = nullptr;        // BetaE MLP input / intersection input
-    float* h1 = nullptr;
-    float* h2 = nullptr;
-    float* logits = nullptr;
-    float* zfeat = nullptr;
-    float* zmean = nullptr;
-    float* gate = nullptr;
-    float* qpack = nullptr;
-    double* cq = nullptr;
-    float* scores = nullptr;
-    int32_t* cand_idx[2] = {nullptr, nullptr};   // top-k candidates of long rows
-    float* cand_score[2] = {nullptr, nullptr};
-    int* dflag = nullptr;
-    int* hflag = nullptr;         // pinned
-
-    // plan images: per-structure cache slots + a ring for mixed batches
+    // scratch lanes (each sized for max_batch at create): executes on
+    // different lanes may run concurrently on different streams
+    std::vector<std::unique_ptr<Lane>> lanes;
+    int next_lane = 0;
     int64_t plan_words = 0;
-    int32_t* plan_dev = nullptr;  // (kNumStructures + 2) slots
-    int32_t* plan_host = nullptr; // pinned staging, same slot layout
-    hipEvent_t slot_event[kNumStructures + 2]{};
-    bool slot_event_live[kNumStructures + 2]{};
-    int cached_B[kNumStructures];
-    std::unique_ptr<Plan> cached_plan[kNumStructures];
-    int ring_next = 0;
-    Plan mixed_plan;
 
     std::vector<void*> allocations;
 
@@ -89,6 +99,8 @@ struct kgq_handle {
     std::vector<hipEvent_t> prof_pool;
     double prof_ms[KGQ_NUM_STAGES]{};
     int64_t prof_n[KGQ_NUM_STAGES]{};
+    hipEvent_t prof_ref = nullptr;                     // time origin of the intervals
+    std::vector<double> prof_iv[KGQ_NUM_STAGES];       // (start, end) ms pairs
 };
 
 namespace {
@@ -180,15 +192,20 @@ void free_all(kgq_handle* h)
     (void)hipDeviceSynchronize();
     for (void* p : h->allocations) (void)hipFree(p);
     h->allocations.clear();
-    if (h->hflag) (void)hipHostFree(h->hflag);
-    if (h->plan_host) (void)hipHostFree(h->plan_host);
-    for (int i = 0; i < kNumStructures + 2; ++i)
-        if (h->slot_event[i]) (void)hipEventDestroy(h->slot_event[i]);
+    for (auto& L : h->lanes) {
+        if (L->hflag) (void)hipHostFree(L->hflag);
+        if (L->plan_host) (void)hipHostFree(L->plan_host);
+        for (int i = 0; i < kNumStructures + 2; ++i)
+            if (L->slot_event[i]) (void)hipEventDestroy(L->slot_event[i]);
+        if (L->done) (void)hipEventDestroy(L->done);
+    }
+    h->lanes.clear();
     for (auto& pp : h->prof_pending) {
         (void)hipEventDestroy(pp.start);
         (void)hipEventDestroy(pp.stop);
     }
     for (hipEvent_t e : h->prof_pool) (void)hipEventDestroy(e);
+    if (h->prof_ref) (void)hipEventDestroy(h->prof_ref);
 }
 
 kgq_status allocate_all(kgq_handle* h)
@@ -216,43 +233,50 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(h->ent_blk, n_pad * d);
         if (c.model == KGQ_Q2B) ALLOC(h->rel_o_sp, (int64_t)c.n_relations * d);
     }
-    const int64_t rows = Bm * kStateRowsPerQuery;
-    ALLOC(h->states, rows * W);
-    const int64_t m_max = 3 * Bm;   // rows of one MLP level / intersection inputs
-    if (c.model == KGQ_BETAE) {
-        ALLOC(h->xbuf, m_max * 2 * d);
-        ALLOC(h->h1, m_max * 4 * d);
-        ALLOC(h->h2, m_max * 4 * d);
-    } else {
-        ALLOC(h->h1, m_max * d);
-        if (c.model == KGQ_Q2B) {
-            ALLOC(h->zfeat, m_max * d);
-            ALLOC(h->zmean, Bm * d);
-            ALLOC(h->gate, Bm * d);
-        }
-    }
-    ALLOC(h->logits, m_max * d);
-    const int tq = score_tq(c.model);
-    const int64_t prow = ((2 * Bm + tq - 1) / tq) * tq;
-    ALLOC(h->qpack, prow * 2 * d);
-    ALLOC(h->cq, prow);
-    ALLOC(h->scores, Bm * N);
-    const int64_t ncand = topk_scratch_elems(Bm, N, kMaxK);
-    for (int i = 0; i < 2; ++i) {
-        ALLOC(h->cand_idx[i], ncand);
-        ALLOC(h->cand_score[i], ncand);
-    }
-    ALLOC(h->dflag, 1);
     h->plan_words = plan_image_words((int)Bm);
-    ALLOC(h->plan_dev, (int64_t)(kNumStructures + 2) * h->plan_words);
+    const int n_lanes = c.concurrency > 0 ? c.concurrency : 1;
+    for (int li = 0; li < n_lanes; ++li) {
+        h->lanes.emplace_back(new Lane());
+        Lane& L = *h->lanes.back();
+        const int64_t rows = Bm * kStateRowsPerQuery;
+        ALLOC(L.states, rows * W);
+        const int64_t m_max = 3 * Bm;   // rows of one MLP level / intersection inputs
+        if (c.model == KGQ_BETAE) {
+            ALLOC(L.xbuf, m_max * 2 * d);
+            ALLOC(L.h1, m_max * 4 * d);
+            ALLOC(L.h2, m_max * 4 * d);
+        } else {
+            ALLOC(L.h1, m_max * d);
+            if (c.model == KGQ_Q2B) {
+                ALLOC(L.zfeat, m_max * d);
+                ALLOC(L.zmean, Bm * d);
+                ALLOC(L.gate, Bm * d);
+            }
+        }
+        ALLOC(L.logits, m_max * d);
+        const int tq = score_tq(c.model);
+        const int64_t prow = ((2 * Bm + tq - 1) / tq) * tq;
+        ALLOC(L.qpack, prow * 2 * d);
+        ALLOC(L.cq, prow);
+        ALLOC(L.scores, Bm * N);
+        const int64_t ncand = topk_scratch_elems(Bm, N, kMaxK);
+        for (int i = 0; i < 2; ++i) {
+            ALLOC(L.cand_idx[i], ncand);
+            ALLOC(L.cand_score[i], ncand);
+        }
+        ALLOC(L.dflag, 1);
+        ALLOC(L.plan_dev, (int64_t)(kNumStructures + 2) * h->plan_words);
+        hipError_t e = hipHostMalloc((void**)&L.hflag, sizeof(int), hipHostMallocDefault);
+        if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(flag)");
+        e = hipHostMalloc((void**)&L.plan_host, sizeof(int32_t) * (kNumStructures + 2) * h->plan_words,
+                          hipHostMallocDefault);
+        if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(plan staging)");
+        for (int i = 0; i < kNumStructures + 2; ++i)
+            HIP_TRY(h, hipEventCreateWithFlags(&L.slot_event[i], hipEventDisableTiming));
+        HIP_TRY(h, hipEventCreateWithFlags(&L.done, hipEventDisableTiming));
+        HIP_TRY(h, hipMemset(L.dflag, 0, sizeof(int)));
+    }
 #undef ALLOC
-    hipError_t e = hipHostMalloc((void**)&h->hflag, sizeof(int), hipHostMallocDefault);
-    if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(flag)");
-    e = hipHostMalloc((void**)&h->plan_host, sizeof(int32_t) * (kNumStructures + 2) * h->plan_words,
-                      hipHostMallocDefault);
-    if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(plan staging)");
-    for (int i = 0; i < kNumStructures + 2; ++i) HIP_TRY(h, hipEventCreateWithFlags(&h->slot_event[i], hipEventDisableTiming));
-    HIP_TRY(h, hipMemset(h->dflag, 0, sizeof(int)));
     return KGQ_OK;
 }
 
@@ -292,10 +316,15 @@ struct StageTimer {
 void prof_collect(kgq_handle* h)
 {
     for (auto& pp : h->prof_pending) {
-        float ms = 0.f;
+        float ms = 0.f, t0 = 0.f, t1 = 0.f;
         if (hipEventSynchronize(pp.stop) == hipSuccess && hipEventElapsedTime(&ms, pp.start, pp.stop) == hipSuccess) {
             h->prof_ms[pp.stage] += ms;
             h->prof_n[pp.stage] += 1;
+            if (h->prof_ref && hipEventElapsedTime(&t0, h->prof_ref, pp.start) == hipSuccess &&
+                hipEventElapsedTime(&t1, h->prof_ref, pp.stop) == hipSuccess) {
+                h->prof_iv[pp.stage].push_back(t0);
+                h->prof_iv[pp.stage].push_back(t1);
+            }
         }
         h->prof_pool.push_back(pp.start);
         h->prof_pool.push_back(pp.stop);
@@ -336,18 +365,29 @@ kgq_status check_outputs(kgq_handle* h, int32_t batch, const void* anchors, cons
 }
 
 // Upload a plan image into device slot `slot` (after the slot's last use).
-kgq_status upload_plan(kgq_handle* h, const Plan& p, int slot, hipStream_t s)
+kgq_status upload_plan(kgq_handle* h, Lane& L, const Plan& p, int slot, hipStream_t s)
 {
     if ((int64_t)p.image.size() > h->plan_words) return fail(h, KGQ_E_DEVICE, "plan image exceeds its slot");
-    if (h->slot_event_live[slot]) HIP_TRY(h, hipEventSynchronize(h->slot_event[slot]));
-    int32_t* host = h->plan_host + (int64_t)slot * h->plan_words;
+    if (L.slot_event_live[slot]) HIP_TRY(h, hipEventSynchronize(L.slot_event[slot]));
+    int32_t* host = L.plan_host + (int64_t)slot * h->plan_words;
     std::memcpy(host, p.image.data(), p.image.size() * sizeof(int32_t));
-    HIP_TRY(h, hipMemcpyAsync(h->plan_dev + (int64_t)slot * h->plan_words, host,
+    HIP_TRY(h, hipMemcpyAsync(L.plan_dev + (int64_t)slot * h->plan_words, host,
                               p.image.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
     return KGQ_OK;
 }
 
-kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_t* anchors,
+// Next scratch lane, round-robin. The caller's stream waits (on the device)
+// until the lane's previous execute, possibly on another stream, is done.
+kgq_status acquire_lane(kgq_handle* h, hipStream_t s, Lane** out)
+{
+    Lane* L = h->lanes[h->next_lane].get();
+    h->next_lane = (h->next_lane + 1) % (int)h->lanes.size();
+    if (L->done_live) HIP_TRY(h, hipStreamWaitEvent(s, L->done, 0));
+    *out = L;
+    return KGQ_OK;
+}
+
+kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, const int32_t* anchors,
                     const int32_t* rels, int sa, int sr, int fixed_na, int fixed_nr, bool mixed, int32_t k,
                     float* out_scores, int32_t* out_idx, float* out_score, hipStream_t s)
 {
@@ -359,9 +399,9 @@ kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_
     auto param = [&](const char* n) { return h->dparam.at(n); };
 
     if (h->checked) {
-        launch_clear_flag(h->dflag, s);
+        launch_clear_flag(L.dflag, s);
         launch_validate(anchors, rels, mixed ? P + p.off.arity : nullptr, p.B, sa, sr, fixed_na, fixed_nr,
-                        N, n_rel, h->dflag, s);
+                        N, n_rel, L.dflag, s);
     }
     GroupArgs g{P + p.off.g_in_start, P + p.off.g_n, P + p.off.g_out, P + p.off.g_post, P + p.off.g_neg,
                 p.n_groups};
@@ -372,38 +412,38 @@ kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_
         {
             StageTimer t(h, 0, s);
             launch_chain(c.model, P + p.off.chain_anchor, P + p.off.chain_rel, p.n_chain, anchors, rels,
-                         h->ent_rm, rel_c, h->rel_o_sp, N, n_rel, d, h->states, h->dflag, s);
+                         h->ent_rm, rel_c, h->rel_o_sp, N, n_rel, d, L.states, L.dflag, s);
         }
         if (p.n_groups) {
             const std::string pre = q2b ? "inter.center." : "inter.";
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({h->states, W, param((pre + "w1").c_str()), d, param((pre + "b1").c_str()), h->h1, d,
+                launch_gemm({L.states, W, param((pre + "w1").c_str()), d, param((pre + "b1").c_str()), L.h1, d,
                              nullptr, p.n_int_in, d, d, EPI_RELU}, s);
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({h->h1, d, param((pre + "w2").c_str()), d, param((pre + "b2").c_str()), h->logits, d,
+                launch_gemm({L.h1, d, param((pre + "w2").c_str()), d, param((pre + "b2").c_str()), L.logits, d,
                              nullptr, p.n_int_in, d, d, EPI_NONE}, s);
             }
             if (q2b) {
                 StageTimer t(h, 1, s);
-                launch_gemm({h->states + d, W, param("inter.offset.w1"), d, param("inter.offset.b1"), h->zfeat, d,
+                launch_gemm({L.states + d, W, param("inter.offset.w1"), d, param("inter.offset.b1"), L.zfeat, d,
                              nullptr, p.n_int_in, d, d, EPI_RELU}, s);
             }
             {
                 StageTimer t(h, 2, s);
-                launch_combine_center(c.model, g, h->states, W, h->logits, h->zfeat, h->zmean, rels, rel_c, n_rel,
-                                      d, h->states, h->dflag, s);
+                launch_combine_center(c.model, g, L.states, W, L.logits, L.zfeat, L.zmean, rels, rel_c, n_rel,
+                                      d, L.states, L.dflag, s);
             }
             if (q2b) {
                 {
                     StageTimer t(h, 1, s);
-                    launch_gemm({h->zmean, d, param("inter.offset.w2"), d, param("inter.offset.b2"), h->gate, d,
+                    launch_gemm({L.zmean, d, param("inter.offset.w2"), d, param("inter.offset.b2"), L.gate, d,
                                  nullptr, p.n_groups, d, d, EPI_NONE}, s);
                 }
                 StageTimer t(h, 2, s);
-                launch_combine_offset(g, h->states, W, h->gate, rels, h->rel_o_sp, n_rel, d, h->states, h->dflag, s);
+                launch_combine_offset(g, L.states, W, L.gate, rels, h->rel_o_sp, n_rel, d, L.states, L.dflag, s);
             }
         }
     } else {
@@ -414,40 +454,40 @@ kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_
             {
                 StageTimer t(h, 0, s);
                 launch_betae_proj_prep(P + p.off.lv_src[l], P + p.off.lv_anchor[l], P + p.off.lv_rel[l], M, anchors,
-                                       rels, h->states, h->ent_rm, rel, N, n_rel, d, h->xbuf, h->dflag, s);
+                                       rels, L.states, h->ent_rm, rel, N, n_rel, d, L.xbuf, L.dflag, s);
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({h->xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), h->h1, 4 * d, nullptr, M,
+                launch_gemm({L.xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), L.h1, 4 * d, nullptr, M,
                              4 * d, 2 * d, EPI_RELU}, s);
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({h->h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), h->h2, 4 * d, nullptr, M,
+                launch_gemm({L.h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), L.h2, 4 * d, nullptr, M,
                              4 * d, 4 * d, EPI_RELU}, s);
             }
             StageTimer t(h, 1, s);
-            launch_gemm({h->h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), h->states, 2 * d,
+            launch_gemm({L.h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), L.states, 2 * d,
                          P + p.off.lv_dst[l], M, 2 * d, 4 * d, EPI_BETA_REG}, s);
         };
         for (int l = 0; l < 3; ++l) mlp_level(l);
         if (p.n_groups) {
             {
                 StageTimer t(h, 2, s);
-                launch_betae_int_prep(g, h->states, d, h->xbuf, s);
+                launch_betae_int_prep(g, L.states, d, L.xbuf, s);
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({h->xbuf, 2 * d, param("inter.w1"), 2 * d, param("inter.b1"), h->h1, 2 * d, nullptr,
+                launch_gemm({L.xbuf, 2 * d, param("inter.w1"), 2 * d, param("inter.b1"), L.h1, 2 * d, nullptr,
                              p.n_int_in, 2 * d, 2 * d, EPI_RELU}, s);
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({h->h1, 2 * d, param("inter.w2"), 2 * d, param("inter.b2"), h->logits, d, nullptr,
+                launch_gemm({L.h1, 2 * d, param("inter.w2"), 2 * d, param("inter.b2"), L.logits, d, nullptr,
                              p.n_int_in, d, 2 * d, EPI_NONE}, s);
             }
             StageTimer t(h, 2, s);
-            launch_betae_combine(g, h->xbuf, h->logits, d, h->states, s);
+            launch_betae_combine(g, L.xbuf, L.logits, d, L.states, s);
         }
         mlp_level(3);
     }
@@ -456,12 +496,12 @@ kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_
     const int n_rows_pad = ((p.n_score_rows + tq - 1) / tq) * tq;
     {
         StageTimer t(h, 3, s);
-        launch_pack(c.model, P + p.off.score_src, p.n_score_rows, n_rows_pad, h->states, W, d, h->qpack, h->cq, s);
+        launch_pack(c.model, P + p.off.score_src, p.n_score_rows, n_rows_pad, L.states, W, d, L.qpack, L.cq, s);
     }
-    float* dst = out_scores ? out_scores : h->scores;
+    float* dst = out_scores ? out_scores : L.scores;
     {
         StageTimer t(h, 4, s);
-        ScoreArgs a{c.model, h->qpack, h->ent_blk, h->cq, h->ent_const, P + p.off.out_dest, p.n_score_rows,
+        ScoreArgs a{c.model, L.qpack, h->ent_blk, L.cq, h->ent_const, P + p.off.out_dest, p.n_score_rows,
                     p.n_union_rows, d, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
         launch_score(a, s);
     }
@@ -476,19 +516,19 @@ kgq_status run_plan(kgq_handle* h, const Plan& p, const int32_t* P, const int32_
         ta.out_idx = out_idx;
         ta.out_score = out_score;
         for (int i = 0; i < 2; ++i) {
-            ta.cand_idx[i] = h->cand_idx[i];
-            ta.cand_score[i] = h->cand_score[i];
+            ta.cand_idx[i] = L.cand_idx[i];
+            ta.cand_score[i] = L.cand_score[i];
         }
         launch_topk(ta, s);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(h, KGQ_E_DEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
     if (h->checked) {
-        HIP_TRY(h, hipMemcpyAsync(h->hflag, h->dflag, sizeof(int), hipMemcpyDeviceToHost, s));
+        HIP_TRY(h, hipMemcpyAsync(L.hflag, L.dflag, sizeof(int), hipMemcpyDeviceToHost, s));
         HIP_TRY(h, hipStreamSynchronize(s));
-        if (*h->hflag & kErrPadding)
+        if (*L.hflag & kErrPadding)
             return fail(h, KGQ_E_INVALID_ARG, "a mixed-batch unused anchor/relation slot is not -1");
-        if (*h->hflag & kErrRange) return fail(h, KGQ_E_OUT_OF_RANGE, "an anchor or relation id is out of range");
+        if (*L.hflag & kErrRange) return fail(h, KGQ_E_OUT_OF_RANGE, "an anchor or relation id is out of range");
     }
     return KGQ_OK;
 }
@@ -548,13 +588,13 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out)
     if (!(c.gamma == c.gamma)) return bad("gamma is NaN");
     if (c.model == KGQ_Q2B && !(c.center_reg >= 0.f && c.center_reg <= 1.f)) return bad("center_reg outside [0, 1]");
     if (c.device < -1) return bad("device must be >= -1");
+    if (c.concurrency < 0 || c.concurrency > 64) return bad("concurrency outside [0, 64]");
 
     std::unique_ptr<kgq_handle> h(new kgq_handle());
     h->cfg = c;
     h->dry = c.device < 0;
     const char* env = std::getenv("KGQ_CHECKED");
     h->checked = env && env[0] == '1';
-    for (int i = 0; i < kNumStructures; ++i) h->cached_B[i] = -1;
     build_specs(h.get());
     if (h->dry) {
         *out = h.release();
@@ -665,22 +705,26 @@ kgq_status kgq_execute(kgq_handle* h, int32_t structure_id, int32_t batch, const
     if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
     HIP_TRY(h, hipSetDevice(h->cfg.device));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    Lane* L = nullptr;
+    st = acquire_lane(h, s, &L);
+    if (st != KGQ_OK) return st;
     const int slot = structure_id;
-    if (h->cached_B[slot] != batch || !h->cached_plan[slot]) {
+    if (L->cached_B[slot] != batch || !L->cached_plan[slot]) {
         std::unique_ptr<Plan> p(new Plan());
         std::string err;
         int es = 0;
         if (!lower(h->cfg.model, batch, nullptr, structure_id, sd->n_anchors, sd->n_relations, false, *p, err, es))
             return fail(h, (kgq_status)es, err);
-        st = upload_plan(h, *p, slot, s);
+        st = upload_plan(h, *L, *p, slot, s);
         if (st != KGQ_OK) return st;
-        h->cached_plan[slot] = std::move(p);
-        h->cached_B[slot] = batch;
+        L->cached_plan[slot] = std::move(p);
+        L->cached_B[slot] = batch;
     }
-    const int32_t* P = h->plan_dev + (int64_t)slot * h->plan_words;
-    st = run_plan(h, *h->cached_plan[slot], P, anchors, relations, sd->n_anchors, sd->n_relations, sd->n_anchors,
-                  sd->n_relations, false, k, out_scores, out_topk_idx, out_topk_score, s);
-    h->slot_event_live[slot] = hipEventRecord(h->slot_event[slot], s) == hipSuccess;
+    const int32_t* P = L->plan_dev + (int64_t)slot * h->plan_words;
+    st = run_plan(h, *L, *L->cached_plan[slot], P, anchors, relations, sd->n_anchors, sd->n_relations,
+                  sd->n_anchors, sd->n_relations, false, k, out_scores, out_topk_idx, out_topk_score, s);
+    L->slot_event_live[slot] = hipEventRecord(L->slot_event[slot], s) == hipSuccess;
+    L->done_live = hipEventRecord(L->done, s) == hipSuccess;
     return st;
 }
 
@@ -694,19 +738,24 @@ kgq_status kgq_execute_mixed(kgq_handle* h, int32_t batch, const int32_t* struct
     if (st != KGQ_OK) return st;
     std::string err;
     int es = 0;
-    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, h->mixed_plan, err, es))
+    Plan plan;
+    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, plan, err, es))
         return fail(h, (kgq_status)es, err);
     if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
     HIP_TRY(h, hipSetDevice(h->cfg.device));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const int slot = kNumStructures + h->ring_next;
-    h->ring_next ^= 1;
-    st = upload_plan(h, h->mixed_plan, slot, s);
+    Lane* L = nullptr;
+    st = acquire_lane(h, s, &L);
     if (st != KGQ_OK) return st;
-    const int32_t* P = h->plan_dev + (int64_t)slot * h->plan_words;
-    st = run_plan(h, h->mixed_plan, P, anchors, relations, 3, 3, 0, 0, true, k, out_scores, out_topk_idx,
+    const int slot = kNumStructures + L->ring_next;
+    L->ring_next ^= 1;
+    st = upload_plan(h, *L, plan, slot, s);
+    if (st != KGQ_OK) return st;
+    const int32_t* P = L->plan_dev + (int64_t)slot * h->plan_words;
+    st = run_plan(h, *L, plan, P, anchors, relations, 3, 3, 0, 0, true, k, out_scores, out_topk_idx,
                   out_topk_score, s);
-    h->slot_event_live[slot] = hipEventRecord(h->slot_event[slot], s) == hipSuccess;
+    L->slot_event_live[slot] = hipEventRecord(L->slot_event[slot], s) == hipSuccess;
+    L->done_live = hipEventRecord(L->done, s) == hipSuccess;
     return st;
 }
 
@@ -754,6 +803,11 @@ kgq_status kgq_profile_enable(kgq_handle* h, int32_t on)
 {
     if (!h) return KGQ_E_INVALID_ARG;
     if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    if (on && !h->prof_ref) {
+        // time origin for kgq_profile_intervals, on the null stream
+        HIP_TRY(h, hipEventCreate(&h->prof_ref));
+        HIP_TRY(h, hipEventRecord(h->prof_ref, nullptr));
+    }
     if (on < 0 || on >= (1 << KGQ_NUM_STAGES)) return fail(h, KGQ_E_INVALID_ARG, "stage mask out of range");
     if (!on && h->prof) prof_collect(h);
     h->prof = on;
@@ -778,7 +832,20 @@ kgq_status kgq_profile_reset(kgq_handle* h)
     for (int i = 0; i < KGQ_NUM_STAGES; ++i) {
         h->prof_ms[i] = 0.0;
         h->prof_n[i] = 0;
+        h->prof_iv[i].clear();
     }
+    return KGQ_OK;
+}
+
+kgq_status kgq_profile_intervals(kgq_handle* h, int32_t stage, double* out, int64_t cap, int64_t* n)
+{
+    if (!h || stage < 0 || stage >= KGQ_NUM_STAGES || !n || (cap > 0 && !out)) return KGQ_E_INVALID_ARG;
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    prof_collect(h);
+    const std::vector<double>& v = h->prof_iv[stage];
+    *n = (int64_t)v.size() / 2;
+    const int64_t m = *n < cap ? *n : cap;
+    for (int64_t i = 0; i < 2 * m; ++i) out[i] = v[(size_t)i];
     return KGQ_OK;
 }
 

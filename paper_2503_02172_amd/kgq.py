@@ -40,7 +40,8 @@ class KgqError(RuntimeError):
 class Config(ctypes.Structure):
     _fields_ = [("model", ctypes.c_int32), ("dim", ctypes.c_int32), ("n_entities", ctypes.c_int64),
                 ("n_relations", ctypes.c_int32), ("entity_dtype", ctypes.c_int32), ("gamma", ctypes.c_float),
-                ("center_reg", ctypes.c_float), ("max_batch", ctypes.c_int32), ("device", ctypes.c_int32)]
+                ("center_reg", ctypes.c_float), ("max_batch", ctypes.c_int32), ("device", ctypes.c_int32),
+                ("concurrency", ctypes.c_int32)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -73,6 +74,7 @@ def lib() -> ctypes.CDLL:
         "kgq_profile_enable": ([vp, i32], i32),
         "kgq_profile_read": ([vp, i32, dp, i64p], i32),
         "kgq_profile_reset": ([vp], i32),
+        "kgq_profile_intervals": ([vp, i32, dp, i64, i64p], i32),
         "kgq_destroy": ([vp], i32),
         "kgq_status_string": ([i32], ctypes.c_char_p),
         "kgq_last_error": ([vp], ctypes.c_char_p),
@@ -116,9 +118,10 @@ class Engine:
     """One kgq handle: a model's parameters on one GPU plus scratch space."""
 
     def __init__(self, model: int, n_entities: int, n_relations: int, dim: int, gamma: float,
-                 max_batch: int, center_reg: float = 0.02, entity_dtype: int = F32, device: int = 0):
+                 max_batch: int, center_reg: float = 0.02, entity_dtype: int = F32, device: int = 0,
+                 concurrency: int = 1):
         self.cfg = Config(model, dim, n_entities, n_relations, entity_dtype, gamma, center_reg,
-                          max_batch, device)
+                          max_batch, device, concurrency)
         h = ctypes.c_void_p()
         rc = lib().kgq_create(ctypes.byref(self.cfg), ctypes.byref(h))
         if rc != OK:
@@ -251,6 +254,16 @@ class Engine:
     def profile_reset(self):
         self._check(lib().kgq_profile_reset(self.h))
 
+    def profile_intervals(self, stage: str) -> np.ndarray:
+        """[n x 2] start/end (ms) of every timed launch of a stage since the last reset."""
+        i = STAGES.index(stage)
+        n = ctypes.c_int64()
+        self._check(lib().kgq_profile_intervals(self.h, i, None, 0, ctypes.byref(n)))
+        out = np.zeros(2 * max(n.value, 1), np.float64)
+        self._check(lib().kgq_profile_intervals(self.h, i, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                                n.value, ctypes.byref(n)))
+        return out[: 2 * n.value].reshape(n.value, 2)
+
     def profile_read(self) -> Dict[str, tuple]:
         out = {}
         for i, name in enumerate(STAGES):
@@ -261,13 +274,13 @@ class Engine:
 
 
 def engine_for(workload, max_batch: Optional[int] = None, device: int = 0, model: Optional[int] = None,
-               params: Optional[Dict[str, np.ndarray]] = None) -> Engine:
+               params: Optional[Dict[str, np.ndarray]] = None, concurrency: int = 1) -> Engine:
     """Create an Engine for a synthetic workload and load its parameters."""
     m = workload.model if model is None else model
     p = workload.params if params is None else params
     bmax = max_batch or max(b.batch for b in workload.batches)
     bf16 = workload.entity_bf16 if (m == BETAE and workload.entity_bf16 is not None) else None
     eng = Engine(m, workload.n_entities, workload.n_relations, workload.dim, workload.gamma, bmax,
-                 workload.center_reg, BF16 if bf16 is not None else F32, device)
+                 workload.center_reg, BF16 if bf16 is not None else F32, device, concurrency)
     eng.load_all(p, entity_bf16=bf16)
     return eng

@@ -183,3 +183,29 @@ def test_gpu_dense_matches_fp64(M, N, K, act):
     # fp32 accumulation of K products of magnitude <= 1/sqrt(K)
     np.testing.assert_allclose(y.cpu().numpy(), ref, rtol=1e-5, atol=1e-5 * np.sqrt(K) / 10 + 1e-6)
     eng.close()
+
+
+def test_gpu_concurrent_streams_match_sequential():
+    """Executes on different streams use separate scratch sets and may overlap;
+    their results equal those of the same calls on one stream."""
+    import torch
+    from paper_2503_02172_amd import kgq
+    w = synth.make_tiny(O.Q2B, n_ent=5000, n_rel=11, dim=16, seed=95)
+    seq = kgq.engine_for(w, max_batch=64, concurrency=1)
+    con = kgq.engine_for(w, max_batch=64, concurrency=2)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    qs = [synth.draw_queries(n, 40 + i, 5000, 11, seed=96 + i) for i, n in enumerate(["2i", "up", "3p", "pi"])]
+    ref = []
+    for qb in qs:
+        ref.append(seq.execute(S[qb.structure], qb.anchors, qb.relations, k=25, scores=True))
+    torch.cuda.synchronize()
+    outs = []
+    for i, qb in enumerate(qs):
+        with torch.cuda.stream(streams[i % 2]):
+            outs.append(con.execute(S[qb.structure], qb.anchors, qb.relations, k=25, scores=True))
+    torch.cuda.synchronize()
+    for r, o in zip(ref, outs):
+        for key in ("scores", "idx", "score"):
+            assert torch.equal(r[key], o[key]), key
+    seq.close()
+    con.close()
