@@ -2,20 +2,21 @@
 
 One step = one pass of the whole hot path over one batch of the headline
 workload: Query2Box at 14,505 entities x 474 relations, d = 400, 512 queries
-for each of the 9 structures without negation (4,608 queries, nine
-single-structure execute calls), every query scored against all entities,
-top-100. Inputs are resident in HBM before the timed region starts. The nine
-calls are independent, so they are spread round-robin over two streams (the
-handle has one scratch set per stream) and overlap on the GPU.
+for each of the 9 structures without negation (4,608 queries), every query
+scored against all entities, top-100. Inputs are resident in HBM before the
+timed region starts. By default the nine per-structure batches go to the
+library together as one mixed-structure execute call (the plan lowering
+groups the operators of all structures, and one scorer launch covers every
+query row); --per-structure issues one execute call per structure instead,
+spread round-robin over --streams streams.
 
 Prints one JSON line. `value` is queries/s over the timed steps.
-`roofline` describes the dominant kernel (the entity scorer): its
-algorithmic VALU operations over the timed region divided by the time a
-scorer launch was in flight (the union of the launch intervals, measured
-with HIP events around each launch on its stream), against the FP32 VALU
-lane-operation peak of the chip. `cpu_baseline` times the CPU
+`roofline` describes the dominant kernel (the entity scorer): the
+algorithmic VALU operations of one launch divided by the launch's average
+duration (HIP events around each launch on the stream it runs on), against
+the FP32 VALU lane-operation peak of the chip. `cpu_baseline` times the CPU
 oracle on a bounded sample of the same workload. `others` reports the other
-four workloads (throughput only).
+four workloads (throughput and scorer fraction).
 """
 
 from __future__ import annotations
@@ -46,7 +47,7 @@ K_TOP = 100
 WORKLOAD_DESC = {
     "C1": "GQE, 1,000 entities x 20 relations, d=32, fp32; 16 x 1p + 16 x 2i; top-10",
     "C2": "Query2Box, 14,505 entities x 474 relations, d=400, fp32; 512 queries per structure over "
-          "1p,2p,3p,2i,3i,pi,ip,2u,up (4,608 queries, 9 execute calls); top-100",
+          "1p,2p,3p,2i,3i,pi,ip,2u,up (4,608 queries); top-100",
     "C3": "BetaE, 14,505 entities x 474 relations, d=400, fp32; 512 queries per structure over "
           "1p,2in,3in,inp,pin,pni; top-100",
     "C4-q2b": "Query2Box, 63,361 entities x 400 relations, d=400, fp32; 1,024 mixed 3p/ip/pi/up/3i; top-100",
@@ -61,9 +62,14 @@ def log(*a):
 
 
 class Prepared:
-    """A workload on the device: engine, resident inputs and outputs."""
+    """A workload on the device: engine, resident inputs and outputs.
 
-    def __init__(self, name: str, n_streams: int = 1):
+    merge: execute all of the workload's batches as one mixed-structure call
+    (anchors/relations padded to 3 columns with -1, queries kept in batch
+    order); otherwise one call per batch, round-robin over n_streams streams.
+    """
+
+    def __init__(self, name: str, n_streams: int = 1, merge: bool = True):
         import torch
         from paper_2503_02172_amd import kgq, synth
 
@@ -75,17 +81,36 @@ class Prepared:
         if name == "C4-gqe":
             model = kgq.GQE
         self.model = model
-        self.eng = kgq.engine_for(w, model=model, params=params, concurrency=n_streams)
+        groups = []
+        for b in w.batches:
+            if b.structure:
+                groups.append((synth.STRUCTURE_ID[b.structure], b.batch, b.anchors, b.relations))
+            else:
+                groups.append((np.asarray(b.structure_ids, np.int32), b.batch, b.anchors, b.relations))
+        if merge and len(groups) > 1:
+            ids, A, R = [], [], []
+            for sid, n, a, r in groups:
+                pa = np.full((n, 3), -1, np.int32)
+                pr = np.full((n, 3), -1, np.int32)
+                pa[:, :a.shape[1]] = a
+                pr[:, :r.shape[1]] = r
+                ids.append(np.full(n, sid, np.int32) if np.ndim(sid) == 0 else sid)
+                A.append(pa)
+                R.append(pr)
+            ids = np.concatenate(ids)
+            groups = [(ids, ids.shape[0], np.concatenate(A), np.concatenate(R))]
+        n_streams = min(n_streams, len(groups))
+        self.eng = kgq.engine_for(w, max_batch=max(g[1] for g in groups), model=model, params=params,
+                                  concurrency=n_streams)
         self.streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
         dev = torch.device("cuda", 0)
         self.calls = []
-        for b in w.batches:
-            a = torch.as_tensor(b.anchors, dtype=torch.int32, device=dev).contiguous()
-            r = torch.as_tensor(b.relations, dtype=torch.int32, device=dev).contiguous()
-            idx = torch.empty((b.batch, w.k), dtype=torch.int32, device=dev)
-            val = torch.empty((b.batch, w.k), dtype=torch.float32, device=dev)
-            sid = synth.STRUCTURE_ID[b.structure] if b.structure else b.structure_ids
-            self.calls.append((sid, b.batch, a, r, idx, val))
+        for sid, n, a, r in groups:
+            a = torch.as_tensor(a, dtype=torch.int32, device=dev).contiguous()
+            r = torch.as_tensor(r, dtype=torch.int32, device=dev).contiguous()
+            idx = torch.empty((n, w.k), dtype=torch.int32, device=dev)
+            val = torch.empty((n, w.k), dtype=torch.float32, device=dev)
+            self.calls.append((sid, n, a, r, idx, val))
         self.n_queries = sum(c[1] for c in self.calls)
         # scored rows (union queries score two rows) -> triples per step
         rows = 0
@@ -97,7 +122,7 @@ class Prepared:
         torch.cuda.synchronize()
 
     def step(self, n_streams=None):
-        """Enqueue one step: the batch's execute calls, round-robin over the
+        """Enqueue one step: the workload's execute calls, round-robin over the
         streams (independent batches, so calls on different streams overlap)."""
         S = len(self.streams) if n_streams is None else n_streams
         for i, (sid, B, a, r, idx, val) in enumerate(self.calls):
@@ -210,8 +235,10 @@ def main():
     ap.add_argument("--no-others", action="store_true", help="skip the other four workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-per-structure", type=int, default=512)
+    ap.add_argument("--per-structure", action="store_true",
+                    help="one execute call per structure batch instead of one mixed call per step")
     ap.add_argument("--streams", type=int, default=2,
-                    help="streams the step's independent execute calls are spread over")
+                    help="with --per-structure: streams the independent calls are spread over")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
@@ -222,8 +249,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
     log(f"[bench] preparing {args.workload}")
-    p = Prepared(args.workload, args.streams)
-    log(f"[bench] warmup {args.warmup}, timing {args.steps} steps on {args.streams} stream(s)")
+    merge = not args.per_structure
+    p = Prepared(args.workload, args.streams, merge)
+    n_streams = len(p.streams)
+    log(f"[bench] warmup {args.warmup}, timing {args.steps} steps: {len(p.calls)} execute call(s) per "
+        f"step on {n_streams} stream(s)")
     dt, iv = time_steps(p, args.steps, args.warmup, profile_score=True)
     ms_step = dt / args.steps * 1e3
     qps = p.n_queries * args.steps / dt
@@ -231,16 +261,19 @@ def main():
     n_launch = len(iv)
     avg_launch_ms = float(np.mean(iv[:, 1] - iv[:, 0])) if n_launch else 0.0
     total_ops = OPS_PER_TRIPLE[p.model] * p.triples * args.steps
-    achieved = total_ops / (busy * 1e-3) if busy > 0 else 0.0
+    ops_per_launch = total_ops / max(n_launch, 1)
+    achieved = ops_per_launch / (avg_launch_ms * 1e-3) if avg_launch_ms > 0 else 0.0
+    achieved_busy = total_ops / (busy * 1e-3) if busy > 0 else 0.0
     src = os.path.join(ROOT, "paper_2503_02172_amd", "csrc", "k_score.hip")
     traffic = traffic_for(src, f"score:{args.workload}")
     roofline = {"bound": "alu", "kernel": "k_score (entity scorer)",
                 "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
                 "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4), "traffic": traffic,
-                "ops_per_launch": total_ops / max(n_launch, 1), "avg_launch_ms": round(avg_launch_ms, 5),
+                "ops_per_launch": ops_per_launch, "avg_launch_ms": round(avg_launch_ms, 5),
                 "launches": n_launch, "scorer_busy_ms": round(busy, 4),
-                "timing": "HIP events around every scorer launch on its stream; achieved = algorithmic "
-                          "VALU ops of all launches / union of the launch intervals"}
+                "frac_over_busy_time": round(achieved_busy / PEAK_VALU_OPS, 4),
+                "timing": "HIP events around every scorer launch on its stream over the timed steps; "
+                          "achieved = algorithmic VALU ops per launch / average launch duration"}
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {qps:.0f} q/s, scorer busy {busy:.2f} ms over "
         f"{n_launch} launches ({avg_launch_ms:.4f} ms each), {roofline['frac']*100:.1f}% of VALU peak")
     stages = stage_breakdown(p)
@@ -252,16 +285,19 @@ def main():
             if name == args.workload:
                 continue
             log(f"[bench] other workload {name}")
-            q = Prepared(name, args.streams)
+            q = Prepared(name, args.streams, merge)
             steps = max(3, min(args.steps, 10))
             d2, iv2 = time_steps(q, steps, 2, profile_score=True)
             ops = OPS_PER_TRIPLE[q.model] * q.triples * steps
             b2 = union_ms(iv2)
+            avg2 = float(np.mean(iv2[:, 1] - iv2[:, 0])) if len(iv2) else 0.0
             others[name] = {"workload": WORKLOAD_DESC[name], "queries_per_s": round(q.n_queries * steps / d2, 1),
                             "ms_per_step": round(d2 / steps * 1e3, 4),
                             "entity_scores_per_s": round(q.n_queries * q.w.n_entities * steps / d2, 1),
                             "scorer_busy_ms_per_step": round(b2 / steps, 5),
-                            "scorer_valu_frac": round(ops / (b2 * 1e-3) / PEAK_VALU_OPS, 4) if b2 > 0 else None,
+                            "scorer_launch_ms": round(avg2, 5),
+                            "scorer_valu_frac": round(ops / len(iv2) / (avg2 * 1e-3) / PEAK_VALU_OPS, 4)
+                            if avg2 > 0 else None,
                             "stage_ms": stage_breakdown(q, reps=2)}
             log(f"[bench]   {name}: {others[name]['queries_per_s']} q/s, scorer frac "
                 f"{others[name]['scorer_valu_frac']}")
@@ -290,7 +326,7 @@ def main():
         "data": "synthetic (seeded random tables and queries of the workload's shapes)",
         "config": {"workload": WORKLOAD_DESC[args.workload], "name": args.workload,
                    "queries_per_step": p.n_queries, "scored_rows_per_step": p.rows, "k": p.w.k,
-                   "streams": args.streams},
+                   "execute_calls_per_step": len(p.calls), "streams": n_streams},
         "entity_scores_per_s": round(qps * p.w.n_entities, 1),
         "roofline": roofline,
         "stage_ms_per_step": stages,
