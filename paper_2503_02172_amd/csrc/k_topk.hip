@@ -2,9 +2,11 @@
 // evaluates with MRR, Experiments/Metrics). Order: score descending, equal
 // scores by entity index ascending.
 //
-// One workgroup of 1024 threads selects the top k of one segment of at most
-// 16 Ki scores, held in registers (KPT keys per thread, element i =
-// j * 1024 + tid). Scores map to order-preserving 32-bit keys. Bits that
+// One workgroup of NT threads (256, or 1024 for the short candidate lists of
+// later rounds) selects the top k of one segment of at most 16 Ki scores, held
+// in registers (KPT keys per thread, element i = j * NT + tid). Small
+// workgroups keep several rows in flight per compute unit, which hides the
+// latency of the selection's barrier-separated phases. Scores map to order-preserving 32-bit keys. Bits that
 // every key of the segment shares (typically the sign and most of the
 // exponent) are found with a block-wide OR / AND and skipped. One histogram
 // pass over the next 11 bits then locates the bin that holds the k-th key;
@@ -29,8 +31,6 @@
 
 namespace kgq {
 
-constexpr int TK_THREADS = 1024;
-constexpr int TK_WAVES = TK_THREADS / 64;
 
 __device__ __forceinline__ uint32_t score_key(float f)
 {
@@ -42,6 +42,15 @@ __device__ __forceinline__ uint32_t score_key(float f)
 __device__ __forceinline__ float key_score(uint32_t key)
 {
     return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
+
+// Key of segment position j * NT + tid through the segment's buffer resource;
+// positions past the end give the padding key 0.
+template <int NT>
+__device__ __forceinline__ uint32_t fetch_key(__amdgpu_buffer_rsrc_t rsrc, int tid, int j, int n)
+{
+    const uint32_t u = __builtin_amdgcn_raw_buffer_load_b32(rsrc, tid * 4, j * NT * 4, 0);
+    return (tid < n - j * NT) ? max(score_key(__uint_as_float(u)), 1u) : 0u;
 }
 
 // composite c = key << 32 | (2^32 - 1 - index): descending c = score
@@ -59,17 +68,17 @@ __device__ __forceinline__ void store_one(const TopkArgs& a, int64_t orow, int p
 
 // Sort the n selected entries inside one wavefront (P = 64 * E >= n
 // positions, lane l holds positions e * 64 + l; padding sorts last) and
-// write out the first k.
+// write out the first k. Entry p is the composite of sel_key[p] and sel_idx[p].
 template <int E>
-__device__ __forceinline__ void bitonic_wave(const uint64_t* sel, int n, int k, int64_t orow, int lane,
-                                             const TopkArgs& a)
+__device__ __forceinline__ void bitonic_wave(const uint32_t* sel_key, const uint32_t* sel_idx, int n, int k,
+                                             int64_t orow, int lane, const TopkArgs& a)
 {
     constexpr int P = 64 * E;
     uint64_t v[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         const int p = e * 64 + lane;
-        v[e] = p < n ? sel[p] : 0ull;
+        v[e] = p < n ? (((uint64_t)sel_key[p] << 32) | sel_idx[p]) : 0ull;
     }
 #pragma unroll
     for (int size = 2; size <= P; size <<= 1) {
@@ -109,14 +118,14 @@ __device__ __forceinline__ void bitonic_wave(const uint64_t* sel, int n, int k, 
     }
 }
 
-// Exclusive prefix, in place, over the KPT * 16 per-(step, wavefront) counts
-// in (step, wavefront) order, which is element index order. Run by the whole
-// workgroup; only wavefront 0 works.
-template <int KPT>
+// Exclusive prefix, in place, over the KPT * NT / 64 per-(step, wavefront)
+// counts in (step, wavefront) order, which is element index order. Run by the
+// whole workgroup; only wavefront 0 works.
+template <int NT, int KPT>
 __device__ __forceinline__ void block_exclusive_prefix(int* cnt, int tid)
 {
     if (tid >= 64) return;
-    constexpr int NC = KPT * TK_WAVES;
+    constexpr int NC = KPT * (NT / 64);
     constexpr int PER = (NC + 63) / 64;
     int s = 0;
 #pragma unroll
@@ -142,13 +151,21 @@ __device__ __forceinline__ void block_exclusive_prefix(int* cnt, int tid)
     }
 }
 
-template <int KPT>
-__global__ __launch_bounds__(TK_THREADS) void k_topk(TopkArgs a)
+template <int NT, int KPT>
+__global__ __launch_bounds__(NT) void k_topk(TopkArgs a)
 {
-    __shared__ uint32_t hist[2048];
-    __shared__ uint64_t sel[kMaxK];
+    constexpr int TK_THREADS = NT;
+    constexpr int TK_WAVES = NT / 64;
+    // The selected entries are kept as separate 32-bit key and inverted-index
+    // arrays (a key never has to sit in the high half of a 64-bit register
+    // pair, which would cost a second register per key). The LDS sort for
+    // long candidate lists builds 64-bit composites in the histogram's
+    // storage, which is free by then.
+    __shared__ uint64_t srt[kMaxK];
+    __shared__ uint32_t sel_key[kMaxK], sel_idx[kMaxK];
+    uint32_t* hist = reinterpret_cast<uint32_t*>(srt);    // 2048 bins
     __shared__ int sh_bin, sh_rem;
-    __shared__ uint32_t sh_or[TK_WAVES], sh_and[TK_WAVES];
+    __shared__ uint32_t sh_or[TK_WAVES], sh_and[TK_WAVES];   // per-wavefront max / min key
     __shared__ int cnt_gt[KPT * TK_WAVES], cnt_eq[KPT * TK_WAVES];
 
     const int tid = threadIdx.x;
@@ -162,37 +179,55 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(TopkArgs a)
     const int32_t* __restrict__ ir = a.in_idx ? a.in_idx + row * a.ld + seg0 : nullptr;
     const int k = a.k < n ? a.k : (int)n;   // a segment shorter than k yields all of it
 
+    // Positions past the segment's end hold key 0; real keys are at least 1
+    // (only the one NaN pattern whose key would be 0 moves up to 1), so no
+    // per-element validity mask has to stay live through the passes below.
+    // Buffer loads against a resource sized to the segment: every position
+    // loads (past the end the hardware returns 0), so the loads carry no
+    // branch, share one address register and are all in flight together.
+    const int nn = (int)n;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sr), (short)0, nn * 4, 0x00020000);
     uint32_t keys[KPT];
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-        const int64_t i = (int64_t)j * TK_THREADS + tid;
-        keys[j] = i < n ? score_key(sr[i]) : 0u;
-    }
+    for (int j = 0; j < KPT; ++j)
+        keys[j] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, tid * 4, j * TK_THREADS * 4, 0);
+    // The empty asm uses every loaded value unconditionally, so the compiler
+    // cannot move a load into the validity branch below (which would make
+    // the loads wait for each other one by one).
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) asm volatile("" : "+v"(keys[j]));
+#pragma unroll
+    for (int j = 0; j < KPT; ++j)
+        keys[j] = (tid < nn - j * TK_THREADS) ? max(score_key(__uint_as_float(keys[j])), 1u) : 0u;
 
-    // bits shared by every key: OR and AND over the segment
+    // Bits shared by every key: the keys' common leading bits are those of the
+    // smallest and the largest key. Padding (0) drops out of the maximum, and
+    // of the minimum taken over key - 1 (where it wraps to the top).
     {
-        uint32_t o = 0u, an = 0xFFFFFFFFu;
+        uint32_t mx = 0u, mn1 = 0xFFFFFFFFu;
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
-            if ((int64_t)j * TK_THREADS + tid < n) { o |= keys[j]; an &= keys[j]; }
+            mx = max(mx, keys[j]);
+            mn1 = min(mn1, keys[j] - 1u);
         }
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
-            o |= __shfl_xor(o, off, 64);
-            an &= __shfl_xor(an, off, 64);
+            mx = max(mx, (uint32_t)__shfl_xor(mx, off, 64));
+            mn1 = min(mn1, (uint32_t)__shfl_xor(mn1, off, 64));
         }
-        if (lane == 0) { sh_or[wave] = o; sh_and[wave] = an; }
+        if (lane == 0) { sh_or[wave] = mx; sh_and[wave] = mn1 + 1u; }
     }
     __syncthreads();
-    uint32_t all_or = 0u, all_and = 0xFFFFFFFFu;
+    uint32_t kmax = 0u, kmin = 0xFFFFFFFFu;
 #pragma unroll
-    for (int w = 0; w < TK_WAVES; ++w) { all_or |= sh_or[w]; all_and &= sh_and[w]; }
-    const uint32_t diff = all_or ^ all_and;            // bits that differ somewhere
+    for (int w = 0; w < TK_WAVES; ++w) { kmax = max(kmax, sh_or[w]); kmin = min(kmin, sh_and[w]); }
+    const uint32_t diff = kmax ^ kmin;                 // zero iff all keys are equal
     int top = diff ? 31 - __clz(diff) : -1;            // highest differing bit
 
     // bits above `top` are common to all keys: they start the prefix
     uint32_t pmask = diff ? ~(0xFFFFFFFFu >> (31 - top)) : 0xFFFFFFFFu;
-    uint32_t prefix = all_and & pmask;
+    uint32_t prefix = kmax & pmask;
 
     // --- one wide histogram pass: the bin of the k-th key -------------------
     // digit = bits [wlo, top], at most 11 bits
@@ -204,23 +239,9 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(TopkArgs a)
         for (int b = tid; b < 2048; b += TK_THREADS) hist[b] = 0;
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < KPT; ++j) {
-            const int64_t i = (int64_t)j * TK_THREADS + tid;
-            const bool act = i < n;
-            const uint32_t bin = (keys[j] >> wlo) & wmask;
-            const uint64_t am = __ballot(act);
-            if (act) {
-                const int first = __ffsll((unsigned long long)am) - 1;
-                const uint32_t b0 = __shfl(bin, first, 64);
-                const uint64_t same = __ballot(bin == b0);
-                if ((same & am) == am) {
-                    if (lane == first) atomicAdd(&hist[b0], (uint32_t)__popcll(am));
-                } else {
-                    atomicAdd(&hist[bin], 1u);
-                }
-            }
-        }
+        for (int j = 0; j < KPT; ++j) atomicAdd(&hist[(keys[j] >> wlo) & wmask], 1u);
         __syncthreads();
+        if (tid == 0) hist[0] -= (uint32_t)(KPT * TK_THREADS - nn);   // the padding landed in bin 0
         if (tid < 64) {
             // lane l owns bins 32l .. 32l+31; inclusive suffix sum over lanes
             uint32_t s = 0;
@@ -251,45 +272,56 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(TopkArgs a)
         n_cand = sh_rem;
     }
 
-    int n_sel;                 // entries placed in sel[]
+    int n_sel;                 // entries placed in sel_key[] / sel_idx[]
     if (n_cand <= kMaxK) {
         // --- candidates fit: take every key whose digit is >= dmin ----------
+        // All keys share the bits above `top`, so digit >= dmin is the same
+        // as key >= thr with thr = (common bits, dmin, zeros); thr >= 1 keeps
+        // the padding out.
         n_sel = n_cand;
+        const uint32_t thr = max(top >= 0 ? (prefix | (dmin << wlo)) : prefix, 1u);
+        // The sort below orders candidates completely by (key, index), so
+        // their slots only need to be distinct: each wavefront takes a range
+        // sized by its candidate count and fills it in step order.
+        int wc = 0;
 #pragma unroll
-        for (int j = 0; j < KPT; ++j) {
-            const int64_t i = (int64_t)j * TK_THREADS + tid;
-            const uint64_t bc = __ballot(i < n && ((keys[j] >> wlo) & wmask) >= dmin);
-            if (lane == 0) cnt_gt[j * TK_WAVES + wave] = __popcll(bc);
-        }
+        for (int j = 0; j < KPT; ++j) wc += __popcll(__ballot(keys[j] >= thr));
+        if (lane == 0) cnt_gt[wave] = wc;
         __syncthreads();
-        block_exclusive_prefix<KPT>(cnt_gt, tid);
-        __syncthreads();
+        int base = 0;
+        for (int w = 0; w < wave; ++w) base += cnt_gt[w];
         const uint64_t lt = (1ull << lane) - 1ull;
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
-            const int64_t i = (int64_t)j * TK_THREADS + tid;
-            const bool f = i < n && ((keys[j] >> wlo) & wmask) >= dmin;
+            const bool f = keys[j] >= thr;
             const uint64_t bc = __ballot(f);
             if (f) {
-                const int slot = cnt_gt[j * TK_WAVES + wave] + __popcll(bc & lt);
-                if (slot < kMaxK) sel[slot] = composite(keys[j], ir ? ir[i] : (int32_t)(seg0 + i));
+                const int i = j * TK_THREADS + tid;
+                const int slot = base + __popcll(bc & lt);
+                if (slot < kMaxK) {
+                    sel_key[slot] = keys[j];
+                    sel_idx[slot] = 0xFFFFFFFFu - (uint32_t)(ir ? ir[i] : (int32_t)seg0 + i);
+                }
             }
+            base += __popcll(bc);
         }
     } else {
         // --- too many candidates: exact radix passes find T ------------------
+        // (rare: very many equal or nearly equal scores). Keys are fetched
+        // again from memory in loops that are not unrolled, so this path adds
+        // no register pressure to the common one above.
         int rem = k;
         for (int lo = top - 7; top >= 0; lo -= 8) {
             // digit = bits [max(lo, 0), top] of the key
             const int shift = lo > 0 ? lo : 0;
             const int width = top - shift + 1;
             const uint32_t dmask = (1u << width) - 1u;      // width <= 8
-            if (tid < 256) hist[tid] = 0;
+            for (int b = tid; b < 256; b += TK_THREADS) hist[b] = 0;
             __syncthreads();
-#pragma unroll
+#pragma unroll 1
             for (int j = 0; j < KPT; ++j) {
-                const int64_t i = (int64_t)j * TK_THREADS + tid;
-                const uint32_t key = keys[j];
-                const bool act = i < n && (key & pmask) == prefix;
+                const uint32_t key = fetch_key<NT>(rsrc, tid, j, nn);
+                const bool act = key != 0u && (key & pmask) == prefix;
                 const uint32_t bin = (key >> shift) & dmask;
                 const uint64_t am = __ballot(act);
                 if (act) {
@@ -340,26 +372,27 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(TopkArgs a)
         const uint32_t T = prefix;
         const int n_gt = k - rem;
         n_sel = k;
-#pragma unroll
+#pragma unroll 1
         for (int j = 0; j < KPT; ++j) {
-            const int64_t i = (int64_t)j * TK_THREADS + tid;
-            const uint64_t bg = __ballot(i < n && keys[j] > T);
-            const uint64_t be = __ballot(i < n && keys[j] == T);
+            const uint32_t key = fetch_key<NT>(rsrc, tid, j, nn);
+            const uint64_t bg = __ballot(key > T);
+            const uint64_t be = __ballot(key == T);
             if (lane == 0) {
                 cnt_gt[j * TK_WAVES + wave] = __popcll(bg);
                 cnt_eq[j * TK_WAVES + wave] = __popcll(be);
             }
         }
         __syncthreads();
-        block_exclusive_prefix<KPT>(cnt_gt, tid);
+        block_exclusive_prefix<NT, KPT>(cnt_gt, tid);
         __syncthreads();
-        block_exclusive_prefix<KPT>(cnt_eq, tid);
+        block_exclusive_prefix<NT, KPT>(cnt_eq, tid);
         __syncthreads();
         const uint64_t lt = (1ull << lane) - 1ull;
-#pragma unroll
+#pragma unroll 1
         for (int j = 0; j < KPT; ++j) {
-            const int64_t i = (int64_t)j * TK_THREADS + tid;
-            const bool fg = i < n && keys[j] > T, fe = i < n && keys[j] == T;
+            const int i = j * TK_THREADS + tid;
+            const uint32_t key = fetch_key<NT>(rsrc, tid, j, nn);
+            const bool fg = key > T, fe = key == T;
             const uint64_t bg = __ballot(fg);
             const uint64_t be = __ballot(fe);
             int slot = -1;
@@ -370,8 +403,10 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(TopkArgs a)
             }
             // slots stay below k by construction; the check keeps LDS accesses
             // inside the buffer regardless
-            if (slot >= 0 && slot < k)
-                sel[slot] = composite(keys[j], ir ? ir[i] : (int32_t)(seg0 + i));
+            if (slot >= 0 && slot < k) {
+                sel_key[slot] = key;
+                sel_idx[slot] = 0xFFFFFFFFu - (uint32_t)(ir ? ir[i] : (int32_t)seg0 + i);
+            }
         }
     }
     __syncthreads();
@@ -385,41 +420,44 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(TopkArgs a)
     }
     if (n_sel <= 256) {
         if (tid < 64) {
-            if (n_sel <= 64) bitonic_wave<1>(sel, n_sel, k, orow, lane, a);
-            else if (n_sel <= 128) bitonic_wave<2>(sel, n_sel, k, orow, lane, a);
-            else bitonic_wave<4>(sel, n_sel, k, orow, lane, a);
+            if (n_sel <= 64) bitonic_wave<1>(sel_key, sel_idx, n_sel, k, orow, lane, a);
+            else if (n_sel <= 128) bitonic_wave<2>(sel_key, sel_idx, n_sel, k, orow, lane, a);
+            else bitonic_wave<4>(sel_key, sel_idx, n_sel, k, orow, lane, a);
         }
     } else {
         int P = 512;
         while (P < n_sel) P <<= 1;             // 512 or 1024
-        for (int p = n_sel + tid; p < P; p += TK_THREADS) sel[p] = 0ull;
+        for (int p = tid; p < P; p += TK_THREADS)
+            srt[p] = p < n_sel ? (((uint64_t)sel_key[p] << 32) | sel_idx[p]) : 0ull;
         for (int size = 2; size <= P; size <<= 1) {
             for (int stride = size >> 1; stride > 0; stride >>= 1) {
                 __syncthreads();
-                if (tid < P) {
-                    const int q = tid ^ stride;
-                    if (q > tid) {
-                        const bool desc = (tid & size) == 0;
-                        const uint64_t a0 = sel[tid], a1 = sel[q];
-                        if (desc ? (a0 < a1) : (a0 > a1)) { sel[tid] = a1; sel[q] = a0; }
-                    }
+                // P / 2 compare-exchange pairs per stage; pair t is (p, p + stride)
+                for (int t = tid; t < P / 2; t += TK_THREADS) {
+                    const int p = ((t & ~(stride - 1)) << 1) | (t & (stride - 1));
+                    const int q = p + stride;
+                    const bool desc = (p & size) == 0;
+                    const uint64_t a0 = srt[p], a1 = srt[q];
+                    if (desc ? (a0 < a1) : (a0 > a1)) { srt[p] = a1; srt[q] = a0; }
                 }
             }
         }
         __syncthreads();
-        if (tid < k) store_one(a, orow, tid, sel[tid]);
+        for (int p = tid; p < k; p += TK_THREADS) store_one(a, orow, p, srt[p]);
     }
 }
 
 static void launch_segments(const TopkArgs& a, hipStream_t s)
 {
-    const int64_t per = (a.seg_len + TK_THREADS - 1) / TK_THREADS;
-    dim3 grid((unsigned)((a.N + a.seg_len - 1) / a.seg_len), (unsigned)a.n_rows), block(TK_THREADS);
-    if (per <= 1) hipLaunchKernelGGL(k_topk<1>, grid, block, 0, s, a);
-    else if (per <= 2) hipLaunchKernelGGL(k_topk<2>, grid, block, 0, s, a);
-    else if (per <= 4) hipLaunchKernelGGL(k_topk<4>, grid, block, 0, s, a);
-    else if (per <= 8) hipLaunchKernelGGL(k_topk<8>, grid, block, 0, s, a);
-    else hipLaunchKernelGGL(k_topk<16>, grid, block, 0, s, a);
+    dim3 grid((unsigned)((a.N + a.seg_len - 1) / a.seg_len), (unsigned)a.n_rows);
+    // 256 threads with up to 64 keys each for long segments; short ones
+    // (k-candidate lists of later rounds) use as many keys per thread as fit
+    const int64_t per = (a.seg_len + 255) / 256;
+    if (per <= 4) hipLaunchKernelGGL((k_topk<256, 4>), grid, dim3(256), 0, s, a);
+    else if (per <= 8) hipLaunchKernelGGL((k_topk<256, 8>), grid, dim3(256), 0, s, a);
+    else if (per <= 16) hipLaunchKernelGGL((k_topk<256, 16>), grid, dim3(256), 0, s, a);
+    else if (per <= 32) hipLaunchKernelGGL((k_topk<256, 32>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_topk<256, 64>), grid, dim3(256), 0, s, a);
 }
 
 int64_t topk_scratch_elems(int64_t n_rows, int64_t N, int k)
