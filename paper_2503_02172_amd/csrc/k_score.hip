@@ -12,9 +12,12 @@
 //     the query values come through the scalar cache into SGPRs and feed the
 //     VALU as scalar operands: no LDS traffic and no cross-lane reduction;
 //   - the 4 wavefronts of a workgroup share one entity block (L1 reuse), and
-//     workgroups are assigned so that each XCD sweeps a contiguous range of
-//     entity blocks with all query groups, keeping its share of the table in
-//     that XCD's L2.
+//     workgroups are ordered so that each XCD takes a chunk of query groups
+//     (about an eighth of them, at most ~2 MiB of packed queries) and sweeps
+//     every entity block against it: the chunk's queries stay in that XCD's
+//     L2 for the whole sweep and each entity block is fetched once per XCD
+//     (entity-block-major order within an XCD would instead re-fetch every
+//     query once per entity block).
 //
 // Per-triple work (one non-packed VALU op each):
 //   GQE     d = e - q;  acc += |d|                                       (2)
@@ -30,6 +33,7 @@
 //           C_q = sum_i lnB(alpha_q, beta_q)  (entity a, b; query alpha_q, beta_q).
 // Union (disjunctive normal form, Eq. 1 of the paper): a union query has two
 // adjacent rows; its score is the max of the two rows' scores.
+#include <algorithm>
 #include <type_traits>
 
 #include "kgq_internal.hpp"
@@ -37,14 +41,22 @@
 namespace kgq {
 
 template <int MODEL, int TQ>
-__global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int total_wg, int wg_per_xcd)
+__global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk, int total_wg, int wg_per_xcd)
 {
-    // XCD-aware mapping: workgroup b runs on XCD b % 8 (round-robin dispatch).
+    // XCD-aware mapping: workgroup b runs on XCD b % 8 (round-robin dispatch),
+    // so XCD x executes positions [x * wg_per_xcd, (x + 1) * wg_per_xcd) of
+    // the global order, in order. The global order is: query chunks of qchunk
+    // query groups (the last one may be short); within a chunk, entity blocks;
+    // within an entity block, the chunk's query groups.
     const int b = blockIdx.x;
     const int L = (b & 7) * wg_per_xcd + (b >> 3);
     if (L >= total_wg) return;
-    const int eb = L / nqg;
-    const int qg = L - eb * nqg;
+    const int chunk_wg = qchunk * (int)a.n_blocks;
+    const int c = L / chunk_wg;
+    const int r = L - c * chunk_wg;
+    const int qcc = min(qchunk, nqg - c * qchunk);     // query groups in this chunk
+    const int eb = r / qcc;
+    const int qg = c * qchunk + (r - eb * qcc);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int qb = qg * 4 + wave;
@@ -196,13 +208,19 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
     const int nqg = (nqb + 3) / 4;
     const int total = (int)(a.n_blocks * nqg);
     const int per_xcd = (total + 7) / 8;
+    // query chunk: an eighth of the query groups, capped at ~2 MiB of packed
+    // queries so that a chunk and the entity blocks in flight fit one XCD's L2
+    const int64_t qg_bytes = (int64_t)4 * tq * a.d * (a.model == 0 ? 1 : 2) * 4;
+    int qc = (nqg + 7) / 8;
+    const int qc_cap = (int)std::max<int64_t>(1, (int64_t)(2 << 20) / qg_bytes);
+    if (qc > qc_cap) qc = qc_cap;
     dim3 grid(per_xcd * 8);
     if (a.model == 0)
-        hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, a, nqg, total, per_xcd);
+        hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
     else if (a.model == 1)
-        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, a, nqg, total, per_xcd);
+        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
     else
-        hipLaunchKernelGGL((k_score<2, kTqBetae>), grid, dim3(256), 0, s, a, nqg, total, per_xcd);
+        hipLaunchKernelGGL((k_score<2, kTqBetae>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
 }
 
 }  // namespace kgq
