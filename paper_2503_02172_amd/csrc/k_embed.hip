@@ -204,14 +204,21 @@ __global__ void k_chain(int model, const int32_t* anchor_ref, const int32_t* rel
     }
     const int W = model == 0 ? d : 2 * d;
     float* out = states + (int64_t)c * W;
-    for (int k = threadIdx.x; k < d; k += blockDim.x) {
-        float x = ent_rm[a * d + k];
-        for (int h = 0; h < nh; ++h) x += rel_c[(int64_t)r[h] * d + k];
-        out[k] = x;
+    // d is a multiple of 4: 128-bit accesses, one float4 per thread per step
+    for (int k = threadIdx.x * 4; k < d; k += blockDim.x * 4) {
+        float4 x = *reinterpret_cast<const float4*>(ent_rm + a * d + k);
+        for (int h = 0; h < nh; ++h) {
+            const float4 v = *reinterpret_cast<const float4*>(rel_c + (int64_t)r[h] * d + k);
+            x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
+        }
+        *reinterpret_cast<float4*>(out + k) = x;
         if (model == 1) {
-            float o = 0.f;
-            for (int h = 0; h < nh; ++h) o += rel_o[(int64_t)r[h] * d + k];
-            out[d + k] = o;
+            float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int h = 0; h < nh; ++h) {
+                const float4 v = *reinterpret_cast<const float4*>(rel_o + (int64_t)r[h] * d + k);
+                o.x += v.x; o.y += v.y; o.z += v.z; o.w += v.w;
+            }
+            *reinterpret_cast<float4*>(out + d + k) = o;
         }
     }
 }
@@ -392,33 +399,82 @@ void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, c
 
 // ---------------------------------------------------------------------------
 // Query packing for the scorer: [row_block][k][field][TQ]; BetaE also C_q.
+// One workgroup per block of TQ rows transposes through LDS, KC dimensions at
+// a time (as many as a 32 KiB tile holds, so that all loads of a chunk are in
+// flight together): the state rows are read along k and the packed block is
+// written in its own order, both contiguous.
 // ---------------------------------------------------------------------------
 
-template <int TQ, int F>
-__global__ __launch_bounds__(64) void k_pack(int model, const int32_t* src_row, int n_rows, const float* states, int W, int d,
-                       float* qpack, double* cq)
+template <int MODEL, int TQ, int F>
+__global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows, const float* states, int W, int d,
+                                              float* qpack, double* cq)
 {
-    const int j = blockIdx.x;           // padded row index
-    const int qb = j / TQ, i = j % TQ;
-    const int32_t src = j < n_rows ? src_row[j] : -1;
+    constexpr int KC = 8192 / (TQ * F);       // dimensions per chunk: a 32 KiB tile (d = 400: one or two chunks)
+    constexpr int RS = F * KC + 1;            // padded LDS row: the transposed reads hit distinct banks
+    constexpr int TPR = 256 / TQ;             // threads per row for the C_q sums
+    __shared__ float tile[TQ * RS];
+    __shared__ int srcs[TQ];
+    const int qb = blockIdx.x;
+    const int t = threadIdx.x;
+    if (t < TQ) {
+        const int j = qb * TQ + t;
+        srcs[t] = j < n_rows ? src_row[j] : -1;
+    }
+    __syncthreads();
+    const int ci = t / TPR, cr = t % TPR;     // C_q: row and lane within the row
     double lnb = 0.0;
-    for (int k = threadIdx.x; k < d; k += blockDim.x) {
-        float* dst = qpack + (((int64_t)qb * d + k) * F) * TQ + i;
-        if (src >= 0) {
-            const float* st = states + (int64_t)src * W;
-            for (int f = 0; f < F; ++f) dst[f * TQ] = st[f * d + k];
-            if (model == 2) {
-                const double a = st[k], b = st[d + k];
+    float* out = qpack + (int64_t)qb * d * F * TQ;
+    for (int k0 = 0; k0 < d; k0 += KC) {
+        const int kc = min(KC, d - k0);           // a multiple of 4
+        const int n4 = TQ * F * kc / 4;            // float4 elements of this chunk
+        constexpr int PER4 = TQ * F * KC / 4 / 256;
+        // All loads of the chunk are issued before any is used: each reads a
+        // valid address (row 0 for padding rows or past the chunk's end) and
+        // the empty asm keeps the compiler from moving a load into the
+        // validity branch, where the loads would wait for each other.
+        float4 v[PER4];
+#pragma unroll
+        for (int u = 0; u < PER4; ++u) {
+            const int e = 4 * (t + 256 * u);
+            const int i = min(e / (F * kc), TQ - 1), rem = e - i * (F * kc);
+            const int f = rem / kc, kk = rem - f * kc;
+            const int src = srcs[i];
+            const bool ok = t + 256 * u < n4 && src >= 0;
+            const int64_t off = ok ? (int64_t)src * W + f * d + k0 + kk : 0;
+            v[u] = *reinterpret_cast<const float4*>(states + off);
+        }
+#pragma unroll
+        for (int u = 0; u < PER4; ++u) asm volatile("" : "+v"(v[u].x), "+v"(v[u].y), "+v"(v[u].z), "+v"(v[u].w));
+#pragma unroll
+        for (int u = 0; u < PER4; ++u) {
+            if (t + 256 * u >= n4) break;
+            const int e = 4 * (t + 256 * u);
+            const int i = e / (F * kc), rem = e - i * (F * kc);
+            const int f = rem / kc, kk = rem - f * kc;
+            const bool ok = srcs[i] >= 0;
+            float* dst = tile + i * RS + f * KC + kk;
+            dst[0] = ok ? v[u].x : 0.f;
+            dst[1] = ok ? v[u].y : 0.f;
+            dst[2] = ok ? v[u].z : 0.f;
+            dst[3] = ok ? v[u].w : 0.f;
+        }
+        __syncthreads();
+        for (int o = t; o < kc * F * TQ; o += 256) {
+            const int i = o % TQ, f = (o / TQ) % F, kk = o / (TQ * F);
+            out[(int64_t)k0 * F * TQ + o] = tile[i * RS + f * KC + kk];
+        }
+        if (MODEL == 2 && srcs[ci] >= 0) {
+            for (int kk = cr; kk < kc; kk += TPR) {
+                const double a = tile[ci * RS + kk], b = tile[ci * RS + KC + kk];
                 lnb += lgamma(a) + lgamma(b) - lgamma(a + b);
             }
-        } else {
-            for (int f = 0; f < F; ++f) dst[f * TQ] = 0.f;
         }
+        __syncthreads();
     }
-    if (model == 2) {
-        // wavefront reduction (blockDim == 64)
-        for (int off = 32; off > 0; off >>= 1) lnb += __shfl_down(lnb, off, 64);
-        if (threadIdx.x == 0) cq[j] = lnb;
+    if (MODEL == 2) {
+        // the TPR threads of a row are adjacent lanes of one wavefront
+        for (int off = TPR / 2; off > 0; off >>= 1) lnb += __shfl_xor(lnb, off, 64);
+        if (cr == 0) cq[qb * TQ + ci] = lnb;
     }
 }
 
@@ -426,15 +482,14 @@ void launch_pack(int model, const int32_t* src_row, int n_rows, int n_rows_pad, 
                  int W, int d, float* qpack, double* cq, hipStream_t s)
 {
     if (n_rows_pad <= 0) return;
+    const int tq = score_tq(model);
+    const dim3 grid(n_rows_pad / tq);          // n_rows_pad is a multiple of tq
     if (model == 0)
-        hipLaunchKernelGGL((k_pack<kTqGqe, 1>), dim3(n_rows_pad), dim3(64), 0, s, model, src_row, n_rows,
-                           states, W, d, qpack, cq);
+        hipLaunchKernelGGL((k_pack<0, kTqGqe, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack, cq);
     else if (model == 1)
-        hipLaunchKernelGGL((k_pack<kTqQ2b, 2>), dim3(n_rows_pad), dim3(64), 0, s, model, src_row, n_rows,
-                           states, W, d, qpack, cq);
+        hipLaunchKernelGGL((k_pack<1, kTqQ2b, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack, cq);
     else
-        hipLaunchKernelGGL((k_pack<kTqBetae, 2>), dim3(n_rows_pad), dim3(64), 0, s, model, src_row, n_rows,
-                           states, W, d, qpack, cq);
+        hipLaunchKernelGGL((k_pack<2, kTqBetae, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack, cq);
 }
 
 }  // namespace kgq
