@@ -33,15 +33,23 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-# MI355X FP32 VALU peak in lane-operations per second: 256 CUs x 4 SIMDs x
-# 32 lanes per clock x 2.4 GHz = 78.64e12, the published 157.3 TFLOP/s FP32
-# vector peak counted at 2 flops per lane-operation. Each sub / add / min /
-# max / fma of the scorers counts as one lane-operation (packed FP32 is
-# disabled in this build, so every instruction does one operation per lane).
+# Scorer rooflines.
+# GQE and Query2Box score on the vector units: peak in lane-operations per
+# second, 256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.64e12 (the
+# published 157.3 TFLOP/s FP32 vector peak counted at 2 flops per
+# lane-operation); each sub / add / min of the scorer is one lane-operation
+# (packed FP32 is disabled in this build).
+# BetaE scores on the matrix cores: the published dense FP32 MFMA peak,
+# 157.3 TFLOP/s; each (row, entity, dimension) triple is 2 multiply-adds
+# (alpha * U + beta * V), 4 flops.
 PEAK_VALU_OPS = 256 * 4 * 32 * 2.4e9
+PEAK_MFMA_F32 = 157.3e12
 HBM_PEAK = 8.0e12
-# algorithmic VALU operations per (query row, entity, dimension) triple
-OPS_PER_TRIPLE = {0: 2, 1: 4, 2: 2}
+# algorithmic operations per (query row, entity, dimension) triple, the peak
+# they are counted against, and its unit
+OPS_PER_TRIPLE = {0: 2, 1: 4, 2: 4}
+SCORER_PEAK = {0: (PEAK_VALU_OPS, "alu", "TOP/s"), 1: (PEAK_VALU_OPS, "alu", "TOP/s"),
+               2: (PEAK_MFMA_F32, "mfma", "TFLOP/s")}
 K_TOP = 100
 
 WORKLOAD_DESC = {
@@ -264,18 +272,19 @@ def main():
     ops_per_launch = total_ops / max(n_launch, 1)
     achieved = ops_per_launch / (avg_launch_ms * 1e-3) if avg_launch_ms > 0 else 0.0
     achieved_busy = total_ops / (busy * 1e-3) if busy > 0 else 0.0
-    src = os.path.join(ROOT, "paper_2503_02172_amd", "csrc", "k_score.hip")
+    src = os.path.join(ROOT, "paper_2503_02172_amd", "csrc", "k_score_kl.hip" if p.model == 2 else "k_score.hip")
     traffic = traffic_for(src, f"score:{args.workload}")
-    roofline = {"bound": "alu", "kernel": "k_score (entity scorer)",
-                "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
-                "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4), "traffic": traffic,
+    peak, bound, unit = SCORER_PEAK[p.model]
+    roofline = {"bound": bound, "kernel": "k_score (entity scorer)" if p.model != 2 else "k_score_kl (entity scorer)",
+                "achieved": round(achieved / 1e12, 3), "peak": round(peak / 1e12, 2),
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
                 "ops_per_launch": ops_per_launch, "avg_launch_ms": round(avg_launch_ms, 5),
                 "launches": n_launch, "scorer_busy_ms": round(busy, 4),
-                "frac_over_busy_time": round(achieved_busy / PEAK_VALU_OPS, 4),
+                "frac_over_busy_time": round(achieved_busy / peak, 4),
                 "timing": "HIP events around every scorer launch on its stream over the timed steps; "
                           "achieved = algorithmic VALU ops per launch / average launch duration"}
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {qps:.0f} q/s, scorer busy {busy:.2f} ms over "
-        f"{n_launch} launches ({avg_launch_ms:.4f} ms each), {roofline['frac']*100:.1f}% of VALU peak")
+        f"{n_launch} launches ({avg_launch_ms:.4f} ms each), {roofline['frac']*100:.1f}% of the {bound} peak")
     stages = stage_breakdown(p)
     log(f"[bench] stage ms per step (one stream, instrumented): {stages}")
 
@@ -296,11 +305,12 @@ def main():
                             "entity_scores_per_s": round(q.n_queries * q.w.n_entities * steps / d2, 1),
                             "scorer_busy_ms_per_step": round(b2 / steps, 5),
                             "scorer_launch_ms": round(avg2, 5),
-                            "scorer_valu_frac": round(ops / len(iv2) / (avg2 * 1e-3) / PEAK_VALU_OPS, 4)
+                            "scorer_bound": SCORER_PEAK[q.model][1],
+                            "scorer_frac": round(ops / len(iv2) / (avg2 * 1e-3) / SCORER_PEAK[q.model][0], 4)
                             if avg2 > 0 else None,
                             "stage_ms": stage_breakdown(q, reps=2)}
             log(f"[bench]   {name}: {others[name]['queries_per_s']} q/s, scorer frac "
-                f"{others[name]['scorer_valu_frac']}")
+                f"{others[name]['scorer_frac']} of the {others[name]['scorer_bound']} peak")
             q.eng.close()
             del q
             torch.cuda.empty_cache()

@@ -81,15 +81,14 @@ __device__ double digamma_d(double x)
 }
 
 // BetaE entity tables: alpha|beta decoded to fp32 (row-major, for anchor
-// gathers), U/V blocked for the scorer, and E_e, all from the stored values.
+// gathers), U|V row-major for the matrix-core scorer (zero rows past N), and
+// E_e, all from the stored values.
 __global__ __launch_bounds__(128) void k_betae_entity_prep(const void* src, int bf16, int64_t N, int d, int64_t n_pad,
-                                    float* ab_rowmajor, float* uv_blocked, double* e_const)
+                                    float* ab_rowmajor, float* uv_rowmajor, double* e_const)
 {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= n_pad) return;
-    const int64_t blk = e / kEntBlock;
-    const int lo = (int)(e % kEntBlock);
-    float* dst = uv_blocked + blk * (int64_t)d * 2 * kEntBlock + lo;
+    float* dst = uv_rowmajor + e * 2 * d;
     double acc = 0.0;
     for (int k = 0; k < d; ++k) {
         float u = 0.f, v = 0.f;
@@ -105,18 +104,18 @@ __global__ __launch_bounds__(128) void k_betae_entity_prep(const void* src, int 
             const double lnb = lgamma(a) + lgamma(b) - lgamma(a + b);
             acc += -lnb + a * pa + b * pb - (a + b) * pab;
         }
-        dst[(int64_t)k * 2 * kEntBlock] = u;
-        dst[(int64_t)k * 2 * kEntBlock + kEntBlock] = v;
+        dst[k] = u;
+        dst[d + k] = v;
     }
     e_const[e] = acc;
 }
 
 void launch_betae_entity_prep(const void* src, int src_bf16, int64_t N, int d, int64_t n_blocks,
-                              float* ab_rowmajor, float* uv_blocked, double* e_const, hipStream_t s)
+                              float* ab_rowmajor, float* uv_rowmajor, double* e_const, hipStream_t s)
 {
     const int64_t n_pad = n_blocks * kEntBlock;
     hipLaunchKernelGGL(k_betae_entity_prep, dim3((unsigned)((n_pad + 127) / 128)), dim3(128), 0, s,
-                       src, src_bf16, N, d, n_pad, ab_rowmajor, uv_blocked, e_const);
+                       src, src_bf16, N, d, n_pad, ab_rowmajor, uv_rowmajor, e_const);
 }
 
 __global__ void k_softplus(const float* src, float* dst, int64_t n)
@@ -398,20 +397,19 @@ void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, c
 }
 
 // ---------------------------------------------------------------------------
-// Query packing for the scorer: [row_block][k][field][TQ]; BetaE also C_q.
+// Query packing for the VALU scorers (GQE, Query2Box): [row_block][k][field][TQ].
 // One workgroup per block of TQ rows transposes through LDS, KC dimensions at
 // a time (as many as a 32 KiB tile holds, so that all loads of a chunk are in
 // flight together): the state rows are read along k and the packed block is
 // written in its own order, both contiguous.
 // ---------------------------------------------------------------------------
 
-template <int MODEL, int TQ, int F>
+template <int TQ, int F>
 __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows, const float* states, int W, int d,
-                                              float* qpack, double* cq)
+                                              float* qpack)
 {
     constexpr int KC = 8192 / (TQ * F);       // dimensions per chunk: a 32 KiB tile (d = 400: one or two chunks)
     constexpr int RS = F * KC + 1;            // padded LDS row: the transposed reads hit distinct banks
-    constexpr int TPR = 256 / TQ;             // threads per row for the C_q sums
     __shared__ float tile[TQ * RS];
     __shared__ int srcs[TQ];
     const int qb = blockIdx.x;
@@ -421,8 +419,6 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows
         srcs[t] = j < n_rows ? src_row[j] : -1;
     }
     __syncthreads();
-    const int ci = t / TPR, cr = t % TPR;     // C_q: row and lane within the row
-    double lnb = 0.0;
     float* out = qpack + (int64_t)qb * d * F * TQ;
     for (int k0 = 0; k0 < d; k0 += KC) {
         const int kc = min(KC, d - k0);           // a multiple of 4
@@ -463,33 +459,53 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows
             const int i = o % TQ, f = (o / TQ) % F, kk = o / (TQ * F);
             out[(int64_t)k0 * F * TQ + o] = tile[i * RS + f * KC + kk];
         }
-        if (MODEL == 2 && srcs[ci] >= 0) {
-            for (int kk = cr; kk < kc; kk += TPR) {
-                const double a = tile[ci * RS + kk], b = tile[ci * RS + KC + kk];
-                lnb += lgamma(a) + lgamma(b) - lgamma(a + b);
-            }
-        }
         __syncthreads();
     }
-    if (MODEL == 2) {
-        // the TPR threads of a row are adjacent lanes of one wavefront
-        for (int off = TPR / 2; off > 0; off >>= 1) lnb += __shfl_xor(lnb, off, 64);
-        if (cr == 0) cq[qb * TQ + ci] = lnb;
+}
+
+// BetaE: the query rows row-major, [row][alpha (d) | beta (d)], the A operand
+// of the matrix-core scorer, and C_q = sum_i lnB(alpha_i, beta_i) per row in
+// double precision. One workgroup per row; padding rows are zero with C_q = 0.
+__global__ __launch_bounds__(256) void k_pack_rows(const int32_t* src_row, int n_rows, const float* states, int d,
+                                                   float* qrows, double* cq)
+{
+    __shared__ double part[4];
+    const int j = blockIdx.x;
+    const int t = threadIdx.x;
+    const int src = j < n_rows ? src_row[j] : -1;
+    const float* st = states + (int64_t)(src >= 0 ? src : 0) * 2 * d;
+    float* dst = qrows + (int64_t)j * 2 * d;
+    for (int k = 4 * t; k < 2 * d; k += 4 * 256) {
+        const float4 v = *reinterpret_cast<const float4*>(st + k);
+        *reinterpret_cast<float4*>(dst + k) = src >= 0 ? v : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    double lnb = 0.0;
+    if (src >= 0) {
+        for (int k = t; k < d; k += 256) {
+            const double a = st[k], b = st[d + k];
+            lnb += lgamma(a) + lgamma(b) - lgamma(a + b);
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) lnb += __shfl_xor(lnb, off, 64);
+    if ((t & 63) == 0) part[t >> 6] = lnb;
+    __syncthreads();
+    if (t == 0) cq[j] = (part[0] + part[1]) + (part[2] + part[3]);
 }
 
 void launch_pack(int model, const int32_t* src_row, int n_rows, int n_rows_pad, const float* states,
                  int W, int d, float* qpack, double* cq, hipStream_t s)
 {
     if (n_rows_pad <= 0) return;
-    const int tq = score_tq(model);
+    if (model == 2) {
+        hipLaunchKernelGGL(k_pack_rows, dim3(n_rows_pad), dim3(256), 0, s, src_row, n_rows, states, d, qpack, cq);
+        return;
+    }
+    const int tq = score_row_pad(model);
     const dim3 grid(n_rows_pad / tq);          // n_rows_pad is a multiple of tq
     if (model == 0)
-        hipLaunchKernelGGL((k_pack<0, kTqGqe, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack, cq);
-    else if (model == 1)
-        hipLaunchKernelGGL((k_pack<1, kTqQ2b, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack, cq);
+        hipLaunchKernelGGL((k_pack<kTqGqe, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
     else
-        hipLaunchKernelGGL((k_pack<2, kTqBetae, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack, cq);
+        hipLaunchKernelGGL((k_pack<kTqQ2b, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
 }
 
 }  // namespace kgq

@@ -1,11 +1,12 @@
-// Entity scoring: the "entity similarity query" that the paper times
-// together with operator execution (Experiments, Metrics): every query
-// embedding is scored against every entity.
+// Entity scoring for GQE and Query2Box: the "entity similarity query" that
+// the paper times together with operator execution (Experiments, Metrics):
+// every query embedding is scored against every entity. (BetaE's regrouped
+// KL score is a dense contraction and runs on the matrix cores,
+// k_score_kl.hip.)
 //
 // This is VALU work, not a dense contraction: per (query, entity, dim)
-// triple GQE needs |q - e| accumulated, Query2Box a box distance, BetaE a KL
-// divergence. The kernel is organised like a register-blocked GEMM without
-// the multiply-add:
+// triple GQE needs |q - e| accumulated, Query2Box a box distance. The kernel
+// is organised like a register-blocked GEMM without the multiply-add:
 //   - a lane owns 4 consecutive entities (one 128-bit load per dimension
 //     from the blocked, dimension-major entity table);
 //   - a wavefront owns kTq query rows that are uniform across its lanes, so
@@ -25,12 +26,6 @@
 //           score = gamma - acc1 + (1 - center_reg) * acc2, the exact
 //           regrouping of dist_out + center_reg * dist_in
 //           (t <= o: center_reg * t; t > o: (t - o) + center_reg * o)
-//   BetaE   acc += alpha_q * U_e + beta_q * V_e                          (2 FMA)
-//           score = gamma - (C_q + E_e + acc), the exact regrouping of
-//           sum_i KL(Beta(entity_i) || Beta(query_i)) with
-//           U = psi(a + b) - psi(a), V = psi(a + b) - psi(b),
-//           E_e = sum_i [-lnB(a,b) + a psi(a) + b psi(b) - (a+b) psi(a+b)],
-//           C_q = sum_i lnB(alpha_q, beta_q)  (entity a, b; query alpha_q, beta_q).
 // Union (disjunctive normal form, Eq. 1 of the paper): a union query has two
 // adjacent rows; its score is the max of the two rows' scores.
 #include <algorithm>
@@ -63,10 +58,9 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     if (qb * TQ >= a.n_rows) return;
 
     constexpr int F = (MODEL == 0) ? 1 : 2;      // query fields per row
-    constexpr int EF = (MODEL == 2) ? 2 : 1;     // entity fields per dim
     const int d = a.d;
     const float* __restrict__ qp = a.qpack + (int64_t)qb * d * F * TQ;
-    const float* __restrict__ ep = a.ent + (int64_t)eb * d * EF * kEntBlock + lane * 4;
+    const float* __restrict__ ep = a.ent + (int64_t)eb * d * kEntBlock + lane * 4;
 
     float acc[TQ][4];
     float acc2[(MODEL == 1) ? TQ : 1][4];
@@ -88,38 +82,24 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     // The packed queries are read-only for the whole kernel; reading them
     // through the constant address space keeps them on scalar loads.
     const __attribute__((address_space(4))) float* qc = (const __attribute__((address_space(4))) float*)qp;
-    auto load_e = [&](int k, float4& u, float4& v) {
-        u = *reinterpret_cast<const float4*>(ep + (int64_t)k * EF * kEntBlock);
-        if (MODEL == 2) v = *reinterpret_cast<const float4*>(ep + (int64_t)k * 2 * kEntBlock + kEntBlock);
-    };
+    auto load_e = [&](int k, float4& u) { u = *reinterpret_cast<const float4*>(ep + (int64_t)k * kEntBlock); };
     // rows [R0, R1) of one step
-    auto compute = [&](const float4& eu, const float4& ev, const float* qv, auto R0c, auto R1c) {
+    auto compute = [&](const float4& eu, const float* qv, auto R0c, auto R1c) {
         constexpr int R0 = decltype(R0c)::value, R1 = decltype(R1c)::value;
-        if (MODEL == 2) {
+        const float e4[4] = {eu.x, eu.y, eu.z, eu.w};
 #pragma unroll
-            for (int i = R0; i < R1; ++i) {
-                const float al = qv[i], be = qv[TQ + i];
-                acc[i][0] = fmaf(be, ev.x, fmaf(al, eu.x, acc[i][0]));
-                acc[i][1] = fmaf(be, ev.y, fmaf(al, eu.y, acc[i][1]));
-                acc[i][2] = fmaf(be, ev.z, fmaf(al, eu.z, acc[i][2]));
-                acc[i][3] = fmaf(be, ev.w, fmaf(al, eu.w, acc[i][3]));
-            }
-        } else {
-            const float e4[4] = {eu.x, eu.y, eu.z, eu.w};
+        for (int i = R0; i < R1; ++i) {
+            const float c = qv[i];
+            if (MODEL == 0) {
 #pragma unroll
-            for (int i = R0; i < R1; ++i) {
-                const float c = qv[i];
-                if (MODEL == 0) {
+                for (int j = 0; j < 4; ++j) acc[i][j] += fabsf(e4[j] - c);
+            } else {
+                const float o = qv[TQ + i];
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[i][j] += fabsf(e4[j] - c);
-                } else {
-                    const float o = qv[TQ + i];
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const float t = fabsf(e4[j] - c);
-                        acc[i][j] += t;
-                        acc2[i][j] += __builtin_fminf(t, o);
-                    }
+                for (int j = 0; j < 4; ++j) {
+                    const float t = fabsf(e4[j] - c);
+                    acc[i][j] += t;
+                    acc2[i][j] += __builtin_fminf(t, o);
                 }
             }
         }
@@ -127,38 +107,33 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     using H0 = std::integral_constant<int, 0>;
     using H1 = std::integral_constant<int, TQ / 2>;
     using H2 = std::integral_constant<int, TQ>;
-    float4 ua, va, ub, vb;
+    float4 ua, ub;
     float qa[QN], qb2[QN];
-    load_e(0, ua, va);
+    load_e(0, ua);
 #pragma unroll
     for (int t = 0; t < QN; ++t) qa[t] = qc[t];
     for (int k = 0; k < d; k += 2) {
-        load_e(k + 1, ub, vb);                              // B <- step k + 1
+        load_e(k + 1, ub);                                  // B <- step k + 1
         __builtin_amdgcn_sched_barrier(0);
-        compute(ua, va, qa, H0{}, H1{});
+        compute(ua, qa, H0{}, H1{});
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int t = 0; t < QN; ++t) qb2[t] = qc[(k + 1) * QN + t];
         __builtin_amdgcn_sched_barrier(0);
-        compute(ua, va, qa, H1{}, H2{});
+        compute(ua, qa, H1{}, H2{});
         const int k2 = (k + 2 < d) ? k + 2 : k + 1;         // A <- step k + 2 (last trip: in bounds, unused)
-        load_e(k2, ua, va);
+        load_e(k2, ua);
         __builtin_amdgcn_sched_barrier(0);
-        compute(ub, vb, qb2, H0{}, H1{});
+        compute(ub, qb2, H0{}, H1{});
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int t = 0; t < QN; ++t) qa[t] = qc[k2 * QN + t];
         __builtin_amdgcn_sched_barrier(0);
-        compute(ub, vb, qb2, H1{}, H2{});
+        compute(ub, qb2, H1{}, H2{});
     }
 
     // Epilogue: finish the scores, merge union pairs, store.
     const int64_t e0 = (int64_t)eb * kEntBlock + lane * 4;
-    double ee[4] = {0.0, 0.0, 0.0, 0.0};
-    if (MODEL == 2) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) ee[j] = (e0 + j < a.N) ? a.ee[e0 + j] : 0.0;
-    }
     const int nu_pairs = a.n_union_rows >> 1;
 #pragma unroll
     for (int i = 0; i < TQ; i += 2) {
@@ -170,13 +145,10 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
             if (MODEL == 0) {
                 s0[j] = a.gamma - acc[i][j];
                 s1[j] = a.gamma - acc[i + 1][j];
-            } else if (MODEL == 1) {
+            } else {
                 const float w = 1.0f - a.center_reg;
                 s0[j] = a.gamma - acc[i][j] + w * acc2[i][j];
                 s1[j] = a.gamma - acc[i + 1][j] + w * acc2[i + 1][j];
-            } else {
-                s0[j] = (float)((double)a.gamma - (a.cq[row] + ee[j] + (double)acc[i][j]));
-                s1[j] = (float)((double)a.gamma - (a.cq[row + 1] + ee[j] + (double)acc[i + 1][j]));
             }
         }
         if (row < a.n_union_rows) {
@@ -203,24 +175,26 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
 void launch_score(const ScoreArgs& a, hipStream_t s)
 {
     if (a.n_rows <= 0) return;
-    const int tq = score_tq(a.model);
+    if (a.model == 2) {
+        launch_score_kl(a, s);
+        return;
+    }
+    const int tq = score_row_pad(a.model);
     const int nqb = (a.n_rows + tq - 1) / tq;
     const int nqg = (nqb + 3) / 4;
     const int total = (int)(a.n_blocks * nqg);
     const int per_xcd = (total + 7) / 8;
     // query chunk: an eighth of the query groups, capped at ~2 MiB of packed
     // queries so that a chunk and the entity blocks in flight fit one XCD's L2
-    const int64_t qg_bytes = (int64_t)4 * tq * a.d * (a.model == 0 ? 1 : 2) * 4;
+    const int64_t qg_bytes = (int64_t)4 * tq * a.d * (a.model == 0 ? 1 : 2) * 4;   // packed queries of one group
     int qc = (nqg + 7) / 8;
     const int qc_cap = (int)std::max<int64_t>(1, (int64_t)(2 << 20) / qg_bytes);
     if (qc > qc_cap) qc = qc_cap;
     dim3 grid(per_xcd * 8);
     if (a.model == 0)
         hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
-    else if (a.model == 1)
-        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
     else
-        hipLaunchKernelGGL((k_score<2, kTqBetae>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
+        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
 }
 
 }  // namespace kgq

@@ -81,7 +81,7 @@ struct kgq_handle {
     // derived entity tables
     int64_t n_blocks = 0;
     float* ent_rm = nullptr;      // GQE/Q2B [N x d]; BetaE alpha|beta [N x 2d]
-    float* ent_blk = nullptr;     // GQE/Q2B blocked points; BetaE blocked U|V
+    float* ent_blk = nullptr;     // scoring table: GQE/Q2B blocked points; BetaE row-major U|V
     double* ent_const = nullptr;  // BetaE E_e [n_pad]
     float* rel_o_sp = nullptr;    // Q2B softplus(offset_raw) [R x d]
 
@@ -254,7 +254,7 @@ kgq_status allocate_all(kgq_handle* h)
             }
         }
         ALLOC(L.logits, m_max * d);
-        const int tq = score_tq(c.model);
+        const int tq = score_row_pad(c.model);
         const int64_t prow = ((2 * Bm + tq - 1) / tq) * tq;
         ALLOC(L.qpack, prow * 2 * d);
         ALLOC(L.cq, prow);
@@ -492,7 +492,7 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
         mlp_level(3);
     }
 
-    const int tq = score_tq(c.model);
+    const int tq = score_row_pad(c.model);
     const int n_rows_pad = ((p.n_score_rows + tq - 1) / tq) * tq;
     {
         StageTimer t(h, 3, s);

@@ -8,24 +8,28 @@ namespace kgq {
 
 // ---- data layout constants -------------------------------------------------
 
-// Entities are scored in blocks of 256: 64 lanes of one wavefront, each lane
-// owning 4 consecutive entities. The entity table is stored block by block,
-// dimension-major inside a block: element (e, k) lives at
-//   [e / 256][k][e % 256]            (GQE, Query2Box points)
-//   [e / 256][k][f][e % 256], f=0,1  (BetaE: f=0 U, f=1 V)
-// so that a wavefront reads 1 KiB contiguous per dimension.
+// Entities are scored in blocks of 256 (the table is padded with zeros to a
+// multiple of 256 entities). GQE and Query2Box points are stored block by
+// block, dimension-major inside a block, element (e, k) at
+//   [e / 256][k][e % 256]
+// so that a VALU wavefront (64 lanes x 4 entities) reads 1 KiB contiguous per
+// dimension. BetaE's scoring table is row-major [e][U (d) | V (d)], the B
+// operand of the matrix-core scorer.
 constexpr int kEntBlock = 256;
 
 // Largest k of a top-k request (the selection buffer lives in LDS).
 constexpr int kMaxK = 1024;
 
-// Query rows per wavefront in the scorer (rows are wave-uniform and read
-// through the scalar cache). Packed layout [row_block][k][field][kTq].
+// Query rows per wavefront in the VALU scorers (rows are wave-uniform and
+// read through the scalar cache). Packed layout [row_block][k][field][kTq].
 constexpr int kTqGqe = 16;
 constexpr int kTqQ2b = 8;
-constexpr int kTqBetae = 16;
+// BetaE query rows are packed row-major [row][alpha (d) | beta (d)] and
+// padded to the matrix-core scorer's 64-row tile.
+constexpr int kRowTileBetae = 64;
 
-inline int score_tq(int model) { return model == 0 ? kTqGqe : (model == 1 ? kTqQ2b : kTqBetae); }
+// Scored rows are padded to a multiple of this per model.
+inline int score_row_pad(int model) { return model == 0 ? kTqGqe : (model == 1 ? kTqQ2b : kRowTileBetae); }
 
 // Device error flag bits.
 constexpr int kErrRange = 1;    // an anchor or relation id outside its table
@@ -114,7 +118,8 @@ struct ScoreArgs {
     float gamma, center_reg;
     float* scores; int64_t ld;
 };
-void launch_score(const ScoreArgs& a, hipStream_t s);
+void launch_score(const ScoreArgs& a, hipStream_t s);      // GQE, Query2Box: VALU
+void launch_score_kl(const ScoreArgs& a, hipStream_t s);   // BetaE: matrix cores
 
 // Top-k works on segments of at most kTopkSegment scores per workgroup;
 // longer rows take extra rounds over per-segment candidates.
