@@ -25,8 +25,8 @@ constexpr int kMaxK = 1024;
 constexpr int kTqGqe = 16;
 constexpr int kTqQ2b = 8;
 // BetaE query rows are packed row-major [row][alpha (d) | beta (d)] and
-// padded to the matrix-core scorer's 64-row tile.
-constexpr int kRowTileBetae = 64;
+// padded to the matrix-core scorer's 128-row tile.
+constexpr int kRowTileBetae = 128;
 
 // Scored rows are padded to a multiple of this per model.
 inline int score_row_pad(int model) { return model == 0 ? kTqGqe : (model == 1 ? kTqQ2b : kRowTileBetae); }
