@@ -118,8 +118,12 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out);
  * or a device pointer if src_is_device is non-zero; it is read before the
  * call returns (the call synchronises). Loading a name again replaces it.
  * Derived tables are rebuilt here, not in execute: the blocked entity
- * layout for scoring, Query2Box's softplus offsets, and BetaE's per-entity
- * digamma / log-Beta tables.
+ * layout for scoring, Query2Box's softplus offsets, BetaE's per-entity
+ * digamma / log-Beta tables, and BetaE's first-projection-layer tables
+ * (entity alpha|beta . W1^T [N x 4d] and relation . W1^T + b1 [R x 4d]; the
+ * layer is linear in its input [alpha; beta] + Rel[r], Eq. 4), which are
+ * rebuilt when "entity.alpha_beta", "relation", "proj.w1" or "proj.b1" is
+ * loaded and all four are present.
  * Errors: INVALID_ARG (unknown name, wrong nbytes or dtype, null src), OOM, DEVICE. */
 kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, size_t nbytes,
                            int32_t dtype, int32_t src_is_device);

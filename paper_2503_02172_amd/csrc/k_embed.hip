@@ -396,6 +396,41 @@ void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, c
                        rels, states, ent_ab, rel, n_ent, n_rel, d, x, flag);
 }
 
+// BetaE first-hop projection, first layer, from the precomputed tables: the
+// layer is linear in its input [alpha; beta] + Rel[r], so
+// W1 (E[a] + Rel[r]) + b1 = (E W1^T)[a] + (Rel W1^T + b1)[r].
+__global__ __launch_bounds__(256) void k_betae_proj1(const int32_t* anchor_ref, const int32_t* rel_ref,
+                                                     const int32_t* anchors, const int32_t* rels, const float* pe,
+                                                     const float* pr, int64_t n_ent, int n_rel, int w, float* h1,
+                                                     int* flag)
+{
+    const int m = blockIdx.x;
+    const int64_t a = checked_id(anchors[anchor_ref[m]], n_ent, flag);
+    const int64_t r = checked_id(rels[rel_ref[m]], n_rel, flag);
+    const float* x = pe + a * w;
+    const float* y = pr + r * w;
+    float* dst = h1 + (int64_t)m * w;
+    for (int k = 4 * threadIdx.x; k < w; k += 4 * 256) {      // w = 4d is a multiple of 16
+        const float4 u = *reinterpret_cast<const float4*>(x + k);
+        const float4 v = *reinterpret_cast<const float4*>(y + k);
+        float4 o;
+        o.x = fmaxf(u.x + v.x, 0.f);
+        o.y = fmaxf(u.y + v.y, 0.f);
+        o.z = fmaxf(u.z + v.z, 0.f);
+        o.w = fmaxf(u.w + v.w, 0.f);
+        *reinterpret_cast<float4*>(dst + k) = o;
+    }
+}
+
+void launch_betae_proj1(const int32_t* anchor_ref, const int32_t* rel_ref, int M, const int32_t* anchors,
+                        const int32_t* rels, const float* pe, const float* pr, int64_t n_ent, int n_rel, int w,
+                        float* h1, int* flag, hipStream_t s)
+{
+    if (M <= 0) return;
+    hipLaunchKernelGGL(k_betae_proj1, dim3(M), dim3(256), 0, s, anchor_ref, rel_ref, anchors, rels, pe, pr, n_ent,
+                       n_rel, w, h1, flag);
+}
+
 // ---------------------------------------------------------------------------
 // Query packing for the VALU scorers (GQE, Query2Box): [row_block][k][field][TQ].
 // One workgroup per block of TQ rows transposes through LDS, KC dimensions at

@@ -84,6 +84,12 @@ struct kgq_handle {
     float* ent_blk = nullptr;     // scoring table: GQE/Q2B blocked points; BetaE row-major U|V
     double* ent_const = nullptr;  // BetaE E_e [n_pad]
     float* rel_o_sp = nullptr;    // Q2B softplus(offset_raw) [R x d]
+    // BetaE: the first projection layer is linear in [alpha; beta] + Rel[r],
+    // so for first-hop projections (input = an anchor entity) it splits into
+    // two parameter-only tables, built when their inputs are loaded:
+    float* proj1_ent = nullptr;   // [N x 4d]  entity alpha|beta . W1^T
+    float* proj1_rel = nullptr;   // [R x 4d]  Rel . W1^T + b1
+    bool proj1_ready = false;
 
     // scratch lanes (each sized for max_batch at create): executes on
     // different lanes may run concurrently on different streams
@@ -228,6 +234,8 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(h->ent_rm, N * 2 * d);
         ALLOC(h->ent_blk, n_pad * 2 * d);
         ALLOC(h->ent_const, n_pad);
+        ALLOC(h->proj1_ent, N * 4 * d);
+        ALLOC(h->proj1_rel, (int64_t)c.n_relations * 4 * d);
     } else {
         ALLOC(h->ent_rm, N * d);
         ALLOC(h->ent_blk, n_pad * d);
@@ -451,12 +459,18 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
         auto mlp_level = [&](int l) {
             const int M = (int)p.lv_dst[l].size();
             if (!M) return;
-            {
+            if (l == 0) {
+                // first hop: every input is an anchor entity, so the first
+                // layer is a gather from the precomputed tables
                 StageTimer t(h, 0, s);
-                launch_betae_proj_prep(P + p.off.lv_src[l], P + p.off.lv_anchor[l], P + p.off.lv_rel[l], M, anchors,
-                                       rels, L.states, h->ent_rm, rel, N, n_rel, d, L.xbuf, L.dflag, s);
-            }
-            {
+                launch_betae_proj1(P + p.off.lv_anchor[0], P + p.off.lv_rel[0], M, anchors, rels, h->proj1_ent,
+                                   h->proj1_rel, N, n_rel, 4 * d, L.h1, L.dflag, s);
+            } else {
+                {
+                    StageTimer t(h, 0, s);
+                    launch_betae_proj_prep(P + p.off.lv_src[l], P + p.off.lv_anchor[l], P + p.off.lv_rel[l], M,
+                                           anchors, rels, L.states, h->ent_rm, rel, N, n_rel, d, L.xbuf, L.dflag, s);
+                }
                 StageTimer t(h, 1, s);
                 launch_gemm({L.xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), L.h1, 4 * d, nullptr, M,
                              4 * d, 2 * d, EPI_RELU}, s);
@@ -634,6 +648,25 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on)
     return KGQ_OK;
 }
 
+// BetaE first-layer tables (see proj1_ent / proj1_rel): rebuilt whenever
+// one of their inputs is (re)loaded and all of them are present.
+static kgq_status build_proj1(kgq_handle* h)
+{
+    const kgq_config& c = h->cfg;
+    h->proj1_ready = false;
+    for (const char* n : {"entity.alpha_beta", "relation", "proj.w1", "proj.b1"})
+        if (!h->loaded[n]) return KGQ_OK;
+    const int d = c.dim;
+    launch_gemm({h->ent_rm, 2 * d, h->dparam.at("proj.w1"), 2 * d, nullptr, h->proj1_ent, 4 * d, nullptr,
+                 (int)c.n_entities, 4 * d, 2 * d, EPI_NONE}, nullptr);
+    launch_gemm({h->dparam.at("relation"), 2 * d, h->dparam.at("proj.w1"), 2 * d, h->dparam.at("proj.b1"),
+                 h->proj1_rel, 4 * d, nullptr, c.n_relations, 4 * d, 2 * d, EPI_NONE}, nullptr);
+    HIP_TRY(h, hipGetLastError());
+    HIP_TRY(h, hipStreamSynchronize(nullptr));
+    h->proj1_ready = true;
+    return KGQ_OK;
+}
+
 kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, size_t nbytes, int32_t dtype,
                            int32_t src_is_device)
 {
@@ -668,6 +701,9 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
             HIP_TRY(h, hipStreamSynchronize(nullptr));
         }
         h->loaded[name] = true;
+        if (c.model == KGQ_BETAE && (!std::strcmp(name, "relation") || !std::strcmp(name, "proj.w1") ||
+                                     !std::strcmp(name, "proj.b1")))
+            return build_proj1(h);
         return KGQ_OK;
     }
     // entity table: stage, then build the derived layouts
@@ -688,6 +724,7 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
     (void)hipFree(stage);
     if (e != hipSuccess) return fail(h, KGQ_E_DEVICE, std::string("entity table load: ") + hipGetErrorString(e));
     h->loaded[name] = true;
+    if (c.model == KGQ_BETAE) return build_proj1(h);
     return KGQ_OK;
 }
 

@@ -62,6 +62,13 @@ void launch_betae_entity_prep(const void* src, int src_bf16, int64_t N, int d, i
 
 void launch_softplus(const float* src, float* dst, int64_t n, hipStream_t s);
 
+// BetaE first-hop projections, first layer: h1[m] = ReLU(pe[anchor_m] +
+// pr[rel_m]) with pe = entity alpha|beta . W1^T and pr = Rel . W1^T + b1
+// (rows of width w = 4d). Ids are range-checked like the other gathers.
+void launch_betae_proj1(const int32_t* anchor_ref, const int32_t* rel_ref, int M, const int32_t* anchors,
+                        const int32_t* rels, const float* pe, const float* pr, int64_t n_ent, int n_rel, int w,
+                        float* h1, int* flag, hipStream_t s);
+
 void launch_clear_flag(int* flag, hipStream_t s);
 
 // Checked-mode validation of a batch's ids (and mixed padding).

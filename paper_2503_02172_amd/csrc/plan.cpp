@@ -45,8 +45,10 @@ int plan_launches(const Plan& p, bool topk)
 {
     int n = 0;
     if (p.model == KGQ_BETAE) {
+        // first hop: table gather (first layer) + 2 dense layers; later
+        // levels: prep + 3 dense layers
         for (int l = 0; l < 4; ++l)
-            if (!p.lv_dst[l].empty()) n += 4;          // prep + 3 dense layers
+            if (!p.lv_dst[l].empty()) n += (l == 0) ? 3 : 4;
         if (p.n_groups) n += 4;                         // prep, 2 dense layers, combine
     } else {
         n += 1;                                         // chains

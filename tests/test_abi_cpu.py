@@ -153,6 +153,9 @@ def test_plan_counts_per_structure():
     # BetaE hop levels: 3p -> 1,1,1; up -> 2,2; pi -> 2,1; ip/inp -> post level
     p = plan(kgq.BETAE, [S["3p"]])
     assert (p["level1"], p["level2"], p["level3"], p["post"]) == (1, 1, 1, 0)
+    # first hop: table gather + 2 dense layers; later hops: prep + 3 dense
+    # layers; then pack, score, top-k
+    assert p["launches"] == 3 + 4 + 4 + 3
     p = plan(kgq.BETAE, [S["up"], S["pi"], S["inp"], S["pni"]])
     assert p["level1"] == 2 + 2 + 2 + 2
     assert p["level2"] == 2 + 1 + 0 + 1
