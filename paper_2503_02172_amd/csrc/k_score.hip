@@ -13,12 +13,11 @@
 //     the query values come through the scalar cache into SGPRs and feed the
 //     VALU as scalar operands: no LDS traffic and no cross-lane reduction;
 //   - the 4 wavefronts of a workgroup share one entity block (L1 reuse), and
-//     workgroups are ordered so that each XCD takes a chunk of query groups
-//     (about an eighth of them, at most ~2 MiB of packed queries) and sweeps
-//     every entity block against it: the chunk's queries stay in that XCD's
-//     L2 for the whole sweep and each entity block is fetched once per XCD
-//     (entity-block-major order within an XCD would instead re-fetch every
-//     query once per entity block).
+//     workgroups are ordered in chunks of query groups (~2 MiB of packed
+//     queries), each swept against every entity block: the chunk's queries
+//     stay in L2 for the whole sweep and the entity table is fetched once
+//     per chunk (entity-block-major order would instead re-fetch every query
+//     once per entity block).
 //
 // Per-triple work (one non-packed VALU op each):
 //   GQE     d = e - q;  acc += |d|                                       (2)
@@ -184,12 +183,11 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
     const int nqg = (nqb + 3) / 4;
     const int total = (int)(a.n_blocks * nqg);
     const int per_xcd = (total + 7) / 8;
-    // query chunk: an eighth of the query groups, capped at ~2 MiB of packed
-    // queries so that a chunk and the entity blocks in flight fit one XCD's L2
+    // query chunk: as many query groups as ~2 MiB of packed queries (about
+    // half an XCD's L2); the entity table is streamed once per chunk, and the
+    // XCDs split the global order evenly whatever the chunk size
     const int64_t qg_bytes = (int64_t)4 * tq * a.d * (a.model == 0 ? 1 : 2) * 4;   // packed queries of one group
-    int qc = (nqg + 7) / 8;
-    const int qc_cap = (int)std::max<int64_t>(1, (int64_t)(2 << 20) / qg_bytes);
-    if (qc > qc_cap) qc = qc_cap;
+    const int qc = (int)std::min<int64_t>(nqg, std::max<int64_t>(1, (int64_t)(2 << 20) / qg_bytes));
     dim3 grid(per_xcd * 8);
     if (a.model == 0)
         hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);

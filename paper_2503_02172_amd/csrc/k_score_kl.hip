@@ -16,8 +16,9 @@
 // tiles, 4 x 4 MFMA tiles of 16 x 16 per wavefront. The epilogue adds
 // C_q + E_e in double precision, takes the max over union pairs (two adjacent
 // rows, held by the same lane) and scatters rows to their output positions.
-// Workgroups are ordered so that each XCD takes a chunk of row tiles and
-// sweeps every entity tile: the chunk's query rows stay in that XCD's L2.
+// Workgroups are ordered in chunks of row tiles (about 2 MiB of query rows),
+// each swept against every entity tile: the chunk's rows stay in L2 while
+// the entity table streams past.
 #include <algorithm>
 
 #include "kgq_internal.hpp"
@@ -91,10 +92,12 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
     const int n_nt = (int)((a.N + KL_BN - 1) / KL_BN);
     const int total = n_mt * n_nt;
     const int per_xcd = (total + 7) / 8;
-    // row-tile chunk per XCD: an eighth of the row tiles, at most ~2 MiB of queries
+    // Row-tile chunk: as many row tiles as ~2 MiB of query rows (about half an
+    // XCD's L2). The entity table is streamed once per chunk, and the XCDs
+    // split the global order evenly whatever the chunk size, so larger
+    // chunks cost no balance.
     const int64_t tile_bytes = (int64_t)KL_BM * 2 * a.d * 4;
-    int qchunk = (n_mt + 7) / 8;
-    qchunk = (int)std::min<int64_t>(qchunk, std::max<int64_t>(1, (int64_t)(2 << 20) / tile_bytes));
+    const int qchunk = (int)std::min<int64_t>(n_mt, std::max<int64_t>(1, (int64_t)(2 << 20) / tile_bytes));
     hipLaunchKernelGGL(k_score_kl, dim3(per_xcd * 8), dim3(256), 0, s, a, n_mt, n_nt, qchunk, total, per_xcd);
 }
 
