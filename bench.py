@@ -212,6 +212,48 @@ def traffic_for(kernel_src: str, name: str):
     return rec.get("bytes_per_launch")
 
 
+def batch_sweep(name: str, sizes, reps: int):
+    """Per-query time and device memory against batch size, per structure
+    (the paper's batch-size study, Experiments RQ2), on the tables of one
+    workload. One engine per batch size (max_batch = B): its memory is the
+    handle's whole device footprint (parameters + scratch; execute allocates
+    nothing). Prints one JSON line per batch size."""
+    import torch
+    from paper_2503_02172_amd import kgq, synth
+
+    w = synth.make_workload(name)
+    structures = list(synth.STRUCTURES) if w.model == kgq.BETAE else list(synth.STRUCTURES[:9])
+    dev = torch.device("cuda", 0)
+    for B in sizes:
+        eng = kgq.engine_for(w, max_batch=B)
+        mem = eng.memory()
+        per_q = {}
+        for si, st in enumerate(structures):
+            qb = synth.draw_queries(st, B, w.n_entities, w.n_relations, seed=1000 + si)
+            a = torch.as_tensor(qb.anchors, dtype=torch.int32, device=dev).contiguous()
+            r = torch.as_tensor(qb.relations, dtype=torch.int32, device=dev).contiguous()
+            idx = torch.empty((B, w.k), dtype=torch.int32, device=dev)
+            val = torch.empty((B, w.k), dtype=torch.float32, device=dev)
+            sid = synth.STRUCTURE_ID[st]
+            for _ in range(3):
+                eng.execute_into(sid, B, a, r, w.k, None, idx, val)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                eng.execute_into(sid, B, a, r, w.k, None, idx, val)
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t0) / reps
+            per_q[st] = round(dt / B * 1e3, 6)
+        print(json.dumps({"sweep": name, "batch": B, "ms_per_query": per_q,
+                          "device_bytes": mem["param_bytes"] + mem["scratch_bytes"],
+                          "param_bytes": mem["param_bytes"], "scratch_bytes": mem["scratch_bytes"]}), flush=True)
+        log(f"[sweep] {name} B={B}: memory {(mem['param_bytes'] + mem['scratch_bytes']) / 2**20:.1f} MiB, "
+            f"ms/query {per_q}")
+        eng.close()
+        del eng
+        torch.cuda.empty_cache()
+
+
 def cpu_baseline(name: str, per_structure: int):
     from oracle import oracle as O
     from paper_2503_02172_amd import synth
@@ -247,6 +289,9 @@ def main():
                     help="one execute call per structure batch instead of one mixed call per step")
     ap.add_argument("--streams", type=int, default=2,
                     help="with --per-structure: streams the independent calls are spread over")
+    ap.add_argument("--sweep", default=None, metavar="SIZES",
+                    help="instead of the benchmark: per-query time and device memory against batch size, per "
+                         "structure, on --workload's tables (comma-separated batch sizes, e.g. 1,16,256,1024)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
@@ -255,6 +300,9 @@ def main():
 
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.sweep:
+        batch_sweep(args.workload, [int(x) for x in args.sweep.split(",")], max(args.steps, 1))
+        return
 
     log(f"[bench] preparing {args.workload}")
     merge = not args.per_structure

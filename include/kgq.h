@@ -181,6 +181,16 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
 kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* structure_ids,
                              int32_t* counts);
 
+/* Device memory the handle holds, in bytes (the paper measures peak memory
+ * against batch size; Experiments, RQ2). param_bytes: every parameter and
+ * derived table (entity layouts, softplus offsets, BetaE digamma / log-Beta
+ * and first-layer tables). scratch_bytes: the execute scratch of all
+ * concurrency lanes, sized by max_batch at create. Execute allocates
+ * nothing, so their sum is the handle's peak; transient load staging is not
+ * included. A validation-only handle (device = -1) holds none.
+ * Either output may be NULL. Errors: INVALID_ARG (null handle). */
+kgq_status kgq_memory(const kgq_handle* h, int64_t* param_bytes, int64_t* scratch_bytes);
+
 /* Per-stage timing. kgq_profile_enable takes a bitmask of stages (bit i =
  * stage i; 0 turns profiling off). While a stage's bit is set, execute
  * records a pair of HIP events around every kernel of that stage it

@@ -98,6 +98,8 @@ struct kgq_handle {
     int64_t plan_words = 0;
 
     std::vector<void*> allocations;
+    int64_t bytes_total = 0;      // device bytes allocated by the handle
+    int64_t bytes_params = 0;     // ... of which parameters and derived tables
 
     // profiling
     int prof = 0;                 // bitmask of stages being timed
@@ -178,6 +180,7 @@ kgq_status dev_alloc(kgq_handle* h, void** p, size_t bytes)
                     std::string("hipMalloc(") + std::to_string(bytes) + "): " + hipGetErrorString(e));
     }
     h->allocations.push_back(*p);
+    h->bytes_total += (int64_t)bytes;
     return KGQ_OK;
 }
 
@@ -241,6 +244,7 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(h->ent_blk, n_pad * d);
         if (c.model == KGQ_Q2B) ALLOC(h->rel_o_sp, (int64_t)c.n_relations * d);
     }
+    h->bytes_params = h->bytes_total;   // everything after this is execute scratch
     h->plan_words = plan_image_words((int)Bm);
     const int n_lanes = c.concurrency > 0 ? c.concurrency : 1;
     for (int li = 0; li < n_lanes; ++li) {
@@ -630,6 +634,14 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out)
         return s;
     }
     *out = h.release();
+    return KGQ_OK;
+}
+
+kgq_status kgq_memory(const kgq_handle* h, int64_t* param_bytes, int64_t* scratch_bytes)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (param_bytes) *param_bytes = h->bytes_params;
+    if (scratch_bytes) *scratch_bytes = h->bytes_total - h->bytes_params;
     return KGQ_OK;
 }
 

@@ -70,6 +70,7 @@ def lib() -> ctypes.CDLL:
         "kgq_execute_mixed": ([vp, i32, i32p, vp, vp, i32, vp, vp, vp, vp], i32),
         "kgq_set_checked": ([vp, i32], i32),
         "kgq_describe_plan": ([vp, i32, i32p, i32p], i32),
+        "kgq_memory": ([vp, i64p, i64p], i32),
         "kgq_dense": ([vp, vp, i32, i32, vp, vp, i32, i32, vp, vp], i32),
         "kgq_profile_enable": ([vp, i32], i32),
         "kgq_profile_read": ([vp, i32, dp, i64p], i32),
@@ -220,6 +221,13 @@ class Engine:
         self._check(lib().kgq_describe_plan(self.h, sid.shape[0],
                                             sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), counts))
         return dict(zip(PLAN_FIELDS, list(counts)))
+
+    def memory(self) -> Dict[str, int]:
+        """Device bytes held by the handle: parameters and derived tables,
+        and the execute scratch (sized by max_batch and concurrency)."""
+        pb, sb = ctypes.c_int64(0), ctypes.c_int64(0)
+        self._check(lib().kgq_memory(self.h, ctypes.byref(pb), ctypes.byref(sb)))
+        return {"param_bytes": pb.value, "scratch_bytes": sb.value}
 
     def dense(self, x, w, b=None, act: int = 0, out=None, stream=None):
         """y = act(x @ w.T + b) with the library's MFMA kernel (torch tensors)."""

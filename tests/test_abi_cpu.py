@@ -175,3 +175,8 @@ def test_plan_mixed_c5_shape():
     assert p["union_pairs"] == n["2u"] + n["up"]
     assert p["scored_rows"] == 2048 + n["2u"] + n["up"]
     assert p["post"] == n["ip"] + n["inp"]
+
+
+def test_memory_of_validation_only_handle_is_zero():
+    e = dry()
+    assert e.memory() == {"param_bytes": 0, "scratch_bytes": 0}

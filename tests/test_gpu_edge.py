@@ -209,3 +209,22 @@ def test_gpu_concurrent_streams_match_sequential():
             assert torch.equal(r[key], o[key]), key
     seq.close()
     con.close()
+
+
+def test_gpu_memory_accounting():
+    """Parameters do not depend on max_batch; the execute scratch grows with
+    max_batch and scales with the number of concurrency lanes; BetaE holds the
+    first-layer tables ([N x 4d] + [R x 4d] floats) among its parameters."""
+    from paper_2503_02172_amd import kgq
+    w = synth.make_tiny(O.BETAE, n_ent=300, n_rel=7, dim=16, seed=5)
+    m8 = _eng(w, max_batch=8).memory()
+    m64 = _eng(w, max_batch=64).memory()
+    m8x2 = _eng(w, max_batch=8, concurrency=2).memory()
+    assert m8["param_bytes"] == m64["param_bytes"] == m8x2["param_bytes"] > 0
+    assert m64["scratch_bytes"] > m8["scratch_bytes"] > 0
+    assert m8x2["scratch_bytes"] == 2 * m8["scratch_bytes"]
+    d, N, R = 16, 300, 7
+    assert m8["param_bytes"] >= 4 * (N * 4 * d + R * 4 * d)
+    g = synth.make_tiny(O.GQE, n_ent=300, n_rel=7, dim=16, seed=5)
+    assert _eng(g, max_batch=8).memory()["param_bytes"] < m8["param_bytes"]
+    assert kgq.BETAE == O.BETAE
