@@ -196,20 +196,22 @@ def stage_breakdown(p: Prepared, reps: int = 3):
 
 def traffic_for(kernel_src: str, name: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel source (else None)."""
+    taken on the current kernel source (else (None, None)): FETCH_SIZE and
+    WRITE_SIZE scaled by a plain copy kernel's readings, and the fetch counted
+    by read-request size (plus WRITE_SIZE)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
-        return None
+        return None, None
     try:
         rec = json.load(open(path)).get(name)
     except Exception:
-        return None
+        return None, None
     if not rec:
-        return None
+        return None, None
     h = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
     if rec.get("kernel_sha256") != h:
-        return None
-    return rec.get("bytes_per_launch")
+        return None, None
+    return rec.get("bytes_per_launch"), rec.get("bytes_per_launch_by_request_size")
 
 
 def batch_sweep(name: str, sizes, reps: int):
@@ -321,11 +323,12 @@ def main():
     achieved = ops_per_launch / (avg_launch_ms * 1e-3) if avg_launch_ms > 0 else 0.0
     achieved_busy = total_ops / (busy * 1e-3) if busy > 0 else 0.0
     src = os.path.join(ROOT, "paper_2503_02172_amd", "csrc", "k_score_kl.hip" if p.model == 2 else "k_score.hip")
-    traffic = traffic_for(src, f"score:{args.workload}")
+    traffic, traffic_req = traffic_for(src, f"score:{args.workload}")
     peak, bound, unit = SCORER_PEAK[p.model]
     roofline = {"bound": bound, "kernel": "k_score (entity scorer)" if p.model != 2 else "k_score_kl (entity scorer)",
                 "achieved": round(achieved / 1e12, 3), "peak": round(peak / 1e12, 2),
                 "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+                "traffic_by_request_size": traffic_req,
                 "ops_per_launch": ops_per_launch, "avg_launch_ms": round(avg_launch_ms, 5),
                 "launches": n_launch, "scorer_busy_ms": round(busy, 4),
                 "frac_over_busy_time": round(achieved_busy / peak, 4),
