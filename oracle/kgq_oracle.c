@@ -585,3 +585,63 @@ int kgo_topk(const double* scores, int32_t B, int64_t N, int32_t k, int32_t* idx
     }
     return 0;
 }
+
+
+/* Filtered ranks of answer entities and ranking metrics (the paper reports
+ * MRR; Experiments). For query q with answer set A_q (ids[offsets[q] ..
+ * offsets[q+1]), all distinct), the filtered rank of answer a is
+ *   1 + #{ e in [0, N) : e not in A_q and e ranks before a },
+ * "ranks before" being the ranking order above (higher score first, equal
+ * scores by lower entity index), applied to the float32 scores as given.
+ * Metrics per query over its hard answers H_q (hard[i] != 0; hard == NULL:
+ * every answer is hard), in double precision in answer-list order:
+ *   metrics[4q + 0] = mean over H_q of 1 / rank      (MRR)
+ *   metrics[4q + j] = mean over H_q of [rank <= K_j]  (Hits@1, @3, @10)
+ * A query without hard answers gets NaN metrics. Returns 0, or -1 for an
+ * answer id outside [0, N) or a negative list length. */
+int kgo_rank_answers(const float* scores, int32_t B, int64_t N, const int32_t* offsets, const int32_t* ids,
+                     const int32_t* hard, int32_t* rank, double* metrics, int nthreads)
+{
+    static const int hits_k[3] = {1, 3, 10};
+    for (int32_t q = 0; q < B; ++q) {
+        if (offsets[q + 1] < offsets[q]) return -1;
+        for (int32_t i = offsets[q]; i < offsets[q + 1]; ++i)
+            if (ids[i] < 0 || ids[i] >= N) return -1;
+    }
+    set_threads(nthreads);
+#pragma omp parallel
+    {
+        unsigned char* is_ans = (unsigned char*)calloc((size_t)N, 1);
+#pragma omp for schedule(dynamic, 1)
+        for (int32_t q = 0; q < B; ++q) {
+            const float* row = scores + (size_t)q * N;
+            const int32_t lo = offsets[q], hi = offsets[q + 1];
+            for (int32_t i = lo; i < hi; ++i) is_ans[ids[i]] = 1;
+            for (int32_t i = lo; i < hi; ++i) {
+                const int64_t a = ids[i];
+                int64_t before = 0;
+                for (int64_t e = 0; e < N; ++e)
+                    if (!is_ans[e] && ranks_before(row[e], e, row[a], a)) ++before;
+                rank[i] = (int32_t)(1 + before);
+            }
+            double mrr = 0.0, hk[3] = {0.0, 0.0, 0.0};
+            int64_t nh = 0;
+            for (int32_t i = lo; i < hi; ++i) {
+                if (hard && !hard[i]) continue;
+                ++nh;
+                mrr += 1.0 / (double)rank[i];
+                for (int j = 0; j < 3; ++j) hk[j] += rank[i] <= hits_k[j] ? 1.0 : 0.0;
+            }
+            double* m = metrics + (size_t)4 * q;
+            if (nh == 0) {
+                m[0] = m[1] = m[2] = m[3] = NAN;
+            } else {
+                m[0] = mrr / (double)nh;
+                for (int j = 0; j < 3; ++j) m[1 + j] = hk[j] / (double)nh;
+            }
+            for (int32_t i = lo; i < hi; ++i) is_ans[ids[i]] = 0;
+        }
+        free(is_ans);
+    }
+    return 0;
+}

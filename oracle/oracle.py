@@ -78,6 +78,9 @@ def lib() -> ctypes.CDLL:
         L.kgo_topk.restype = ctypes.c_int
         L.kgo_topk.argtypes = [dp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ip, dp,
                                ctypes.c_int]
+        fp = ctypes.POINTER(ctypes.c_float)
+        L.kgo_rank_answers.restype = ctypes.c_int
+        L.kgo_rank_answers.argtypes = [fp, ctypes.c_int32, ctypes.c_int64, ip, ip, ip, ip, dp, ctypes.c_int]
         L.kgo_max_threads.restype = ctypes.c_int
         L.kgo_max_threads.argtypes = [ctypes.c_int]
         _lib = L
@@ -226,6 +229,26 @@ def topk(scores: np.ndarray, k: int, nthreads: int = 0):
     if rc != 0:
         raise ValueError("bad k")
     return idx, val
+
+
+def rank_answers(scores: np.ndarray, offsets: np.ndarray, ids: np.ndarray, hard: Optional[np.ndarray] = None,
+                 nthreads: int = 0):
+    """Filtered ranks of each query's answers in its float32 score row, and
+    per-query [MRR, Hits@1, Hits@3, Hits@10] over the hard answers (NaN for a
+    query without hard answers). Answer lists are CSR: ids[offsets[q]:offsets[q+1]]."""
+    s = np.ascontiguousarray(scores, np.float32)
+    B, N = s.shape
+    off = np.ascontiguousarray(offsets, np.int32)
+    idv = np.ascontiguousarray(ids, np.int32)
+    assert off.shape == (B + 1,) and off[0] == 0 and off[-1] == idv.shape[0]
+    hv = None if hard is None else np.ascontiguousarray(hard, np.int32)
+    rank = np.empty(idv.shape[0], np.int32)
+    met = np.empty((B, 4), np.float64)
+    rc = lib().kgo_rank_answers(s.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), B, N, _ip(off), _ip(idv),
+                                _ip(hv) if hv is not None else None, _ip(rank), _dp(met), nthreads)
+    if rc != 0:
+        raise ValueError("bad answer lists")
+    return rank, met
 
 
 def digamma(x: float) -> float:
