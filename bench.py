@@ -256,6 +256,41 @@ def batch_sweep(name: str, sizes, reps: int):
         torch.cuda.empty_cache()
 
 
+def rank_bench(p: Prepared, reps: int = 20):
+    """Filtered ranking metrics (kgq_rank_answers) over the workload's whole
+    score matrix, with synthetic answer sets of 1..32 answers per query: mean
+    launch time (HIP events on the stream) and the bytes it must move (the
+    score matrix read once, answer lists read, ranks and metrics written)
+    against the HBM peak."""
+    import torch
+    from paper_2503_02172_amd import synth
+
+    w = p.w
+    sid, B, a, r, idx, val = p.calls[0]
+    if len(p.calls) != 1 or np.ndim(sid) == 0:
+        return None
+    dev = torch.device("cuda", 0)
+    scores = torch.empty((B, w.n_entities), dtype=torch.float32, device=dev)
+    p.eng.execute_mixed_into(sid, a, r, w.k, scores, idx, val)
+    off, ids, hard = synth.draw_answers(B, w.n_entities, seed=77, max_len=32)
+    to, ti, th = (torch.as_tensor(x, device=dev) for x in (off, ids, hard))
+    for _ in range(3):
+        p.eng.rank_answers(scores, to, ti, th)
+    st = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record(st)
+        p.eng.rank_answers(scores, to, ti, th)
+        e1.record(st)
+    torch.cuda.synchronize()
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    nbytes = B * w.n_entities * 4 + (B + 1) * 4 + ids.size * (4 + 4 + 4) + B * 4 * 8
+    return {"kernel": "k_rank_answers", "queries": B, "answers": int(ids.size), "avg_launch_ms": round(ms, 5),
+            "bytes_per_launch": nbytes, "achieved_GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(nbytes / (ms * 1e-3) / HBM_PEAK, 4),
+            "queries_per_s": round(B / (ms * 1e-3), 1)}
+
+
 def cpu_baseline(name: str, per_structure: int):
     from oracle import oracle as O
     from paper_2503_02172_amd import synth
@@ -338,6 +373,10 @@ def main():
         f"{n_launch} launches ({avg_launch_ms:.4f} ms each), {roofline['frac']*100:.1f}% of the {bound} peak")
     stages = stage_breakdown(p)
     log(f"[bench] stage ms per step (one stream, instrumented): {stages}")
+    rank = rank_bench(p)
+    if rank:
+        log(f"[bench] ranking metrics over the score matrix: {rank['avg_launch_ms']} ms, "
+            f"{rank['achieved_GBps']} GB/s ({rank['frac_of_hbm_peak'] * 100:.1f}% of HBM peak)")
 
     others = {}
     if not args.no_others:
@@ -391,6 +430,7 @@ def main():
         "entity_scores_per_s": round(qps * p.w.n_entities, 1),
         "roofline": roofline,
         "stage_ms_per_step": stages,
+        "ranking_metrics": rank,
         "cpu_baseline": cpu,
         "others": others,
     }

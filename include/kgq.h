@@ -181,6 +181,30 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
 kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* structure_ids,
                              int32_t* counts);
 
+/* Filtered ranks of known answers, and ranking metrics per query (the paper
+ * reports MRR; Experiments). For query q, with score row
+ * scores + q * ld (N = cfg.n_entities columns, ld >= N; e.g. the out_scores
+ * of an execute) and answer set A_q = ans_ids[ans_offsets[q] ..
+ * ans_offsets[q + 1]) (distinct entity ids, at most KGQ_MAX_ANSWERS), the
+ * filtered rank of answer a is
+ *   1 + #{ e not in A_q : e ranks before a },
+ * in the library's ranking order (higher score first, equal scores by lower
+ * entity index: the order of the top-k). out_rank[i] receives the rank of
+ * ans_ids[i]. out_metrics (or NULL) receives per query, over its hard
+ * answers (ans_hard[i] != 0; ans_hard == NULL: every answer is hard), in
+ * double precision: [MRR = mean 1/rank, Hits@1, Hits@3, Hits@10]; NaN for a
+ * query without hard answers. All arrays are device memory; the call
+ * enqueues on stream and returns.
+ * Errors: INVALID_ARG (null pointers, batch < 1, ld < N), NO_DEVICE; in
+ * checked mode the call synchronises and reports OUT_OF_RANGE for an answer
+ * id outside [0, N) and INVALID_ARG for a list longer than KGQ_MAX_ANSWERS
+ * or of negative length (such ranks are -1, such metrics NaN, in either
+ * mode). */
+#define KGQ_MAX_ANSWERS 1024
+kgq_status kgq_rank_answers(kgq_handle* h, int32_t batch, const float* scores, int64_t ld,
+                            const int32_t* ans_offsets, const int32_t* ans_ids, const int32_t* ans_hard,
+                            int32_t* out_rank, double* out_metrics, void* stream);
+
 /* Device memory the handle holds, in bytes (the paper measures peak memory
  * against batch size; Experiments, RQ2). param_bytes: every parameter and
  * derived table (entity layouts, softplus offsets, BetaE digamma / log-Beta

@@ -637,6 +637,37 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out)
     return KGQ_OK;
 }
 
+kgq_status kgq_rank_answers(kgq_handle* h, int32_t batch, const float* scores, int64_t ld,
+                            const int32_t* ans_offsets, const int32_t* ans_ids, const int32_t* ans_hard,
+                            int32_t* out_rank, double* out_metrics, void* stream)
+{
+    static_assert(KGQ_MAX_ANSWERS == kMaxAnswers, "answer-list limit");
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (!scores || !ans_offsets || !ans_ids || !out_rank)
+        return fail(h, KGQ_E_INVALID_ARG, "scores, ans_offsets, ans_ids and out_rank must not be NULL");
+    if (batch < 1) return fail(h, KGQ_E_INVALID_ARG, "batch must be >= 1");
+    const int64_t N = h->cfg.n_entities;
+    if (ld < N) return fail(h, KGQ_E_INVALID_ARG, "ld must be >= n_entities");
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    HIP_TRY(h, hipSetDevice(h->cfg.device));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    Lane* L = nullptr;
+    kgq_status st = acquire_lane(h, s, &L);
+    if (st != KGQ_OK) return st;
+    if (h->checked) launch_clear_flag(L->dflag, s);
+    launch_rank_answers(scores, ld, N, batch, ans_offsets, ans_ids, ans_hard, out_rank, out_metrics, L->dflag, s);
+    HIP_TRY(h, hipGetLastError());
+    L->done_live = hipEventRecord(L->done, s) == hipSuccess;
+    if (h->checked) {
+        HIP_TRY(h, hipMemcpyAsync(L->hflag, L->dflag, sizeof(int), hipMemcpyDeviceToHost, s));
+        HIP_TRY(h, hipStreamSynchronize(s));
+        if (*L->hflag & kErrAnswers)
+            return fail(h, KGQ_E_INVALID_ARG, "an answer list is longer than KGQ_MAX_ANSWERS or of negative length");
+        if (*L->hflag & kErrRange) return fail(h, KGQ_E_OUT_OF_RANGE, "an answer id is out of range");
+    }
+    return KGQ_OK;
+}
+
 kgq_status kgq_memory(const kgq_handle* h, int64_t* param_bytes, int64_t* scratch_bytes)
 {
     if (!h) return KGQ_E_INVALID_ARG;

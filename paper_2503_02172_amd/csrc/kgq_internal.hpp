@@ -34,6 +34,10 @@ inline int score_row_pad(int model) { return model == 0 ? kTqGqe : (model == 1 ?
 // Device error flag bits.
 constexpr int kErrRange = 1;    // an anchor or relation id outside its table
 constexpr int kErrPadding = 2;  // a mixed-batch unused slot that is not -1
+constexpr int kErrAnswers = 4;  // an answer list longer than kMaxAnswers or of negative length
+
+// Largest answer list of one query for the ranking metrics (sorted in LDS).
+constexpr int kMaxAnswers = 1024;
 
 enum Epilogue { EPI_NONE = 0, EPI_RELU = 1, EPI_BETA_REG = 2 };
 
@@ -125,6 +129,11 @@ struct ScoreArgs {
     float gamma, center_reg;
     float* scores; int64_t ld;
 };
+// Filtered answer ranks and per-query [MRR, Hits@1, @3, @10] (k_rank.hip).
+void launch_rank_answers(const float* scores, int64_t ld, int64_t N, int batch, const int32_t* off,
+                         const int32_t* ids, const int32_t* hard, int32_t* rank, double* metrics, int* flag,
+                         hipStream_t s);
+
 void launch_score(const ScoreArgs& a, hipStream_t s);      // GQE, Query2Box: VALU
 void launch_score_kl(const ScoreArgs& a, hipStream_t s);   // BetaE: matrix cores
 

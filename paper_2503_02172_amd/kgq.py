@@ -71,6 +71,7 @@ def lib() -> ctypes.CDLL:
         "kgq_set_checked": ([vp, i32], i32),
         "kgq_describe_plan": ([vp, i32, i32p, i32p], i32),
         "kgq_memory": ([vp, i64p, i64p], i32),
+        "kgq_rank_answers": ([vp, i32, vp, i64, vp, vp, vp, vp, vp, vp], i32),
         "kgq_dense": ([vp, vp, i32, i32, vp, vp, i32, i32, vp, vp], i32),
         "kgq_profile_enable": ([vp, i32], i32),
         "kgq_profile_read": ([vp, i32, dp, i64p], i32),
@@ -221,6 +222,27 @@ class Engine:
         self._check(lib().kgq_describe_plan(self.h, sid.shape[0],
                                             sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), counts))
         return dict(zip(PLAN_FIELDS, list(counts)))
+
+    def rank_answers(self, scores, offsets, ids, hard=None, metrics: bool = True, stream=None):
+        """Filtered ranks of each query's answers (CSR: ids[offsets[q]:offsets[q+1]])
+        in its score row, and per-query [MRR, Hits@1, Hits@3, Hits@10] over
+        the hard answers (torch tensors on the device; scores [B x ld] float32,
+        offsets [B+1] / ids / hard int32). Returns (ranks int32, metrics
+        float64 [B x 4] or None), enqueued on the current stream."""
+        import torch
+        if scores.dtype != torch.float32 or scores.dim() != 2 or scores.stride(1) != 1:
+            raise TypeError("rank_answers: scores must be a float32 [B x ld] tensor with unit column stride")
+        for name, t in (("offsets", offsets), ("ids", ids), ("hard", hard)):
+            if t is not None and (t.dtype != torch.int32 or not t.is_contiguous() or not t.is_cuda):
+                raise TypeError(f"rank_answers: {name} must be a contiguous int32 CUDA tensor")
+        B = scores.shape[0]
+        if offsets.numel() != B + 1:
+            raise ValueError("rank_answers: offsets must have B + 1 entries")
+        ranks = torch.empty(ids.numel(), dtype=torch.int32, device=scores.device)
+        met = torch.empty((B, 4), dtype=torch.float64, device=scores.device) if metrics else None
+        self._check(lib().kgq_rank_answers(self.h, B, _ptr(scores), scores.stride(0), _ptr(offsets), _ptr(ids),
+                                           _ptr(hard), _ptr(ranks), _ptr(met), _stream(stream)))
+        return ranks, met
 
     def memory(self) -> Dict[str, int]:
         """Device bytes held by the handle: parameters and derived tables,

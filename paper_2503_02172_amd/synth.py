@@ -246,3 +246,23 @@ def draw_queries(structure: str, n: int, n_ent: int, n_rel: int, seed: int) -> Q
 def draw_mixed(structures: List[str], n: int, n_ent: int, n_rel: int, seed: int) -> QueryBatch:
     rng = np.random.Generator(np.random.PCG64(seed))
     return _draw_mixed(rng, structures, n, n_ent, n_rel)
+
+
+def draw_answers(B: int, N: int, seed: int, max_len: int = 32, hard_share: float = 0.6,
+                 special: Optional[Dict[int, int]] = None):
+    """Synthetic answer sets for the ranking metrics (the datasets' answer
+    sets are not available): query q gets n_q distinct entity ids, n_q
+    uniform in [1, max_len] (special: {q: n_q} overrides, n_q may be 0), each
+    marked hard with probability hard_share. Returns CSR (offsets [B+1],
+    ids, hard) as int32 arrays."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    sizes = rng.integers(1, max_len + 1, size=B)
+    for q, n in (special or {}).items():
+        sizes[q] = n
+    off = np.zeros(B + 1, np.int64)
+    off[1:] = np.cumsum(sizes)
+    ids = np.empty(int(off[-1]), np.int32)
+    for q in range(B):
+        ids[off[q]:off[q + 1]] = rng.choice(N, size=int(sizes[q]), replace=False)
+    hard = (rng.random(ids.shape[0]) < hard_share).astype(np.int32)
+    return off.astype(np.int32), ids, hard

@@ -180,3 +180,16 @@ def test_plan_mixed_c5_shape():
 def test_memory_of_validation_only_handle_is_zero():
     e = dry()
     assert e.memory() == {"param_bytes": 0, "scratch_bytes": 0}
+
+
+def test_rank_answers_validation():
+    import ctypes
+    e = dry(N=50)
+    L = kgq.lib()
+    p = ctypes.c_void_p(16)
+    bad = [(0, p, 50, p, p, p), (2, None, 50, p, p, p), (2, p, 49, p, p, p), (2, p, 50, None, p, p),
+           (2, p, 50, p, None, p), (2, p, 50, p, p, None)]
+    for batch, sc, ld, off, ids, out in bad:
+        assert L.kgq_rank_answers(e.h, batch, sc, ld, off, ids, None, out, None, None) == -1
+    assert L.kgq_rank_answers(e.h, 2, p, 50, p, p, None, p, None, None) == -5
+    assert L.kgq_rank_answers(None, 2, p, 50, p, p, None, p, None, None) == -1
