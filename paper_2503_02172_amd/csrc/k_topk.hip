@@ -171,8 +171,12 @@ __global__ __launch_bounds__(NT) void k_topk(TopkArgs a)
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int64_t row = blockIdx.y;
-    const int64_t seg0 = (int64_t)blockIdx.x * a.seg_len;     // first element of this segment
+    // one-dimensional grid, row-major over (row, segment): gridDim.y is too
+    // small for large batches
+    const int64_t nseg = (a.N + a.seg_len - 1) / a.seg_len;
+    const int64_t row = (int64_t)blockIdx.x / nseg;
+    const int64_t seg = (int64_t)blockIdx.x - row * nseg;
+    const int64_t seg0 = seg * a.seg_len;                      // first element of this segment
     int64_t n = a.N - seg0;
     if (n > a.seg_len) n = a.seg_len;
     const float* __restrict__ sr = a.scores + row * a.ld + seg0;
@@ -413,7 +417,7 @@ __global__ __launch_bounds__(NT) void k_topk(TopkArgs a)
 
     // order the n_sel selected entries and write the first k; a short
     // segment pads its list to a.k entries with -inf
-    const int64_t orow = row * a.out_rows_per_row + blockIdx.x;
+    const int64_t orow = row * a.out_rows_per_row + seg;
     for (int p = k + tid; p < a.k; p += TK_THREADS) {
         a.out_idx[orow * a.out_ld + p] = 0x7FFFFFFF;
         a.out_score[orow * a.out_ld + p] = -__builtin_inff();
@@ -449,7 +453,8 @@ __global__ __launch_bounds__(NT) void k_topk(TopkArgs a)
 
 static void launch_segments(const TopkArgs& a, hipStream_t s)
 {
-    dim3 grid((unsigned)((a.N + a.seg_len - 1) / a.seg_len), (unsigned)a.n_rows);
+    // (rows x segments fits 32 bits: the score buffer holds rows x N floats)
+    dim3 grid((unsigned)(((a.N + a.seg_len - 1) / a.seg_len) * a.n_rows));
     // 256 threads with up to 64 keys each for long segments; short ones
     // (k-candidate lists of later rounds) use as many keys per thread as fit
     const int64_t per = (a.seg_len + 255) / 256;

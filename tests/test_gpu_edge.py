@@ -228,3 +228,21 @@ def test_gpu_memory_accounting():
     g = synth.make_tiny(O.GQE, n_ent=300, n_rel=7, dim=16, seed=5)
     assert _eng(g, max_batch=8).memory()["param_bytes"] < m8["param_bytes"]
     assert kgq.BETAE == O.BETAE
+
+
+def test_gpu_batch_above_65535():
+    """A batch larger than the 65,535 limit of a grid's y and z dimensions:
+    every kernel launches over a one-dimensional grid (or y within limits)."""
+    import torch
+    B = 70000
+    w = synth.make_tiny(O.GQE, n_ent=37, n_rel=5, dim=8, seed=21)
+    eng = _eng(w, max_batch=B)
+    q = synth.draw_queries("2i", B, 37, 5, seed=22)
+    out = eng.execute(S["2i"], q.anchors, q.relations, k=5, scores=True)
+    torch.cuda.synchronize()
+    m = O.Model(O.GQE, w.params, w.gamma)
+    rows = np.r_[0:50, B - 50:B, 30000:30050]
+    ref = m.scores(np.full(rows.size, S["2i"]), q.anchors[rows], q.relations[rows])
+    check_scores(out["scores"].cpu().numpy()[rows], ref, w.rtol, w.gamma, "2i B=70000")
+    check_topk(out["idx"].cpu().numpy()[rows], out["score"].cpu().numpy()[rows], ref, 5, w.rtol, w.gamma,
+               "2i B=70000")
