@@ -9,6 +9,8 @@
 // fill the chip, and measured faster than 64 x 128 or 128 x 128 tiles there.
 // The epilogue adds the bias, applies the activation and stores each row m at
 // C + map(m) * ldc.
+#include <algorithm>
+
 #include "kgq_internal.hpp"
 #include "mfma_tile.hpp"
 
@@ -44,10 +46,69 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
     }
 }
 
+// Split-K for small M: with few 64 x 64 output tiles the K loop is a latency
+// chain (one stage of 32 per LDS round trip) on a handful of compute units.
+// Each of S workgroups per tile runs a K slice and writes its partial tile;
+// a second kernel adds the S partials in slice order (deterministic), then
+// the bias and activation, and stores through the row map.
+__global__ __launch_bounds__(256) void k_gemm_part(GemmArgs g, int kc)
+{
+    __shared__ float sm[GemmTile::SMEM];
+    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+    const int k0 = blockIdx.z * kc;
+    const int kn = min(kc, g.K - k0);
+    v4f acc[GemmTile::TM][GemmTile::TN];
+    GemmTile::run(g.A + k0, g.lda, g.M, g.W + k0, g.ldw, g.N, kn, m0, n0, sm, acc);
+    float* part = g.ws + (int64_t)blockIdx.z * g.M * g.N;
+#pragma unroll
+    for (int j = 0; j < GemmTile::TN; ++j) {
+        const int n = n0 + GemmTile::col_of(j);
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int i = 0; i < GemmTile::TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + GemmTile::row_of(i) + r;
+                if (m < g.M) part[(int64_t)m * g.N + n] = acc[i][j][r];
+            }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_gemm_reduce(GemmArgs g, int splits)
+{
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= (int64_t)g.M * g.N) return;
+    const int m = (int)(t / g.N), n = (int)(t - (int64_t)m * g.N);
+    float v = 0.f;
+    for (int z = 0; z < splits; ++z) v += g.ws[(int64_t)z * g.M * g.N + t];
+    v += g.bias ? g.bias[n] : 0.f;
+    if (g.epi == EPI_RELU) v = v > 0.f ? v : 0.f;
+    else if (g.epi == EPI_BETA_REG) v = fminf(fmaxf(v + 1.0f, 0.05f), 1e9f);
+    const int64_t row = g.c_rowmap ? (int64_t)g.c_rowmap[m] : (int64_t)m;
+    g.C[row * g.ldc + n] = v;
+}
+
 void launch_gemm(const GemmArgs& g, hipStream_t s)
 {
     if (g.M <= 0 || g.N <= 0) return;
-    dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
+    const int tn = (g.N + 63) / 64, tm = (g.M + 63) / 64;
+    const int tiles = tn * tm;
+    // split K when the tiles alone leave most of the chip idle, keeping at
+    // least two stages (64 of K) per slice
+    int splits = 1;
+    if (g.ws && tiles < 128 && g.K >= 128) {
+        splits = std::min({16, (256 + tiles - 1) / tiles, g.K / 64});
+        while (splits > 1 && (int64_t)splits * g.M * g.N > g.ws_elems) --splits;
+    }
+    if (splits > 1) {
+        const int kc = (((g.K + splits - 1) / splits) + 31) / 32 * 32;   // slice: a multiple of the 32-wide stage
+        const int z = (g.K + kc - 1) / kc;
+        hipLaunchKernelGGL(k_gemm_part, dim3(tn, tm, z), dim3(256), 0, s, g, kc);
+        const int64_t total = (int64_t)g.M * g.N;
+        hipLaunchKernelGGL(k_gemm_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, g, z);
+        return;
+    }
+    dim3 grid(tn, tm);
     hipLaunchKernelGGL(k_gemm, grid, dim3(256), 0, s, g);
 }
 

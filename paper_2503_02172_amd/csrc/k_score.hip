@@ -35,7 +35,8 @@
 namespace kgq {
 
 template <int MODEL, int TQ>
-__global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk, int total_wg, int wg_per_xcd)
+__global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk, int total_wg, int wg_per_xcd,
+                                               int kslice)
 {
     // XCD-aware mapping: workgroup b runs on XCD b % 8 (round-robin dispatch),
     // so XCD x executes positions [x * wg_per_xcd, (x + 1) * wg_per_xcd) of
@@ -57,9 +58,13 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     if (qb * TQ >= a.n_rows) return;
 
     constexpr int F = (MODEL == 0) ? 1 : 2;      // query fields per row
-    const int d = a.d;
-    const float* __restrict__ qp = a.qpack + (int64_t)qb * d * F * TQ;
-    const float* __restrict__ ep = a.ent + (int64_t)eb * d * kEntBlock + lane * 4;
+    // Small batches split the dimensions over blockIdx.y: slice z covers
+    // [z * kslice, z * kslice + d) (kslice and d multiples of 4) and writes
+    // its raw accumulators to a.part instead of scores.
+    const int k_begin = blockIdx.y * kslice;
+    const int d = min(kslice, a.d - k_begin);
+    const float* __restrict__ qp = a.qpack + ((int64_t)qb * a.d + k_begin) * F * TQ;
+    const float* __restrict__ ep = a.ent + ((int64_t)eb * a.d + k_begin) * kEntBlock + lane * 4;
 
     float acc[TQ][4];
     float acc2[(MODEL == 1) ? TQ : 1][4];
@@ -133,6 +138,21 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
 
     // Epilogue: finish the scores, merge union pairs, store.
     const int64_t e0 = (int64_t)eb * kEntBlock + lane * 4;
+    if (a.part) {
+        // split-d: raw accumulators of this slice, [slice][field][row][entity]
+        // over the padded rows (nqg * 4 * TQ) and entities (n_blocks * 256)
+        const int64_t n_pad = a.n_blocks * kEntBlock, rows_pad = (int64_t)nqg * 4 * TQ;
+        float* pz = a.part + (int64_t)blockIdx.y * F * rows_pad * n_pad;
+#pragma unroll
+        for (int i = 0; i < TQ; ++i) {
+            const int64_t row = (int64_t)qb * TQ + i;
+            *reinterpret_cast<float4*>(pz + row * n_pad + e0) = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+            if (MODEL == 1)
+                *reinterpret_cast<float4*>(pz + (rows_pad + row) * n_pad + e0) =
+                    make_float4(acc2[i][0], acc2[i][1], acc2[i][2], acc2[i][3]);
+        }
+        return;
+    }
     const int nu_pairs = a.n_union_rows >> 1;
 #pragma unroll
     for (int i = 0; i < TQ; i += 2) {
@@ -171,6 +191,35 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     }
 }
 
+// Split-d finish: output row o (union pairs first, then single rows, the
+// order of out_dest) and entity e: sum the slices in order, score, max over
+// a union pair, store.
+template <int MODEL>
+__global__ __launch_bounds__(256) void k_score_sum(ScoreArgs a, int splits, int64_t rows_pad, int n_out)
+{
+    constexpr int F = (MODEL == 0) ? 1 : 2;
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= (int64_t)n_out * a.N) return;
+    const int o = (int)(t / a.N);
+    const int64_t e = t - (int64_t)o * a.N;
+    const int64_t n_pad = a.n_blocks * kEntBlock;
+    const int nu_pairs = a.n_union_rows >> 1;
+    const int r0 = o < nu_pairs ? 2 * o : a.n_union_rows + (o - nu_pairs);
+    const int nr = o < nu_pairs ? 2 : 1;
+    float best = 0.f;
+    for (int u = 0; u < nr; ++u) {
+        float s1 = 0.f, s2 = 0.f;
+        for (int z = 0; z < splits; ++z) {
+            const float* pz = a.part + (int64_t)z * F * rows_pad * n_pad;
+            s1 += pz[(int64_t)(r0 + u) * n_pad + e];
+            if (MODEL == 1) s2 += pz[(rows_pad + r0 + u) * n_pad + e];
+        }
+        const float v = MODEL == 0 ? a.gamma - s1 : a.gamma - s1 + (1.0f - a.center_reg) * s2;
+        best = u == 0 ? v : fmaxf(best, v);
+    }
+    a.scores[(int64_t)a.out_dest[o] * a.ld + e] = best;
+}
+
 void launch_score(const ScoreArgs& a, hipStream_t s)
 {
     if (a.n_rows <= 0) return;
@@ -188,11 +237,39 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
     // XCDs split the global order evenly whatever the chunk size
     const int64_t qg_bytes = (int64_t)4 * tq * a.d * (a.model == 0 ? 1 : 2) * 4;   // packed queries of one group
     const int qc = (int)std::min<int64_t>(nqg, std::max<int64_t>(1, (int64_t)(2 << 20) / qg_bytes));
-    dim3 grid(per_xcd * 8);
+    // Small batches: with fewer than 128 workgroups the dimension loop is a
+    // latency chain on a few compute units, so the dimensions are split over
+    // up to 16 slices (each at least 16 dimensions) whose partials fit the
+    // lane's workspace; a second kernel sums them.
+    const int F = a.model == 0 ? 1 : 2;
+    const int64_t rows_pad = (int64_t)nqg * 4 * tq, n_pad = a.n_blocks * kEntBlock;
+    int splits = 1;
+    if (a.part && total < 128 && a.d >= 32) {
+        splits = std::min({16, (512 + total - 1) / total, a.d / 16});
+        while (splits > 1 && (int64_t)splits * F * rows_pad * n_pad > a.part_elems) --splits;
+    }
+    ScoreArgs b = a;
+    int kslice = a.d, z = 1;
+    if (splits > 1) {
+        kslice = (((a.d + splits - 1) / splits) + 3) / 4 * 4;
+        z = (a.d + kslice - 1) / kslice;
+    } else {
+        b.part = nullptr;
+    }
+    dim3 grid(per_xcd * 8, z);
     if (a.model == 0)
-        hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
+        hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
     else
-        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, a, nqg, qc, total, per_xcd);
+        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+    if (z > 1) {
+        const int n_out = (a.n_union_rows >> 1) + (a.n_rows - a.n_union_rows);
+        const int64_t tot = (int64_t)n_out * a.N;
+        const dim3 g2((unsigned)((tot + 255) / 256));
+        if (a.model == 0)
+            hipLaunchKernelGGL((k_score_sum<0>), g2, dim3(256), 0, s, b, z, rows_pad, n_out);
+        else
+            hipLaunchKernelGGL((k_score_sum<1>), g2, dim3(256), 0, s, b, z, rows_pad, n_out);
+    }
 }
 
 }  // namespace kgq

@@ -26,13 +26,15 @@
 
 namespace kgq {
 
-constexpr int KL_BM = kRowTileBetae;   // query rows per workgroup tile (128)
-constexpr int KL_BN = 128;             // entities per workgroup tile
-using KlTile = MfmaTile<KL_BM, KL_BN>;
-
+// Workgroup tiles: 128 rows x 128 entities, or 64 x 64 for small batches,
+// where the larger tile leaves the chip underfilled and each workgroup's K
+// loop is a latency chain. Query rows are padded to 128 (kRowTileBetae), a
+// multiple of both.
+template <int KL_BM, int KL_BN>
 __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int n_nt, int qchunk, int total,
                                                      int per_xcd)
 {
+    using KlTile = MfmaTile<KL_BM, KL_BN>;
     __shared__ float sm[KlTile::SMEM];
 
     // XCD-aware order (workgroup b runs on XCD b % 8): chunks of qchunk row
@@ -48,7 +50,7 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     const int mt = c * qchunk + (r - nt * qcc);
     const int m0 = mt * KL_BM, n0 = nt * KL_BN;
 
-    // Query rows are padded (with zeros) to a multiple of KL_BM and entity
+    // Query rows are padded (with zeros) to a multiple of 128 and entity
     // rows to a multiple of 256, so the whole tile is inside both buffers.
     const int K = 2 * a.d;
     v4f acc[KlTile::TM][KlTile::TN];
@@ -85,20 +87,29 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     }
 }
 
-void launch_score_kl(const ScoreArgs& a, hipStream_t s)
+template <int BM, int BN>
+static void launch_tiles(const ScoreArgs& a, hipStream_t s)
 {
-    if (a.n_rows <= 0) return;
-    const int n_mt = (a.n_rows + KL_BM - 1) / KL_BM;
-    const int n_nt = (int)((a.N + KL_BN - 1) / KL_BN);
+    const int n_mt = (a.n_rows + BM - 1) / BM;
+    const int n_nt = (int)((a.N + BN - 1) / BN);
     const int total = n_mt * n_nt;
     const int per_xcd = (total + 7) / 8;
     // Row-tile chunk: as many row tiles as ~2 MiB of query rows (about half an
     // XCD's L2). The entity table is streamed once per chunk, and the XCDs
     // split the global order evenly whatever the chunk size, so larger
     // chunks cost no balance.
-    const int64_t tile_bytes = (int64_t)KL_BM * 2 * a.d * 4;
+    const int64_t tile_bytes = (int64_t)BM * 2 * a.d * 4;
     const int qchunk = (int)std::min<int64_t>(n_mt, std::max<int64_t>(1, (int64_t)(2 << 20) / tile_bytes));
-    hipLaunchKernelGGL(k_score_kl, dim3(per_xcd * 8), dim3(256), 0, s, a, n_mt, n_nt, qchunk, total, per_xcd);
+    hipLaunchKernelGGL((k_score_kl<BM, BN>), dim3(per_xcd * 8), dim3(256), 0, s, a, n_mt, n_nt, qchunk, total,
+                       per_xcd);
+}
+
+void launch_score_kl(const ScoreArgs& a, hipStream_t s)
+{
+    if (a.n_rows <= 0) return;
+    const int64_t big_tiles = (int64_t)((a.n_rows + 127) / 128) * ((a.N + 127) / 128);
+    if (big_tiles < 512) launch_tiles<64, 64>(a, s);
+    else launch_tiles<kRowTileBetae, 128>(a, s);
 }
 
 }  // namespace kgq

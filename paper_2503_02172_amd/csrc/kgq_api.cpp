@@ -47,6 +47,10 @@ struct Lane {
     float* qpack = nullptr;
     double* cq = nullptr;
     float* scores = nullptr;
+    float* gemm_ws = nullptr;     // split-K partials of small dense layers
+    int64_t gemm_ws_elems = 0;
+    float* score_ws = nullptr;    // split-d partials of the VALU scorers at small batches
+    int64_t score_ws_elems = 0;
     int32_t* cand_idx[2] = {nullptr, nullptr};   // top-k candidates of long rows
     float* cand_score[2] = {nullptr, nullptr};
     int* dflag = nullptr;
@@ -271,6 +275,19 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(L.qpack, prow * 2 * d);
         ALLOC(L.cq, prow);
         ALLOC(L.scores, Bm * N);
+        // split-K runs only while a layer has fewer than 128 output tiles of
+        // 64 x 64, so 16 slices of it stay below 16 x 128 x 4096 floats
+        {
+            const int64_t n_max = c.model == KGQ_BETAE ? 4 * d : d;
+            L.gemm_ws_elems = std::min<int64_t>(16 * 3 * Bm * n_max, (int64_t)16 * 128 * 4096);
+            ALLOC(L.gemm_ws, L.gemm_ws_elems);
+        }
+        if (c.model != KGQ_BETAE) {
+            // 16 slices x 2 fields x the padded rows of a small batch x the
+            // padded entities, at most 8 Mi floats (fewer slices if tight)
+            L.score_ws_elems = std::min<int64_t>(16 * 2 * (2 * Bm + 64) * n_pad, (int64_t)8 << 20);
+            ALLOC(L.score_ws, L.score_ws_elems);
+        }
         const int64_t ncand = topk_scratch_elems(Bm, N, kMaxK);
         for (int i = 0; i < 2; ++i) {
             ALLOC(L.cand_idx[i], ncand);
@@ -409,6 +426,12 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
     const int64_t N = c.n_entities;
     const int n_rel = c.n_relations;
     auto param = [&](const char* n) { return h->dparam.at(n); };
+    // dense layers of this execute may split K over the lane's workspace
+    auto gemm = [&](GemmArgs g) {
+        g.ws = L.gemm_ws;
+        g.ws_elems = L.gemm_ws_elems;
+        launch_gemm(g, s);
+    };
 
     if (h->checked) {
         launch_clear_flag(L.dflag, s);
@@ -430,18 +453,18 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
             const std::string pre = q2b ? "inter.center." : "inter.";
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({L.states, W, param((pre + "w1").c_str()), d, param((pre + "b1").c_str()), L.h1, d,
-                             nullptr, p.n_int_in, d, d, EPI_RELU}, s);
+                gemm({L.states, W, param((pre + "w1").c_str()), d, param((pre + "b1").c_str()), L.h1, d,
+                             nullptr, p.n_int_in, d, d, EPI_RELU});
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({L.h1, d, param((pre + "w2").c_str()), d, param((pre + "b2").c_str()), L.logits, d,
-                             nullptr, p.n_int_in, d, d, EPI_NONE}, s);
+                gemm({L.h1, d, param((pre + "w2").c_str()), d, param((pre + "b2").c_str()), L.logits, d,
+                             nullptr, p.n_int_in, d, d, EPI_NONE});
             }
             if (q2b) {
                 StageTimer t(h, 1, s);
-                launch_gemm({L.states + d, W, param("inter.offset.w1"), d, param("inter.offset.b1"), L.zfeat, d,
-                             nullptr, p.n_int_in, d, d, EPI_RELU}, s);
+                gemm({L.states + d, W, param("inter.offset.w1"), d, param("inter.offset.b1"), L.zfeat, d,
+                             nullptr, p.n_int_in, d, d, EPI_RELU});
             }
             {
                 StageTimer t(h, 2, s);
@@ -451,8 +474,8 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
             if (q2b) {
                 {
                     StageTimer t(h, 1, s);
-                    launch_gemm({L.zmean, d, param("inter.offset.w2"), d, param("inter.offset.b2"), L.gate, d,
-                                 nullptr, p.n_groups, d, d, EPI_NONE}, s);
+                    gemm({L.zmean, d, param("inter.offset.w2"), d, param("inter.offset.b2"), L.gate, d,
+                                 nullptr, p.n_groups, d, d, EPI_NONE});
                 }
                 StageTimer t(h, 2, s);
                 launch_combine_offset(g, L.states, W, L.gate, rels, h->rel_o_sp, n_rel, d, L.states, L.dflag, s);
@@ -476,17 +499,17 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
                                            anchors, rels, L.states, h->ent_rm, rel, N, n_rel, d, L.xbuf, L.dflag, s);
                 }
                 StageTimer t(h, 1, s);
-                launch_gemm({L.xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), L.h1, 4 * d, nullptr, M,
-                             4 * d, 2 * d, EPI_RELU}, s);
+                gemm({L.xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), L.h1, 4 * d, nullptr, M,
+                             4 * d, 2 * d, EPI_RELU});
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({L.h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), L.h2, 4 * d, nullptr, M,
-                             4 * d, 4 * d, EPI_RELU}, s);
+                gemm({L.h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), L.h2, 4 * d, nullptr, M,
+                             4 * d, 4 * d, EPI_RELU});
             }
             StageTimer t(h, 1, s);
-            launch_gemm({L.h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), L.states, 2 * d,
-                         P + p.off.lv_dst[l], M, 2 * d, 4 * d, EPI_BETA_REG}, s);
+            gemm({L.h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), L.states, 2 * d,
+                         P + p.off.lv_dst[l], M, 2 * d, 4 * d, EPI_BETA_REG});
         };
         for (int l = 0; l < 3; ++l) mlp_level(l);
         if (p.n_groups) {
@@ -496,13 +519,13 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({L.xbuf, 2 * d, param("inter.w1"), 2 * d, param("inter.b1"), L.h1, 2 * d, nullptr,
-                             p.n_int_in, 2 * d, 2 * d, EPI_RELU}, s);
+                gemm({L.xbuf, 2 * d, param("inter.w1"), 2 * d, param("inter.b1"), L.h1, 2 * d, nullptr,
+                             p.n_int_in, 2 * d, 2 * d, EPI_RELU});
             }
             {
                 StageTimer t(h, 1, s);
-                launch_gemm({L.h1, 2 * d, param("inter.w2"), 2 * d, param("inter.b2"), L.logits, d, nullptr,
-                             p.n_int_in, d, 2 * d, EPI_NONE}, s);
+                gemm({L.h1, 2 * d, param("inter.w2"), 2 * d, param("inter.b2"), L.logits, d, nullptr,
+                             p.n_int_in, d, 2 * d, EPI_NONE});
             }
             StageTimer t(h, 2, s);
             launch_betae_combine(g, L.xbuf, L.logits, d, L.states, s);
@@ -521,6 +544,8 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
         StageTimer t(h, 4, s);
         ScoreArgs a{c.model, L.qpack, h->ent_blk, L.cq, h->ent_const, P + p.off.out_dest, p.n_score_rows,
                     p.n_union_rows, d, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
+        a.part = L.score_ws;
+        a.part_elems = L.score_ws_elems;
         launch_score(a, s);
     }
     if (out_idx) {

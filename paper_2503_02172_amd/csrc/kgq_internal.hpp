@@ -51,6 +51,8 @@ struct GemmArgs {
     const int32_t* c_rowmap;           // nullptr = identity
     int M, N, K;                       // K % 4 == 0, A/W 16-byte aligned rows
     int epi;
+    float* ws = nullptr;               // split-K partials for small M (nullptr: never split)
+    int64_t ws_elems = 0;
 };
 void launch_gemm(const GemmArgs& g, hipStream_t s);
 
@@ -128,6 +130,8 @@ struct ScoreArgs {
     int64_t N, n_blocks;
     float gamma, center_reg;
     float* scores; int64_t ld;
+    float* part = nullptr;             // GQE / Query2Box split-d partials for small batches
+    int64_t part_elems = 0;            //   (nullptr: never split)
 };
 // Filtered answer ranks and per-query [MRR, Hits@1, @3, @10] (k_rank.hip).
 void launch_rank_answers(const float* scores, int64_t ld, int64_t N, int batch, const int32_t* off,
