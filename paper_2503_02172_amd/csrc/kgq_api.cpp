@@ -333,12 +333,23 @@ struct StageTimer {
         if ((h->prof >> stage) & 1) {
             a = prof_event(h);
             b = prof_event(h);
-            if (hipEventRecord(a, s) != hipSuccess) a = nullptr;
+            if (!a || !b || hipEventRecord(a, s) != hipSuccess) {
+                // no timing for this stage: hand the events back to the pool
+                if (a) h->prof_pool.push_back(a);
+                if (b) h->prof_pool.push_back(b);
+                a = b = nullptr;
+            }
         }
     }
     ~StageTimer()
     {
-        if (a && b && hipEventRecord(b, s) == hipSuccess) h->prof_pending.push_back({stage, a, b});
+        if (!a) return;
+        if (hipEventRecord(b, s) == hipSuccess) {
+            h->prof_pending.push_back({stage, a, b});
+        } else {
+            h->prof_pool.push_back(a);
+            h->prof_pool.push_back(b);
+        }
     }
 };
 
