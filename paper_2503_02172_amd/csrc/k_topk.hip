@@ -151,8 +151,12 @@ __device__ __forceinline__ void block_exclusive_prefix(int* cnt, int tid)
     }
 }
 
+// At 64 keys per thread the kernel needs 99 VGPRs, three above the budget
+// of five wavefronts per SIMD; asking for five (a few values spill to
+// scratch) keeps five rows in flight per compute unit instead of four:
+// measured 110 -> 100 us over 4,608 rows of 14,505 scores.
 template <int NT, int KPT>
-__global__ __launch_bounds__(NT) void k_topk(TopkArgs a)
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(5))) void k_topk(TopkArgs a)
 {
     constexpr int TK_THREADS = NT;
     constexpr int TK_WAVES = NT / 64;
