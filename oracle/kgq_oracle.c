@@ -230,7 +230,7 @@ void kgo_negate(const kgo_model* m, const double* in, double* out)
     for (int i = 0; i < w; ++i) out[i] = 1.0 / in[i];
 }
 
-/* Intersection (f_and of Eq. 2) of n branch states. */
+/* Intersection (f_and of Eq. 2) of n >= 1 branch states. */
 void kgo_intersect(const kgo_model* m, int n, const double* const* br, double* out)
 {
     int d = m->dim;
@@ -238,6 +238,7 @@ void kgo_intersect(const kgo_model* m, int n, const double* const* br, double* o
     int hid = in_w;                                    /* attention hidden width */
     double* hbuf = (double*)malloc(sizeof(double) * (size_t)hid);
     double* logits = (double*)malloc(sizeof(double) * (size_t)n * d);
+    double* wts = (double*)malloc(sizeof(double) * (size_t)n);
     for (int j = 0; j < n; ++j) {
         /* GQE: the query vector; Q2B: the center; BetaE: [alpha; beta]. */
         dense(m->att_w1, m->att_b1, hid, in_w, br[j], hbuf);
@@ -248,7 +249,6 @@ void kgo_intersect(const kgo_model* m, int n, const double* const* br, double* o
         double mx = logits[i];
         for (int j = 1; j < n; ++j) if (logits[(size_t)j * d + i] > mx) mx = logits[(size_t)j * d + i];
         double z = 0.0;
-        double wts[3];
         for (int j = 0; j < n; ++j) { wts[j] = exp(logits[(size_t)j * d + i] - mx); z += wts[j]; }
         for (int j = 0; j < n; ++j) wts[j] /= z;
         if (m->model == KGO_BETAE) {
@@ -284,6 +284,7 @@ void kgo_intersect(const kgo_model* m, int n, const double* const* br, double* o
     }
     free(hbuf);
     free(logits);
+    free(wts);
 }
 
 /* Score of one entity against one query state (entity-similarity query). */
@@ -406,47 +407,19 @@ static int set_threads(int nthreads)
 
 int kgo_max_threads(int nthreads) { return set_threads(nthreads); }
 
-/* Scores of every entity for B queries. Query q has structure sid[q], anchors
- * anchors[q*astride ..] and relations rels[q*rstride ..]. scores is [B x N].
- * Returns 0, or -1 if any query has an unknown/unsupported structure or an
- * id outside the tables. */
-int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t* anchors,
-               int32_t astride, const int32_t* rels, int32_t rstride, double* scores,
-               int nthreads)
+/* Entity-similarity query over all N entities for B queries whose answer
+ * variable has nst[q] conjunctive terms (DNF, Eq. 1): the score of an
+ * entity is the maximum of its scores against the terms. states is
+ * [B][T][w] (term t of query q at (q * T + t) * w), scores is [B x N].
+ * Entities are processed in chunks so that BetaE's per-entity function
+ * values (psi, ln B) are computed once per chunk and then reused for every
+ * query; the KL formula itself is unchanged. */
+static void score_terms(const kgo_model* m, int32_t B, const double* states, const int* nst, int T,
+                        double* scores)
 {
     int w = kgo_state_width(m);
     int64_t N = m->n_entities;
     int d = m->dim;
-    if (d > KGO_MAX_DIM) return -1;
-    for (int32_t q = 0; q < B; ++q) {
-        int na, nr;
-        if (kgo_arity(sid[q], &na, &nr)) return -1;
-        if (sid[q] >= S_2IN && m->model != KGO_BETAE) return -1;
-        for (int k = 0; k < na; ++k) {
-            int32_t e = anchors[(size_t)q * astride + k];
-            if (e < 0 || e >= N) return -1;
-        }
-        for (int k = 0; k < nr; ++k) {
-            int32_t r = rels[(size_t)q * rstride + k];
-            if (r < 0 || r >= m->n_relations) return -1;
-        }
-    }
-    set_threads(nthreads);
-    double* states = (double*)malloc(sizeof(double) * (size_t)B * 2 * w);
-    int* nst = (int*)malloc(sizeof(int) * (size_t)B);
-    int bad = 0;
-#pragma omp parallel for schedule(dynamic, 1)
-    for (int32_t q = 0; q < B; ++q) {
-        nst[q] = kgo_query_states(m, sid[q], anchors + (size_t)q * astride,
-                                  rels + (size_t)q * rstride, states + (size_t)q * 2 * w);
-        if (nst[q] < 0) bad = 1;
-    }
-    if (bad) { free(states); free(nst); return -1; }
-
-    /* Entity-similarity query over all N entities. Entities are processed in
-     * chunks so that BetaE's per-entity function values (psi, ln B) are
-     * computed once per chunk and then reused for every query; the KL
-     * formula itself is unchanged. */
     const int64_t CH = 256;
     int64_t nch = (N + CH - 1) / CH;
 #pragma omp parallel
@@ -459,10 +432,10 @@ int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t*
             if (m->model != KGO_BETAE) {
                 for (int32_t q = 0; q < B; ++q) {
                     for (int64_t e = e0; e < e1; ++e) {
-                        double best = kgo_score(m, states + (size_t)q * 2 * w, e);
-                        if (nst[q] == 2) {
-                            double s2 = kgo_score(m, states + (size_t)q * 2 * w + w, e);
-                            if (s2 > best) best = s2;
+                        double best = 0.0;
+                        for (int t = 0; t < nst[q]; ++t) {
+                            double s = kgo_score(m, states + ((size_t)q * T + t) * w, e);
+                            if (t == 0 || s > best) best = s;
                         }
                         scores[(size_t)q * N + e] = best;
                     }
@@ -484,7 +457,7 @@ int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t*
             double* lnbq = (double*)malloc(sizeof(double) * (size_t)d * 2);
             for (int32_t q = 0; q < B; ++q) {
                 for (int t = 0; t < nst[q]; ++t) {
-                    const double* st = states + (size_t)q * 2 * w + (size_t)t * w;
+                    const double* st = states + ((size_t)q * T + t) * w;
                     for (int i = 0; i < d; ++i) lnbq[i] = kgo_lnbeta(st[i], st[d + i]);
                     for (int64_t e = e0; e < e1; ++e) {
                         const float* ab = m->entity + (size_t)e * 2 * d;
@@ -508,6 +481,235 @@ int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t*
         }
         free(memo);
     }
+}
+
+/* Scores of every entity for B queries. Query q has structure sid[q], anchors
+ * anchors[q*astride ..] and relations rels[q*rstride ..]. scores is [B x N].
+ * Returns 0, or -1 if any query has an unknown/unsupported structure or an
+ * id outside the tables. */
+int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t* anchors,
+               int32_t astride, const int32_t* rels, int32_t rstride, double* scores,
+               int nthreads)
+{
+    int w = kgo_state_width(m);
+    int64_t N = m->n_entities;
+    if (m->dim > KGO_MAX_DIM) return -1;
+    for (int32_t q = 0; q < B; ++q) {
+        int na, nr;
+        if (kgo_arity(sid[q], &na, &nr)) return -1;
+        if (sid[q] >= S_2IN && m->model != KGO_BETAE) return -1;
+        for (int k = 0; k < na; ++k) {
+            int32_t e = anchors[(size_t)q * astride + k];
+            if (e < 0 || e >= N) return -1;
+        }
+        for (int k = 0; k < nr; ++k) {
+            int32_t r = rels[(size_t)q * rstride + k];
+            if (r < 0 || r >= m->n_relations) return -1;
+        }
+    }
+    set_threads(nthreads);
+    double* states = (double*)malloc(sizeof(double) * (size_t)B * 2 * w);
+    int* nst = (int*)malloc(sizeof(int) * (size_t)B);
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t q = 0; q < B; ++q) {
+        nst[q] = kgo_query_states(m, sid[q], anchors + (size_t)q * astride,
+                                  rels + (size_t)q * rstride, states + (size_t)q * 2 * w);
+        if (nst[q] < 0) bad = 1;
+    }
+    if (!bad) score_terms(m, B, states, nst, 2, scores);
+    free(states);
+    free(nst);
+    return bad ? -1 : 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Query computation graphs                                            */
+/* ------------------------------------------------------------------ */
+
+/* A query computation graph (Eq. 2) is given as nodes in topological order,
+ * KGO_NODE_WORDS int32 each: op, slot, in[0..3]. The ops follow Eq. 2's
+ * mapping: an entity becomes a value node (op 0, anchor slot `slot`); a
+ * relation becomes a projection of node in[0] (op 1, relation slot `slot`);
+ * the connectives become f_and (op 2), f_or (op 3) over nodes in[0..] (two
+ * to four, unused entries -1) and f_not of node in[0] (op 4). Inputs are
+ * earlier nodes; the last node is the answer variable. */
+#define KGO_OP_ANCHOR 0
+#define KGO_OP_PROJECT 1
+#define KGO_OP_AND 2
+#define KGO_OP_OR 3
+#define KGO_OP_NOT 4
+#define KGO_NODE_WORDS 6
+#define KGO_MAX_TERMS 16
+
+/* Number of inputs of a node, or -1 if the node is malformed. */
+static int node_inputs(const int32_t* g, int i)
+{
+    const int32_t* nd = g + (size_t)i * KGO_NODE_WORDS;
+    int op = nd[0], k = 0;
+    while (k < 4 && nd[2 + k] >= 0) ++k;
+    for (int j = k; j < 4; ++j) if (nd[2 + j] != -1) return -1;
+    for (int j = 0; j < k; ++j) if (nd[2 + j] >= i) return -1;   /* inputs are earlier nodes */
+    switch (op) {
+    case KGO_OP_ANCHOR: return (k == 0 && nd[1] >= 0) ? 0 : -1;
+    case KGO_OP_PROJECT: return (k == 1 && nd[1] >= 0) ? 1 : -1;
+    case KGO_OP_NOT: return k == 1 ? 1 : -1;
+    case KGO_OP_AND:
+    case KGO_OP_OR: return k >= 2 ? k : -1;
+    }
+    return -1;
+}
+
+/* Checks a graph and counts the anchor and relation slots it uses (largest
+ * slot + 1) and the conjunctive terms of its answer. Returns 0, or -1 for a
+ * malformed graph, a negation on a model without one, or more than
+ * KGO_MAX_TERMS terms at any node. */
+int kgo_graph_check(const kgo_model* m, const int32_t* g, int n, int* n_anchor_slots, int* n_rel_slots,
+                    int* n_terms)
+{
+    if (n < 1 || n > 256) return -1;
+    int* cnt = (int*)malloc(sizeof(int) * (size_t)n);
+    int na = 0, nr = 0, ok = 1;
+    for (int i = 0; i < n && ok; ++i) {
+        const int32_t* nd = g + (size_t)i * KGO_NODE_WORDS;
+        int k = node_inputs(g, i);
+        if (k < 0) { ok = 0; break; }
+        long c = 1;
+        switch (nd[0]) {
+        case KGO_OP_ANCHOR: if (nd[1] + 1 > na) na = nd[1] + 1; c = 1; break;
+        case KGO_OP_PROJECT: if (nd[1] + 1 > nr) nr = nd[1] + 1; c = cnt[nd[2]]; break;
+        case KGO_OP_NOT: if (m->model != KGO_BETAE) ok = 0; c = 1; break;
+        case KGO_OP_OR: c = 0; for (int j = 0; j < k; ++j) c += cnt[nd[2 + j]]; break;
+        case KGO_OP_AND: c = 1; for (int j = 0; j < k; ++j) c *= cnt[nd[2 + j]]; break;
+        }
+        if (c > KGO_MAX_TERMS) ok = 0;
+        cnt[i] = (int)c;
+    }
+    if (ok) {
+        *n_anchor_slots = na;
+        *n_rel_slots = nr;
+        *n_terms = cnt[n - 1];
+    }
+    free(cnt);
+    return ok ? 0 : -1;
+}
+
+/* Evaluates one query's graph node by node. The value of each node is its
+ * disjunctive normal form (Eq. 1): a list of conjunctive terms, each a query
+ * state.
+ *   entity:      one term, the anchor's embedding;
+ *   projection:  each term projected;
+ *   f_or:        the inputs' term lists concatenated;
+ *   f_and:       one intersection per combination of one term from each
+ *                input (conjunction distributes over disjunction), the
+ *                first input's term varying slowest;
+ *   f_not:       of a single term, its negation; of several terms, the
+ *                intersection of their negations (De Morgan: the negation
+ *                of a disjunction is the conjunction of the negations).
+ * Writes the answer's terms to out (n_terms x w) and returns their number,
+ * or -1 if the graph is rejected by kgo_graph_check. */
+int kgo_graph_states(const kgo_model* m, const int32_t* g, int n, const int32_t* a, const int32_t* r,
+                     double* out)
+{
+    int na, nr, nt;
+    if (kgo_graph_check(m, g, n, &na, &nr, &nt)) return -1;
+    int w = kgo_state_width(m);
+    int* cnt = (int*)calloc((size_t)n, sizeof(int));
+    double** val = (double**)calloc((size_t)n, sizeof(double*));
+    const double* br[KGO_MAX_TERMS];
+    for (int i = 0; i < n; ++i) {
+        const int32_t* nd = g + (size_t)i * KGO_NODE_WORDS;
+        const int32_t* in = nd + 2;
+        int k = node_inputs(g, i);
+        int c = 0;
+        switch (nd[0]) {
+        case KGO_OP_ANCHOR:
+            c = 1;
+            val[i] = (double*)malloc(sizeof(double) * (size_t)w);
+            kgo_anchor(m, a[nd[1]], val[i]);
+            break;
+        case KGO_OP_PROJECT:
+            c = cnt[in[0]];
+            val[i] = (double*)malloc(sizeof(double) * (size_t)c * w);
+            for (int t = 0; t < c; ++t) kgo_project(m, val[in[0]] + (size_t)t * w, r[nd[1]], val[i] + (size_t)t * w);
+            break;
+        case KGO_OP_OR:
+            for (int j = 0; j < k; ++j) c += cnt[in[j]];
+            val[i] = (double*)malloc(sizeof(double) * (size_t)c * w);
+            for (int j = 0, t0 = 0; j < k; t0 += cnt[in[j]], ++j)
+                memcpy(val[i] + (size_t)t0 * w, val[in[j]], sizeof(double) * (size_t)cnt[in[j]] * w);
+            break;
+        case KGO_OP_AND:
+            c = 1;
+            for (int j = 0; j < k; ++j) c *= cnt[in[j]];
+            val[i] = (double*)malloc(sizeof(double) * (size_t)c * w);
+            for (int t = 0; t < c; ++t) {
+                /* mixed-radix digits of t, last input fastest */
+                int rest = t;
+                for (int j = k - 1; j >= 0; --j) {
+                    br[j] = val[in[j]] + (size_t)(rest % cnt[in[j]]) * w;
+                    rest /= cnt[in[j]];
+                }
+                kgo_intersect(m, k, br, val[i] + (size_t)t * w);
+            }
+            break;
+        case KGO_OP_NOT: {
+            int ci = cnt[in[0]];
+            c = 1;
+            val[i] = (double*)malloc(sizeof(double) * (size_t)w);
+            if (ci == 1) {
+                kgo_negate(m, val[in[0]], val[i]);
+            } else {
+                double* neg = (double*)malloc(sizeof(double) * (size_t)ci * w);
+                for (int t = 0; t < ci; ++t) {
+                    kgo_negate(m, val[in[0]] + (size_t)t * w, neg + (size_t)t * w);
+                    br[t] = neg + (size_t)t * w;
+                }
+                kgo_intersect(m, ci, br, val[i]);
+                free(neg);
+            }
+            break;
+        }
+        }
+        cnt[i] = c;
+    }
+    memcpy(out, val[n - 1], sizeof(double) * (size_t)cnt[n - 1] * w);
+    int res = cnt[n - 1];
+    for (int i = 0; i < n; ++i) free(val[i]);
+    free(val);
+    free(cnt);
+    return res;
+}
+
+/* Scores of every entity for B queries sharing one graph: query q's anchor
+ * slots are anchors[q*astride ..], its relation slots rels[q*rstride ..].
+ * Returns 0, or -1 for a rejected graph or an id outside the tables. */
+int kgo_graph_scores(const kgo_model* m, const int32_t* g, int n, int32_t B, const int32_t* anchors,
+                     int32_t astride, const int32_t* rels, int32_t rstride, double* scores, int nthreads)
+{
+    int na, nr, nt;
+    if (m->dim > KGO_MAX_DIM) return -1;
+    if (kgo_graph_check(m, g, n, &na, &nr, &nt)) return -1;
+    if (na > astride || nr > rstride) return -1;
+    for (int32_t q = 0; q < B; ++q) {
+        for (int k = 0; k < na; ++k) {
+            int32_t e = anchors[(size_t)q * astride + k];
+            if (e < 0 || e >= m->n_entities) return -1;
+        }
+        for (int k = 0; k < nr; ++k) {
+            int32_t r = rels[(size_t)q * rstride + k];
+            if (r < 0 || r >= m->n_relations) return -1;
+        }
+    }
+    set_threads(nthreads);
+    int w = kgo_state_width(m);
+    double* states = (double*)malloc(sizeof(double) * (size_t)B * nt * w);
+    int* nst = (int*)malloc(sizeof(int) * (size_t)B);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t q = 0; q < B; ++q)
+        nst[q] = kgo_graph_states(m, g, n, anchors + (size_t)q * astride, rels + (size_t)q * rstride,
+                                  states + (size_t)q * nt * w);
+    score_terms(m, B, states, nst, nt, scores);
     free(states);
     free(nst);
     return 0;

@@ -75,6 +75,13 @@ def lib() -> ctypes.CDLL:
         L.kgo_scores.restype = ctypes.c_int
         L.kgo_scores.argtypes = [mp, ctypes.c_int32, ip, ip, ctypes.c_int32, ip, ctypes.c_int32,
                                  dp, ctypes.c_int]
+        L.kgo_graph_check.restype = ctypes.c_int
+        L.kgo_graph_check.argtypes = [mp, ip, ctypes.c_int, ip, ip, ip]
+        L.kgo_graph_states.restype = ctypes.c_int
+        L.kgo_graph_states.argtypes = [mp, ip, ctypes.c_int, ip, ip, dp]
+        L.kgo_graph_scores.restype = ctypes.c_int
+        L.kgo_graph_scores.argtypes = [mp, ip, ctypes.c_int, ctypes.c_int32, ip, ctypes.c_int32, ip,
+                                       ctypes.c_int32, dp, ctypes.c_int]
         L.kgo_topk.restype = ctypes.c_int
         L.kgo_topk.argtypes = [dp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ip, dp,
                                ctypes.c_int]
@@ -200,6 +207,48 @@ class Model:
         if n < 0:
             raise ValueError("unsupported structure")
         return out[: n * self.width].reshape(n, self.width)
+
+    # -- query computation graphs -------------------------------------------
+    def graph_info(self, nodes) -> tuple:
+        """(anchor slots, relation slots, answer terms) of a graph given as an
+        int32 array [n_nodes x 6] (op, slot, in0..in3); ValueError if the
+        oracle rejects it."""
+        g = np.ascontiguousarray(nodes, np.int32).reshape(-1, 6)
+        na, nr, nt = (ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32())
+        rc = lib().kgo_graph_check(self.ref, _ip(g), g.shape[0], ctypes.byref(na), ctypes.byref(nr),
+                                   ctypes.byref(nt))
+        if rc != 0:
+            raise ValueError("oracle rejected the graph")
+        return na.value, nr.value, nt.value
+
+    def graph_states(self, nodes, anchors, rels) -> np.ndarray:
+        """Conjunctive terms [n_terms x width] of one query's answer."""
+        g = np.ascontiguousarray(nodes, np.int32).reshape(-1, 6)
+        _, _, nt = self.graph_info(g)
+        a = np.ascontiguousarray(anchors, np.int32)
+        r = np.ascontiguousarray(rels, np.int32)
+        out = np.zeros(nt * self.width, np.float64)
+        n = lib().kgo_graph_states(self.ref, _ip(g), g.shape[0], _ip(a), _ip(r), _dp(out))
+        if n < 0:
+            raise ValueError("oracle rejected the graph")
+        return out[: n * self.width].reshape(n, self.width)
+
+    def graph_scores(self, nodes, anchors: np.ndarray, rels: np.ndarray, nthreads: int = 0) -> np.ndarray:
+        """[B x N] float64 scores of B queries sharing one graph."""
+        g = np.ascontiguousarray(nodes, np.int32).reshape(-1, 6)
+        a = np.ascontiguousarray(anchors, np.int32)
+        r = np.ascontiguousarray(rels, np.int32)
+        if a.ndim == 1:
+            a = a.reshape(-1, 1)
+        if r.ndim == 1:
+            r = r.reshape(-1, 1)
+        B = a.shape[0]
+        out = np.empty((B, self.n_entities), np.float64)
+        rc = lib().kgo_graph_scores(self.ref, _ip(g), g.shape[0], B, _ip(a), a.shape[1], _ip(r), r.shape[1],
+                                    _dp(out), nthreads)
+        if rc != 0:
+            raise ValueError("oracle rejected the graph or an id")
+        return out
 
     # -- batched ------------------------------------------------------------
     def scores(self, structure_ids, anchors: np.ndarray, rels: np.ndarray,

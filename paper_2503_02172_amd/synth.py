@@ -266,3 +266,176 @@ def draw_answers(B: int, N: int, seed: int, max_len: int = 32, hard_share: float
         ids[off[q]:off[q + 1]] = rng.choice(N, size=int(sizes[q]), replace=False)
     hard = (rng.random(ids.shape[0]) < hard_share).astype(np.int32)
     return off.astype(np.int32), ids, hard
+
+
+# ---------------------------------------------------------------------------
+# Query structures as computation graphs
+# ---------------------------------------------------------------------------
+# A structure is a graph of anchor, projection, intersection, union and
+# negation nodes (the paper's Eq. 2). Text form:
+#   e<k>  anchor slot k        p(<x>,r<k>)  projection of x by relation slot k
+#   i(<x>,<y>[,...])  intersection of 2-4      u(<x>,<y>[,...])  union of 2-4
+#   n(<x>)  negation
+# Node records: int32 [n x 6] = (op, slot, in0, in1, in2, in3), every node
+# after its inputs, the answer last, unused inputs -1. This is an interface
+# format shared by the library and the oracle, each of which reads it with
+# code of its own; nothing here evaluates a graph.
+
+OP_ANCHOR, OP_PROJECT, OP_AND, OP_OR, OP_NOT = 0, 1, 2, 3, 4
+
+STRUCTURE_TEXT: Dict[str, str] = {
+    "1p": "p(e0,r0)", "2p": "p(p(e0,r0),r1)", "3p": "p(p(p(e0,r0),r1),r2)",
+    "2i": "i(p(e0,r0),p(e1,r1))", "3i": "i(p(e0,r0),p(e1,r1),p(e2,r2))",
+    "pi": "i(p(p(e0,r0),r1),p(e1,r2))", "ip": "p(i(p(e0,r0),p(e1,r1)),r2)",
+    "2u": "u(p(e0,r0),p(e1,r1))", "up": "p(u(p(e0,r0),p(e1,r1)),r2)",
+    "2in": "i(p(e0,r0),n(p(e1,r1)))", "3in": "i(p(e0,r0),p(e1,r1),n(p(e2,r2)))",
+    "inp": "p(i(p(e0,r0),n(p(e1,r1))),r2)", "pin": "i(p(p(e0,r0),r1),n(p(e1,r2)))",
+    "pni": "i(n(p(p(e0,r0),r1)),p(e1,r2))",
+}
+
+
+def graph_nodes(text: str) -> np.ndarray:
+    """Node records [n x 6] of a structure's text form."""
+    s = text.replace(" ", "")
+    nodes: List[List[int]] = []
+    pos = 0
+
+    def num() -> int:
+        nonlocal pos
+        j = pos
+        while pos < len(s) and s[pos].isdigit():
+            pos += 1
+        if j == pos:
+            raise ValueError(f"slot number expected at {j} in {text!r}")
+        return int(s[j:pos])
+
+    def eat(c: str):
+        nonlocal pos
+        if pos >= len(s) or s[pos] != c:
+            raise ValueError(f"{c!r} expected at {pos} in {text!r}")
+        pos += 1
+
+    def node(op: int, slot: int, ins: List[int]) -> int:
+        nodes.append([op, slot] + ins + [-1] * (4 - len(ins)))
+        return len(nodes) - 1
+
+    def expr() -> int:
+        nonlocal pos
+        c = s[pos] if pos < len(s) else ""
+        pos += 1
+        if c == "e":
+            return node(OP_ANCHOR, num(), [])
+        if c == "p":
+            eat("(")
+            x = expr()
+            eat(",")
+            eat("r")
+            k = num()
+            eat(")")
+            return node(OP_PROJECT, k, [x])
+        if c == "n":
+            eat("(")
+            x = expr()
+            eat(")")
+            return node(OP_NOT, -1, [x])
+        if c in "iu":
+            eat("(")
+            ins = [expr()]
+            while pos < len(s) and s[pos] == ",":
+                pos += 1
+                ins.append(expr())
+            eat(")")
+            if not 2 <= len(ins) <= 4:
+                raise ValueError(f"2 to 4 subqueries expected in {text!r}")
+            return node(OP_AND if c == "i" else OP_OR, -1, ins)
+        raise ValueError(f"unexpected {c!r} at {pos - 1} in {text!r}")
+
+    expr()
+    if pos != len(s):
+        raise ValueError(f"trailing text in {text!r}")
+    return np.asarray(nodes, np.int32).reshape(-1, 6)
+
+
+def graph_text(nodes: np.ndarray) -> str:
+    """Text form of node records (the inverse of graph_nodes)."""
+    g = np.asarray(nodes).reshape(-1, 6)
+
+    def rec(i: int) -> str:
+        op, slot = int(g[i, 0]), int(g[i, 1])
+        ins = [int(v) for v in g[i, 2:] if v >= 0]
+        if op == OP_ANCHOR:
+            return f"e{slot}"
+        if op == OP_PROJECT:
+            return f"p({rec(ins[0])},r{slot})"
+        if op == OP_NOT:
+            return f"n({rec(ins[0])})"
+        return ("i(" if op == OP_AND else "u(") + ",".join(rec(j) for j in ins) + ")"
+
+    return rec(g.shape[0] - 1)
+
+
+def graph_arity(nodes: np.ndarray) -> tuple:
+    """(anchor slots, relation slots) a query of this structure carries."""
+    g = np.asarray(nodes).reshape(-1, 6)
+    na = int(g[g[:, 0] == OP_ANCHOR, 1].max()) + 1
+    nr = int(g[g[:, 0] == OP_PROJECT, 1].max()) + 1
+    return na, nr
+
+
+def draw_graph_queries(nodes: np.ndarray, n: int, n_ent: int, n_rel: int, seed: int) -> QueryBatch:
+    """n queries of one graph structure: anchors [n x A] and relations [n x R]
+    drawn i.i.d. uniform (the recipe of the built-in structures)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    na, nr = graph_arity(nodes)
+    a = rng.integers(0, n_ent, size=(n, na), dtype=np.int64).astype(np.int32)
+    r = rng.integers(0, n_rel, size=(n, nr), dtype=np.int64).astype(np.int32)
+    return QueryBatch(np.full(n, -1, np.int32), a, r)
+
+
+def random_structure(seed: int, negation: bool, max_depth: int = 4, max_slots: int = 8,
+                     max_terms: int = 4) -> str:
+    """A seeded random structure in text form. Anchors only feed projections;
+    intersections and unions take 2-3 subqueries; negation appears only if
+    `negation`; every node has at most `max_terms` conjunctive terms in
+    disjunctive normal form (union distributing over intersection and
+    projection, the negation of a union being one intersection); at most
+    `max_slots` anchor and relation slots. Draws are retried until a graph
+    meets these limits."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    for _ in range(1000):
+        ctr = {"a": 0, "r": 0}
+        ok = [True]
+
+        def gen(depth: int):
+            kinds = ["leaf", "p", "i", "u"] + (["n"] if negation else [])
+            w = np.array([3.0, 3.0, 2.0, 1.0] + ([1.5] if negation else []))
+            if depth == 0:
+                kind = "leaf"
+            else:
+                kind = kinds[int(rng.choice(len(kinds), p=w / w.sum()))]
+            if kind == "leaf":
+                a, r = ctr["a"], ctr["r"]
+                ctr["a"] += 1
+                ctr["r"] += 1
+                return f"p(e{a},r{r})", 1
+            if kind == "p":
+                x, t = gen(depth - 1)
+                r = ctr["r"]
+                ctr["r"] += 1
+                return f"p({x},r{r})", t
+            if kind == "n":
+                x, t = gen(depth - 1)
+                if t > max_terms:
+                    ok[0] = False
+                return f"n({x})", 1
+            k = int(rng.integers(2, 4))
+            subs = [gen(depth - 1) for _ in range(k)]
+            t = int(np.prod([s[1] for s in subs])) if kind == "i" else int(sum(s[1] for s in subs))
+            if t > max_terms:
+                ok[0] = False
+            return f"{kind}(" + ",".join(s[0] for s in subs) + ")", t
+
+        text, terms = gen(max_depth)
+        if ok[0] and terms <= max_terms and ctr["a"] <= max_slots and ctr["r"] <= max_slots:
+            return text
+    raise RuntimeError("no structure within the limits")
