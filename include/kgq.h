@@ -128,11 +128,13 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out);
 kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, size_t nbytes,
                            int32_t dtype, int32_t src_is_device);
 
-/* Number of anchor entities and relations a query of this structure takes.
+/* Number of anchor entities and relations a query of a built-in structure
+ * takes (compiled structures: kgq_structure_info).
  * Errors: INVALID_ARG (unknown structure id or null outputs). */
 kgq_status kgq_structure_arity(int32_t structure_id, int32_t* n_anchors, int32_t* n_relations);
 
-/* Execute a batch of queries that all have the same structure.
+/* Execute a batch of queries that all have the same structure (built-in,
+ * or compiled on this handle).
  *   anchors   device int32 [batch x n_anchors(structure)]
  *   relations device int32 [batch x n_relations(structure)]
  *   k         1 <= k <= min(N, KGQ_MAX_K) when top-k outputs are requested
@@ -147,6 +149,8 @@ kgq_status kgq_structure_arity(int32_t structure_id, int32_t* n_anchors, int32_t
  * them and raises a flag. In checked mode (environment KGQ_CHECKED=1 at
  * create, or kgq_set_checked) execute then synchronises the stream and
  * returns OUT_OF_RANGE; otherwise the affected outputs are unspecified.
+ * A structure larger than the built-in ones may bound the batch below
+ * max_batch (kgq_structure_info); a larger batch is INVALID_ARG.
  * Errors: INVALID_ARG, UNSUPPORTED, NOT_LOADED, OUT_OF_RANGE (checked),
  * NO_DEVICE, DEVICE. */
 kgq_status kgq_execute(kgq_handle* h, int32_t structure_id, int32_t batch,
@@ -171,15 +175,104 @@ kgq_status kgq_execute_mixed(kgq_handle* h, int32_t batch, const int32_t* struct
 /* Turn checked mode on (non-zero) or off for this handle. */
 kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
 
-/* Describe the lowered plan of a batch (host structure ids) without running
- * it. counts receives KGQ_PLAN_NCOUNTS values, in this order:
- *   0 chain rows (branch states), 1 intersection groups, 2 intersection inputs,
- *   3..6 BetaE projection rows at hop levels 1, 2, 3 and after the
- *   intersection, 7 scored rows, 8 union pairs, 9 kernel launches per execute.
+/* Describe the lowered plan of a batch (host structure ids, built-in or
+ * compiled) without running it. counts receives KGQ_PLAN_NCOUNTS values, in
+ * this order:
+ *   0 projection chains starting at an anchor, 1 intersection groups,
+ *   2 intersection inputs, 3..6 BetaE projection rows at hops 1, 2 and >= 3
+ *   from the anchors and after an intersection, 7 scored rows, 8 union
+ *   pairs, 9 kernel launches per execute (with top-k), 10 intersection
+ *   stages, 11 unions scored as groups of four rows (3 or 4 terms),
+ *   12 state rows.
  * Errors: INVALID_ARG, UNSUPPORTED. */
-#define KGQ_PLAN_NCOUNTS 10
+#define KGQ_PLAN_NCOUNTS 13
 kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* structure_ids,
                              int32_t* counts);
+
+/* ---- Query structures as computation graphs -------------------------------
+ * Any query structure built from the four operators can be compiled into a
+ * structure id of a handle and then executed like a built-in one. This is
+ * the paper's compilation pipeline (Methodology, Fig. 2):
+ *   Graph Capturer (Eq. 2): the caller describes the query as a graph.
+ *   Entities are value nodes (KGQ_OP_ANCHOR), each relation a projection
+ *   node (KGQ_OP_PROJECT), and the connectives the functions f_and, f_or and
+ *   f_not (KGQ_OP_AND, KGQ_OP_OR, KGQ_OP_NOT).
+ *   Pattern Recognizer: the graph is rewritten into disjunctive normal form
+ *   (Eq. 1): projection and intersection distribute over unions, the
+ *   negation of a union becomes the intersection of the negations, and
+ *   chains of negations reduce to their parity.
+ *   Operator Fuser (Algorithm 1): each maximal run of projections on one
+ *   path becomes one fused chain (horizontal fusion), each intersection one
+ *   combine over all its branches (vertical fusion), and for GQE and
+ *   Query2Box a run of projections that follows an intersection is folded
+ *   into that combine (hybrid fusion). At execute time every fused operator
+ *   of one kind and schedule position runs as a single launch for the whole
+ *   batch, across structures.
+ * The built-in structures 0..13 are such graphs, compiled the same way; their
+ * text forms are listed with kgq_parse_structure. */
+typedef enum {
+    KGQ_OP_ANCHOR = 0,    /* anchor entity in anchor slot `slot` */
+    KGQ_OP_PROJECT = 1,   /* projection of in[0] by the relation in relation slot `slot` */
+    KGQ_OP_AND = 2,       /* intersection of in[0..] (2 to 4 inputs) */
+    KGQ_OP_OR = 3,        /* union of in[0..] (2 to 4 inputs) */
+    KGQ_OP_NOT = 4        /* negation of in[0] (BetaE only) */
+} kgq_op;
+
+typedef struct {
+    int32_t op;      /* kgq_op */
+    int32_t slot;    /* anchor or relation slot (0 .. KGQ_MAX_SLOTS-1); ignored for AND, OR, NOT */
+    int32_t in[4];   /* indices of earlier nodes, from in[0]; unused entries -1 */
+} kgq_node;
+
+#define KGQ_MAX_GRAPH_NODES 64   /* nodes of one graph */
+#define KGQ_MAX_SLOTS 8          /* anchor slots and relation slots of one structure */
+#define KGQ_MAX_DISJUNCTS 4      /* conjunctive terms of any node in disjunctive normal form */
+#define KGQ_MAX_COMPILED 64      /* compiled structures per handle */
+
+/* Read the text form of a graph into nodes (host memory, capacity entries),
+ * in post-order: every node after its inputs, the answer last.
+ *   e<k>               anchor slot k            p(<x>, r<k>)  projection of x by relation slot k
+ *   i(<x>, <y>[, ...]) intersection of 2-4       u(<x>, <y>[, ...]) union of 2-4
+ *   n(<x>)             negation                 whitespace is ignored
+ * The built-in structures, in this form:
+ *   1p p(e0,r0)   2p p(p(e0,r0),r1)   3p p(p(p(e0,r0),r1),r2)   2i i(p(e0,r0),p(e1,r1))
+ *   3i i(p(e0,r0),p(e1,r1),p(e2,r2))   pi i(p(p(e0,r0),r1),p(e1,r2))   ip p(i(p(e0,r0),p(e1,r1)),r2)
+ *   2u u(p(e0,r0),p(e1,r1))   up p(u(p(e0,r0),p(e1,r1)),r2)   2in i(p(e0,r0),n(p(e1,r1)))
+ *   3in i(p(e0,r0),p(e1,r1),n(p(e2,r2)))   inp p(i(p(e0,r0),n(p(e1,r1))),r2)
+ *   pin i(p(p(e0,r0),r1),n(p(e1,r2)))   pni i(n(p(p(e0,r0),r1)),p(e1,r2))
+ * *n_nodes receives the node count. The text is not checked beyond its
+ * syntax (kgq_compile_structure checks the graph).
+ * Errors: INVALID_ARG (NULL argument, syntax error, more than capacity or
+ * KGQ_MAX_GRAPH_NODES nodes). */
+kgq_status kgq_parse_structure(const char* text, kgq_node* nodes, int32_t capacity, int32_t* n_nodes);
+
+/* Compile a graph (host nodes[n_nodes], the answer last) for this handle's
+ * model and return its new structure id (>= KGQ_NUM_STRUCTURES) in
+ * *structure_id, valid for this handle's kgq_execute, kgq_execute_mixed,
+ * kgq_describe_plan and kgq_structure_info until kgq_destroy. A query of the
+ * structure takes anchors[slot] for slots 0..A-1 and relations[slot] for
+ * slots 0..R-1; both slot sets must be used without gaps (a mixed batch
+ * holds at most 3 of each). Rules: inputs are earlier nodes; every node but
+ * the last feeds a later one; an anchor feeds only projections; at most
+ * KGQ_MAX_DISJUNCTS conjunctive terms at any node in normal form (so at most
+ * 4 intersection inputs after a negated union).
+ * Compiling allocates nothing on the device; the handle's scratch, sized by
+ * max_batch for the built-in structures, bounds the batch of a larger
+ * structure (kgq_structure_info reports the bound).
+ * Errors: INVALID_ARG (NULL argument, a rule broken, KGQ_MAX_COMPILED
+ * reached, a structure that does not fit even one query), UNSUPPORTED
+ * (negation on GQE or Query2Box). */
+kgq_status kgq_compile_structure(kgq_handle* h, const kgq_node* nodes, int32_t n_nodes, int32_t* structure_id);
+
+/* Facts about a built-in or compiled structure on this handle. info receives
+ * KGQ_INFO_NCOUNTS values: 0 anchors, 1 relations, 2 conjunctive terms of the
+ * answer, 3 fused operators per query, 4 intersection stages, 5 kernel
+ * launches per execute (with top-k), 6 largest batch of this structure alone
+ * that the handle's scratch holds, 7 uses negation (0/1).
+ * Errors: INVALID_ARG (NULL argument or unknown id), UNSUPPORTED (a
+ * built-in negation structure on GQE or Query2Box). */
+#define KGQ_INFO_NCOUNTS 8
+kgq_status kgq_structure_info(const kgq_handle* h, int32_t structure_id, int32_t* info);
 
 /* Filtered ranks of known answers, and ranking metrics per query (the paper
  * reports MRR; Experiments). For query q, with score row

@@ -188,63 +188,67 @@ void launch_validate(const int32_t* anchors, const int32_t* rels, const int32_t*
 // projections: the whole chain is one pass over the row)
 // ---------------------------------------------------------------------------
 
-__global__ void k_chain(int model, const int32_t* anchor_ref, const int32_t* rel_ref,
-                        const int32_t* anchors, const int32_t* rels, const float* ent_rm,
-                        const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
-                        float* states, int* flag)
+__global__ void k_chain(int model, const int32_t* anchor_ref, const int32_t* rel_off, const int32_t* rel_ref,
+                        const int32_t* dst_row, const int32_t* anchors, const int32_t* rels, const float* ent_rm,
+                        const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d, float* states,
+                        int* flag)
 {
     const int c = blockIdx.x;
     const int64_t a = checked_id(anchors[anchor_ref[c]], n_ent, flag);
-    int32_t r[3];
-    int nh = 0;
-    for (int h = 0; h < 3; ++h) {
-        const int32_t ref = rel_ref[3 * c + h];
-        if (ref >= 0) r[nh++] = checked_id(rels[ref], n_rel, flag);
-    }
+    const int h0 = rel_off[c], h1 = rel_off[c + 1];
     const int W = model == 0 ? d : 2 * d;
-    float* out = states + (int64_t)c * W;
+    float* out = states + (int64_t)dst_row[c] * W;
     // d is a multiple of 4: 128-bit accesses, one float4 per thread per step
     for (int k = threadIdx.x * 4; k < d; k += blockDim.x * 4) {
         float4 x = *reinterpret_cast<const float4*>(ent_rm + a * d + k);
-        for (int h = 0; h < nh; ++h) {
-            const float4 v = *reinterpret_cast<const float4*>(rel_c + (int64_t)r[h] * d + k);
+        float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int h = h0; h < h1; ++h) {
+            const int64_t r = checked_id(rels[rel_ref[h]], n_rel, flag);
+            const float4 v = *reinterpret_cast<const float4*>(rel_c + r * d + k);
             x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
+            if (model == 1) {
+                const float4 u = *reinterpret_cast<const float4*>(rel_o + r * d + k);
+                o.x += u.x; o.y += u.y; o.z += u.z; o.w += u.w;
+            }
         }
         *reinterpret_cast<float4*>(out + k) = x;
-        if (model == 1) {
-            float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-            for (int h = 0; h < nh; ++h) {
-                const float4 v = *reinterpret_cast<const float4*>(rel_o + (int64_t)r[h] * d + k);
-                o.x += v.x; o.y += v.y; o.z += v.z; o.w += v.w;
-            }
-            *reinterpret_cast<float4*>(out + d + k) = o;
-        }
+        if (model == 1) *reinterpret_cast<float4*>(out + d + k) = o;
     }
 }
 
-void launch_chain(int model, const int32_t* anchor_ref, const int32_t* rel_ref, int n_chain,
-                  const int32_t* anchors, const int32_t* rels, const float* ent_rm,
-                  const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
+void launch_chain(int model, const int32_t* anchor_ref, const int32_t* rel_off, const int32_t* rel_ref,
+                  const int32_t* dst_row, int n_chain, const int32_t* anchors, const int32_t* rels,
+                  const float* ent_rm, const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
                   float* states, int* flag, hipStream_t s)
 {
     if (n_chain <= 0) return;
-    hipLaunchKernelGGL(k_chain, dim3(n_chain), dim3(128), 0, s, model, anchor_ref, rel_ref, anchors, rels,
-                       ent_rm, rel_c, rel_o, n_ent, n_rel, d, states, flag);
+    hipLaunchKernelGGL(k_chain, dim3(n_chain), dim3(128), 0, s, model, anchor_ref, rel_off, rel_ref, dst_row,
+                       anchors, rels, ent_rm, rel_c, rel_o, n_ent, n_rel, d, states, flag);
 }
 
 // ---------------------------------------------------------------------------
 // Intersections (vertical fusion: all branches of a group in one pass)
 // ---------------------------------------------------------------------------
 
-// Attention weights across the n (<= 3) branches of one dimension.
-__device__ __forceinline__ void softmax_branches(const float* logits, int64_t ld, int n, int k, float* w)
+// Attention weights across the n (2 .. kGroupInputs) branches of one
+// dimension. Unrolled over the maximum with a guard, so that w stays in
+// registers.
+__device__ __forceinline__ void softmax_branches(const float* logits, int64_t ld, int n, int k,
+                                                 float (&w)[kGroupInputs])
 {
     float mx = logits[k];
-    for (int j = 1; j < n; ++j) mx = fmaxf(mx, logits[j * ld + k]);
+#pragma unroll
+    for (int j = 1; j < kGroupInputs; ++j)
+        if (j < n) mx = fmaxf(mx, logits[j * ld + k]);
     float z = 0.f;
-    for (int j = 0; j < n; ++j) { w[j] = expf(logits[j * ld + k] - mx); z += w[j]; }
+#pragma unroll
+    for (int j = 0; j < kGroupInputs; ++j) {
+        w[j] = j < n ? expf(logits[j * ld + k] - mx) : 0.f;
+        z += w[j];
+    }
     const float inv = 1.0f / z;
-    for (int j = 0; j < n; ++j) w[j] *= inv;
+#pragma unroll
+    for (int j = 0; j < kGroupInputs; ++j) w[j] *= inv;
 }
 
 __global__ void k_combine_center(int model, GroupArgs g, const float* states, int W,
@@ -256,14 +260,14 @@ __global__ void k_combine_center(int model, GroupArgs g, const float* states, in
     const int i0 = g.in_start[gi];
     const int n = g.n_in[gi];
     const int64_t orow = g.out_row[gi];
-    const int32_t pref = g.post_ref[gi];
-    const int32_t pr = pref >= 0 ? checked_id(rels[pref], n_rel, flag) : -1;
+    const int p0 = g.post_off[gi], p1 = g.post_off[gi + 1];
     for (int k = threadIdx.x; k < d; k += blockDim.x) {
-        float w[3];
+        float w[kGroupInputs];
         softmax_branches(logits + (int64_t)i0 * d, d, n, k, w);
         float c = 0.f;
         for (int j = 0; j < n; ++j) c += w[j] * states[(int64_t)(i0 + j) * W + k];
-        if (pr >= 0) c += rel_c[(int64_t)pr * d + k];
+        // folded post-chain: the translations of the projections that follow
+        for (int h = p0; h < p1; ++h) c += rel_c[(int64_t)checked_id(rels[g.post_ref[h]], n_rel, flag) * d + k];
         out_states[orow * W + k] = c;
         if (model == 1) {
             float z = 0.f;
@@ -291,14 +295,13 @@ __global__ void k_combine_offset(GroupArgs g, const float* states, int W, const 
     const int i0 = g.in_start[gi];
     const int n = g.n_in[gi];
     const int64_t orow = g.out_row[gi];
-    const int32_t pref = g.post_ref[gi];
-    const int32_t pr = pref >= 0 ? checked_id(rels[pref], n_rel, flag) : -1;
+    const int p0 = g.post_off[gi], p1 = g.post_off[gi + 1];
     for (int k = threadIdx.x; k < d; k += blockDim.x) {
         float m = states[(int64_t)i0 * W + d + k];
         for (int j = 1; j < n; ++j) m = fminf(m, states[(int64_t)(i0 + j) * W + d + k]);
         const float gv = gate[(int64_t)gi * d + k];
         float o = m * (1.0f / (1.0f + expf(-gv)));
-        if (pr >= 0) o += rel_o[(int64_t)pr * d + k];
+        for (int h = p0; h < p1; ++h) o += rel_o[(int64_t)checked_id(rels[g.post_ref[h]], n_rel, flag) * d + k];
         out_states[orow * W + d + k] = o;
     }
 }
@@ -346,7 +349,7 @@ __global__ void k_betae_combine(GroupArgs g, const float* x_int, const float* lo
     const int64_t orow = g.out_row[gi];
     const int W = 2 * d;
     for (int k = threadIdx.x; k < d; k += blockDim.x) {
-        float w[3];
+        float w[kGroupInputs];
         softmax_branches(logits + (int64_t)i0 * d, d, n, k, w);
         float al = 0.f, be = 0.f;
         for (int j = 0; j < n; ++j) {
@@ -366,9 +369,9 @@ void launch_betae_combine(const GroupArgs& g, const float* x_int, const float* l
 }
 
 __global__ void k_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
-                                  const int32_t* anchors, const int32_t* rels, const float* states,
-                                  const float* ent_ab, const float* rel, int64_t n_ent, int n_rel, int d,
-                                  float* x, int* flag)
+                                  const int32_t* neg, const int32_t* anchors, const int32_t* rels,
+                                  const float* states, const float* ent_ab, const float* rel, int64_t n_ent,
+                                  int n_rel, int d, float* x, int* flag)
 {
     const int m = blockIdx.x;
     const int W = 2 * d;
@@ -380,19 +383,23 @@ __global__ void k_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_
         const int64_t a = checked_id(anchors[anchor_ref[m]], n_ent, flag);
         base = ent_ab + a * W;
     }
+    const bool inv = neg && neg[m];   // negated source: reciprocal of both shape parameters
     const int64_t r = checked_id(rels[rel_ref[m]], n_rel, flag);
     const float* rr = rel + r * W;
     float* dst = x + (int64_t)m * W;
-    for (int k = threadIdx.x; k < W; k += blockDim.x) dst[k] = base[k] + rr[k];
+    for (int k = threadIdx.x; k < W; k += blockDim.x) {
+        const float v = base[k];
+        dst[k] = (inv ? 1.0f / v : v) + rr[k];
+    }
 }
 
 void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
-                            int M, const int32_t* anchors, const int32_t* rels,
+                            const int32_t* neg, int M, const int32_t* anchors, const int32_t* rels,
                             const float* states, const float* ent_ab, const float* rel,
                             int64_t n_ent, int n_rel, int d, float* x, int* flag, hipStream_t s)
 {
     if (M <= 0) return;
-    hipLaunchKernelGGL(k_betae_proj_prep, dim3(M), dim3(256), 0, s, src_row, anchor_ref, rel_ref, anchors,
+    hipLaunchKernelGGL(k_betae_proj_prep, dim3(M), dim3(256), 0, s, src_row, anchor_ref, rel_ref, neg, anchors,
                        rels, states, ent_ab, rel, n_ent, n_rel, d, x, flag);
 }
 
@@ -500,24 +507,33 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows
 
 // BetaE: the query rows row-major, [row][alpha (d) | beta (d)], the A operand
 // of the matrix-core scorer, and C_q = sum_i lnB(alpha_i, beta_i) per row in
-// double precision. One workgroup per row; padding rows are zero with C_q = 0.
-__global__ __launch_bounds__(256) void k_pack_rows(const int32_t* src_row, int n_rows, const float* states, int d,
-                                                   float* qrows, double* cq)
+// double precision. A negated answer row (neg[j] != 0) is packed as the
+// reciprocals of its shape parameters. One workgroup per row; padding rows
+// are zero with C_q = 0.
+__global__ __launch_bounds__(256) void k_pack_rows(const int32_t* src_row, const int32_t* neg, int n_rows,
+                                                   const float* states, int d, float* qrows, double* cq)
 {
     __shared__ double part[4];
     const int j = blockIdx.x;
     const int t = threadIdx.x;
     const int src = j < n_rows ? src_row[j] : -1;
+    const bool inv = src >= 0 && neg && neg[j];
     const float* st = states + (int64_t)(src >= 0 ? src : 0) * 2 * d;
     float* dst = qrows + (int64_t)j * 2 * d;
     for (int k = 4 * t; k < 2 * d; k += 4 * 256) {
-        const float4 v = *reinterpret_cast<const float4*>(st + k);
+        float4 v = *reinterpret_cast<const float4*>(st + k);
+        if (inv) v = make_float4(1.0f / v.x, 1.0f / v.y, 1.0f / v.z, 1.0f / v.w);
         *reinterpret_cast<float4*>(dst + k) = src >= 0 ? v : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     double lnb = 0.0;
     if (src >= 0) {
         for (int k = t; k < d; k += 256) {
-            const double a = st[k], b = st[d + k];
+            float af = st[k], bf = st[d + k];
+            if (inv) {
+                af = 1.0f / af;
+                bf = 1.0f / bf;
+            }
+            const double a = af, b = bf;
             lnb += lgamma(a) + lgamma(b) - lgamma(a + b);
         }
     }
@@ -527,12 +543,13 @@ __global__ __launch_bounds__(256) void k_pack_rows(const int32_t* src_row, int n
     if (t == 0) cq[j] = (part[0] + part[1]) + (part[2] + part[3]);
 }
 
-void launch_pack(int model, const int32_t* src_row, int n_rows, int n_rows_pad, const float* states,
-                 int W, int d, float* qpack, double* cq, hipStream_t s)
+void launch_pack(int model, const int32_t* src_row, const int32_t* neg, int n_rows, int n_rows_pad,
+                 const float* states, int W, int d, float* qpack, double* cq, hipStream_t s)
 {
     if (n_rows_pad <= 0) return;
     if (model == 2) {
-        hipLaunchKernelGGL(k_pack_rows, dim3(n_rows_pad), dim3(256), 0, s, src_row, n_rows, states, d, qpack, cq);
+        hipLaunchKernelGGL(k_pack_rows, dim3(n_rows_pad), dim3(256), 0, s, src_row, neg, n_rows, states, d, qpack,
+                           cq);
         return;
     }
     const int tq = score_row_pad(model);

@@ -25,8 +25,11 @@
 //           score = gamma - acc1 + (1 - center_reg) * acc2, the exact
 //           regrouping of dist_out + center_reg * dist_in
 //           (t <= o: center_reg * t; t > o: (t - o) + center_reg * o)
-// Union (disjunctive normal form, Eq. 1 of the paper): a union query has two
-// adjacent rows; its score is the max of the two rows' scores.
+// Union (disjunctive normal form, Eq. 1 of the paper): a query whose answer
+// has 2 conjunctive terms has two adjacent rows (a pair), one with 3 or 4
+// terms a group of four rows; its score is the max over the rows' scores.
+// Groups come first, then pairs, then single rows, so that every group and
+// pair lies inside one lane's TQ rows.
 #include <algorithm>
 #include <type_traits>
 
@@ -153,47 +156,55 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
         }
         return;
     }
-    const int nu_pairs = a.n_union_rows >> 1;
+    const int n_grouped = a.n_quad + a.n_pair;
 #pragma unroll
-    for (int i = 0; i < TQ; i += 2) {
+    for (int i = 0; i < TQ; i += 4) {
         const int row = qb * TQ + i;
         if (row >= a.n_rows) break;
-        float s0[4], s1[4];
+        float sc[4][4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (MODEL == 0) {
-                s0[j] = a.gamma - acc[i][j];
-                s1[j] = a.gamma - acc[i + 1][j];
-            } else {
-                const float w = 1.0f - a.center_reg;
-                s0[j] = a.gamma - acc[i][j] + w * acc2[i][j];
-                s1[j] = a.gamma - acc[i + 1][j] + w * acc2[i + 1][j];
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (MODEL == 0) sc[u][j] = a.gamma - acc[i + u][j];
+                else sc[u][j] = a.gamma - acc[i + u][j] + (1.0f - a.center_reg) * acc2[i + u][j];
             }
+        if (row < a.n_quad) {
+            float* dst = a.scores + (int64_t)a.out_dest[row >> 2] * a.ld;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (e0 + j < a.N) dst[e0 + j] = fmaxf(fmaxf(sc[0][j], sc[1][j]), fmaxf(sc[2][j], sc[3][j]));
+            continue;
         }
-        if (row < a.n_union_rows) {
-            float* dst = a.scores + (int64_t)a.out_dest[row >> 1] * a.ld;
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (e0 + j < a.N) dst[e0 + j] = fmaxf(s0[j], s1[j]);
-        } else {
-            const int o0 = nu_pairs + (row - a.n_union_rows);
-            float* dst0 = a.scores + (int64_t)a.out_dest[o0] * a.ld;
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (e0 + j < a.N) dst0[e0 + j] = s0[j];
-            if (row + 1 < a.n_rows) {
-                float* dst1 = a.scores + (int64_t)a.out_dest[o0 + 1] * a.ld;
+        for (int h = 0; h < 2; ++h) {
+            const int r = row + 2 * h;
+            if (r >= a.n_rows) break;
+            const int o = score_out_index(r, a.n_quad, a.n_pair);
+            if (r < n_grouped) {
+                float* dst = a.scores + (int64_t)a.out_dest[o] * a.ld;
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    if (e0 + j < a.N) dst1[e0 + j] = s1[j];
+                    if (e0 + j < a.N) dst[e0 + j] = fmaxf(sc[2 * h][j], sc[2 * h + 1][j]);
+            } else {
+                float* dst0 = a.scores + (int64_t)a.out_dest[o] * a.ld;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (e0 + j < a.N) dst0[e0 + j] = sc[2 * h][j];
+                if (r + 1 < a.n_rows) {
+                    float* dst1 = a.scores + (int64_t)a.out_dest[o + 1] * a.ld;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (e0 + j < a.N) dst1[e0 + j] = sc[2 * h + 1][j];
+                }
             }
         }
     }
 }
 
-// Split-d finish: output row o (union pairs first, then single rows, the
-// order of out_dest) and entity e: sum the slices in order, score, max over
-// a union pair, store.
+// Split-d finish: output o (groups of four, then pairs, then single rows,
+// the order of out_dest) and entity e: sum the slices in order, score, max
+// over the output's rows, store.
 template <int MODEL>
 __global__ __launch_bounds__(256) void k_score_sum(ScoreArgs a, int splits, int64_t rows_pad, int n_out)
 {
@@ -203,9 +214,18 @@ __global__ __launch_bounds__(256) void k_score_sum(ScoreArgs a, int splits, int6
     const int o = (int)(t / a.N);
     const int64_t e = t - (int64_t)o * a.N;
     const int64_t n_pad = a.n_blocks * kEntBlock;
-    const int nu_pairs = a.n_union_rows >> 1;
-    const int r0 = o < nu_pairs ? 2 * o : a.n_union_rows + (o - nu_pairs);
-    const int nr = o < nu_pairs ? 2 : 1;
+    const int nq = a.n_quad >> 2, np = a.n_pair >> 1;
+    int r0, nr;
+    if (o < nq) {
+        r0 = 4 * o;
+        nr = 4;
+    } else if (o < nq + np) {
+        r0 = a.n_quad + 2 * (o - nq);
+        nr = 2;
+    } else {
+        r0 = a.n_quad + a.n_pair + (o - nq - np);
+        nr = 1;
+    }
     float best = 0.f;
     for (int u = 0; u < nr; ++u) {
         float s1 = 0.f, s2 = 0.f;
@@ -262,7 +282,7 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
     else
         hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
     if (z > 1) {
-        const int n_out = (a.n_union_rows >> 1) + (a.n_rows - a.n_union_rows);
+        const int n_out = (a.n_quad >> 2) + (a.n_pair >> 1) + (a.n_rows - a.n_quad - a.n_pair);
         const int64_t tot = (int64_t)n_out * a.N;
         const dim3 g2((unsigned)((tot + 255) / 256));
         if (a.model == 0)

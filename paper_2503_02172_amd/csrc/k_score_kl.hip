@@ -14,8 +14,9 @@
 //
 // Tiling: MfmaTile (mfma_tile.hpp) with 128-row x 128-entity workgroup
 // tiles, 4 x 4 MFMA tiles of 16 x 16 per wavefront. The epilogue adds
-// C_q + E_e in double precision, takes the max over union pairs (two adjacent
-// rows, held by the same lane) and scatters rows to their output positions.
+// C_q + E_e in double precision, takes the max over union groups of four
+// and pairs of rows (held by the same lane) and scatters rows to their
+// output positions.
 // Workgroups are ordered in chunks of row tiles (about 2 MiB of query rows),
 // each swept against every entity tile: the chunk's rows stay in L2 while
 // the entity table streams past.
@@ -56,9 +57,9 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     v4f acc[KlTile::TM][KlTile::TN];
     KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent, K, (int)(a.n_blocks * kEntBlock), K, m0, n0, sm, acc);
 
-    // Epilogue. Lane rows are 4 consecutive rows starting at a multiple of 4;
-    // union pairs are rows (2p, 2p + 1): r = 0, 1 and r = 2, 3 of one lane.
-    const int nu_pairs = a.n_union_rows >> 1;
+    // Epilogue. Lane rows are 4 consecutive rows starting at a multiple of 4:
+    // a group of four is one lane's rows, a pair rows r = 0, 1 or r = 2, 3.
+    const int n_grouped = a.n_quad + a.n_pair;
 #pragma unroll
     for (int j = 0; j < KlTile::TN; ++j) {
         const int64_t n = n0 + KlTile::col_of(j);
@@ -67,18 +68,23 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
 #pragma unroll
         for (int i = 0; i < KlTile::TM; ++i) {
             const int mb = m0 + KlTile::row_of(i);
+            if (mb >= a.n_rows) continue;
             float s[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q)
                 s[q] = (float)((double)a.gamma - (a.cq[mb + q] + ee + (double)acc[i][j][q]));
+            if (mb < a.n_quad) {
+                a.scores[(int64_t)a.out_dest[mb >> 2] * a.ld + n] = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+                continue;
+            }
 #pragma unroll
             for (int pr = 0; pr < 2; ++pr) {
                 const int m = mb + 2 * pr;
                 if (m >= a.n_rows) break;
-                if (m < a.n_union_rows) {
-                    a.scores[(int64_t)a.out_dest[m >> 1] * a.ld + n] = fmaxf(s[2 * pr], s[2 * pr + 1]);
+                const int o = score_out_index(m, a.n_quad, a.n_pair);
+                if (m < n_grouped) {
+                    a.scores[(int64_t)a.out_dest[o] * a.ld + n] = fmaxf(s[2 * pr], s[2 * pr + 1]);
                 } else {
-                    const int o = nu_pairs + (m - a.n_union_rows);
                     a.scores[(int64_t)a.out_dest[o] * a.ld + n] = s[2 * pr];
                     if (m + 1 < a.n_rows) a.scores[(int64_t)a.out_dest[o + 1] * a.ld + n] = s[2 * pr + 1];
                 }

@@ -2,6 +2,7 @@
 // argument validation, plan upload and the per-model stage sequence.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdlib>
 #include <cstring>
 #include <map>
@@ -95,11 +96,19 @@ struct kgq_handle {
     float* proj1_rel = nullptr;   // [R x 4d]  Rel . W1^T + b1
     bool proj1_ready = false;
 
+    // structure id -> compiled program: the built-ins for this model, then
+    // the structures compiled on this handle
+    std::vector<const Program*> table;
+    std::vector<std::unique_ptr<Program>> compiled;
+
     // scratch lanes (each sized for max_batch at create): executes on
     // different lanes may run concurrently on different streams
     std::vector<std::unique_ptr<Lane>> lanes;
     int next_lane = 0;
     int64_t plan_words = 0;
+    // what one lane holds: state rows, rows of one dense-layer level or
+    // intersection stage, groups of one intersection stage, scored rows
+    int64_t cap_rows = 0, cap_mlp = 0, cap_groups = 0, cap_score_rows = 0;
 
     std::vector<void*> allocations;
     int64_t bytes_total = 0;      // device bytes allocated by the handle
@@ -171,6 +180,44 @@ void build_specs(kgq_handle* h)
         break;
     }
     for (auto& kv : s) h->loaded[kv.first] = false;
+}
+
+// Structure table and the capacities of one lane (also for a
+// validation-only handle, which allocates nothing).
+void build_table(kgq_handle* h)
+{
+    const kgq_config& c = h->cfg;
+    const int64_t Bm = c.max_batch;
+    int words = 64;   // plan-image words per query: room for structures larger than the built-ins
+    for (int id = 0; id < kNumStructures; ++id) {
+        const Program* g = builtin_program(c.model, id);
+        h->table.push_back(g);
+        if (g->supported) words = std::max(words, g->image_words);
+    }
+    h->plan_words = Bm * words + kPlanOverheadWords;
+    h->cap_rows = Bm * kStateRowsPerQuery;
+    h->cap_mlp = 3 * Bm;
+    h->cap_groups = h->cap_mlp / 2;   // a group has at least two inputs
+    const int tq = score_row_pad(c.model);
+    h->cap_score_rows = ((2 * Bm + tq - 1) / tq) * tq;
+}
+
+// Largest batch of one structure that a lane holds.
+int64_t max_batch_for(const kgq_handle* h, const Program& g)
+{
+    int64_t mb = h->cfg.max_batch;
+    mb = std::min<int64_t>(mb, h->cap_rows / std::max<int64_t>(1, (int64_t)g.ops.size()));
+    if (g.max_stage_level) mb = std::min<int64_t>(mb, h->cap_mlp / g.max_stage_level);
+    if (g.max_stage_inputs) mb = std::min<int64_t>(mb, h->cap_mlp / g.max_stage_inputs);
+    if (g.max_stage_groups) mb = std::min<int64_t>(mb, h->cap_groups / g.max_stage_groups);
+    mb = std::min<int64_t>(mb, h->cap_score_rows / (int64_t)g.answer.size());
+    mb = std::min<int64_t>(mb, (h->plan_words - kPlanOverheadWords) / g.image_words);
+    return mb;
+}
+
+const Program* program_of(const kgq_handle* h, int id)
+{
+    return (id >= 0 && id < (int)h->table.size()) ? h->table[id] : nullptr;
 }
 
 kgq_status dev_alloc(kgq_handle* h, void** p, size_t bytes)
@@ -249,14 +296,12 @@ kgq_status allocate_all(kgq_handle* h)
         if (c.model == KGQ_Q2B) ALLOC(h->rel_o_sp, (int64_t)c.n_relations * d);
     }
     h->bytes_params = h->bytes_total;   // everything after this is execute scratch
-    h->plan_words = plan_image_words((int)Bm);
     const int n_lanes = c.concurrency > 0 ? c.concurrency : 1;
     for (int li = 0; li < n_lanes; ++li) {
         h->lanes.emplace_back(new Lane());
         Lane& L = *h->lanes.back();
-        const int64_t rows = Bm * kStateRowsPerQuery;
-        ALLOC(L.states, rows * W);
-        const int64_t m_max = 3 * Bm;   // rows of one MLP level / intersection inputs
+        ALLOC(L.states, h->cap_rows * W);
+        const int64_t m_max = h->cap_mlp;   // rows of one MLP level / intersection stage inputs
         if (c.model == KGQ_BETAE) {
             ALLOC(L.xbuf, m_max * 2 * d);
             ALLOC(L.h1, m_max * 4 * d);
@@ -265,15 +310,13 @@ kgq_status allocate_all(kgq_handle* h)
             ALLOC(L.h1, m_max * d);
             if (c.model == KGQ_Q2B) {
                 ALLOC(L.zfeat, m_max * d);
-                ALLOC(L.zmean, Bm * d);
-                ALLOC(L.gate, Bm * d);
+                ALLOC(L.zmean, h->cap_groups * d);
+                ALLOC(L.gate, h->cap_groups * d);
             }
         }
         ALLOC(L.logits, m_max * d);
-        const int tq = score_row_pad(c.model);
-        const int64_t prow = ((2 * Bm + tq - 1) / tq) * tq;
-        ALLOC(L.qpack, prow * 2 * d);
-        ALLOC(L.cq, prow);
+        ALLOC(L.qpack, h->cap_score_rows * 2 * d);
+        ALLOC(L.cq, h->cap_score_rows);
         ALLOC(L.scores, Bm * N);
         // split-K runs only while a layer has fewer than 128 output tiles of
         // 64 x 64, so 16 slices of it stay below 16 x 128 x 4096 floats
@@ -404,6 +447,25 @@ kgq_status check_outputs(kgq_handle* h, int32_t batch, const void* anchors, cons
     return KGQ_OK;
 }
 
+// A lowered batch must fit the lane's scratch.
+kgq_status check_capacity(kgq_handle* h, const Plan& p)
+{
+    const int tq = score_row_pad(h->cfg.model);
+    const int64_t srows = ((int64_t)(p.n_score_rows + tq - 1) / tq) * tq;
+    const char* what = nullptr;
+    if (p.n_state_rows > h->cap_rows) what = "state rows";
+    else if (p.max_level > h->cap_mlp || p.max_and_in > h->cap_mlp) what = "dense-layer rows";
+    else if (p.max_and_groups > h->cap_groups) what = "intersection groups";
+    else if (srows > h->cap_score_rows) what = "scored rows";
+    else if ((int64_t)p.image.size() > h->plan_words) what = "plan words";
+    if (!what) return KGQ_OK;
+    return fail(h, KGQ_E_INVALID_ARG,
+                std::string("the batch needs more ") + what + " than the handle's scratch (sized for max_batch=" +
+                    std::to_string(h->cfg.max_batch) +
+                    " built-in queries) holds; split it (kgq_structure_info gives the largest batch of one "
+                    "structure)");
+}
+
 // Upload a plan image into device slot `slot` (after the slot's last use).
 kgq_status upload_plan(kgq_handle* h, Lane& L, const Plan& p, int slot, hipStream_t s)
 {
@@ -446,115 +508,117 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
 
     if (h->checked) {
         launch_clear_flag(L.dflag, s);
-        launch_validate(anchors, rels, mixed ? P + p.off.arity : nullptr, p.B, sa, sr, fixed_na, fixed_nr,
+        launch_validate(anchors, rels, mixed ? P + p.off_arity : nullptr, p.B, sa, sr, fixed_na, fixed_nr,
                         N, n_rel, L.dflag, s);
     }
-    GroupArgs g{P + p.off.g_in_start, P + p.off.g_n, P + p.off.g_out, P + p.off.g_post, P + p.off.g_neg,
-                p.n_groups};
+    const bool betae = c.model == KGQ_BETAE, q2b = c.model == KGQ_Q2B;
+    const float* rel_c = betae ? nullptr : q2b ? param("relation.center") : param("relation");
+    const float* rel_ab = betae ? param("relation") : nullptr;
+    const std::string pre = q2b ? "inter.center." : "inter.";
 
-    if (c.model == KGQ_GQE || c.model == KGQ_Q2B) {
-        const bool q2b = c.model == KGQ_Q2B;
-        const float* rel_c = q2b ? param("relation.center") : param("relation");
-        {
+    for (const Stage& st : p.stages) {
+        if (st.kind == ST_CHAIN) {
+            // GQE / Query2Box: every translation chain of the batch
             StageTimer t(h, 0, s);
-            launch_chain(c.model, P + p.off.chain_anchor, P + p.off.chain_rel, p.n_chain, anchors, rels,
-                         h->ent_rm, rel_c, h->rel_o_sp, N, n_rel, d, L.states, L.dflag, s);
-        }
-        if (p.n_groups) {
-            const std::string pre = q2b ? "inter.center." : "inter.";
-            {
+            launch_chain(c.model, P + st.a, P + st.b, P + st.c, P + st.d, st.count, anchors, rels, h->ent_rm, rel_c,
+                         h->rel_o_sp, N, n_rel, d, L.states, L.dflag, s);
+        } else if (st.kind == ST_LEVEL) {
+            // BetaE: one projection MLP pass over every projection at this
+            // stage and hop
+            const int M = st.count;
+            if (st.table) {
+                // first hop from the anchors: the first layer is a gather
+                // from the precomputed tables
+                StageTimer t(h, 0, s);
+                launch_betae_proj1(P + st.b, P + st.c, M, anchors, rels, h->proj1_ent, h->proj1_rel, N, n_rel, 4 * d,
+                                   L.h1, L.dflag, s);
+            } else {
+                {
+                    StageTimer t(h, 0, s);
+                    launch_betae_proj_prep(P + st.a, P + st.b, P + st.c, P + st.d, M, anchors, rels, L.states,
+                                           h->ent_rm, rel_ab, N, n_rel, d, L.xbuf, L.dflag, s);
+                }
                 StageTimer t(h, 1, s);
-                gemm({L.states, W, param((pre + "w1").c_str()), d, param((pre + "b1").c_str()), L.h1, d,
-                             nullptr, p.n_int_in, d, d, EPI_RELU});
+                gemm({L.xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), L.h1, 4 * d, nullptr, M, 4 * d,
+                      2 * d, EPI_RELU});
             }
             {
                 StageTimer t(h, 1, s);
-                gemm({L.h1, d, param((pre + "w2").c_str()), d, param((pre + "b2").c_str()), L.logits, d,
-                             nullptr, p.n_int_in, d, d, EPI_NONE});
+                gemm({L.h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), L.h2, 4 * d, nullptr, M, 4 * d, 4 * d,
+                      EPI_RELU});
+            }
+            StageTimer t(h, 1, s);
+            gemm({L.h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), L.states, 2 * d, P + st.e, M, 2 * d,
+                  4 * d, EPI_BETA_REG});
+        } else {
+            // every intersection group of one stage; its inputs are the rows
+            // in_base .. in_base + n_in - 1 of the state buffer
+            GroupArgs g{P + st.a, P + st.b, P + st.c, P + st.d, P + st.e, P + st.f, st.count};
+            const float* sin = L.states + (int64_t)st.in_base * W;
+            const int n_in = st.n_in;
+            if (betae) {
+                {
+                    StageTimer t(h, 2, s);
+                    launch_betae_int_prep(g, sin, d, L.xbuf, s);
+                }
+                {
+                    StageTimer t(h, 1, s);
+                    gemm({L.xbuf, 2 * d, param("inter.w1"), 2 * d, param("inter.b1"), L.h1, 2 * d, nullptr, n_in,
+                          2 * d, 2 * d, EPI_RELU});
+                }
+                {
+                    StageTimer t(h, 1, s);
+                    gemm({L.h1, 2 * d, param("inter.w2"), 2 * d, param("inter.b2"), L.logits, d, nullptr, n_in, d,
+                          2 * d, EPI_NONE});
+                }
+                StageTimer t(h, 2, s);
+                launch_betae_combine(g, L.xbuf, L.logits, d, L.states, s);
+                continue;
+            }
+            {
+                StageTimer t(h, 1, s);
+                gemm({sin, W, param((pre + "w1").c_str()), d, param((pre + "b1").c_str()), L.h1, d, nullptr, n_in, d,
+                      d, EPI_RELU});
+            }
+            {
+                StageTimer t(h, 1, s);
+                gemm({L.h1, d, param((pre + "w2").c_str()), d, param((pre + "b2").c_str()), L.logits, d, nullptr,
+                      n_in, d, d, EPI_NONE});
             }
             if (q2b) {
                 StageTimer t(h, 1, s);
-                gemm({L.states + d, W, param("inter.offset.w1"), d, param("inter.offset.b1"), L.zfeat, d,
-                             nullptr, p.n_int_in, d, d, EPI_RELU});
+                gemm({sin + d, W, param("inter.offset.w1"), d, param("inter.offset.b1"), L.zfeat, d, nullptr, n_in,
+                      d, d, EPI_RELU});
             }
             {
                 StageTimer t(h, 2, s);
-                launch_combine_center(c.model, g, L.states, W, L.logits, L.zfeat, L.zmean, rels, rel_c, n_rel,
-                                      d, L.states, L.dflag, s);
+                launch_combine_center(c.model, g, sin, W, L.logits, L.zfeat, L.zmean, rels, rel_c, n_rel, d,
+                                      L.states, L.dflag, s);
             }
             if (q2b) {
                 {
                     StageTimer t(h, 1, s);
-                    gemm({L.zmean, d, param("inter.offset.w2"), d, param("inter.offset.b2"), L.gate, d,
-                                 nullptr, p.n_groups, d, d, EPI_NONE});
+                    gemm({L.zmean, d, param("inter.offset.w2"), d, param("inter.offset.b2"), L.gate, d, nullptr,
+                          st.count, d, d, EPI_NONE});
                 }
                 StageTimer t(h, 2, s);
-                launch_combine_offset(g, L.states, W, L.gate, rels, h->rel_o_sp, n_rel, d, L.states, L.dflag, s);
+                launch_combine_offset(g, sin, W, L.gate, rels, h->rel_o_sp, n_rel, d, L.states, L.dflag, s);
             }
         }
-    } else {
-        const float* rel = param("relation");
-        auto mlp_level = [&](int l) {
-            const int M = (int)p.lv_dst[l].size();
-            if (!M) return;
-            if (l == 0) {
-                // first hop: every input is an anchor entity, so the first
-                // layer is a gather from the precomputed tables
-                StageTimer t(h, 0, s);
-                launch_betae_proj1(P + p.off.lv_anchor[0], P + p.off.lv_rel[0], M, anchors, rels, h->proj1_ent,
-                                   h->proj1_rel, N, n_rel, 4 * d, L.h1, L.dflag, s);
-            } else {
-                {
-                    StageTimer t(h, 0, s);
-                    launch_betae_proj_prep(P + p.off.lv_src[l], P + p.off.lv_anchor[l], P + p.off.lv_rel[l], M,
-                                           anchors, rels, L.states, h->ent_rm, rel, N, n_rel, d, L.xbuf, L.dflag, s);
-                }
-                StageTimer t(h, 1, s);
-                gemm({L.xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), L.h1, 4 * d, nullptr, M,
-                             4 * d, 2 * d, EPI_RELU});
-            }
-            {
-                StageTimer t(h, 1, s);
-                gemm({L.h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), L.h2, 4 * d, nullptr, M,
-                             4 * d, 4 * d, EPI_RELU});
-            }
-            StageTimer t(h, 1, s);
-            gemm({L.h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), L.states, 2 * d,
-                         P + p.off.lv_dst[l], M, 2 * d, 4 * d, EPI_BETA_REG});
-        };
-        for (int l = 0; l < 3; ++l) mlp_level(l);
-        if (p.n_groups) {
-            {
-                StageTimer t(h, 2, s);
-                launch_betae_int_prep(g, L.states, d, L.xbuf, s);
-            }
-            {
-                StageTimer t(h, 1, s);
-                gemm({L.xbuf, 2 * d, param("inter.w1"), 2 * d, param("inter.b1"), L.h1, 2 * d, nullptr,
-                             p.n_int_in, 2 * d, 2 * d, EPI_RELU});
-            }
-            {
-                StageTimer t(h, 1, s);
-                gemm({L.h1, 2 * d, param("inter.w2"), 2 * d, param("inter.b2"), L.logits, d, nullptr,
-                             p.n_int_in, d, 2 * d, EPI_NONE});
-            }
-            StageTimer t(h, 2, s);
-            launch_betae_combine(g, L.xbuf, L.logits, d, L.states, s);
-        }
-        mlp_level(3);
     }
 
     const int tq = score_row_pad(c.model);
     const int n_rows_pad = ((p.n_score_rows + tq - 1) / tq) * tq;
     {
         StageTimer t(h, 3, s);
-        launch_pack(c.model, P + p.off.score_src, p.n_score_rows, n_rows_pad, L.states, W, d, L.qpack, L.cq, s);
+        launch_pack(c.model, P + p.off_score_src, betae ? P + p.off_score_neg : nullptr, p.n_score_rows, n_rows_pad,
+                    L.states, W, d, L.qpack, L.cq, s);
     }
     float* dst = out_scores ? out_scores : L.scores;
     {
         StageTimer t(h, 4, s);
-        ScoreArgs a{c.model, L.qpack, h->ent_blk, L.cq, h->ent_const, P + p.off.out_dest, p.n_score_rows,
-                    p.n_union_rows, d, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
+        ScoreArgs a{c.model, L.qpack, h->ent_blk, L.cq, h->ent_const, P + p.off_out_dest, p.n_score_rows,
+                    p.n_quad_rows, p.n_pair_rows, d, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
         a.part = L.score_ws;
         a.part_elems = L.score_ws_elems;
         launch_score(a, s);
@@ -616,10 +680,59 @@ const char* kgq_create_error(void) { return g_create_error.c_str(); }
 
 kgq_status kgq_structure_arity(int32_t structure_id, int32_t* n_anchors, int32_t* n_relations)
 {
-    const StructureDef* d = structure_def(structure_id);
-    if (!d || !n_anchors || !n_relations) return KGQ_E_INVALID_ARG;
-    *n_anchors = d->n_anchors;
-    *n_relations = d->n_relations;
+    const Program* g = builtin_program(KGQ_BETAE, structure_id);   // every built-in compiles for BetaE
+    if (!g || !n_anchors || !n_relations) return KGQ_E_INVALID_ARG;
+    *n_anchors = g->n_anchors;
+    *n_relations = g->n_relations;
+    return KGQ_OK;
+}
+
+kgq_status kgq_parse_structure(const char* text, kgq_node* nodes, int32_t capacity, int32_t* n_nodes)
+{
+    if (!text || !nodes || !n_nodes || capacity < 1) return KGQ_E_INVALID_ARG;
+    std::vector<kgq_node> v;
+    std::string err;
+    if (!parse_graph(text, v, err) || (int32_t)v.size() > capacity) return KGQ_E_INVALID_ARG;
+    std::memcpy(nodes, v.data(), v.size() * sizeof(kgq_node));
+    *n_nodes = (int32_t)v.size();
+    return KGQ_OK;
+}
+
+kgq_status kgq_compile_structure(kgq_handle* h, const kgq_node* nodes, int32_t n_nodes, int32_t* structure_id)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (!nodes || !structure_id) return fail(h, KGQ_E_INVALID_ARG, "nodes and structure_id must not be NULL");
+    if ((int)h->compiled.size() >= KGQ_MAX_COMPILED)
+        return fail(h, KGQ_E_INVALID_ARG, "the handle already holds KGQ_MAX_COMPILED compiled structures");
+    std::unique_ptr<Program> g(new Program());
+    std::string err;
+    int st = 0;
+    const int id = kNumStructures + (int)h->compiled.size();
+    if (!compile_graph(h->cfg.model, nodes, n_nodes, "#" + std::to_string(id), *g, err, st))
+        return fail(h, (kgq_status)st, err);
+    if (max_batch_for(h, *g) < 1)
+        return fail(h, KGQ_E_INVALID_ARG, "structure #" + std::to_string(id) +
+                                              " needs more scratch for one query than the handle holds");
+    h->table.push_back(g.get());
+    h->compiled.push_back(std::move(g));
+    *structure_id = id;
+    return KGQ_OK;
+}
+
+kgq_status kgq_structure_info(const kgq_handle* h, int32_t structure_id, int32_t* info)
+{
+    if (!h || !info) return KGQ_E_INVALID_ARG;
+    const Program* g = program_of(h, structure_id);
+    if (!g) return KGQ_E_INVALID_ARG;
+    if (!g->supported) return KGQ_E_UNSUPPORTED;
+    info[0] = g->n_anchors;
+    info[1] = g->n_relations;
+    info[2] = g->n_terms;
+    info[3] = (int32_t)g->ops.size();
+    info[4] = g->and_stages;
+    info[5] = program_launches(h->cfg.model, *g, true);
+    info[6] = (int32_t)max_batch_for(h, *g);
+    info[7] = g->negation ? 1 : 0;
     return KGQ_OK;
 }
 
@@ -650,6 +763,7 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out)
     const char* env = std::getenv("KGQ_CHECKED");
     h->checked = env && env[0] == '1';
     build_specs(h.get());
+    build_table(h.get());
     if (h->dry) {
         *out = h.release();
         return KGQ_OK;
@@ -812,33 +926,61 @@ kgq_status kgq_execute(kgq_handle* h, int32_t structure_id, int32_t batch, const
                        float* out_topk_score, void* stream)
 {
     if (!h) return KGQ_E_INVALID_ARG;
-    const StructureDef* sd = structure_def(structure_id);
-    if (!sd) return fail(h, KGQ_E_INVALID_ARG, "unknown structure id " + std::to_string(structure_id));
-    if (sd->negation && h->cfg.model != KGQ_BETAE)
-        return fail(h, KGQ_E_UNSUPPORTED, std::string("structure ") + sd->name + " needs negation (BetaE only)");
+    const Program* g = program_of(h, structure_id);
+    if (!g) return fail(h, KGQ_E_INVALID_ARG, "unknown structure id " + std::to_string(structure_id));
+    if (!g->supported)
+        return fail(h, KGQ_E_UNSUPPORTED, "structure " + g->name + " needs negation (BetaE only)");
     kgq_status st = check_outputs(h, batch, anchors, relations, k, out_scores, out_topk_idx, out_topk_score);
     if (st != KGQ_OK) return st;
+    // built-in structures keep their lowered plan per batch size in a slot
+    // of their own; compiled ones are lowered into the ring slots
+    const bool cached = structure_id < kNumStructures;
+    std::unique_ptr<Plan> fresh;
+    if (!cached || h->dry) {
+        fresh.reset(new Plan());
+        std::string err;
+        int es = 0;
+        if (!lower(h->cfg.model, batch, nullptr, structure_id, g->n_anchors, g->n_relations, false, h->table, *fresh,
+                   err, es))
+            return fail(h, (kgq_status)es, err);
+        st = check_capacity(h, *fresh);
+        if (st != KGQ_OK) return st;
+    }
     if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
     HIP_TRY(h, hipSetDevice(h->cfg.device));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     Lane* L = nullptr;
     st = acquire_lane(h, s, &L);
     if (st != KGQ_OK) return st;
-    const int slot = structure_id;
-    if (L->cached_B[slot] != batch || !L->cached_plan[slot]) {
-        std::unique_ptr<Plan> p(new Plan());
-        std::string err;
-        int es = 0;
-        if (!lower(h->cfg.model, batch, nullptr, structure_id, sd->n_anchors, sd->n_relations, false, *p, err, es))
-            return fail(h, (kgq_status)es, err);
-        st = upload_plan(h, *L, *p, slot, s);
+    const Plan* plan = nullptr;
+    int slot;
+    if (cached) {
+        slot = structure_id;
+        if (L->cached_B[slot] != batch || !L->cached_plan[slot]) {
+            std::unique_ptr<Plan> p(new Plan());
+            std::string err;
+            int es = 0;
+            if (!lower(h->cfg.model, batch, nullptr, structure_id, g->n_anchors, g->n_relations, false, h->table, *p,
+                       err, es))
+                return fail(h, (kgq_status)es, err);
+            st = check_capacity(h, *p);
+            if (st != KGQ_OK) return st;
+            st = upload_plan(h, *L, *p, slot, s);
+            if (st != KGQ_OK) return st;
+            L->cached_plan[slot] = std::move(p);
+            L->cached_B[slot] = batch;
+        }
+        plan = L->cached_plan[slot].get();
+    } else {
+        slot = kNumStructures + L->ring_next;
+        L->ring_next ^= 1;
+        st = upload_plan(h, *L, *fresh, slot, s);
         if (st != KGQ_OK) return st;
-        L->cached_plan[slot] = std::move(p);
-        L->cached_B[slot] = batch;
+        plan = fresh.get();
     }
     const int32_t* P = L->plan_dev + (int64_t)slot * h->plan_words;
-    st = run_plan(h, *L, *L->cached_plan[slot], P, anchors, relations, sd->n_anchors, sd->n_relations,
-                  sd->n_anchors, sd->n_relations, false, k, out_scores, out_topk_idx, out_topk_score, s);
+    st = run_plan(h, *L, *plan, P, anchors, relations, g->n_anchors, g->n_relations, g->n_anchors, g->n_relations,
+                  false, k, out_scores, out_topk_idx, out_topk_score, s);
     L->slot_event_live[slot] = hipEventRecord(L->slot_event[slot], s) == hipSuccess;
     L->done_live = hipEventRecord(L->done, s) == hipSuccess;
     return st;
@@ -855,8 +997,10 @@ kgq_status kgq_execute_mixed(kgq_handle* h, int32_t batch, const int32_t* struct
     std::string err;
     int es = 0;
     Plan plan;
-    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, plan, err, es))
+    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, h->table, plan, err, es))
         return fail(h, (kgq_status)es, err);
+    st = check_capacity(h, plan);
+    if (st != KGQ_OK) return st;
     if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
     HIP_TRY(h, hipSetDevice(h->cfg.device));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -881,17 +1025,20 @@ kgq_status kgq_describe_plan(const kgq_handle* h, int32_t batch, const int32_t* 
     Plan p;
     std::string err;
     int es = 0;
-    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, p, err, es)) {
+    if (!lower(h->cfg.model, batch, structure_ids, 0, kMaxSlots, kMaxSlots, true, h->table, p, err, es)) {
         const_cast<kgq_handle*>(h)->err = err;
         return (kgq_status)es;
     }
-    counts[0] = p.n_chain;
+    counts[0] = p.n_anchor_chains;
     counts[1] = p.n_groups;
     counts[2] = p.n_int_in;
-    for (int l = 0; l < 4; ++l) counts[3 + l] = (int32_t)p.lv_dst[l].size();
+    for (int l = 0; l < 4; ++l) counts[3 + l] = p.level_rows[l];
     counts[7] = p.n_score_rows;
-    counts[8] = p.n_union_rows / 2;
+    counts[8] = p.n_pair_rows / 2;
     counts[9] = plan_launches(p, true);
+    counts[10] = p.n_and_stages;
+    counts[11] = p.n_quad_rows / 4;
+    counts[12] = p.n_state_rows;
     return KGQ_OK;
 }
 

@@ -82,19 +82,25 @@ void launch_validate(const int32_t* anchors, const int32_t* rels, const int32_t*
                      int B, int sa, int sr, int fixed_na, int fixed_nr,
                      int64_t n_ent, int n_rel, int* flag, hipStream_t s);
 
-// GQE / Query2Box translation chains: row c = E[a] + sum_h C[r_h]
-// (Q2B also offset = sum_h softplus(O[r_h])). Width W = d (GQE) or 2d (Q2B).
-void launch_chain(int model, const int32_t* anchor_ref, const int32_t* rel_ref, int n_chain,
-                  const int32_t* anchors, const int32_t* rels, const float* ent_rm,
-                  const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
+// GQE / Query2Box translation chains: row dst[c] = E[a] + sum_h C[r_h]
+// (Q2B also offset = sum_h softplus(O[r_h])) over chain c's relations
+// rel_ref[rel_off[c] .. rel_off[c+1]). Width W = d (GQE) or 2d (Q2B).
+void launch_chain(int model, const int32_t* anchor_ref, const int32_t* rel_off, const int32_t* rel_ref,
+                  const int32_t* dst_row, int n_chain, const int32_t* anchors, const int32_t* rels,
+                  const float* ent_rm, const float* rel_c, const float* rel_o, int64_t n_ent, int n_rel, int d,
                   float* states, int* flag, hipStream_t s);
 
-// Intersection combine, GQE / Q2B centers: softmax over branches of logits,
-// weighted center sum; Q2B also the mean of the offset features. Optional
-// post-projection (center part; Q2B offset part is added in combine2).
+// Intersection groups of one stage. Group g reads input rows in_start[g] ..
+// in_start[g] + n_in[g] - 1 of the stage's block (the `states` argument of
+// the combine kernels points at the block; logits, features and BetaE's
+// prepared inputs are indexed the same way) and writes row out_row[g] of
+// the full state buffer. neg_mask bit j: input j is negated (BetaE). A
+// folded post-chain (GQE / Query2Box) adds the relations
+// post_ref[post_off[g] .. post_off[g+1]).
+constexpr int kGroupInputs = 4;
 struct GroupArgs {
     const int32_t* in_start; const int32_t* n_in; const int32_t* out_row;
-    const int32_t* post_ref; const int32_t* neg_mask; int n_groups;
+    const int32_t* neg_mask; const int32_t* post_off; const int32_t* post_ref; int n_groups;
 };
 void launch_combine_center(int model, const GroupArgs& g, const float* states, int W,
                            const float* logits, const float* zfeat, float* zmean,
@@ -112,21 +118,26 @@ void launch_betae_int_prep(const GroupArgs& g, const float* states, int d, float
 void launch_betae_combine(const GroupArgs& g, const float* x_int, const float* logits, int d,
                           float* states, hipStream_t s);
 // BetaE projection input rows x = base + Rel[r] (base = a state row, or an
-// anchor entity when src_row < 0).
+// anchor entity when src_row < 0; its reciprocal where neg[m] != 0, neg may
+// be NULL).
 void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
-                            int M, const int32_t* anchors, const int32_t* rels,
+                            const int32_t* neg, int M, const int32_t* anchors, const int32_t* rels,
                             const float* states, const float* ent_ab, const float* rel,
                             int64_t n_ent, int n_rel, int d, float* x, int* flag, hipStream_t s);
 
-// Pack scored rows into the scorer's layout; BetaE also C_q = sum lnB(a, b).
-void launch_pack(int model, const int32_t* src_row, int n_rows, int n_rows_pad, const float* states,
-                 int W, int d, float* qpack, double* cq, hipStream_t s);
+// Pack scored rows into the scorer's layout; BetaE also C_q = sum lnB(a, b)
+// and the reciprocal of rows with neg[j] != 0 (neg may be NULL).
+void launch_pack(int model, const int32_t* src_row, const int32_t* neg, int n_rows, int n_rows_pad,
+                 const float* states, int W, int d, float* qpack, double* cq, hipStream_t s);
 
 struct ScoreArgs {
     int model;
     const float* qpack; const float* ent; const double* cq; const double* ee;
+    // Scored rows: [0, n_quad) groups of four (one output each: the max),
+    // then n_pair rows in pairs, then single rows; out_dest lists the output
+    // row of each group, pair and single row in that order.
     const int32_t* out_dest;
-    int n_rows, n_union_rows, d;
+    int n_rows, n_quad, n_pair, d;
     int64_t N, n_blocks;
     float gamma, center_reg;
     float* scores; int64_t ld;
@@ -137,6 +148,14 @@ struct ScoreArgs {
 void launch_rank_answers(const float* scores, int64_t ld, int64_t N, int batch, const int32_t* off,
                          const int32_t* ids, const int32_t* hard, int32_t* rank, double* metrics, int* flag,
                          hipStream_t s);
+
+// Output of the group, pair or single row that starts at scored row r.
+__host__ __device__ inline int score_out_index(int r, int n_quad, int n_pair)
+{
+    if (r < n_quad) return r >> 2;
+    if (r < n_quad + n_pair) return (n_quad >> 2) + ((r - n_quad) >> 1);
+    return (n_quad >> 2) + (n_pair >> 1) + (r - n_quad - n_pair);
+}
 
 void launch_score(const ScoreArgs& a, hipStream_t s);      // GQE, Query2Box: VALU
 void launch_score_kl(const ScoreArgs& a, hipStream_t s);   // BetaE: matrix cores

@@ -1,20 +1,34 @@
-// Host-side plan lowering: a batch of queries (structure ids + the layout of
-// the caller's anchor / relation arrays) -> the row layout and index lists
-// that the device stages consume.
+// Host-side compilation of query structures and lowering of batches.
 //
-// The paper's Graph Capturer (Eq. 2) maps each query to a computation graph
-// whose operator nodes are projections, intersections, unions and
-// negations, and its Operator Fuser groups them horizontally (a projection
-// chain on one path), vertically (an intersection or union across paths)
-// or both. Here that grouping is fixed per structure and per batch:
-//   - every branch of every query is one "chain" row; all chains of the batch
-//     run in one stage (GQE / Query2Box: one kernel; BetaE: one MLP pass per
-//     hop level across all chains that reach that level);
-//   - every intersection of the batch runs in one stage (all groups at once),
-//     with negation folded into the intersection inputs;
-//   - a union keeps its two branches as separate scored rows and the scorer
-//     takes the max (disjunctive normal form, Eq. 1);
-//   - scoring and top-k run once over all scored rows of the batch.
+// The paper's pipeline (Methodology, Fig. 2) maps a first-order query to a
+// computation graph (Graph Capturer, Eq. 2), recognises the operator
+// patterns in it (Pattern Recognizer) and fuses them (Operator Fuser,
+// Algorithm 1: decide a strategy per operator, merge each group into one
+// fused operator, rewrite the graph). Here:
+//
+//   capture     a structure is given as its graph (kgq_node list, or the
+//               text form read by parse_graph); the 14 benchmark structures
+//               are predefined graphs compiled the same way;
+//   recognise   the graph is rewritten into disjunctive normal form (Eq. 1):
+//               unions move to the top (projection and intersection
+//               distribute over them; the negation of a union becomes the
+//               intersection of the negations), and chains of negations
+//               reduce to their parity;
+//   fuse        each maximal run of projections on one path becomes one
+//               chain (horizontal fusion); each intersection becomes one
+//               group whose branches are combined in one pass (vertical
+//               fusion); for GQE / Query2Box a projection run that follows
+//               an intersection is folded into that intersection's combine
+//               (hybrid fusion). Negations become flags on the edges that
+//               read them (an intersection input, a projection source or
+//               the answer).
+//
+// The result, a Program, is a list of fused operators with their schedule
+// position: its intersection stage (one more than the deepest stage below
+// it) and, for BetaE projections, the position within the run of
+// projections since the last stage. lower() then builds one plan for a
+// whole batch, in which every fused operator kind at one schedule position
+// runs as one launch across all queries, whatever their structures.
 #pragma once
 
 #include <stdint.h>
@@ -22,72 +36,120 @@
 #include <string>
 #include <vector>
 
+#include "../../include/kgq.h"
+
 namespace kgq {
 
-struct BranchDef {
-    int anchor;      // anchor slot
-    int n_hops;      // projections on this branch (1..3)
-    int rel[3];      // relation slots in hop order
-    bool negated;    // BetaE: negated before the intersection
+constexpr int kNumStructures = KGQ_NUM_STRUCTURES;   // built-in structure ids 0 .. 13
+constexpr int kMaxTerms = KGQ_MAX_DISJUNCTS;          // conjunctive terms of a node's DNF
+constexpr int kMaxBranches = 4;                       // inputs of one intersection
+constexpr int kMaxSlots = KGQ_MAX_SLOTS;              // anchor slots, relation slots
+constexpr int kMaxGraphNodes = KGQ_MAX_GRAPH_NODES;
+constexpr int kMaxFusedOps = 256;                     // fused operators of one structure
+
+enum OpKind { OP_CHAIN = 0, OP_PROJ = 1, OP_AND = 2 };
+
+struct FusedOp {
+    int kind = OP_CHAIN;
+    // Schedule: CHAIN / PROJ take the stage of their source (0 for an
+    // anchor); AND is stage 1 + the deepest stage among its inputs.
+    int stage = 0;
+    int hop = 0;                  // PROJ: 1 + hop of a PROJ source, else 1
+    int src = -1;                 // CHAIN / PROJ: producing op, or -1 for an anchor
+    int anchor = -1;              //   anchor slot when src < 0
+    bool src_neg = false;         // PROJ: the source is read negated (BetaE)
+    std::vector<int> rels;        // CHAIN: relation slots in hop order; PROJ: one;
+                                  // AND: relation slots of a folded post-chain (GQE / Query2Box)
+    std::vector<int> in;          // AND: input ops, in the graph's order
+    std::vector<char> in_neg;     // AND: inputs read negated (BetaE)
 };
 
-enum MergeKind { MERGE_NONE = 0, MERGE_AND = 1, MERGE_OR = 2 };
-
-struct StructureDef {
-    const char* name;
-    int n_anchors, n_relations;
-    int n_branches;
-    BranchDef br[3];
-    int merge;
-    int post_rel;    // relation slot projected after the intersection, or -1
-    bool negation;   // uses negation (BetaE only)
+struct Program {
+    std::string name;
+    int n_anchors = 0, n_relations = 0;
+    bool negation = false;        // uses negation (BetaE only)
+    bool supported = true;        // false: a built-in structure this model cannot run
+    std::vector<FusedOp> ops;     // every op after its inputs
+    int n_terms = 1;              // conjunctive terms of the answer (1 .. 4)
+    std::vector<int> answer;      // op of each scored row: 1, 2 or 4 rows (3 terms repeat the last)
+    std::vector<char> answer_neg;
+    int and_stages = 0;
+    // per-query needs, for capacity checks
+    int max_stage_level = 0;      // BetaE: largest projection level (rows at one stage and hop)
+    int max_stage_inputs = 0;     // largest intersection-stage input count
+    int max_stage_groups = 0;     // largest intersection-stage group count
+    int image_words = 0;          // plan-image words per query (without per-stage padding)
 };
 
-const StructureDef* structure_def(int id);   // nullptr if out of range
-constexpr int kNumStructures = 14;
+// Read the text form of a graph (post-order nodes, the answer last):
+//   e<k>                 anchor slot k
+//   p(<x>, r<k>)         projection of x by relation slot k
+//   i(<x>, <y>[, ...])   intersection of 2 to 4 subqueries
+//   u(<x>, <y>[, ...])   union of 2 to 4 subqueries
+//   n(<x>)               negation
+// Whitespace is ignored.
+bool parse_graph(const char* text, std::vector<kgq_node>& out, std::string& err);
+
+// Compile a graph for one model. Fails with KGQ_E_INVALID_ARG for a
+// malformed graph and KGQ_E_UNSUPPORTED for negation on GQE / Query2Box.
+bool compile_graph(int model, const kgq_node* nodes, int n, const std::string& name, Program& out,
+                   std::string& err, int& err_status);
+
+// The built-in structures (ids 0 .. 13) compiled for a model.
+const Program* builtin_program(int model, int id);
+const char* builtin_text(int id);
+
+// A stage of a lowered batch: one launch group.
+enum StageKind { ST_CHAIN = 0, ST_LEVEL = 1, ST_AND = 2 };
+
+struct Stage {
+    int kind = ST_CHAIN;
+    int count = 0;                // chains / projection rows / groups
+    int stage = 0, hop = 0;       // schedule position
+    int in_base = 0, n_in = 0;    // ST_AND: the stage's contiguous input rows
+    bool table = false;           // ST_LEVEL: first hop from anchors (first-layer table path)
+    // Image offsets of the stage's lists:
+    //   ST_CHAIN: a anchor_ref, b rel_off (count + 1), c rel_ref, d dst
+    //   ST_LEVEL: a src_row (-1: anchor), b anchor_ref, c rel_ref, d neg, e dst
+    //   ST_AND:   a in_start (relative to in_base), b n_in, c out_row, d neg_mask,
+    //             e post_off (count + 1), f post_ref
+    int64_t a = 0, b = 0, c = 0, d = 0, e = 0, f = 0;
+};
 
 struct Plan {
     int model = 0, B = 0;
-    // chains (rows 0 .. n_chain-1 of the state buffer)
-    int n_chain = 0;
-    std::vector<int32_t> chain_anchor_ref;   // [n_chain]  index into anchors[]
-    std::vector<int32_t> chain_rel_ref;      // [n_chain * 3], -1 = no hop
-    // intersection groups; inputs are chain rows in_start .. in_start+n-1
-    int n_groups = 0, n_int_in = 0;
-    std::vector<int32_t> g_in_start, g_n, g_out, g_post, g_neg;
-    // BetaE projection levels: 0,1,2 = hop levels, 3 = after the intersection
-    std::vector<int32_t> lv_src[4], lv_anchor[4], lv_rel[4], lv_dst[4];
-    // scoring: rows [0, n_union_rows) are union pairs, then single rows
-    int n_score_rows = 0, n_union_rows = 0;
-    std::vector<int32_t> score_src;          // state row of each scored row
-    std::vector<int32_t> out_dest;           // query index of each output
-    std::vector<int32_t> arity;              // [2B] (mixed batches)
+    std::vector<Stage> stages;    // in execution order
     int n_state_rows = 0;
-
-    // Flattened device image: every list above at a fixed offset.
+    // Scored rows: groups of four (answers with 3 or 4 terms), then pairs,
+    // then single rows, each region in query order; one output per group.
+    int n_score_rows = 0, n_quad_rows = 0, n_pair_rows = 0;
+    // summary counts
+    int n_anchor_chains = 0, n_groups = 0, n_int_in = 0, n_and_stages = 0;
+    int level_rows[4] = {0, 0, 0, 0};   // BetaE: stage-0 hops 1, 2, >= 3; later stages
+    int max_level = 0, max_and_in = 0, max_and_groups = 0;
+    // Flattened device image: every list at a fixed, 16-byte aligned offset.
     std::vector<int32_t> image;
-    struct Off {
-        int64_t chain_anchor, chain_rel, g_in_start, g_n, g_out, g_post, g_neg;
-        int64_t lv_src[4], lv_anchor[4], lv_rel[4], lv_dst[4];
-        int64_t score_src, out_dest, arity;
-    } off{};
+    int64_t off_score_src = 0, off_score_neg = 0, off_out_dest = 0, off_arity = 0;
 };
 
-// Lower a batch. sid(q) gives query q's structure; anchors of query q sit at
-// q * a_stride + slot, relations at q * r_stride + slot. Returns false (with
-// a message) for an unknown structure or a negation structure on a model
-// without negation.
-bool lower(int model, int B, const int32_t* sid, int fixed_sid, int a_stride, int r_stride,
-           bool mixed, Plan& out, std::string& err, int& err_status);
+// Lower a batch. Query q has structure table[sid[q]] (mixed) or
+// table[fixed_sid]; its anchors sit at q * a_stride + slot, its relations at
+// q * r_stride + slot. Returns false with a message for an unknown
+// structure, one the model cannot run, or one with more slots than the
+// strides hold.
+bool lower(int model, int B, const int32_t* sid, int fixed_sid, int a_stride, int r_stride, bool mixed,
+           const std::vector<const Program*>& table, Plan& out, std::string& err, int& err_status);
 
-// Upper bound on the image size (int32 words) for a batch of B queries.
-int64_t plan_image_words(int B);
+// Image words a plan may need beyond the per-query words (list padding and
+// CSR ends).
+constexpr int64_t kPlanOverheadWords = 8192;
 
-// Rows of the state buffer needed per query, at most.
+// Rows of the state buffer reserved per query of max_batch.
 constexpr int kStateRowsPerQuery = 8;
 
-// Number of kernel launches one execute of this plan makes (without the
-// checked-mode validation).
+// Kernel launches one execute of this plan makes (without the checked-mode
+// validation and without the second pass of a split small-batch layer).
 int plan_launches(const Plan& p, bool topk);
+int program_launches(int model, const Program& prog, bool topk);
 
 }  // namespace kgq

@@ -22,7 +22,13 @@ F32, BF16 = 0, 1
 NUM_STRUCTURES = 14
 MAX_K = 1024
 PLAN_FIELDS = ["chains", "groups", "intersection_inputs", "level1", "level2", "level3", "post",
-               "scored_rows", "union_pairs", "launches"]
+               "scored_rows", "union_pairs", "launches", "intersection_stages", "union_quads", "state_rows"]
+INFO_FIELDS = ["anchors", "relations", "terms", "fused_ops", "intersection_stages", "launches", "max_batch",
+               "negation"]
+# Graph node ops (kgq_op) and the node record (kgq_node): op, slot, in[4].
+OP_ANCHOR, OP_PROJECT, OP_AND, OP_OR, OP_NOT = 0, 1, 2, 3, 4
+NODE_WORDS = 6
+MAX_GRAPH_NODES = 64
 STAGES = ["chain", "dense", "combine", "pack", "score", "topk"]
 
 OK = 0
@@ -70,6 +76,9 @@ def lib() -> ctypes.CDLL:
         "kgq_execute_mixed": ([vp, i32, i32p, vp, vp, i32, vp, vp, vp, vp], i32),
         "kgq_set_checked": ([vp, i32], i32),
         "kgq_describe_plan": ([vp, i32, i32p, i32p], i32),
+        "kgq_parse_structure": ([ctypes.c_char_p, i32p, i32, i32p], i32),
+        "kgq_compile_structure": ([vp, i32p, i32, i32p], i32),
+        "kgq_structure_info": ([vp, i32, i32p], i32),
         "kgq_memory": ([vp, i64p, i64p], i32),
         "kgq_rank_answers": ([vp, i32, vp, i64, vp, vp, vp, vp, vp, vp], i32),
         "kgq_dense": ([vp, vp, i32, i32, vp, vp, i32, i32, vp, vp], i32),
@@ -96,6 +105,19 @@ def arity(structure: int):
     if rc != OK:
         raise KgqError(rc, f"structure {structure}")
     return a.value, r.value
+
+
+def parse_structure(text: str) -> np.ndarray:
+    """Nodes [n x 6] int32 (op, slot, in0..in3) of a graph in the library's
+    text form, e.g. "p(i(p(e0,r0),p(e1,r1)),r2)"; raises KgqError on a
+    syntax error."""
+    buf = np.zeros((MAX_GRAPH_NODES, NODE_WORDS), np.int32)
+    n = ctypes.c_int32()
+    rc = lib().kgq_parse_structure(text.encode(), buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                   MAX_GRAPH_NODES, ctypes.byref(n))
+    if rc != OK:
+        raise KgqError(rc, f"cannot parse {text!r}")
+    return buf[: n.value].copy()
 
 
 def _ptr(t) -> int:
@@ -216,9 +238,24 @@ class Engine:
             self.execute_mixed_into(np.asarray(structure), a, r, kk, out_s, out_i, out_v, stream)
         return {"scores": out_s, "idx": out_i, "score": out_v}
 
+    def compile(self, structure) -> int:
+        """Compile a structure (text form or nodes [n x 6]) into a new
+        structure id of this handle."""
+        nodes = parse_structure(structure) if isinstance(structure, str) else structure
+        g = np.ascontiguousarray(nodes, np.int32).reshape(-1, NODE_WORDS)
+        sid = ctypes.c_int32()
+        self._check(lib().kgq_compile_structure(self.h, g.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                                g.shape[0], ctypes.byref(sid)))
+        return sid.value
+
+    def structure_info(self, structure_id: int) -> Dict[str, int]:
+        info = (ctypes.c_int32 * len(INFO_FIELDS))()
+        self._check(lib().kgq_structure_info(self.h, int(structure_id), info))
+        return dict(zip(INFO_FIELDS, list(info)))
+
     def describe_plan(self, structure_ids: Sequence[int]) -> Dict[str, int]:
         sid = np.ascontiguousarray(structure_ids, np.int32)
-        counts = (ctypes.c_int32 * 10)()
+        counts = (ctypes.c_int32 * len(PLAN_FIELDS))()
         self._check(lib().kgq_describe_plan(self.h, sid.shape[0],
                                             sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), counts))
         return dict(zip(PLAN_FIELDS, list(counts)))
