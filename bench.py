@@ -77,7 +77,7 @@ class Prepared:
     order); otherwise one call per batch, round-robin over n_streams streams.
     """
 
-    def __init__(self, name: str, n_streams: int = 1, merge: bool = True):
+    def __init__(self, name: str, n_streams: int = 1, merge: bool = True, inflight: int = 1):
         import torch
         from paper_2503_02172_amd import kgq, synth
 
@@ -108,6 +108,12 @@ class Prepared:
             ids = np.concatenate(ids)
             groups = [(ids, ids.shape[0], np.concatenate(A), np.concatenate(R))]
         n_streams = min(n_streams, len(groups))
+        # steps in flight: with one call per step, consecutive steps go to
+        # `inflight` streams in turn, each with a scratch lane and outputs of
+        # its own, so one step's small kernels overlap another's scorer
+        self.inflight = max(1, inflight) if len(groups) == 1 else 1
+        if self.inflight > 1:
+            n_streams = self.inflight
         self.eng = kgq.engine_for(w, max_batch=max(g[1] for g in groups), model=model, params=params,
                                   concurrency=n_streams)
         self.streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
@@ -119,6 +125,13 @@ class Prepared:
             idx = torch.empty((n, w.k), dtype=torch.int32, device=dev)
             val = torch.empty((n, w.k), dtype=torch.float32, device=dev)
             self.calls.append((sid, n, a, r, idx, val))
+        # outputs of the other in-flight steps
+        self.outs = [(c[4], c[5]) for c in self.calls[:1]]
+        for _ in range(self.inflight - 1):
+            n = self.calls[0][1]
+            self.outs.append((torch.empty((n, w.k), dtype=torch.int32, device=dev),
+                              torch.empty((n, w.k), dtype=torch.float32, device=dev)))
+        self.n_steps = 0
         self.n_queries = sum(c[1] for c in self.calls)
         # scored rows (union queries score two rows) -> triples per step
         rows = 0
@@ -133,6 +146,13 @@ class Prepared:
         """Enqueue one step: the workload's execute calls, round-robin over the
         streams (independent batches, so calls on different streams overlap)."""
         S = len(self.streams) if n_streams is None else n_streams
+        if self.inflight > 1:
+            j = self.n_steps % S
+            self.n_steps += 1
+            sid, B, a, r, _, _ = self.calls[0]
+            idx, val = self.outs[j]
+            self.eng.execute_mixed_into(sid, a, r, self.w.k, None, idx, val, self.streams[j])
+            return
         for i, (sid, B, a, r, idx, val) in enumerate(self.calls):
             st = self.streams[i % S]
             if np.ndim(sid) == 0:
@@ -326,6 +346,9 @@ def main():
                     help="one execute call per structure batch instead of one mixed call per step")
     ap.add_argument("--streams", type=int, default=2,
                     help="with --per-structure: streams the independent calls are spread over")
+    ap.add_argument("--inflight", type=int, default=1,
+                    help="steps in flight: consecutive steps alternate over this many streams (one scratch "
+                         "lane and output buffer each), so that they overlap on the GPU")
     ap.add_argument("--sweep", default=None, metavar="SIZES",
                     help="instead of the benchmark: per-query time and device memory against batch size, per "
                          "structure, on --workload's tables (comma-separated batch sizes, e.g. 1,16,256,1024)")
@@ -343,7 +366,7 @@ def main():
 
     log(f"[bench] preparing {args.workload}")
     merge = not args.per_structure
-    p = Prepared(args.workload, args.streams, merge)
+    p = Prepared(args.workload, args.streams, merge, args.inflight)
     n_streams = len(p.streams)
     log(f"[bench] warmup {args.warmup}, timing {args.steps} steps: {len(p.calls)} execute call(s) per "
         f"step on {n_streams} stream(s)")

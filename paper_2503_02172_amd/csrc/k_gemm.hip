@@ -3,10 +3,14 @@
 // These are the dense contractions of the operators: BetaE's projection MLP
 // (Eq. 4 of the paper: three matmul + bias layers with ReLU between them)
 // and the attention / set-function MLPs of the intersection operators. Both
-// operands are K-contiguous (A rows, W rows). The tile loop is MfmaTile
-// (mfma_tile.hpp) with 64 x 64 workgroup tiles: at the path's shapes (M of a
-// few thousand rows, N and K of 400 to 1,600) it gives enough workgroups to
-// fill the chip, and measured faster than 64 x 128 or 128 x 128 tiles there.
+// operands are K-contiguous (A rows, W rows). The tile loop (mfma_tile.hpp)
+// runs 64 x 64 workgroup tiles: at the path's shapes (M of a few hundred to a
+// few thousand rows, N and K of 400 to 1,600) they give enough workgroups to
+// fill the chip, and measured faster than 64 x 128, 128 x 64 or 128 x 128
+// tiles there. K a multiple of 32 takes the direct-to-LDS ring of three
+// stages, any other K the register-staged loop. Tiles are dispatched in
+// row-major order split into one contiguous range per XCD, so each XCD's L2
+// sees few distinct rows of A at a time.
 // The epilogue adds the bias, applies the activation and stores each row m at
 // C + map(m) * ldc.
 #include <algorithm>
@@ -16,12 +20,20 @@
 
 namespace kgq {
 
-using GemmTile = MfmaTile<64, 64>;
+using GemmTileLds = MfmaTileLds<64, 64, 3>;
+using GemmTileReg = MfmaTileReg<64, 64>;
 
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
+template <class GemmTile>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs g, int tm, int tn, int per_xcd)
 {
     __shared__ float sm[GemmTile::SMEM];
-    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+    // workgroup b runs on XCD b % 8, which takes positions
+    // [x * per_xcd, (x + 1) * per_xcd) of the row-major tile order
+    const int b = blockIdx.x;
+    const int L = (b & 7) * per_xcd + (b >> 3);
+    if (L >= tm * tn) return;
+    const int mt = L / tn, nt = L - mt * tn;
+    const int m0 = mt * 64, n0 = nt * 64;
     v4f acc[GemmTile::TM][GemmTile::TN];
     GemmTile::run(g.A, g.lda, g.M, g.W, g.ldw, g.N, g.K, m0, n0, sm, acc);
 
@@ -51,6 +63,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
 // Each of S workgroups per tile runs a K slice and writes its partial tile;
 // a second kernel adds the S partials in slice order (deterministic), then
 // the bias and activation, and stores through the row map.
+template <class GemmTile>
 __global__ __launch_bounds__(256) void k_gemm_part(GemmArgs g, int kc)
 {
     __shared__ float sm[GemmTile::SMEM];
@@ -103,13 +116,22 @@ void launch_gemm(const GemmArgs& g, hipStream_t s)
     if (splits > 1) {
         const int kc = (((g.K + splits - 1) / splits) + 31) / 32 * 32;   // slice: a multiple of the 32-wide stage
         const int z = (g.K + kc - 1) / kc;
-        hipLaunchKernelGGL(k_gemm_part, dim3(tn, tm, z), dim3(256), 0, s, g, kc);
+        // every slice but the last has kc (a multiple of 32) of K; the last
+        // has K - (z - 1) * kc, a multiple of 32 exactly when K is
+        if (GemmTileLds::supports(g.K))
+            hipLaunchKernelGGL(k_gemm_part<GemmTileLds>, dim3(tn, tm, z), dim3(256), 0, s, g, kc);
+        else
+            hipLaunchKernelGGL(k_gemm_part<GemmTileReg>, dim3(tn, tm, z), dim3(256), 0, s, g, kc);
         const int64_t total = (int64_t)g.M * g.N;
         hipLaunchKernelGGL(k_gemm_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, g, z);
         return;
     }
-    dim3 grid(tn, tm);
-    hipLaunchKernelGGL(k_gemm, grid, dim3(256), 0, s, g);
+    const int per_xcd = (tiles + 7) / 8;
+    const dim3 grid(per_xcd * 8);
+    if (GemmTileLds::supports(g.K))
+        hipLaunchKernelGGL(k_gemm<GemmTileLds>, grid, dim3(256), 0, s, g, tm, tn, per_xcd);
+    else
+        hipLaunchKernelGGL(k_gemm<GemmTileReg>, grid, dim3(256), 0, s, g, tm, tn, per_xcd);
 }
 
 }  // namespace kgq

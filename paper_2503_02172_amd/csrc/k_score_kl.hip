@@ -12,8 +12,11 @@
 // on v_mfma_f32_16x16x4_f32 (full FP32 inputs and accumulation); the VALU
 // form is bound by the half-rate FMA issue of the vector units.
 //
-// Tiling: MfmaTile (mfma_tile.hpp) with 128-row x 128-entity workgroup
-// tiles, 4 x 4 MFMA tiles of 16 x 16 per wavefront. The epilogue adds
+// Tiling (mfma_tile.hpp): 64-row x 64-entity workgroup tiles, 2 x 2 MFMA
+// tiles of 16 x 16 per wavefront, through the direct-to-LDS ring of three
+// stages when 2d is a multiple of 32 (measured faster, epilogue included,
+// than 128 x 64, 64 x 128 or 128 x 128 tiles and than two or four stages);
+// otherwise the register-staged loop with 128 x 128 tiles. The epilogue adds
 // C_q + E_e in double precision, takes the max over union groups of four
 // and pairs of rows (held by the same lane) and scatters rows to their
 // output positions.
@@ -27,15 +30,15 @@
 
 namespace kgq {
 
-// Workgroup tiles: 128 rows x 128 entities, or 64 x 64 for small batches,
-// where the larger tile leaves the chip underfilled and each workgroup's K
-// loop is a latency chain. Query rows are padded to 128 (kRowTileBetae), a
-// multiple of both.
-template <int KL_BM, int KL_BN>
+// Workgroup tiles: 64 x 64 on the direct-to-LDS loop; on the register-staged
+// loop 128 x 128, or 64 x 64 for small batches, where the larger tile leaves
+// the chip underfilled and each workgroup's K loop is a latency chain. Query
+// rows are padded to 128 (kRowTileBetae), a multiple of every tile's rows.
+template <class KlTile>
 __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int n_nt, int qchunk, int total,
                                                      int per_xcd)
 {
-    using KlTile = MfmaTile<KL_BM, KL_BN>;
+    constexpr int KL_BM = KlTile::kBM, KL_BN = KlTile::kBN;
     __shared__ float sm[KlTile::SMEM];
 
     // XCD-aware order (workgroup b runs on XCD b % 8): chunks of qchunk row
@@ -93,9 +96,10 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     }
 }
 
-template <int BM, int BN>
+template <class Tile>
 static void launch_tiles(const ScoreArgs& a, hipStream_t s)
 {
+    constexpr int BM = Tile::kBM, BN = Tile::kBN;
     const int n_mt = (a.n_rows + BM - 1) / BM;
     const int n_nt = (int)((a.N + BN - 1) / BN);
     const int total = n_mt * n_nt;
@@ -106,16 +110,21 @@ static void launch_tiles(const ScoreArgs& a, hipStream_t s)
     // chunks cost no balance.
     const int64_t tile_bytes = (int64_t)BM * 2 * a.d * 4;
     const int qchunk = (int)std::min<int64_t>(n_mt, std::max<int64_t>(1, (int64_t)(2 << 20) / tile_bytes));
-    hipLaunchKernelGGL((k_score_kl<BM, BN>), dim3(per_xcd * 8), dim3(256), 0, s, a, n_mt, n_nt, qchunk, total,
+    hipLaunchKernelGGL((k_score_kl<Tile>), dim3(per_xcd * 8), dim3(256), 0, s, a, n_mt, n_nt, qchunk, total,
                        per_xcd);
 }
 
 void launch_score_kl(const ScoreArgs& a, hipStream_t s)
 {
     if (a.n_rows <= 0) return;
-    const int64_t big_tiles = (int64_t)((a.n_rows + 127) / 128) * ((a.N + 127) / 128);
-    if (big_tiles < 512) launch_tiles<64, 64>(a, s);
-    else launch_tiles<kRowTileBetae, 128>(a, s);
+    using LdsTile = MfmaTileLds<64, 64, 3>;
+    if (LdsTile::supports(2 * a.d)) {
+        launch_tiles<LdsTile>(a, s);
+    } else {
+        const int64_t big_tiles = (int64_t)((a.n_rows + 127) / 128) * ((a.N + 127) / 128);
+        if (big_tiles < 512) launch_tiles<MfmaTileReg<64, 64>>(a, s);
+        else launch_tiles<MfmaTileReg<kRowTileBetae, 128>>(a, s);
+    }
 }
 
 }  // namespace kgq

@@ -1,31 +1,43 @@
-// Device-side FP32 matrix-core tile loop shared by the dense layers and the
+// Device-side FP32 matrix-core tile loops shared by the dense layers and the
 // BetaE scorer: acc = A[m0 : m0 + BM, :K] . B[n0 : n0 + BN, :K]^T, both
 // operands row-major with K contiguous (A rows: inputs or query rows; B rows:
 // weight rows or entity rows).
 //
-// A workgroup of 4 wavefronts (2 x 2) owns a BM x BN tile; each wavefront
-// computes (BM / 32) x (BN / 32) tiles of v_mfma_f32_16x16x4_f32. K advances
-// BK = 32 at a time through double-buffered LDS with one barrier per stage;
-// the next stage's global loads sit in registers while the current stage
-// computes. Within a 16-wide K slice, lane group g = lane / 16 feeds
-// k = 4g .. 4g + 3 to four consecutive MFMAs from one 128-bit LDS read (a
-// permutation of the reduction order over k).
+// Common to both loops: a workgroup of 4 wavefronts (2 x 2) owns a BM x BN
+// tile; each wavefront computes (BM / 32) x (BN / 32) tiles of
+// v_mfma_f32_16x16x4_f32. Within a 16-wide K slice, lane group g = lane / 16
+// feeds k = 4g .. 4g + 3 to four consecutive MFMAs from one 128-bit LDS read
+// (a permutation of the reduction order over k, the same in both loops, so
+// they give identical results). Rows of A at or past M and rows of B at or
+// past N are read from the last valid row (their products only reach outputs
+// the caller discards). Rows must be 16-byte aligned.
 //
-// Edges: rows of A at or past M and rows of B at or past N are read from the
-// last valid row (their products only reach outputs the caller discards);
-// K positions at or past K read as zero. K must be a multiple of 4 and rows
-// 16-byte aligned.
+// MfmaTileLds (K a multiple of 32): a ring of S LDS stages of BK = 32 filled
+//   by direct-to-LDS loads (global_load_lds_dwordx4: each wave instruction
+//   writes 1 KiB of LDS, no staging registers, no LDS store instructions).
+//   Stage kt + S - 1 is requested while stage kt computes; one barrier per
+//   stage. Rows are stored unpadded with their 16-byte chunks XOR-swizzled by
+//   row (chunk c of row r at position c ^ (r & 7)), so the fragment reads of
+//   16 rows at one chunk hit distinct banks. The fragment registers are
+//   double-buffered: the second half-stage's fragments, and the next stage's
+//   first, are read before the current MFMAs issue.
+// MfmaTileReg (any K multiple of 4): double-buffered LDS, the next stage's
+//   global loads held in registers while the current stage computes, padded
+//   LDS rows; the K tail reads as zero.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 namespace kgq {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 template <int BM, int BN>
-struct MfmaTile {
+struct MfmaTileReg {
+    static constexpr int kBM = BM, kBN = BN;
     static constexpr int BK = 32;
     static constexpr int LD = BK + 4;                  // padded LDS row (floats)
     static constexpr int TM = BM / 32, TN = BN / 32;   // MFMA tiles per wavefront
@@ -116,6 +128,142 @@ struct MfmaTile {
 
     // Output position of acc[i][j][r] within the workgroup tile: row
     // wm * BM/2 + i * 16 + 4 * grp + r, column wn * BN/2 + j * 16 + li.
+    __device__ static int row_of(int i) { return ((threadIdx.x >> 6) >> 1) * (BM / 2) + i * 16 + ((threadIdx.x & 63) >> 4) * 4; }
+    __device__ static int col_of(int j) { return ((threadIdx.x >> 6) & 1) * (BN / 2) + j * 16 + (threadIdx.x & 15); }
+};
+
+// s_waitcnt vmcnt(N) lgkmcnt(0); s_barrier. Written as one asm statement with
+// a memory clobber: the compiler neither moves LDS accesses across it nor
+// adds its own vmcnt(0) (which a __syncthreads() would, draining every
+// outstanding direct-to-LDS load of later stages).
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int BM, int BN, int S>
+struct MfmaTileLds {
+    static constexpr int kBM = BM, kBN = BN;
+    static constexpr int BK = 32;
+    static constexpr int CH = BK / 4;                  // 16-byte chunks per row per stage
+    static constexpr int RPI = 64 / CH;                // rows written by one wave instruction
+    static constexpr int AI = BM / (RPI * 4), BI = BN / (RPI * 4);   // instructions per wave per stage
+    static constexpr int LPS = AI + BI;
+    static constexpr int TM = BM / 32, TN = BN / 32;
+    static constexpr int STAGE = (BM + BN) * BK;       // floats
+    static constexpr int SMEM = S * STAGE;             // floats
+    static_assert(S >= 2 && AI >= 1 && BI >= 1, "tile shape");
+    static_assert((S - 2) * LPS < 64, "vmcnt range");
+
+    __device__ static int swz(int row) { return row & 7; }
+    static bool supports(int K) { return K % BK == 0; }
+
+    __device__ static void run(const float* __restrict__ A, int64_t lda, int M, const float* __restrict__ B,
+                               int64_t ldb, int N, int K, int m0, int n0, float* sm, v4f (&acc)[TM][TN])
+    {
+        const int tid = threadIdx.x, lane = tid & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+        const int wm = wave >> 1, wn = wave & 1;
+        const int grp = lane >> 4, li = lane & 15;
+
+        // Loads: wave instruction t = h * 4 + wave writes rows t * RPI ..
+        // t * RPI + RPI - 1 of the stage's A (or B) block; its lane l lands at
+        // row t * RPI + l / CH, chunk position l % CH, so it reads the global
+        // chunk (l % CH) ^ swz(row).
+        const int lr = lane / CH, lp = lane % CH;
+        const float* ag[AI];
+        const float* bg[BI];
+#pragma unroll
+        for (int h = 0; h < AI; ++h) {
+            const int row = (h * 4 + wave) * RPI + lr;
+            ag[h] = A + (int64_t)min(m0 + row, M - 1) * lda + (lp ^ swz(row)) * 4;
+        }
+#pragma unroll
+        for (int h = 0; h < BI; ++h) {
+            const int row = (h * 4 + wave) * RPI + lr;
+            bg[h] = B + (int64_t)min(n0 + row, N - 1) * ldb + (lp ^ swz(row)) * 4;
+        }
+        auto issue = [&](int kt, int slot) {
+            float* st = sm + slot * STAGE;
+#pragma unroll
+            for (int h = 0; h < AI; ++h)
+                __builtin_amdgcn_global_load_lds((const void*)(ag[h] + kt * BK),
+                                                 (lds_void*)(st + (h * 4 + wave) * RPI * BK), 16, 0, 0);
+#pragma unroll
+            for (int h = 0; h < BI; ++h)
+                __builtin_amdgcn_global_load_lds((const void*)(bg[h] + kt * BK),
+                                                 (lds_void*)(st + BM * BK + (h * 4 + wave) * RPI * BK), 16, 0, 0);
+        };
+
+        // Fragment offsets within a stage (floats): half-stage s covers
+        // chunks 4s .. 4s + 3, lane group grp reads chunk 4s + grp.
+        int aoff[TM][2], boff[TN][2];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wm * (BM / 2) + i * 16 + li;
+#pragma unroll
+            for (int s = 0; s < 2; ++s) aoff[i][s] = row * BK + ((s * 4 + grp) ^ swz(row)) * 4;
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int row = wn * (BN / 2) + j * 16 + li;
+#pragma unroll
+            for (int s = 0; s < 2; ++s) boff[j][s] = BM * BK + row * BK + ((s * 4 + grp) ^ swz(row)) * 4;
+        }
+        v4f fa[2][TM], fb[2][TN];
+        auto read = [&](int slot, int s, int f) {
+            const float* st = sm + slot * STAGE;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[f][i] = *reinterpret_cast<const v4f*>(st + aoff[i][s]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[f][j] = *reinterpret_cast<const v4f*>(st + boff[j][s]);
+        };
+        auto mma = [&](int f) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[f][i][q], fb[f][j][q], acc[i][j], 0, 0, 0);
+        };
+
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+        // The vmcnt accounting below counts only this loop's loads: the
+        // caller has no vector-memory load outstanding on entry.
+        const int nk = K / BK;
+#pragma unroll
+        for (int s = 0; s < S - 1; ++s)
+            if (s < nk) issue(s, s);
+        if (nk >= S - 1) wait_vm_barrier<(S - 2) * LPS>();   // stage 0 landed
+        else wait_vm_barrier<0>();
+        read(0, 0, 0);
+        for (int kt = 0; kt < nk; ++kt) {
+            // Slot (kt + S - 1) % S was last read in stage kt - 1; every wave
+            // passed the barrier after finishing those reads.
+            const bool more = kt + S - 1 < nk;
+            if (more) issue(kt + S - 1, (kt + S - 1) % S);
+            read(kt % S, 1, 1);
+            mma(0);
+            if (kt + 1 < nk) {
+                // stage kt + 1 landed for this wave (later stages may still be
+                // in flight); the barrier makes it so for every wave
+                if (more) wait_vm_barrier<(S - 2) * LPS>();
+                else wait_vm_barrier<0>();
+                read((kt + 1) % S, 0, 0);
+            }
+            mma(1);
+        }
+    }
+
     __device__ static int row_of(int i) { return ((threadIdx.x >> 6) >> 1) * (BM / 2) + i * 16 + ((threadIdx.x & 63) >> 4) * 4; }
     __device__ static int col_of(int j) { return ((threadIdx.x >> 6) & 1) * (BN / 2) + j * 16 + (threadIdx.x & 15); }
 };
