@@ -7,7 +7,7 @@
 // runs 64 x 64 workgroup tiles: at the path's shapes (M of a few hundred to a
 // few thousand rows, N and K of 400 to 1,600) they give enough workgroups to
 // fill the chip, and measured faster than 64 x 128, 128 x 64 or 128 x 128
-// tiles there. K a multiple of 32 takes the direct-to-LDS ring of three
+// tiles there. K a multiple of 16 takes the direct-to-LDS ring of three
 // stages, any other K the register-staged loop. Tiles are dispatched in
 // row-major order split into one contiguous range per XCD, so each XCD's L2
 // sees few distinct rows of A at a time.
@@ -21,6 +21,7 @@
 namespace kgq {
 
 using GemmTileLds = MfmaTileLds<64, 64, 3>;
+using GemmTileLdsHalf = MfmaTileLds<64, 64, 3, true>;
 using GemmTileReg = MfmaTileReg<64, 64>;
 
 template <class GemmTile>
@@ -63,15 +64,23 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, int tm, int tn, int pe
 // Each of S workgroups per tile runs a K slice and writes its partial tile;
 // a second kernel adds the S partials in slice order (deterministic), then
 // the bias and activation, and stores through the row map.
-template <class GemmTile>
+// Slices before the last have kc of K (a multiple of 32) and run on
+// SliceTile; the last has the rest and runs on LastTile.
+template <class SliceTile, class LastTile>
 __global__ __launch_bounds__(256) void k_gemm_part(GemmArgs g, int kc)
 {
+    using GemmTile = SliceTile;
+    static_assert(SliceTile::SMEM == LastTile::SMEM && SliceTile::TM == LastTile::TM &&
+                  SliceTile::TN == LastTile::TN, "tile loops of one shape");
     __shared__ float sm[GemmTile::SMEM];
     const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
     const int k0 = blockIdx.z * kc;
     const int kn = min(kc, g.K - k0);
     v4f acc[GemmTile::TM][GemmTile::TN];
-    GemmTile::run(g.A + k0, g.lda, g.M, g.W + k0, g.ldw, g.N, kn, m0, n0, sm, acc);
+    if (blockIdx.z + 1 < gridDim.z)
+        SliceTile::run(g.A + k0, g.lda, g.M, g.W + k0, g.ldw, g.N, kn, m0, n0, sm, acc);
+    else
+        LastTile::run(g.A + k0, g.lda, g.M, g.W + k0, g.ldw, g.N, kn, m0, n0, sm, acc);
     float* part = g.ws + (int64_t)blockIdx.z * g.M * g.N;
 #pragma unroll
     for (int j = 0; j < GemmTile::TN; ++j) {
@@ -117,11 +126,13 @@ void launch_gemm(const GemmArgs& g, hipStream_t s)
         const int kc = (((g.K + splits - 1) / splits) + 31) / 32 * 32;   // slice: a multiple of the 32-wide stage
         const int z = (g.K + kc - 1) / kc;
         // every slice but the last has kc (a multiple of 32) of K; the last
-        // has K - (z - 1) * kc, a multiple of 32 exactly when K is
+        // has K - (z - 1) * kc, congruent to K modulo 32
         if (GemmTileLds::supports(g.K))
-            hipLaunchKernelGGL(k_gemm_part<GemmTileLds>, dim3(tn, tm, z), dim3(256), 0, s, g, kc);
+            hipLaunchKernelGGL((k_gemm_part<GemmTileLds, GemmTileLds>), dim3(tn, tm, z), dim3(256), 0, s, g, kc);
+        else if (GemmTileLdsHalf::supports(g.K))
+            hipLaunchKernelGGL((k_gemm_part<GemmTileLds, GemmTileLdsHalf>), dim3(tn, tm, z), dim3(256), 0, s, g, kc);
         else
-            hipLaunchKernelGGL(k_gemm_part<GemmTileReg>, dim3(tn, tm, z), dim3(256), 0, s, g, kc);
+            hipLaunchKernelGGL((k_gemm_part<GemmTileReg, GemmTileReg>), dim3(tn, tm, z), dim3(256), 0, s, g, kc);
         const int64_t total = (int64_t)g.M * g.N;
         hipLaunchKernelGGL(k_gemm_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, g, z);
         return;
@@ -130,6 +141,8 @@ void launch_gemm(const GemmArgs& g, hipStream_t s)
     const dim3 grid(per_xcd * 8);
     if (GemmTileLds::supports(g.K))
         hipLaunchKernelGGL(k_gemm<GemmTileLds>, grid, dim3(256), 0, s, g, tm, tn, per_xcd);
+    else if (GemmTileLdsHalf::supports(g.K))
+        hipLaunchKernelGGL(k_gemm<GemmTileLdsHalf>, grid, dim3(256), 0, s, g, tm, tn, per_xcd);
     else
         hipLaunchKernelGGL(k_gemm<GemmTileReg>, grid, dim3(256), 0, s, g, tm, tn, per_xcd);
 }

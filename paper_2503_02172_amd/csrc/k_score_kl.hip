@@ -14,7 +14,7 @@
 //
 // Tiling (mfma_tile.hpp): 64-row x 64-entity workgroup tiles, 2 x 2 MFMA
 // tiles of 16 x 16 per wavefront, through the direct-to-LDS ring of three
-// stages when 2d is a multiple of 32 (measured faster, epilogue included,
+// stages when 2d is a multiple of 16 (measured faster, epilogue included,
 // than 128 x 64, 64 x 128 or 128 x 128 tiles and than two or four stages);
 // otherwise the register-staged loop with 128 x 128 tiles. The epilogue adds
 // C_q + E_e in double precision, takes the max over union groups of four
@@ -118,8 +118,11 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
 {
     if (a.n_rows <= 0) return;
     using LdsTile = MfmaTileLds<64, 64, 3>;
+    using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
     if (LdsTile::supports(2 * a.d)) {
         launch_tiles<LdsTile>(a, s);
+    } else if (LdsTileHalf::supports(2 * a.d)) {
+        launch_tiles<LdsTileHalf>(a, s);
     } else {
         const int64_t big_tiles = (int64_t)((a.n_rows + 127) / 128) * ((a.N + 127) / 128);
         if (big_tiles < 512) launch_tiles<MfmaTileReg<64, 64>>(a, s);

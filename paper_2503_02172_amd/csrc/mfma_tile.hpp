@@ -12,7 +12,7 @@
 // past N are read from the last valid row (their products only reach outputs
 // the caller discards). Rows must be 16-byte aligned.
 //
-// MfmaTileLds (K a multiple of 32): a ring of S LDS stages of BK = 32 filled
+// MfmaTileLds (K a multiple of 16): a ring of S LDS stages of BK = 32 filled
 //   by direct-to-LDS loads (global_load_lds_dwordx4: each wave instruction
 //   writes 1 KiB of LDS, no staging registers, no LDS store instructions).
 //   Stage kt + S - 1 is requested while stage kt computes; one barrier per
@@ -20,7 +20,11 @@
 //   row (chunk c of row r at position c ^ (r & 7)), so the fragment reads of
 //   16 rows at one chunk hit distinct banks. The fragment registers are
 //   double-buffered: the second half-stage's fragments, and the next stage's
-//   first, are read before the current MFMAs issue.
+//   first, are read before the current MFMAs issue. The HALF instantiation
+//   serves K an odd multiple of 16: one more stage holds the last 16 of K,
+//   its lanes whose chunk lies past K load a chunk 16 floats lower in the
+//   same row instead (in bounds, never read), and it runs its first half
+//   only. (Kept out of the other instantiation, whose loop it slowed by 3%.)
 // MfmaTileReg (any K multiple of 4): double-buffered LDS, the next stage's
 //   global loads held in registers while the current stage computes, padded
 //   LDS rows; the K tail reads as zero.
@@ -145,7 +149,7 @@ __device__ __forceinline__ void wait_vm_barrier()
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-template <int BM, int BN, int S>
+template <int BM, int BN, int S, bool HALF = false>
 struct MfmaTileLds {
     static constexpr int kBM = BM, kBN = BN;
     static constexpr int BK = 32;
@@ -160,7 +164,7 @@ struct MfmaTileLds {
     static_assert((S - 2) * LPS < 64, "vmcnt range");
 
     __device__ static int swz(int row) { return row & 7; }
-    static bool supports(int K) { return K % BK == 0; }
+    static bool supports(int K) { return K > 0 && K % BK == (HALF ? 16 : 0); }
 
     __device__ static void run(const float* __restrict__ A, int64_t lda, int M, const float* __restrict__ B,
                                int64_t ldb, int N, int K, int m0, int n0, float* sm, v4f (&acc)[TM][TN])
@@ -175,17 +179,22 @@ struct MfmaTileLds {
         // row t * RPI + l / CH, chunk position l % CH, so it reads the global
         // chunk (l % CH) ^ swz(row).
         const int lr = lane / CH, lp = lane % CH;
+        const int nfull = K / BK;                       // full stages
+        const int nk = nfull + (HALF ? 1 : 0);          // HALF: one more stage holding 16 of K
         const float* ag[AI];
         const float* bg[BI];
+        bool aup[AI], bup[BI];                           // loads a chunk of the upper half-stage
 #pragma unroll
         for (int h = 0; h < AI; ++h) {
-            const int row = (h * 4 + wave) * RPI + lr;
-            ag[h] = A + (int64_t)min(m0 + row, M - 1) * lda + (lp ^ swz(row)) * 4;
+            const int row = (h * 4 + wave) * RPI + lr, c = lp ^ swz(row);
+            ag[h] = A + (int64_t)min(m0 + row, M - 1) * lda + c * 4;
+            aup[h] = c >= 4;
         }
 #pragma unroll
         for (int h = 0; h < BI; ++h) {
-            const int row = (h * 4 + wave) * RPI + lr;
-            bg[h] = B + (int64_t)min(n0 + row, N - 1) * ldb + (lp ^ swz(row)) * 4;
+            const int row = (h * 4 + wave) * RPI + lr, c = lp ^ swz(row);
+            bg[h] = B + (int64_t)min(n0 + row, N - 1) * ldb + c * 4;
+            bup[h] = c >= 4;
         }
         auto issue = [&](int kt, int slot) {
             float* st = sm + slot * STAGE;
@@ -197,6 +206,27 @@ struct MfmaTileLds {
             for (int h = 0; h < BI; ++h)
                 __builtin_amdgcn_global_load_lds((const void*)(bg[h] + kt * BK),
                                                  (lds_void*)(st + BM * BK + (h * 4 + wave) * RPI * BK), 16, 0, 0);
+        };
+        // the half stage: chunks past K come from 16 floats lower in the row
+        auto issue_half = [&](int kt, int slot) {
+            float* st = sm + slot * STAGE;
+#pragma unroll
+            for (int h = 0; h < AI; ++h)
+                __builtin_amdgcn_global_load_lds((const void*)(ag[h] + kt * BK - (aup[h] ? 16 : 0)),
+                                                 (lds_void*)(st + (h * 4 + wave) * RPI * BK), 16, 0, 0);
+#pragma unroll
+            for (int h = 0; h < BI; ++h)
+                __builtin_amdgcn_global_load_lds((const void*)(bg[h] + kt * BK - (bup[h] ? 16 : 0)),
+                                                 (lds_void*)(st + BM * BK + (h * 4 + wave) * RPI * BK), 16, 0, 0);
+        };
+        auto issue_any = [&](int kt, int slot) {
+            if constexpr (HALF) {
+                if (kt == nfull) {
+                    issue_half(kt, slot);
+                    return;
+                }
+            }
+            issue(kt, slot);
         };
 
         // Fragment offsets within a stage (floats): half-stage s covers
@@ -239,18 +269,17 @@ struct MfmaTileLds {
 
         // The vmcnt accounting below counts only this loop's loads: the
         // caller has no vector-memory load outstanding on entry.
-        const int nk = K / BK;
 #pragma unroll
         for (int s = 0; s < S - 1; ++s)
-            if (s < nk) issue(s, s);
+            if (s < nk) issue_any(s, s);
         if (nk >= S - 1) wait_vm_barrier<(S - 2) * LPS>();   // stage 0 landed
         else wait_vm_barrier<0>();
         read(0, 0, 0);
-        for (int kt = 0; kt < nk; ++kt) {
+        for (int kt = 0; kt < nfull; ++kt) {
             // Slot (kt + S - 1) % S was last read in stage kt - 1; every wave
             // passed the barrier after finishing those reads.
             const bool more = kt + S - 1 < nk;
-            if (more) issue(kt + S - 1, (kt + S - 1) % S);
+            if (more) issue_any(kt + S - 1, (kt + S - 1) % S);
             read(kt % S, 1, 1);
             mma(0);
             if (kt + 1 < nk) {
@@ -262,6 +291,8 @@ struct MfmaTileLds {
             }
             mma(1);
         }
+        // the half stage: its first half-stage fragments are in buffer 0
+        if constexpr (HALF) mma(0);
     }
 
     __device__ static int row_of(int i) { return ((threadIdx.x >> 6) >> 1) * (BM / 2) + i * 16 + ((threadIdx.x & 63) >> 4) * 4; }

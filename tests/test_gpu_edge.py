@@ -163,7 +163,11 @@ def test_gpu_deterministic_and_stream():
 
 
 @pytest.mark.parametrize("M,N,K,act", [(1, 1, 4, 0), (37, 50, 12, 1), (130, 1600, 800, 1), (700, 800, 1600, 2),
-                                       (64, 64, 64, 0), (1029, 400, 400, 0)])
+                                       (64, 64, 64, 0), (1029, 400, 400, 0),
+                                       # direct-to-LDS loop: one half stage, stages fewer than / equal to
+                                       # the ring, a half last stage after full ones, ragged M and N
+                                       (65, 70, 16, 1), (200, 33, 48, 0), (129, 127, 80, 2), (66, 190, 96, 1),
+                                       (3, 400, 400, 1)])
 def test_gpu_dense_matches_fp64(M, N, K, act):
     import torch
     from paper_2503_02172_amd import kgq
