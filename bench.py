@@ -214,9 +214,22 @@ def stage_breakdown(p: Prepared, reps: int = 3):
     return {k: round(v[0] / reps, 4) for k, v in r.items()}
 
 
-def traffic_for(kernel_src: str, name: str):
+# Sources each scorer kernel is compiled from (the kernel file and the headers
+# it includes); a traffic record is valid only while all of them are unchanged.
+SCORER_SOURCES = {0: ["k_score.hip", "kgq_internal.hpp"], 1: ["k_score.hip", "kgq_internal.hpp"],
+                  2: ["k_score_kl.hip", "mfma_tile.hpp", "kgq_internal.hpp"]}
+
+
+def sources_sha256(files) -> str:
+    h = hashlib.sha256()
+    for f in files:
+        h.update(open(os.path.join(ROOT, "paper_2503_02172_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
+def traffic_for(model: int, name: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel source (else (None, None)): FETCH_SIZE and
+    taken on the current scorer sources (else (None, None)): FETCH_SIZE and
     WRITE_SIZE scaled by a plain copy kernel's readings, and the fetch counted
     by read-request size (plus WRITE_SIZE)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -228,8 +241,8 @@ def traffic_for(kernel_src: str, name: str):
         return None, None
     if not rec:
         return None, None
-    h = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
-    if rec.get("kernel_sha256") != h:
+    files = SCORER_SOURCES[model]
+    if rec.get("kernel_sources") != files or rec.get("sources_sha256") != sources_sha256(files):
         return None, None
     return rec.get("bytes_per_launch"), rec.get("bytes_per_launch_by_request_size")
 
@@ -380,8 +393,7 @@ def main():
     ops_per_launch = total_ops / max(n_launch, 1)
     achieved = ops_per_launch / (avg_launch_ms * 1e-3) if avg_launch_ms > 0 else 0.0
     achieved_busy = total_ops / (busy * 1e-3) if busy > 0 else 0.0
-    src = os.path.join(ROOT, "paper_2503_02172_amd", "csrc", "k_score_kl.hip" if p.model == 2 else "k_score.hip")
-    traffic, traffic_req = traffic_for(src, f"score:{args.workload}")
+    traffic, traffic_req = traffic_for(p.model, f"score:{args.workload}")
     peak, bound, unit = SCORER_PEAK[p.model]
     roofline = {"bound": bound, "kernel": "k_score (entity scorer)" if p.model != 2 else "k_score_kl (entity scorer)",
                 "achieved": round(achieved / 1e12, 3), "peak": round(peak / 1e12, 2),
