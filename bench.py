@@ -324,7 +324,9 @@ def rank_bench(p: Prepared, reps: int = 20):
             "queries_per_s": round(B / (ms * 1e-3), 1)}
 
 
-def cpu_baseline(name: str, per_structure: int):
+def cpu_baseline(name: str, per_structure: int, min_seconds: float = 10.0):
+    """The CPU oracle on the workload's queries (at most per_structure of each
+    structure batch), in whole passes repeated until min_seconds have elapsed."""
     from oracle import oracle as O
     from paper_2503_02172_amd import synth
 
@@ -332,17 +334,23 @@ def cpu_baseline(name: str, per_structure: int):
     m = O.Model(w.model, w.params, w.gamma)
     threads = O.max_threads(0)
     nq = 0
+    passes = 0
     t0 = time.perf_counter()
-    for b in w.batches:
-        n = min(per_structure, b.batch)
-        sid = synth.STRUCTURE_ID[b.structure] if b.structure else b.structure_ids[:n]
-        sc = m.scores(sid, b.anchors[:n], b.relations[:n])
-        O.topk(sc, w.k)
-        nq += n
+    while True:
+        for b in w.batches:
+            n = min(per_structure, b.batch)
+            sid = synth.STRUCTURE_ID[b.structure] if b.structure else b.structure_ids[:n]
+            sc = m.scores(sid, b.anchors[:n], b.relations[:n])
+            O.topk(sc, w.k)
+            nq += n
+        passes += 1
+        if time.perf_counter() - t0 >= min_seconds:
+            break
     dt = time.perf_counter() - t0
+    per_pass = nq // passes
     return {"value": nq / dt, "unit": "queries/s", "cores": threads, "kind": "oracle",
-            "sample": f"{nq} of the {sum(b.batch for b in w.batches)} queries ({per_structure} per "
-                      f"structure), fp64 node-by-node evaluation, full scoring + top-{w.k}",
+            "sample": f"{per_pass} of the {sum(b.batch for b in w.batches)} queries ({per_structure} per "
+                      f"structure) x {passes} passes, fp64 node-by-node evaluation, full scoring + top-{w.k}",
             "seconds": round(dt, 3)}
 
 
