@@ -16,6 +16,8 @@
 // Ids read from device memory are range-checked in every kernel that reads
 // them: an out-of-range id raises a flag bit and is replaced by 0, so no
 // access ever leaves a table.
+#include <algorithm>
+
 #include "kgq_internal.hpp"
 
 namespace kgq {
@@ -140,6 +142,24 @@ __global__ void k_clear_flag(int* flag) { *flag = 0; }
 void launch_clear_flag(int* flag, hipStream_t s)
 {
     hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, flag);
+}
+
+// Plan upload: 16-byte words read from pinned host memory (over the bus)
+// and written to the device slot, by a kernel in the caller's stream order.
+__global__ __launch_bounds__(256) void k_fetch_words(const int4* __restrict__ src, int4* __restrict__ dst,
+                                                     int64_t n4)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256)
+        dst[i] = src[i];
+}
+
+void launch_fetch_words(const int32_t* host_src, int32_t* dst, int64_t n_words, hipStream_t s)
+{
+    const int64_t n4 = (n_words + 3) / 4;
+    if (n4 <= 0) return;
+    const int grid = (int)std::min<int64_t>(64, (n4 + 255) / 256);
+    hipLaunchKernelGGL(k_fetch_words, dim3(grid), dim3(256), 0, s, reinterpret_cast<const int4*>(host_src),
+                       reinterpret_cast<int4*>(dst), n4);
 }
 
 __device__ __forceinline__ int32_t checked_id(int32_t id, int64_t n, int* flag)

@@ -194,7 +194,8 @@ void build_table(kgq_handle* h)
         h->table.push_back(g);
         if (g->supported) words = std::max(words, g->image_words);
     }
-    h->plan_words = Bm * words + kPlanOverheadWords;
+    // slots start at 16-byte boundaries (the upload kernel moves 16-byte words)
+    h->plan_words = (Bm * words + kPlanOverheadWords + 3) / 4 * 4;
     h->cap_rows = Bm * kStateRowsPerQuery;
     h->cap_mlp = 3 * Bm;
     h->cap_groups = h->cap_mlp / 2;   // a group has at least two inputs
@@ -340,8 +341,11 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(L.plan_dev, (int64_t)(kNumStructures + 2) * h->plan_words);
         hipError_t e = hipHostMalloc((void**)&L.hflag, sizeof(int), hipHostMallocDefault);
         if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(flag)");
+        // coherent: the upload kernel reads it over the bus, and a slot is
+        // rewritten by the host after earlier reads, so no stale copy may
+        // stay in a device cache
         e = hipHostMalloc((void**)&L.plan_host, sizeof(int32_t) * (kNumStructures + 2) * h->plan_words,
-                          hipHostMallocDefault);
+                          hipHostMallocCoherent);
         if (e != hipSuccess) return fail(h, KGQ_E_OOM, "hipHostMalloc(plan staging)");
         for (int i = 0; i < kNumStructures + 2; ++i)
             HIP_TRY(h, hipEventCreateWithFlags(&L.slot_event[i], hipEventDisableTiming));
@@ -466,15 +470,20 @@ kgq_status check_capacity(kgq_handle* h, const Plan& p)
                     "structure)");
 }
 
-// Upload a plan image into device slot `slot` (after the slot's last use).
+// Upload a plan image into device slot `slot` (after the slot's last use:
+// the host waits for the execute that last read the slot, which also retires
+// the previous upload out of the slot's pinned staging). The upload is a
+// kernel in the caller's stream that reads the pinned staging over the bus:
+// an asynchronous copy there goes through a copy engine and costs about
+// 26 us of idle device between the previous execute's kernels and this
+// one's, a copy on a stream of its own still about 15 us of cross-queue wait.
 kgq_status upload_plan(kgq_handle* h, Lane& L, const Plan& p, int slot, hipStream_t s)
 {
     if ((int64_t)p.image.size() > h->plan_words) return fail(h, KGQ_E_DEVICE, "plan image exceeds its slot");
     if (L.slot_event_live[slot]) HIP_TRY(h, hipEventSynchronize(L.slot_event[slot]));
     int32_t* host = L.plan_host + (int64_t)slot * h->plan_words;
     std::memcpy(host, p.image.data(), p.image.size() * sizeof(int32_t));
-    HIP_TRY(h, hipMemcpyAsync(L.plan_dev + (int64_t)slot * h->plan_words, host,
-                              p.image.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+    launch_fetch_words(host, L.plan_dev + (int64_t)slot * h->plan_words, (int64_t)p.image.size(), s);
     return KGQ_OK;
 }
 

@@ -77,6 +77,10 @@ void launch_betae_proj1(const int32_t* anchor_ref, const int32_t* rel_ref, int M
 
 void launch_clear_flag(int* flag, hipStream_t s);
 
+// Copy n_words from pinned (device-mapped) host memory to the device with a
+// kernel; both pointers 16-byte aligned, n_words rounded up to a multiple of 4.
+void launch_fetch_words(const int32_t* host_src, int32_t* dst, int64_t n_words, hipStream_t s);
+
 // Checked-mode validation of a batch's ids (and mixed padding).
 void launch_validate(const int32_t* anchors, const int32_t* rels, const int32_t* sid_dev,
                      int B, int sa, int sr, int fixed_na, int fixed_nr,
