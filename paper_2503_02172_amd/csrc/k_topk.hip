@@ -13,9 +13,11 @@
 // every key in that bin or above (k plus the bin's other members) is
 // compacted into LDS as (key, index) composites and sorted, and the first k
 // are the answer, ties included (the composite orders equal keys by index).
-// If that candidate set would exceed the LDS buffer (very many equal or
-// nearly equal scores), exact radix passes of 8 bits narrow the threshold key
-// T down instead, and the keys above T plus the lowest-index keys equal to T
+// If that bin is crowded (scores that span the sign or many exponents make
+// the top bits coarse; more candidates than the 256 of the register sort), a
+// second 11-bit histogram over the bin's keys, still in registers, narrows it. If the candidate set would still exceed the LDS
+// buffer (very many equal or nearly equal scores), exact radix passes of 8
+// bits narrow the threshold key T down instead, and the keys above T plus the lowest-index keys equal to T
 // are taken. Compaction uses a prefix over per-(step, wavefront) ballot
 // counts, so it needs no atomics. Sorting runs in registers inside one
 // wavefront for up to 256 candidates, in LDS across the workgroup otherwise.
@@ -168,7 +170,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(5))) void k_
     __shared__ uint64_t srt[kMaxK];
     __shared__ uint32_t sel_key[kMaxK], sel_idx[kMaxK];
     uint32_t* hist = reinterpret_cast<uint32_t*>(srt);    // 2048 bins
-    __shared__ int sh_bin, sh_rem;
+    __shared__ int sh_bin, sh_rem, sh_binc;
     __shared__ uint32_t sh_or[TK_WAVES], sh_and[TK_WAVES];   // per-wavefront max / min key
     __shared__ int cnt_gt[KPT * TK_WAVES], cnt_eq[KPT * TK_WAVES];
 
@@ -237,57 +239,94 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(5))) void k_
     uint32_t pmask = diff ? ~(0xFFFFFFFFu >> (31 - top)) : 0xFFFFFFFFu;
     uint32_t prefix = kmax & pmask;
 
+    // Bin of the need-th key from the top in hist[0 .. 2047] (run by wavefront
+    // 0; need is at least 1 and at most the histogram's total): sh_bin = that
+    // bin, sh_rem = keys in it and above, sh_binc = keys in it.
+    auto find_bin = [&](uint32_t need) {
+        if (tid >= 64) return;
+        // lane l owns bins 32l .. 32l+31; inclusive suffix sum over lanes
+        uint32_t s = 0;
+#pragma unroll
+        for (int t = 0; t < 32; ++t) s += hist[32 * tid + t];
+        uint32_t incl = s;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t v = __shfl_down(incl, off, 64);
+            if (tid + off < 64) incl += v;
+        }
+        const uint32_t above = incl - s;
+        if (above < need && need <= incl) {
+            uint32_t cum = above;
+            for (int t = 31; t >= 0; --t) {
+                const uint32_t c = hist[32 * tid + t];
+                if (need <= cum + c) {
+                    sh_bin = 32 * tid + t;
+                    sh_rem = (int)(cum + c);
+                    sh_binc = (int)c;
+                    break;
+                }
+                cum += c;
+            }
+        }
+    };
+
     // --- one wide histogram pass: the bin of the k-th key -------------------
     // digit = bits [wlo, top], at most 11 bits
     const int wlo = top >= 10 ? top - 10 : 0;
     const uint32_t wmask = top >= 0 ? ((2u << (top - wlo)) - 1u) : 0u;
     int n_cand = (int)n;       // candidates: keys whose digit is >= the k-th key's digit
     uint32_t dmin = 0;         // smallest candidate digit
+    // every key >= thr is a candidate (thr >= 1 keeps the padding out)
+    uint32_t thr = max(prefix, 1u);
     if (top >= 0) {
         for (int b = tid; b < 2048; b += TK_THREADS) hist[b] = 0;
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < KPT; ++j) atomicAdd(&hist[(keys[j] >> wlo) & wmask], 1u);
         __syncthreads();
-        if (tid == 0) hist[0] -= (uint32_t)(KPT * TK_THREADS - nn);   // the padding landed in bin 0
-        if (tid < 64) {
-            // lane l owns bins 32l .. 32l+31; inclusive suffix sum over lanes
-            uint32_t s = 0;
-#pragma unroll
-            for (int t = 0; t < 32; ++t) s += hist[32 * tid + t];
-            uint32_t incl = s;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const uint32_t v = __shfl_down(incl, off, 64);
-                if (tid + off < 64) incl += v;
-            }
-            const uint32_t above = incl - s;
-            if (above < (uint32_t)k && (uint32_t)k <= incl) {
-                uint32_t cum = above;
-                for (int t = 31; t >= 0; --t) {
-                    const uint32_t c = hist[32 * tid + t];
-                    if ((uint32_t)k <= cum + c) {
-                        sh_bin = 32 * tid + t;
-                        sh_rem = (int)(cum + c);      // candidates: bins >= this one
-                        break;
-                    }
-                    cum += c;
-                }
-            }
-        }
+        // the padding landed in bin 0 (thread 0 is in the wavefront that reads
+        // the histogram next, and one wavefront's LDS accesses stay in order)
+        if (tid == 0) hist[0] -= (uint32_t)(KPT * TK_THREADS - nn);
+        find_bin((uint32_t)k);
         __syncthreads();
         dmin = (uint32_t)sh_bin;
         n_cand = sh_rem;
+        // All keys share the bits above `top`, so digit >= dmin is the same
+        // as key >= (common bits, dmin, zeros).
+        thr = max(prefix | (dmin << wlo), 1u);
+        if (n_cand > 256 && wlo > 0) {
+            // The k-th key's bin is crowded (scores spanning the sign or many
+            // exponents make the top 11 bits coarse), so the candidates would
+            // need the LDS sort (more than 256) or the radix passes (more than
+            // kMaxK): a second histogram over the next lower bits of that
+            // bin's keys, still in registers, finds the sub-bin of the key the
+            // bin must contribute.
+            const int above = n_cand - sh_binc;                   // keys in higher bins
+            const int wlo2 = wlo >= 11 ? wlo - 11 : 0;
+            const uint32_t wmask2 = (1u << (wlo - wlo2)) - 1u;
+            for (int b = tid; b < 2048; b += TK_THREADS) hist[b] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < KPT; ++j) {
+                // (the empty asm keeps the compiler from hoisting this pass's
+                // per-key tests above the first pass, where they would stay
+                // live in registers beside the keys)
+                uint32_t kj = keys[j];
+                asm volatile("" : "+v"(kj));
+                if (kj != 0u && ((kj >> wlo) & wmask) == dmin) atomicAdd(&hist[(kj >> wlo2) & wmask2], 1u);
+            }
+            __syncthreads();
+            find_bin((uint32_t)(k - above));
+            __syncthreads();
+            n_cand = above + sh_rem;
+            thr = max(prefix | (dmin << wlo) | ((uint32_t)sh_bin << wlo2), 1u);
+        }
     }
 
     int n_sel;                 // entries placed in sel_key[] / sel_idx[]
     if (n_cand <= kMaxK) {
-        // --- candidates fit: take every key whose digit is >= dmin ----------
-        // All keys share the bits above `top`, so digit >= dmin is the same
-        // as key >= thr with thr = (common bits, dmin, zeros); thr >= 1 keeps
-        // the padding out.
+        // --- candidates fit: take every key >= thr ---------------------------
         n_sel = n_cand;
-        const uint32_t thr = max(top >= 0 ? (prefix | (dmin << wlo)) : prefix, 1u);
         // The sort below orders candidates completely by (key, index), so
         // their slots only need to be distinct: each wavefront takes a range
         // sized by its candidate count and fills it in step order.
