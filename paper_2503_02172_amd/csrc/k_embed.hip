@@ -82,6 +82,33 @@ __device__ double digamma_d(double x)
     return shift + log(x) - 0.5 / x + tail;
 }
 
+// ln Gamma(x) for x >= 8 by Stirling's series (Abramowitz & Stegun 6.1.41),
+// kept through the z^-11 term; the first dropped term is below 2e-14 at x = 8.
+__device__ __forceinline__ double lngamma_stirling(double x)
+{
+    const double r = 1.0 / x, f = r * r;
+    const double tail = r * (1.0 / 12.0 + f * (-1.0 / 360.0 + f * (1.0 / 1260.0 + f * (-1.0 / 1680.0
+                      + f * (1.0 / 1188.0 + f * (-691.0 / 360360.0))))));
+    return (x - 0.5) * log(x) - x + 0.91893853320467274178 + tail;   // + ln sqrt(2 pi)
+}
+
+// ln B(a, b) = ln Gamma(a) + ln Gamma(b) - ln Gamma(a + b) in double
+// precision. Each argument below 8 is shifted up with
+// ln Gamma(x) = ln Gamma(x + 1) - ln x, and the three products of the shifted
+// factors share one logarithm (at most 8 factors each, all in (0, 8), so the
+// products of fp32-sourced arguments stay within double range). Arguments
+// that are not positive (never produced by the BetaE regulariser) take the
+// library lgamma.
+__device__ __forceinline__ double lnbeta_d(double a, double b)
+{
+    if (!(a > 0.0 && b > 0.0)) return lgamma(a) + lgamma(b) - lgamma(a + b);
+    double c = a + b, pa = 1.0, pb = 1.0, pc = 1.0;
+    while (a < 8.0) { pa *= a; a += 1.0; }
+    while (b < 8.0) { pb *= b; b += 1.0; }
+    while (c < 8.0) { pc *= c; c += 1.0; }
+    return lngamma_stirling(a) + lngamma_stirling(b) - lngamma_stirling(c) - log((pa / pc) * pb);
+}
+
 // BetaE entity tables: alpha|beta decoded to fp32 (row-major, for anchor
 // gathers), U|V row-major for the matrix-core scorer (zero rows past N), and
 // E_e, all from the stored values.
@@ -103,7 +130,7 @@ __global__ __launch_bounds__(128) void k_betae_entity_prep(const void* src, int 
             const double pa = digamma_d(a), pb = digamma_d(b), pab = digamma_d(a + b);
             u = (float)(pab - pa);
             v = (float)(pab - pb);
-            const double lnb = lgamma(a) + lgamma(b) - lgamma(a + b);
+            const double lnb = lnbeta_d(a, b);
             acc += -lnb + a * pa + b * pb - (a + b) * pab;
         }
         dst[k] = u;
@@ -554,7 +581,7 @@ __global__ __launch_bounds__(256) void k_pack_rows(const int32_t* src_row, const
                 bf = 1.0f / bf;
             }
             const double a = af, b = bf;
-            lnb += lgamma(a) + lgamma(b) - lgamma(a + b);
+            lnb += lnbeta_d(a, b);
         }
     }
     for (int off = 32; off > 0; off >>= 1) lnb += __shfl_xor(lnb, off, 64);
