@@ -176,12 +176,14 @@ def union_ms(iv: np.ndarray) -> float:
     return total + ce - cs
 
 
-def time_steps(p: Prepared, steps: int, warmup: int, profile_score: bool):
+def time_steps(p: Prepared, steps: int, warmup: int, profile_score: bool, serial: bool = False):
     """Time `steps` steps. With profile_score, HIP events bracket every scorer
-    launch on its stream; returns (seconds, scorer intervals [n x 2] ms)."""
+    launch on its stream; returns (seconds, scorer intervals [n x 2] ms).
+    serial: one stream, one step at a time (no steps in flight)."""
     import torch
+    ns = 1 if serial else None
     for _ in range(warmup):
-        p.step()
+        p.step(ns)
     torch.cuda.synchronize()
     if profile_score:
         p.eng.profile_reset()
@@ -189,7 +191,7 @@ def time_steps(p: Prepared, steps: int, warmup: int, profile_score: bool):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
-        p.step()
+        p.step(ns)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     iv = None
@@ -357,8 +359,8 @@ def cpu_baseline(name: str, per_structure: int, min_seconds: float = 10.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--no-others", action="store_true", help="skip the other four workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -367,9 +369,10 @@ def main():
                     help="one execute call per structure batch instead of one mixed call per step")
     ap.add_argument("--streams", type=int, default=2,
                     help="with --per-structure: streams the independent calls are spread over")
-    ap.add_argument("--inflight", type=int, default=1,
+    ap.add_argument("--inflight", type=int, default=2,
                     help="steps in flight: consecutive steps alternate over this many streams (one scratch "
-                         "lane and output buffer each), so that they overlap on the GPU")
+                         "lane and output buffer each), so that one step's small kernels overlap another's "
+                         "scorer (1: one step at a time)")
     ap.add_argument("--sweep", default=None, metavar="SIZES",
                     help="instead of the benchmark: per-query time and device memory against batch size, per "
                          "structure, on --workload's tables (comma-separated batch sizes, e.g. 1,16,256,1024)")
@@ -410,10 +413,21 @@ def main():
                 "ops_per_launch": ops_per_launch, "avg_launch_ms": round(avg_launch_ms, 5),
                 "launches": n_launch, "scorer_busy_ms": round(busy, 4),
                 "frac_over_busy_time": round(achieved_busy / peak, 4),
-                "timing": "HIP events around every scorer launch on its stream over the timed steps; "
-                          "achieved = algorithmic VALU ops per launch / average launch duration"}
+                "timing": f"HIP events around every scorer launch on its stream over the timed steps "
+                          f"({p.inflight} step(s) in flight); achieved = algorithmic ops per launch / average "
+                          f"launch duration"}
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {qps:.0f} q/s, scorer busy {busy:.2f} ms over "
         f"{n_launch} launches ({avg_launch_ms:.4f} ms each), {roofline['frac']*100:.1f}% of the {bound} peak")
+    serial = None
+    if p.inflight > 1:
+        ds, ivs = time_steps(p, args.steps, 1, profile_score=True, serial=True)
+        avg_s = float(np.mean(ivs[:, 1] - ivs[:, 0])) if len(ivs) else 0.0
+        serial = {"ms_per_step": round(ds / args.steps * 1e3, 4),
+                  "queries_per_s": round(p.n_queries * args.steps / ds, 2),
+                  "scorer_launch_ms": round(avg_s, 5),
+                  "scorer_frac": round(ops_per_launch / (avg_s * 1e-3) / peak, 4) if avg_s > 0 else None}
+        log(f"[bench] one step at a time: {serial['ms_per_step']:.3f} ms/step, {serial['queries_per_s']:.0f} q/s, "
+            f"scorer {avg_s:.4f} ms per launch ({serial['scorer_frac'] * 100:.1f}% of the {bound} peak)")
     stages = stage_breakdown(p)
     log(f"[bench] stage ms per step (one stream, instrumented): {stages}")
     rank = rank_bench(p)
@@ -427,14 +441,20 @@ def main():
             if name == args.workload:
                 continue
             log(f"[bench] other workload {name}")
-            q = Prepared(name, args.streams, merge)
-            steps = max(3, min(args.steps, 10))
-            d2, iv2 = time_steps(q, steps, 2, profile_score=True)
+            q = Prepared(name, args.streams, merge, args.inflight)
+            steps = max(3, min(args.steps, 30))
+            d2, _ = time_steps(q, steps, 2, profile_score=False)
+            # the scorer's own launch time from a pass with one step at a
+            # time (in flight, its launches share the GPU with the other
+            # step's kernels)
+            d1, iv2 = time_steps(q, steps, 1, profile_score=True, serial=True)
             ops = OPS_PER_TRIPLE[q.model] * q.triples * steps
             b2 = union_ms(iv2)
             avg2 = float(np.mean(iv2[:, 1] - iv2[:, 0])) if len(iv2) else 0.0
             others[name] = {"workload": WORKLOAD_DESC[name], "queries_per_s": round(q.n_queries * steps / d2, 1),
                             "ms_per_step": round(d2 / steps * 1e3, 4),
+                            "steps_in_flight": q.inflight,
+                            "serial_ms_per_step": round(d1 / steps * 1e3, 4),
                             "entity_scores_per_s": round(q.n_queries * q.w.n_entities * steps / d2, 1),
                             "scorer_busy_ms_per_step": round(b2 / steps, 5),
                             "scorer_launch_ms": round(avg2, 5),
@@ -469,9 +489,10 @@ def main():
         "data": "synthetic (seeded random tables and queries of the workload's shapes)",
         "config": {"workload": WORKLOAD_DESC[args.workload], "name": args.workload,
                    "queries_per_step": p.n_queries, "scored_rows_per_step": p.rows, "k": p.w.k,
-                   "execute_calls_per_step": len(p.calls), "streams": n_streams},
+                   "execute_calls_per_step": len(p.calls), "streams": n_streams, "steps_in_flight": p.inflight},
         "entity_scores_per_s": round(qps * p.w.n_entities, 1),
         "roofline": roofline,
+        "one_step_at_a_time": serial,
         "stage_ms_per_step": stages,
         "ranking_metrics": rank,
         "cpu_baseline": cpu,
