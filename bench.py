@@ -38,7 +38,7 @@ sys.path.insert(0, ROOT)
 # second, 256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.64e12 (the
 # published 157.3 TFLOP/s FP32 vector peak counted at 2 flops per
 # lane-operation); each sub / add / min of the scorer is one lane-operation
-# (packed FP32 is disabled in this build).
+# (the library is compiled without packed FP32 instructions).
 # BetaE scores on the matrix cores: the published dense FP32 MFMA peak,
 # 157.3 TFLOP/s; each (row, entity, dimension) triple is 2 multiply-adds
 # (alpha * U + beta * V), 4 flops.
@@ -378,8 +378,8 @@ def main():
                          "structure, on --workload's tables (comma-separated batch sizes, e.g. 1,16,256,1024)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
-              "multi-GPU path; see the sharding notes in DESIGN.md.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no "
+              "multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
     import torch
