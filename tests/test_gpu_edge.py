@@ -215,6 +215,34 @@ def test_gpu_concurrent_streams_match_sequential():
     con.close()
 
 
+
+@pytest.mark.parametrize("model", [O.Q2B, O.BETAE])
+def test_gpu_concurrent_mixed_calls_match_sequential(model):
+    """Mixed-structure executes alternating between two streams on a handle
+    with two scratch lanes (more calls than lanes, no host sync between them,
+    so lanes and plan-upload slots are reused while earlier calls may still
+    run) equal the same calls made one at a time on one stream."""
+    import torch
+    from paper_2503_02172_amd import kgq
+    w = synth.make_tiny(model, n_ent=3000, n_rel=9, dim=32, seed=120 + model)
+    structs = synth.STRUCTURES if model == O.BETAE else synth.STRUCTURES[:9]
+    seq = kgq.engine_for(w, max_batch=64, concurrency=1)
+    con = kgq.engine_for(w, max_batch=64, concurrency=2)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    qs = [synth.draw_mixed(structs, n, 3000, 9, seed=130 + i) for i, n in enumerate([60, 17, 64, 5, 33, 48])]
+    ref = [seq.execute(qb.structure_ids, qb.anchors, qb.relations, k=20, scores=True) for qb in qs]
+    torch.cuda.synchronize()
+    outs = []
+    for i, qb in enumerate(qs):
+        with torch.cuda.stream(streams[i % 2]):
+            outs.append(con.execute(qb.structure_ids, qb.anchors, qb.relations, k=20, scores=True))
+    torch.cuda.synchronize()
+    for r, o in zip(ref, outs):
+        for key in ("scores", "idx", "score"):
+            assert torch.equal(r[key], o[key]), key
+    seq.close()
+    con.close()
+
 def test_gpu_memory_accounting():
     """Parameters do not depend on max_batch; the execute scratch grows with
     max_batch and scales with the number of concurrency lanes; BetaE holds the
