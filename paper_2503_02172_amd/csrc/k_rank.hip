@@ -11,14 +11,15 @@
 //      score key in the high half, the inverted index in the low half, so
 //      that "ranks before" is "composite greater") are sorted ascending in
 //      LDS, at most kMaxAnswers of them;
-//   2. one pass over the score row: each entity finds, by binary search, how
-//      many answer composites lie below its own (the answers it outranks)
-//      and counts itself in that bin of an LDS histogram;
+//   2. one pass over the score row: each entity finds, by a branch-free
+//      binary search, how many answer composites lie below its own (the
+//      answers it outranks) and counts itself in that bin of an LDS histogram;
 //   3. a suffix sum over the bins gives each answer the number of entities
 //      ranked before it; the answers among those are exactly the answers
 //      sorted above it, which are subtracted;
 //   4. the metrics are summed in double precision in answer-list order.
-// The pass over the scores reads each row once (HBM-bound like the top-k).
+// The pass over the scores reads each row once; placing each entity among
+// the answers, not the read, bounds it.
 #include "kgq_internal.hpp"
 
 namespace kgq {
@@ -97,31 +98,34 @@ __global__ __launch_bounds__(RK_THREADS) void k_rank_answers(const float* scores
     if (tid == 0 && sh_bad) atomicOr(flag, kErrRange);
 
     // pass over the row: entity e outranks the answers whose composite is
-    // below its own; j = their count, so e adds to bins j (suffix sums below)
-    // (8 scores per thread in flight: unconditional loads at clamped
-    // positions, pinned by the empty asm so that the compiler does not move
-    // them behind the bounds test, where they would wait one by one)
-    const uint64_t kmin = key[0];
+    // below its own; a = their count, and e adds to bin a (suffix sums
+    // below; bin 0 is never summed). a is a branch-free lower bound over the
+    // P sorted keys (padding ~0 sorts last): one step per halving, the same
+    // for every lane, and the U entities of a thread step together so that
+    // their LDS reads overlap. Loads are unconditional at clamped positions;
+    // entity indices fit 32 bits (n_entities < 2^31).
     constexpr int U = 8;
-    for (int64_t e0 = tid; e0 < N; e0 += (int64_t)RK_THREADS * U) {
+    const uint32_t Nu = (uint32_t)N;
+    for (uint32_t e0 = tid; e0 < Nu; e0 += RK_THREADS * U) {
         float v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = row[min(e0 + (int64_t)u * RK_THREADS, N - 1)];
-#pragma unroll
-        for (int u = 0; u < U; ++u) asm volatile("" : "+v"(v[u]));
+        for (int u = 0; u < U; ++u) v[u] = row[min(e0 + (uint32_t)(u * RK_THREADS), Nu - 1)];
+        uint64_t c[U];
+        int a[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t e = e0 + (int64_t)u * RK_THREADS;
-            if (e >= N) break;
-            const uint64_t c = rank_composite(v[u], e);
-            if (c <= kmin) continue;              // outranks no answer (or is the lowest answer itself)
-            int a = 1, b = n;                     // key[0] < c: find the first index with key >= c
-            while (a < b) {
-                const int m = (a + b) >> 1;
-                if (key[m] < c) a = m + 1; else b = m;
-            }
-            atomicAdd(&hist[a], 1u);
+            c[u] = rank_composite(v[u], (int64_t)(e0 + (uint32_t)(u * RK_THREADS)));
+            a[u] = 0;
         }
+        for (int step = P >> 1; step > 0; step >>= 1) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) a[u] += key[a[u] + step - 1] < c[u] ? step : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) a[u] += key[a[u]] < c[u] ? 1 : 0;   // a was at most P - 1
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (e0 + (uint32_t)(u * RK_THREADS) < Nu && a[u] > 0) atomicAdd(&hist[a[u]], 1u);
     }
     __syncthreads();
 
