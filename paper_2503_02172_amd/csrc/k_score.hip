@@ -37,6 +37,24 @@
 
 namespace kgq {
 
+// A lane's four consecutive scores of one output row: one 16-byte
+// non-temporal store (rows start only 4-byte aligned; gfx950 takes
+// dword-aligned multi-dword global stores), element stores at the ragged end
+// of the row. Non-temporal: the score matrix streams past L2 instead of
+// evicting the packed queries that the other entity blocks still read, and
+// a wavefront writes whole lines.
+typedef float f4u_t __attribute__((ext_vector_type(4), aligned(4)));
+__device__ __forceinline__ void store_scores4(float* dst, int64_t e0, int64_t N, const float (&v)[4])
+{
+    if (e0 + 3 < N) {
+        __builtin_nontemporal_store((f4u_t){v[0], v[1], v[2], v[3]}, reinterpret_cast<f4u_t*>(dst + e0));
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (e0 + j < N) __builtin_nontemporal_store(v[j], dst + e0 + j);
+    }
+}
+
 template <int MODEL, int TQ>
 __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk, int total_wg, int wg_per_xcd,
                                                int kslice)
@@ -171,9 +189,10 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
             }
         if (row < a.n_quad) {
             float* dst = a.scores + (int64_t)a.out_dest[row >> 2] * a.ld;
+            float v[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (e0 + j < a.N) dst[e0 + j] = fmaxf(fmaxf(sc[0][j], sc[1][j]), fmaxf(sc[2][j], sc[3][j]));
+            for (int j = 0; j < 4; ++j) v[j] = fmaxf(fmaxf(sc[0][j], sc[1][j]), fmaxf(sc[2][j], sc[3][j]));
+            store_scores4(dst, e0, a.N, v);
             continue;
         }
 #pragma unroll
@@ -183,20 +202,13 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
             const int o = score_out_index(r, a.n_quad, a.n_pair);
             if (r < n_grouped) {
                 float* dst = a.scores + (int64_t)a.out_dest[o] * a.ld;
+                float v[4];
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (e0 + j < a.N) dst[e0 + j] = fmaxf(sc[2 * h][j], sc[2 * h + 1][j]);
+                for (int j = 0; j < 4; ++j) v[j] = fmaxf(sc[2 * h][j], sc[2 * h + 1][j]);
+                store_scores4(dst, e0, a.N, v);
             } else {
-                float* dst0 = a.scores + (int64_t)a.out_dest[o] * a.ld;
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (e0 + j < a.N) dst0[e0 + j] = sc[2 * h][j];
-                if (r + 1 < a.n_rows) {
-                    float* dst1 = a.scores + (int64_t)a.out_dest[o + 1] * a.ld;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        if (e0 + j < a.N) dst1[e0 + j] = sc[2 * h + 1][j];
-                }
+                store_scores4(a.scores + (int64_t)a.out_dest[o] * a.ld, e0, a.N, sc[2 * h]);
+                if (r + 1 < a.n_rows) store_scores4(a.scores + (int64_t)a.out_dest[o + 1] * a.ld, e0, a.N, sc[2 * h + 1]);
             }
         }
     }
