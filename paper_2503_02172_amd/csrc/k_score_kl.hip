@@ -60,38 +60,71 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     v4f acc[KlTile::TM][KlTile::TN];
     KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent, K, (int)(a.n_blocks * kEntBlock), K, m0, n0, sm, acc);
 
-    // Epilogue. Lane rows are 4 consecutive rows starting at a multiple of 4:
-    // a group of four is one lane's rows, a pair rows r = 0, 1 or r = 2, 3.
-    const int n_grouped = a.n_quad + a.n_pair;
+    // Epilogue, staged through LDS (the ring is free after the K loop):
+    //   1. each lane adds C_q + E_e in double precision to its accumulators
+    //      and writes the scores of its 4 rows x 1 column per MFMA tile into
+    //      a BM x BN tile (rows padded by 4 floats: the 16 lanes of a column
+    //      group and the 4 row groups hit distinct banks, and rows stay
+    //      16-byte aligned);
+    //   2. BN / 4 threads per row read whole rows back, take the max over a
+    //      union group of four rows or a pair (groups start at multiples of
+    //      4, pairs at even rows, neither crosses a tile) and write each
+    //      output row with 16-byte non-temporal stores, so the score matrix
+    //      streams past L2 in whole lines instead of 64-byte pieces that
+    //      evict the entity rows still to be read.
+    // Query rows are padded to a multiple of 128 (C_q = 0 there) and E_e to
+    // the entity blocks, so the constant reads are in bounds for every row
+    // and column of the tile; padding never reaches the output.
+    constexpr int TLD = KL_BN + 4;
+    static_assert(KL_BM * TLD <= KlTile::SMEM, "output tile fits the LDS ring");
+    static_assert(KL_BN % 4 == 0 && 256 % (KL_BN / 4) == 0, "output row pieces");
+    __syncthreads();                                  // every wavefront is done with the ring
+    float* T = sm;
 #pragma unroll
     for (int j = 0; j < KlTile::TN; ++j) {
-        const int64_t n = n0 + KlTile::col_of(j);
-        if (n >= a.N) continue;
-        const double ee = a.ee[n];
+        const int cj = KlTile::col_of(j);
+        const double ee = a.ee[n0 + cj];
 #pragma unroll
         for (int i = 0; i < KlTile::TM; ++i) {
-            const int mb = m0 + KlTile::row_of(i);
-            if (mb >= a.n_rows) continue;
-            float s[4];
+            const int rb = KlTile::row_of(i);
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                s[q] = (float)((double)a.gamma - (a.cq[mb + q] + ee + (double)acc[i][j][q]));
-            if (mb < a.n_quad) {
-                a.scores[(int64_t)a.out_dest[mb >> 2] * a.ld + n] = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-                continue;
-            }
-#pragma unroll
-            for (int pr = 0; pr < 2; ++pr) {
-                const int m = mb + 2 * pr;
-                if (m >= a.n_rows) break;
-                const int o = score_out_index(m, a.n_quad, a.n_pair);
-                if (m < n_grouped) {
-                    a.scores[(int64_t)a.out_dest[o] * a.ld + n] = fmaxf(s[2 * pr], s[2 * pr + 1]);
-                } else {
-                    a.scores[(int64_t)a.out_dest[o] * a.ld + n] = s[2 * pr];
-                    if (m + 1 < a.n_rows) a.scores[(int64_t)a.out_dest[o + 1] * a.ld + n] = s[2 * pr + 1];
-                }
-            }
+                T[(rb + q) * TLD + cj] = (float)((double)a.gamma - (a.cq[m0 + rb + q] + ee + (double)acc[i][j][q]));
+        }
+    }
+    __syncthreads();
+    constexpr int C4 = KL_BN / 4, RPP = 256 / C4;     // 16-byte pieces per row, rows per pass
+    const int c4 = threadIdx.x % C4;
+    const int64_t n = n0 + 4 * c4;
+    if (n >= a.N) return;
+    const int n_grouped = a.n_quad + a.n_pair;
+    for (int r = threadIdx.x / C4; r < KL_BM; r += RPP) {
+        const int m = m0 + r;
+        if (m >= a.n_rows) break;                     // rows only grow along the loop
+        int cnt = 1;
+        if (m < a.n_quad) {
+            if (m & 3) continue;                      // inside a group of four
+            cnt = 4;
+        } else if (m < n_grouped) {
+            if ((m - a.n_quad) & 1) continue;         // second row of a pair
+            cnt = 2;
+        }
+        const float* t = T + r * TLD + 4 * c4;
+        float4 v = *reinterpret_cast<const float4*>(t);
+        for (int u = 1; u < cnt; ++u) {
+            const float4 w = *reinterpret_cast<const float4*>(t + u * TLD);
+            v = make_float4(fmaxf(v.x, w.x), fmaxf(v.y, w.y), fmaxf(v.z, w.z), fmaxf(v.w, w.w));
+        }
+        float* dst = a.scores + (int64_t)a.out_dest[score_out_index(m, a.n_quad, a.n_pair)] * a.ld + n;
+        if (n + 3 < a.N) {
+            // rows start only 4-byte aligned; gfx950 takes dword-aligned
+            // multi-dword global stores
+            typedef float f4u_t __attribute__((ext_vector_type(4), aligned(4)));
+            __builtin_nontemporal_store((f4u_t){v.x, v.y, v.z, v.w}, reinterpret_cast<f4u_t*>(dst));
+        } else {
+            const float e4[4] = {v.x, v.y, v.z, v.w};
+            for (int jj = 0; jj < 4; ++jj)
+                if (n + jj < a.N) __builtin_nontemporal_store(e4[jj], dst + jj);
         }
     }
 }
