@@ -17,9 +17,9 @@
 // stages when 2d is a multiple of 16 (measured faster, epilogue included,
 // than 128 x 64, 64 x 128 or 128 x 128 tiles and than two or four stages);
 // otherwise the register-staged loop with 128 x 128 tiles. The epilogue adds
-// C_q + E_e in double precision, takes the max over union groups of four
-// and pairs of rows (held by the same lane) and scatters rows to their
-// output positions.
+// C_q + E_e in double precision, stages the output tile in LDS, takes the
+// max over union groups of four and pairs of rows and writes each output
+// row with 16-byte non-temporal stores.
 // Workgroups are ordered in chunks of row tiles (about 2 MiB of query rows),
 // each swept against every entity tile: the chunk's rows stay in L2 while
 // the entity table streams past.
