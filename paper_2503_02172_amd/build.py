@@ -79,7 +79,7 @@ def build_microbench(verbose: bool = False) -> list:
     instruction mixes, and a plain copy of known size (HBM bandwidth and
     byte-counter calibration)."""
     outs = []
-    for name, extra in (("valu_peak", ["-fno-honor-nans"]), ("hbm_copy", [])):
+    for name, extra in (("valu_peak", ["-fno-honor-nans"]), ("valu_issue", []), ("hbm_copy", [])):
         src = os.path.join(HERE, "microbench", name + ".hip")
         out = os.path.join(HERE, "microbench", name)
         cmd = [HIPCC] + [f for f in COMMON if f != "-fPIC"] + extra + ["-o", out + ".tmp", src]

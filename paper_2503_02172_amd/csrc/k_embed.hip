@@ -497,7 +497,9 @@ template <int TQ, int F>
 __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows, const float* states, int W, int d,
                                               float* qpack)
 {
-    constexpr int KC = 8192 / (TQ * F);       // dimensions per chunk: a 32 KiB tile (d = 400: one or two chunks)
+    // dimensions per chunk: up to a 32 KiB tile (d = 400: one or two
+    // chunks), a multiple of 4 so that no float4 straddles two fields
+    constexpr int KC = 8192 / (TQ * F) / 4 * 4;
     constexpr int RS = F * KC + 1;            // padded LDS row: the transposed reads hit distinct banks
     __shared__ float tile[TQ * RS];
     __shared__ int srcs[TQ];
@@ -512,7 +514,7 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows
     for (int k0 = 0; k0 < d; k0 += KC) {
         const int kc = min(KC, d - k0);           // a multiple of 4
         const int n4 = TQ * F * kc / 4;            // float4 elements of this chunk
-        constexpr int PER4 = TQ * F * KC / 4 / 256;
+        constexpr int PER4 = (TQ * F * KC / 4 + 255) / 256;   // float4 loads per thread (the last may be idle)
         // All loads of the chunk are issued before any is used: each reads a
         // valid address (row 0 for padding rows or past the chunk's end) and
         // the empty asm keeps the compiler from moving a load into the

@@ -22,8 +22,8 @@ constexpr int kMaxK = 1024;
 
 // Query rows per wavefront in the VALU scorers (rows are wave-uniform and
 // read through the scalar cache). Packed layout [row_block][k][field][kTq].
-constexpr int kTqGqe = 16;
-constexpr int kTqQ2b = 8;
+constexpr int kTqGqe = 24;
+constexpr int kTqQ2b = 12;
 // BetaE query rows are packed row-major [row][alpha (d) | beta (d)] and
 // padded to the matrix-core scorer's 128-row tile.
 constexpr int kRowTileBetae = 128;
