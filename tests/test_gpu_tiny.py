@@ -56,3 +56,19 @@ def test_gpu_tiny_mixed(model):
     print(f"[tiny-mixed] model={model} B=53", flush=True)
     _run_and_check(eng, w, m, qb.structure_ids, qb.anchors, qb.relations, 10, mixed=True)
     eng.close()
+
+
+@pytest.mark.parametrize("model", [O.GQE, O.Q2B], ids=["gqe", "q2b"])
+@pytest.mark.parametrize("dim", [344, 684])
+def test_gpu_pack_chunk_tails(model, dim):
+    """The query pack moves 340 dimensions per chunk at 12 or 24 rows per
+    wavefront: d = 344 and d = 684 end in a 4-dimension tail after one and two
+    full chunks. Mixed batch with unions, so groups and pairs of rows are
+    packed across the chunk boundaries too."""
+    w = synth.make_tiny(model, n_ent=300, n_rel=5, dim=dim, seed=300 + dim + model)
+    m = O.Model(model, w.params, w.gamma)
+    eng = _engine(w, max_batch=64)
+    qb = synth.draw_mixed(synth.STRUCTURES[:9], 53, 300, 5, seed=11)
+    print(f"[pack-tails] model={model} d={dim} B=53", flush=True)
+    _run_and_check(eng, w, m, qb.structure_ids, qb.anchors, qb.relations, 10, mixed=True)
+    eng.close()
