@@ -601,12 +601,16 @@ void launch_pack(int model, const int32_t* src_row, const int32_t* neg, int n_ro
                            cq);
         return;
     }
-    const int tq = score_row_pad(model);
-    const dim3 grid(n_rows_pad / tq);          // n_rows_pad is a multiple of tq
-    if (model == 0)
-        hipLaunchKernelGGL((k_pack<kTqGqe, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
-    else
-        hipLaunchKernelGGL((k_pack<kTqQ2b, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
+    const int tq = score_tq(model, n_rows);
+    const bool small = score_small(n_rows);
+    const dim3 grid(n_rows_pad / tq);          // n_rows_pad is a multiple of score_row_pad, hence of tq
+    if (model == 0) {
+        if (small) hipLaunchKernelGGL((k_pack<kTqGqeSmall, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
+        else hipLaunchKernelGGL((k_pack<kTqGqe, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
+    } else {
+        if (small) hipLaunchKernelGGL((k_pack<kTqQ2bSmall, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
+        else hipLaunchKernelGGL((k_pack<kTqQ2b, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
+    }
 }
 
 }  // namespace kgq

@@ -259,7 +259,8 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
         launch_score_kl(a, s);
         return;
     }
-    const int tq = score_row_pad(a.model);
+    const int tq = score_tq(a.model, a.n_rows);       // the pack's layout for this row count
+    const bool small = score_small(a.n_rows);
     const int nqb = (a.n_rows + tq - 1) / tq;
     const int nqg = (nqb + 3) / 4;
     const int total = (int)(a.n_blocks * nqg);
@@ -289,10 +290,13 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
         b.part = nullptr;
     }
     dim3 grid(per_xcd * 8, z);
-    if (a.model == 0)
-        hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
-    else
-        hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+    if (a.model == 0) {
+        if (small) hipLaunchKernelGGL((k_score<0, kTqGqeSmall>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+        else hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+    } else {
+        if (small) hipLaunchKernelGGL((k_score<1, kTqQ2bSmall>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+        else hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+    }
     if (z > 1) {
         const int n_out = (a.n_quad >> 2) + (a.n_pair >> 1) + (a.n_rows - a.n_quad - a.n_pair);
         const int64_t tot = (int64_t)n_out * a.N;

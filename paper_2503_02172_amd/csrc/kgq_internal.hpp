@@ -31,6 +31,21 @@ constexpr int kRowTileBetae = 128;
 // Scored rows are padded to a multiple of this per model.
 inline int score_row_pad(int model) { return model == 0 ? kTqGqe : (model == 1 ? kTqQ2b : kRowTileBetae); }
 
+// Small batches (at most kSmallScoreRows scored rows) run the GQE / Query2Box
+// pack and scorer with fewer rows per wavefront: there the scorer's dimension
+// loop is a latency chain on a few workgroups, whose length grows with the
+// rows per wavefront. 8 and 4 divide the padding (24 and 12), so the padded
+// layout holds either form; pack and scorer decide from the same row count.
+constexpr int kTqGqeSmall = 8;
+constexpr int kTqQ2bSmall = 4;
+constexpr int kSmallScoreRows = 512;
+inline bool score_small(int n_rows) { return n_rows <= kSmallScoreRows; }
+inline int score_tq(int model, int n_rows)
+{
+    const bool small = score_small(n_rows);
+    return model == 0 ? (small ? kTqGqeSmall : kTqGqe) : (small ? kTqQ2bSmall : kTqQ2b);
+}
+
 // Device error flag bits.
 constexpr int kErrRange = 1;    // an anchor or relation id outside its table
 constexpr int kErrPadding = 2;  // a mixed-batch unused slot that is not -1
