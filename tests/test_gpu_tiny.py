@@ -72,3 +72,18 @@ def test_gpu_pack_chunk_tails(model, dim):
     print(f"[pack-tails] model={model} d={dim} B=53", flush=True)
     _run_and_check(eng, w, m, qb.structure_ids, qb.anchors, qb.relations, 10, mixed=True)
     eng.close()
+
+
+@pytest.mark.parametrize("model", [O.GQE, O.Q2B], ids=["gqe", "q2b"])
+@pytest.mark.parametrize("B", [512, 513])
+def test_gpu_small_form_switch(model, B):
+    """Up to 512 scored rows the pack and scorer use fewer rows per
+    wavefront; 1p queries score one row each, so B = 512 runs the small form
+    and B = 513 the large one, on the same tables."""
+    w = synth.make_tiny(model, n_ent=300, n_rel=5, dim=16, seed=400 + model)
+    m = O.Model(model, w.params, w.gamma)
+    eng = _engine(w, max_batch=B)
+    qb = synth.draw_queries("1p", B, 300, 5, seed=13)
+    print(f"[small-switch] model={model} B={B}", flush=True)
+    _run_and_check(eng, w, m, 0, qb.anchors, qb.relations, 10)
+    eng.close()
