@@ -38,7 +38,7 @@ inline int score_row_pad(int model) { return model == 0 ? kTqGqe : (model == 1 ?
 // layout holds either form; pack and scorer decide from the same row count.
 constexpr int kTqGqeSmall = 8;
 constexpr int kTqQ2bSmall = 4;
-constexpr int kSmallScoreRows = 512;
+constexpr int kSmallScoreRows = 1024;
 inline bool score_small(int n_rows) { return n_rows <= kSmallScoreRows; }
 inline int score_tq(int model, int n_rows)
 {

@@ -75,11 +75,11 @@ def test_gpu_pack_chunk_tails(model, dim):
 
 
 @pytest.mark.parametrize("model", [O.GQE, O.Q2B], ids=["gqe", "q2b"])
-@pytest.mark.parametrize("B", [512, 513])
+@pytest.mark.parametrize("B", [1024, 1025])
 def test_gpu_small_form_switch(model, B):
-    """Up to 512 scored rows the pack and scorer use fewer rows per
-    wavefront; 1p queries score one row each, so B = 512 runs the small form
-    and B = 513 the large one, on the same tables."""
+    """Up to 1,024 scored rows the pack and scorer use fewer rows per
+    wavefront; 1p queries score one row each, so B = 1024 runs the small form
+    and B = 1025 the large one, on the same tables."""
     w = synth.make_tiny(model, n_ent=300, n_rel=5, dim=16, seed=400 + model)
     m = O.Model(model, w.params, w.gamma)
     eng = _engine(w, max_batch=B)
