@@ -345,6 +345,53 @@ def test_oracle_betae_intersection_identity_and_score():
         assert m.score(m.anchor(e), e) == pytest.approx(wb.gamma, abs=1e-12)
 
 
+def _betae_att_model(d, v1, v2):
+    """BetaE model whose intersection attention has the given first and
+    second layers (zero biases); the projection weights are unused."""
+    w = 2 * d
+    p = {"entity.alpha_beta": np.ones((1, w), np.float32), "relation": np.zeros((1, w), np.float32)}
+    for k, shp in (("w1", (2 * w, w)), ("b1", (2 * w,)), ("w2", (2 * w, 2 * w)), ("b2", (2 * w,)),
+                   ("w3", (w, 2 * w)), ("b3", (w,))):
+        p["proj." + k] = np.zeros(shp, np.float32)
+    p["inter.w1"], p["inter.b1"] = v1.astype(np.float32), np.zeros(w, np.float32)
+    p["inter.w2"], p["inter.b2"] = v2.astype(np.float32), np.zeros(d, np.float32)
+    return O.Model(O.BETAE, p, 60.0)
+
+
+def test_oracle_betae_intersection_attention_reads_alpha_and_beta():
+    """The attention MLP of the BetaE intersection takes the whole state
+    [alpha; beta] (width 2d), has hidden width 2d and d logits, and its
+    per-dimension weights apply to alpha and to beta alike (reading R-B4 of
+    Eq. 3's parameters). Selector weights reduce the logits to ReLU(alpha)
+    or ReLU(beta) of each branch, so the weight of branch 0 in dimension i is
+    sigmoid(logit_0i - logit_1i). An oracle that fed only alpha to the MLP,
+    used another hidden width or mixed up the two halves fails one of the
+    two cases, because alpha and beta differ in every dimension."""
+    d = 4
+    eye, zero = np.eye(d), np.zeros((d, d))
+    # V2 = [I | 0]: logits = first d hidden units
+    v2 = np.hstack([eye, zero])
+    a0 = np.array([0.5, 2.0, 0.125, 1.5])
+    b0 = np.array([3.0, 0.25, 1.0, 0.75])
+    a1 = np.array([1.25, 0.5, 2.5, 0.0625])
+    b1 = np.array([0.5, 1.75, 0.375, 4.0])
+    x0, x1 = np.concatenate([a0, b0]), np.concatenate([a1, b1])
+    for v1, l0, l1 in ((np.block([[eye, zero], [zero, zero]]), a0, a1),    # hidden = [alpha; 0]
+                       (np.block([[zero, eye], [zero, zero]]), b0, b1)):   # hidden = [beta; 0]
+        m = _betae_att_model(d, v1, v2)
+        w0 = 1.0 / (1.0 + np.exp(-(np.maximum(l0, 0) - np.maximum(l1, 0))))
+        want = np.concatenate([w0 * a0 + (1 - w0) * a1, w0 * b0 + (1 - w0) * b1])
+        np.testing.assert_allclose(m.intersect([x0, x1]), want, rtol=1e-14, atol=1e-15)
+    # the hidden units beyond the first d feed nothing when V2's right half
+    # is zero, and do feed the logits when it is not: V1 routes beta to the
+    # upper half of the hidden layer, V2 = [0 | I] reads it back
+    v1 = np.block([[zero, zero], [zero, eye]])
+    m = _betae_att_model(d, v1, np.hstack([zero, eye]))
+    w0 = 1.0 / (1.0 + np.exp(-(b0 - b1)))
+    want = np.concatenate([w0 * a0 + (1 - w0) * a1, w0 * b0 + (1 - w0) * b1])
+    np.testing.assert_allclose(m.intersect([x0, x1]), want, rtol=1e-14, atol=1e-15)
+
+
 def test_oracle_betae_kl_direction_in_score():
     # d = 1, entity Beta(2,3), query Beta(1,1): the score is
     # gamma - KL(entity || query) = 60 - (ln 12 - 9/4).
