@@ -74,25 +74,6 @@ def check_no_packed_fp32(lib: str) -> None:
         raise RuntimeError("packed FP32 instructions in device code: " + ", ".join(bad))
 
 
-def build_microbench(verbose: bool = False) -> list:
-    """The standalone microbenchmarks: VALU issue rates of the scorer
-    instruction mixes, and a plain copy of known size (HBM bandwidth and
-    byte-counter calibration)."""
-    outs = []
-    for name, extra in (("valu_peak", ["-fno-honor-nans"]), ("valu_issue", []), ("hbm_copy", [])):
-        src = os.path.join(HERE, "microbench", name + ".hip")
-        out = os.path.join(HERE, "microbench", name)
-        cmd = [HIPCC] + [f for f in COMMON if f != "-fPIC"] + extra + ["-o", out + ".tmp", src]
-        if verbose:
-            print(" ".join(cmd), flush=True)
-        r = subprocess.run(cmd, capture_output=True, text=True)
-        if r.returncode != 0:
-            raise RuntimeError(f"hipcc failed on {name}.hip:\n" + r.stdout + r.stderr)
-        os.replace(out + ".tmp", out)
-        outs.append(out)
-    return outs
-
-
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(6, os.cpu_count() or 1)) as ex:
@@ -106,7 +87,6 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
     check_no_packed_fp32(tmp)
     os.replace(tmp, OUT)
-    build_microbench(verbose)
     return OUT
 
 
