@@ -31,6 +31,12 @@
  *    waits on the device for the set's previous call to finish, so calls on
  *    different streams may overlap (up to cfg.concurrency at once) and calls
  *    on one stream stay in order. The host never blocks for this.
+ *  - Each set stages the lowered plan of a call through two pinned host
+ *    slots, used alternately. A call whose slot is still being read by the
+ *    execute that used it two calls earlier on the same set waits on the host
+ *    for that execute to finish (backpressure): the host runs at most
+ *    2 * cfg.concurrency execute calls ahead of the device. No other host
+ *    wait occurs outside checked mode.
  *  - Host-checkable errors are reported before anything is enqueued.
  */
 #ifndef KGQ_H
@@ -93,8 +99,14 @@ typedef struct {
                              concurrently, up to this many at once */
 } kgq_config;
 
-/* Create a handle. Validates cfg, selects the device, and allocates all
- * scratch space for max_batch queries (execute allocates nothing).
+/* Create a handle for one embedding model on one GPU (GQE, Query2Box or
+ * BetaE: Related Work; Experiments, Baselines). Validates cfg, selects the
+ * device, and allocates all scratch space for max_batch queries (execute
+ * allocates nothing). The handle is the compiled form of the paper's
+ * pipeline for that model (Methodology, Fig. 2): the 14 benchmark
+ * structures are compiled into fused programs (once per process, at the
+ * first create) and the handle refers to them; parameters arrive with
+ * kgq_load_params.
  * Errors: INVALID_ARG (cfg or out null, bad field), NO_DEVICE, OOM, DEVICE.
  * A handle with device = -1 validates arguments exactly like a real one;
  * its execute calls return NO_DEVICE once every argument has passed. */
@@ -134,7 +146,11 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
 kgq_status kgq_structure_arity(int32_t structure_id, int32_t* n_anchors, int32_t* n_relations);
 
 /* Execute a batch of queries that all have the same structure (built-in,
- * or compiled on this handle).
+ * or compiled on this handle): the structure's computation graph (Eq. 2;
+ * unions in disjunctive normal form, Eq. 1) run through its fused plan
+ * (Methodology, Operator Fuser, Algorithm 1), then the entity-similarity
+ * query over all N entities and the top k (the two parts of the paper's
+ * reasoning time; Experiments, Metrics).
  *   anchors   device int32 [batch x n_anchors(structure)]
  *   relations device int32 [batch x n_relations(structure)]
  *   k         1 <= k <= min(N, KGQ_MAX_K) when top-k outputs are requested
@@ -158,7 +174,11 @@ kgq_status kgq_execute(kgq_handle* h, int32_t structure_id, int32_t batch,
                        float* out_scores, int32_t* out_topk_idx, float* out_topk_score,
                        void* stream);
 
-/* Execute a batch whose queries have different structures, in one plan.
+/* Execute a batch whose queries have different structures, in one plan:
+ * the fused operators of all structures (Methodology, Operator Fuser,
+ * Algorithm 1) are grouped by kind and schedule position, so each kind runs
+ * as one launch across the whole batch; then scoring and top-k as in
+ * kgq_execute (Experiments, Metrics).
  *   structure_ids  HOST int32 [batch]: the plan is lowered on the host.
  *   anchors        device int32 [batch x 3], unused slots -1
  *   relations      device int32 [batch x 3], unused slots -1
@@ -339,8 +359,9 @@ kgq_status kgq_profile_intervals(kgq_handle* h, int32_t stage, double* out, int6
 kgq_status kgq_dense(kgq_handle* h, const float* x, int32_t M, int32_t K, const float* w, const float* b,
                      int32_t N, int32_t act, float* y, void* stream);
 
-/* Free the handle and everything it owns (waits for its work first).
- * NULL is accepted. */
+/* Free the handle and everything it owns: parameters, derived tables,
+ * compiled plans and scratch (the counterpart of kgq_create). Waits for the
+ * handle's work in flight first. NULL is accepted. */
 kgq_status kgq_destroy(kgq_handle* h);
 
 /* Static description of a status code. */
