@@ -215,27 +215,44 @@ class Engine:
 
     def execute(self, structure, anchors, relations, k: Optional[int] = None, scores: bool = False,
                 stream=None):
-        """Run a batch on the current stream and return torch tensors.
+        """Run a batch and return torch tensors.
 
         structure: an id (all queries alike; anchors [B x nA], relations
         [B x nR]) or a host int array [B] (mixed; anchors/relations [B x 3]
         padded with -1). Returns dict(scores=[B x N] or None, idx, score).
+        stream: a torch stream or a raw hipStream_t (int); None = the current
+        stream. The device copies of anchors and relations and the outputs
+        are allocated on that stream, so the caching allocator cannot hand
+        their memory to other work before the library's kernels on it are
+        done with them.
         """
         import torch
         dev = torch.device("cuda", self.device)
-        a = torch.as_tensor(anchors, dtype=torch.int32, device=dev).contiguous()
-        r = torch.as_tensor(relations, dtype=torch.int32, device=dev).contiguous()
-        B = a.shape[0]
-        out_s = torch.empty((B, self.n_entities), dtype=torch.float32, device=dev) if scores else None
-        out_i = out_v = None
-        if k is not None:
-            out_i = torch.empty((B, k), dtype=torch.int32, device=dev)
-            out_v = torch.empty((B, k), dtype=torch.float32, device=dev)
-        kk = k if k is not None else 0
-        if np.ndim(structure) == 0:
-            self.execute_into(int(structure), B, a, r, kk, out_s, out_i, out_v, stream)
+        if stream is None:
+            ts = torch.cuda.current_stream(dev)
+        elif isinstance(stream, int):
+            ts = torch.cuda.ExternalStream(stream, device=dev)
         else:
-            self.execute_mixed_into(np.asarray(structure), a, r, kk, out_s, out_i, out_v, stream)
+            ts = stream
+        with torch.cuda.stream(ts):
+            a = torch.as_tensor(anchors, dtype=torch.int32, device=dev).contiguous()
+            r = torch.as_tensor(relations, dtype=torch.int32, device=dev).contiguous()
+            B = a.shape[0]
+            out_s = torch.empty((B, self.n_entities), dtype=torch.float32, device=dev) if scores else None
+            out_i = out_v = None
+            if k is not None:
+                out_i = torch.empty((B, k), dtype=torch.int32, device=dev)
+                out_v = torch.empty((B, k), dtype=torch.float32, device=dev)
+            kk = k if k is not None else 0
+            if np.ndim(structure) == 0:
+                self.execute_into(int(structure), B, a, r, kk, out_s, out_i, out_v, ts)
+            else:
+                self.execute_mixed_into(np.asarray(structure), a, r, kk, out_s, out_i, out_v, ts)
+        # Inputs that were already device tensors on another stream: their
+        # memory must also outlive the kernels on ts.
+        for t, src in ((a, anchors), (r, relations)):
+            if t is src or (hasattr(src, "data_ptr") and t.data_ptr() == src.data_ptr()):
+                t.record_stream(ts)
         return {"scores": out_s, "idx": out_i, "score": out_v}
 
     def compile(self, structure) -> int:

@@ -278,3 +278,30 @@ def test_gpu_batch_above_65535():
     check_scores(out["scores"].cpu().numpy()[rows], ref, w.rtol, w.gamma, "2i B=70000")
     check_topk(out["idx"].cpu().numpy()[rows], out["score"].cpu().numpy()[rows], ref, 5, w.rtol, w.gamma,
                "2i B=70000")
+
+
+def test_gpu_execute_on_a_non_current_stream():
+    """Engine.execute(stream=s) with s not the current stream allocates its
+    device copies of the inputs and its outputs on s, so memory handed out on
+    the current stream right after the call cannot alias buffers the library
+    still reads or writes on s. The results equal a plain call's."""
+    import torch
+    from oracle import oracle as O
+    from paper_2503_02172_amd import kgq, synth
+
+    w = synth.make_tiny(O.Q2B, n_ent=5000, n_rel=7, dim=256, seed=61)
+    qb = synth.draw_mixed(synth.STRUCTURES[:9], 300, 5000, 7, seed=62)
+    with kgq.engine_for(w, max_batch=300) as eng:
+        ref = eng.execute(qb.structure_ids, qb.anchors, qb.relations, k=20, scores=True)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        for it in range(3):
+            out = eng.execute(qb.structure_ids, qb.anchors, qb.relations, k=20, scores=True, stream=s)
+            # immediately allocate and overwrite memory on the current stream
+            junk = [torch.full((300, 5000), -7.0, device="cuda") for _ in range(4)]
+            junk2 = torch.full((300, 3), -1, dtype=torch.int32, device="cuda")
+            s.synchronize()
+            torch.cuda.synchronize()
+            assert torch.equal(out["scores"], ref["scores"]), f"iteration {it}"
+            assert torch.equal(out["idx"], ref["idx"]) and torch.equal(out["score"], ref["score"])
+            del junk, junk2, out
