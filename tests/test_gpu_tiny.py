@@ -59,17 +59,24 @@ def test_gpu_tiny_mixed(model):
 
 
 @pytest.mark.parametrize("model", [O.GQE, O.Q2B], ids=["gqe", "q2b"])
-@pytest.mark.parametrize("dim", [344, 684])
-def test_gpu_pack_chunk_tails(model, dim):
-    """The query pack moves 340 dimensions per chunk at 12 or 24 rows per
-    wavefront: d = 344 and d = 684 end in a 4-dimension tail after one and two
-    full chunks. Mixed batch with unions, so groups and pairs of rows are
-    packed across the chunk boundaries too."""
+@pytest.mark.parametrize("dim,B", [(344, 1100), (684, 1100), (1028, 53)],
+                         ids=["d344-large", "d684-large", "d1028-small"])
+def test_gpu_pack_chunk_tails(model, dim, B):
+    """The query pack transposes a block of TQ rows through LDS, KC
+    dimensions at a time: KC = 340 for the large form (12 Query2Box or 24 GQE
+    rows per wavefront, more than 1,024 scored rows) and KC = 1,024 for the
+    small form (4 or 8 rows). d = 344 and d = 684 at B = 1,100 (more than
+    1,024 scored rows: large form) end in a 4-dimension tail after one and
+    two full chunks; d = 1,028 at B = 53 (small form) after one. Mixed
+    batches with unions, so groups and pairs of rows are packed across the
+    chunk boundaries too."""
     w = synth.make_tiny(model, n_ent=300, n_rel=5, dim=dim, seed=300 + dim + model)
     m = O.Model(model, w.params, w.gamma)
-    eng = _engine(w, max_batch=64)
-    qb = synth.draw_mixed(synth.STRUCTURES[:9], 53, 300, 5, seed=11)
-    print(f"[pack-tails] model={model} d={dim} B=53", flush=True)
+    eng = _engine(w, max_batch=B)
+    qb = synth.draw_mixed(synth.STRUCTURES[:9], B, 300, 5, seed=11)
+    rows = eng.describe_plan(qb.structure_ids)["scored_rows"]
+    assert (rows > 1024) == (B > 1024), rows
+    print(f"[pack-tails] model={model} d={dim} B={B} scored rows={rows}", flush=True)
     _run_and_check(eng, w, m, qb.structure_ids, qb.anchors, qb.relations, 10, mixed=True)
     eng.close()
 
@@ -79,11 +86,16 @@ def test_gpu_pack_chunk_tails(model, dim):
 def test_gpu_small_form_switch(model, B):
     """Up to 1,024 scored rows the pack and scorer use fewer rows per
     wavefront; 1p queries score one row each, so B = 1024 runs the small form
-    and B = 1025 the large one, on the same tables."""
-    w = synth.make_tiny(model, n_ent=300, n_rel=5, dim=16, seed=400 + model)
+    and B = 1025 the large one, on the same tables. At N = 300 (two entity
+    blocks) and d = 48, B = 1025 makes fewer than 128 scorer workgroups
+    (22 Query2Box or 11 GQE query groups x 2 blocks), so the large form also
+    runs its split-dimension path (partials summed by a second kernel). At
+    B = 1024 the small form makes 128 workgroups for Query2Box (no split) and
+    64 for GQE (split)."""
+    w = synth.make_tiny(model, n_ent=300, n_rel=5, dim=48, seed=400 + model)
     m = O.Model(model, w.params, w.gamma)
     eng = _engine(w, max_batch=B)
     qb = synth.draw_queries("1p", B, 300, 5, seed=13)
-    print(f"[small-switch] model={model} B={B}", flush=True)
+    print(f"[small-switch] model={model} B={B} d=48", flush=True)
     _run_and_check(eng, w, m, 0, qb.anchors, qb.relations, 10)
     eng.close()
