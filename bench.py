@@ -1,22 +1,23 @@
 """Benchmark: batched query answering (score every entity + top-k) on one MI355X.
 
 One step = one pass of the whole hot path over one batch of the headline
-workload: Query2Box at 14,505 entities x 474 relations, d = 400, 512 queries
-for each of the 9 structures without negation (4,608 queries), every query
-scored against all entities, top-100. Inputs are resident in HBM before the
-timed region starts. By default the nine per-structure batches go to the
-library together as one mixed-structure execute call (the plan lowering
-groups the operators of all structures, and one scorer launch covers every
-query row); --per-structure issues one execute call per structure instead,
-spread round-robin over --streams streams.
+workload, the largest that runs on one GPU: BetaE at 63,361 entities x 400
+relations, d = 400, entity table stored as bf16, 2,048 queries drawn
+uniformly over all 14 structures, executed as one mixed-structure call (the
+plan lowering groups the operators of every structure, one scorer launch
+covers every scored row), every query scored against all entities, top-100.
+Inputs are resident in HBM before the timed region starts. --workload picks
+another of the five workloads; --per-structure issues one execute call per
+structure batch instead, spread round-robin over --streams streams.
 
 Prints one JSON line. `value` is queries/s over the timed steps.
 `roofline` describes the dominant kernel (the entity scorer): the
-algorithmic VALU operations of one launch divided by the launch's average
+algorithmic operations of one launch divided by the launch's average
 duration (HIP events around each launch on the stream it runs on), against
-the FP32 VALU lane-operation peak of the chip. `cpu_baseline` times the CPU
-oracle on a bounded sample of the same workload. `others` reports the other
-four workloads (throughput and scorer fraction).
+the chip's published peak for the units it runs on (FP32 matrix cores for
+BetaE; FP32 vector units for GQE / Query2Box). `cpu_baseline` times the CPU
+oracle on a bounded sample of the same workload, on every host thread and on
+one. `others` reports the other workloads (throughput and scorer fraction).
 """
 
 from __future__ import annotations
@@ -34,21 +35,28 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 # Scorer rooflines.
-# GQE and Query2Box score on the vector units: peak in lane-operations per
-# second, 256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.64e12 (the
-# published 157.3 TFLOP/s FP32 vector peak counted at 2 flops per
-# lane-operation); each sub / add / min of the scorer is one lane-operation
-# (the library is compiled without packed FP32 instructions).
 # BetaE scores on the matrix cores: the published dense FP32 MFMA peak,
 # 157.3 TFLOP/s; each (row, entity, dimension) triple is 2 multiply-adds
 # (alpha * U + beta * V), 4 flops.
+# GQE and Query2Box score on the vector units. Each sub / add / min of the
+# scorer is one flop and one lane-operation (the library is compiled without
+# packed FP32 instructions, so an instruction does one operation per lane).
+# Two peaks are reported for them:
+#   flops against the published FP32 vector peak, 157.3 TFLOP/s (which counts
+#   a packed FMA, 4 flops per lane per clock: 256 CUs x 64 lanes x 4 x 2.4 GHz);
+#   lane-operations against what one non-packed instruction stream can issue,
+#   256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.64e12 per second
+#   (a wave64 instruction takes 2 cycles on a 32-lane SIMD).
+# The headline fraction of a VALU scorer is the flop one; the lane-operation
+# fraction is reported beside it as `frac_of_issue_peak`.
 PEAK_VALU_OPS = 256 * 4 * 32 * 2.4e9
+PEAK_VALU_F32 = 157.3e12
 PEAK_MFMA_F32 = 157.3e12
 HBM_PEAK = 8.0e12
-# algorithmic operations per (query row, entity, dimension) triple, the peak
+# algorithmic flops per (query row, entity, dimension) triple, the peak
 # they are counted against, and its unit
 OPS_PER_TRIPLE = {0: 2, 1: 4, 2: 4}
-SCORER_PEAK = {0: (PEAK_VALU_OPS, "alu", "TOP/s"), 1: (PEAK_VALU_OPS, "alu", "TOP/s"),
+SCORER_PEAK = {0: (PEAK_VALU_F32, "alu", "TFLOP/s"), 1: (PEAK_VALU_F32, "alu", "TFLOP/s"),
                2: (PEAK_MFMA_F32, "mfma", "TFLOP/s")}
 K_TOP = 100
 
@@ -63,6 +71,15 @@ WORKLOAD_DESC = {
     "C5": "BetaE, 63,361 entities x 400 relations, d=400, bf16 entity table; 2,048 mixed over all 14 "
           "structures; top-100",
 }
+
+
+# Oracle sample per workload (queries per batch on all threads, on one
+# thread), sized for about 10 s and 6 s of CPU work on a 16-thread host.
+# The one-thread leg is one pass: BetaE's per-entity function values are
+# computed once per pass and shared by the pass's queries, so a pass of very
+# few queries would mostly time that table.
+CPU_SAMPLE = {"C1": (16, 16), "C2": (128, 32), "C3": (64, 32), "C4-q2b": (128, 16), "C4-gqe": (128, 16),
+              "C5": (256, 32)}
 
 
 def log(*a):
@@ -159,6 +176,17 @@ class Prepared:
                 self.eng.execute_into(int(sid), B, a, r, self.w.k, None, idx, val, st)
             else:
                 self.eng.execute_mixed_into(sid, a, r, self.w.k, None, idx, val, st)
+
+
+def scorer_derivation(p: "Prepared") -> str:
+    """How the scorer's algorithmic work per launch is counted."""
+    w = p.w
+    per = OPS_PER_TRIPLE[p.model]
+    what = {0: "sub, add of |.| (GQE L1 distance)",
+            1: "sub, add of |.|, min, add (Query2Box box distance, regrouped exactly)",
+            2: "2 multiply-adds alpha_q*U_e + beta_q*V_e (BetaE KL, regrouped exactly)"}[p.model]
+    return (f"{per} flops per (scored row, entity, dimension) triple [{what}] x {p.rows} scored rows x "
+            f"{w.n_entities} entities x {w.dim} dimensions = {per * p.triples:.4g} flops per launch")
 
 
 def union_ms(iv: np.ndarray) -> float:
@@ -326,34 +354,63 @@ def rank_bench(p: Prepared, reps: int = 20):
             "queries_per_s": round(B / (ms * 1e-3), 1)}
 
 
-def cpu_baseline(name: str, per_structure: int, min_seconds: float = 10.0):
-    """The CPU oracle on the workload's queries (at most per_structure of each
-    structure batch), in whole passes repeated until min_seconds have elapsed."""
+def _oracle_pass(m, w, n_queries: int):
+    """The oracle on the first n_queries of every batch of the workload (a
+    uniform sample: each batch's queries are drawn i.i.d.); returns the
+    number of queries evaluated."""
+    from oracle import oracle as O
+    from paper_2503_02172_amd import synth
+
+    nq = 0
+    for b in w.batches:
+        n = min(n_queries, b.batch)
+        sid = synth.STRUCTURE_ID[b.structure] if b.structure else b.structure_ids[:n]
+        sc = m.scores(sid, b.anchors[:n], b.relations[:n])
+        O.topk(sc, w.k)
+        nq += n
+    return nq
+
+
+def cpu_baseline(name: str, n_queries: int, n_queries_1t: int, min_seconds: float = 10.0,
+                 min_seconds_1t: float = 0.0):
+    """The CPU oracle (fp64, node by node, full scoring + top-k) on a bounded
+    sample of the workload: the first n_queries of each batch, in whole passes
+    repeated until min_seconds have elapsed, on every host thread; then the
+    first n_queries_1t of each batch on one thread (one pass by default)."""
     from oracle import oracle as O
     from paper_2503_02172_amd import synth
 
     w = synth.make_workload(name)
-    m = O.Model(w.model, w.params, w.gamma)
-    threads = O.max_threads(0)
-    nq = 0
-    passes = 0
-    t0 = time.perf_counter()
-    while True:
-        for b in w.batches:
-            n = min(per_structure, b.batch)
-            sid = synth.STRUCTURE_ID[b.structure] if b.structure else b.structure_ids[:n]
-            sc = m.scores(sid, b.anchors[:n], b.relations[:n])
-            O.topk(sc, w.k)
-            nq += n
-        passes += 1
-        if time.perf_counter() - t0 >= min_seconds:
-            break
-    dt = time.perf_counter() - t0
-    per_pass = nq // passes
-    return {"value": nq / dt, "unit": "queries/s", "cores": threads, "kind": "oracle",
-            "sample": f"{per_pass} of the {sum(b.batch for b in w.batches)} queries ({per_structure} per "
-                      f"structure) x {passes} passes, fp64 node-by-node evaluation, full scoring + top-{w.k}",
-            "seconds": round(dt, 3)}
+    ent = synth.bf16_decode(w.entity_bf16) if w.entity_bf16 is not None else None
+    m = O.Model(w.model, w.params, w.gamma, entity_override=ent)
+    total = sum(b.batch for b in w.batches)
+
+    def timed(nq_per_batch, threads, min_s):
+        used = O.max_threads(threads)
+        nq, passes, t0 = 0, 0, time.perf_counter()
+        while True:
+            nq += _oracle_pass(m, w, nq_per_batch)
+            passes += 1
+            if time.perf_counter() - t0 >= min_s:
+                break
+        dt = time.perf_counter() - t0
+        return nq, passes, dt, used
+
+    # all threads OpenMP gives the process (OMP_NUM_THREADS where it is set)
+    all_threads = O.max_threads(0)
+    nq, passes, dt, threads = timed(n_queries, all_threads, min_seconds)
+    nq1, passes1, dt1, _ = timed(n_queries_1t, 1, min_seconds_1t)
+    O.max_threads(all_threads)
+    per_batch = f"{min(n_queries, w.batches[0].batch)} per batch" if len(w.batches) > 1 else "first"
+    return {"value": round(nq / dt, 3), "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nq // passes} of the workload's {total} queries ({per_batch}) x {passes} passes on "
+                      f"{threads} threads: fp64 node-by-node evaluation, full scoring of all {w.n_entities} "
+                      f"entities + top-{w.k}" + (" (entity table decoded from bf16)" if ent is not None else ""),
+            "seconds": round(dt, 3),
+            "entity_scores_per_s": round(nq / dt * w.n_entities, 1),
+            "single_thread": {"value": round(nq1 / dt1, 3), "unit": "queries/s", "cores": 1,
+                              "sample": f"{nq1 // passes1} queries x {passes1} passes on 1 thread",
+                              "seconds": round(dt1, 3)}}
 
 
 def main():
@@ -361,18 +418,23 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="C2")
+    ap.add_argument("--workload", default="C5")
     ap.add_argument("--no-others", action="store_true", help="skip the other four workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-per-structure", type=int, default=512)
+    ap.add_argument("--no-other-mode", action="store_true",
+                    help="skip the second timing of the headline workload in the other in-flight mode (so that "
+                         "a kernel trace of the run holds only headline-mode launches)")
+    ap.add_argument("--cpu-queries", type=int, default=None,
+                    help="oracle sample: queries per batch on all host threads (default: sized per workload)")
     ap.add_argument("--per-structure", action="store_true",
                     help="one execute call per structure batch instead of one mixed call per step")
     ap.add_argument("--streams", type=int, default=2,
                     help="with --per-structure: streams the independent calls are spread over")
-    ap.add_argument("--inflight", type=int, default=2,
-                    help="steps in flight: consecutive steps alternate over this many streams (one scratch "
-                         "lane and output buffer each), so that one step's small kernels overlap another's "
-                         "scorer (1: one step at a time)")
+    ap.add_argument("--inflight", type=int, default=1,
+                    help="steps in flight in the headline timed region: 1 (default) times one step at a "
+                         "time; 2 or more alternate consecutive steps over that many streams (one scratch lane "
+                         "and output buffer each), so that one step's small kernels overlap another's scorer. "
+                         "The other mode is timed after the headline and reported beside it")
     ap.add_argument("--sweep", default=None, metavar="SIZES",
                     help="instead of the benchmark: per-query time and device memory against batch size, per "
                          "structure, on --workload's tables (comma-separated batch sizes, e.g. 1,16,256,1024)")
@@ -390,11 +452,15 @@ def main():
 
     log(f"[bench] preparing {args.workload}")
     merge = not args.per_structure
-    p = Prepared(args.workload, args.streams, merge, args.inflight)
-    n_streams = len(p.streams)
+    # The engine always has two scratch lanes and two output buffers, so the
+    # same prepared workload can be timed one step at a time and with two
+    # steps in flight.
+    p = Prepared(args.workload, args.streams, merge, max(2, args.inflight))
+    headline_serial = args.inflight == 1
+    n_streams = 1 if headline_serial else len(p.streams)
     log(f"[bench] warmup {args.warmup}, timing {args.steps} steps: {len(p.calls)} execute call(s) per "
-        f"step on {n_streams} stream(s)")
-    dt, iv = time_steps(p, args.steps, args.warmup, profile_score=True)
+        f"step on {n_streams} stream(s), {1 if headline_serial else p.inflight} step(s) in flight")
+    dt, iv = time_steps(p, args.steps, args.warmup, profile_score=True, serial=headline_serial)
     ms_step = dt / args.steps * 1e3
     qps = p.n_queries * args.steps / dt
     busy = union_ms(iv)                         # time with a scorer launch in flight
@@ -406,6 +472,7 @@ def main():
     achieved_busy = total_ops / (busy * 1e-3) if busy > 0 else 0.0
     traffic, traffic_req = traffic_for(p.model, f"score:{args.workload}")
     peak, bound, unit = SCORER_PEAK[p.model]
+    in_flight_now = 1 if headline_serial else p.inflight
     roofline = {"bound": bound, "kernel": "k_score (entity scorer)" if p.model != 2 else "k_score_kl (entity scorer)",
                 "achieved": round(achieved / 1e12, 3), "peak": round(peak / 1e12, 2),
                 "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
@@ -414,20 +481,28 @@ def main():
                 "launches": n_launch, "scorer_busy_ms": round(busy, 4),
                 "frac_over_busy_time": round(achieved_busy / peak, 4),
                 "timing": f"HIP events around every scorer launch on its stream over the timed steps "
-                          f"({p.inflight} step(s) in flight); achieved = algorithmic ops per launch / average "
+                          f"({in_flight_now} step(s) in flight); achieved = algorithmic ops per launch / average "
                           f"launch duration"}
+    roofline["derivation"] = scorer_derivation(p)
+    if p.model != 2:
+        roofline["frac_of_issue_peak"] = round(achieved / PEAK_VALU_OPS, 4)
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {qps:.0f} q/s, scorer busy {busy:.2f} ms over "
         f"{n_launch} launches ({avg_launch_ms:.4f} ms each), {roofline['frac']*100:.1f}% of the {bound} peak")
-    serial = None
-    if p.inflight > 1:
-        ds, ivs = time_steps(p, args.steps, 1, profile_score=True, serial=True)
-        avg_s = float(np.mean(ivs[:, 1] - ivs[:, 0])) if len(ivs) else 0.0
-        serial = {"ms_per_step": round(ds / args.steps * 1e3, 4),
-                  "queries_per_s": round(p.n_queries * args.steps / ds, 2),
-                  "scorer_launch_ms": round(avg_s, 5),
-                  "scorer_frac": round(ops_per_launch / (avg_s * 1e-3) / peak, 4) if avg_s > 0 else None}
-        log(f"[bench] one step at a time: {serial['ms_per_step']:.3f} ms/step, {serial['queries_per_s']:.0f} q/s, "
-            f"scorer {avg_s:.4f} ms per launch ({serial['scorer_frac'] * 100:.1f}% of the {bound} peak)")
+    # The other mode, reported beside the headline: with two steps in flight
+    # one step's small kernels and launch gaps overlap the other's scorer,
+    # which raises the step rate; the scorer then shares the compute units,
+    # so its launch interval stretches and no longer measures the kernel.
+    other_name = "two_steps_in_flight" if headline_serial else "one_step_at_a_time"
+    other_mode = None
+    if not args.no_other_mode:
+        d2, iv2 = time_steps(p, args.steps, 2, profile_score=True, serial=not headline_serial)
+        avg2 = float(np.mean(iv2[:, 1] - iv2[:, 0])) if len(iv2) else 0.0
+        other_mode = {"ms_per_step": round(d2 / args.steps * 1e3, 4),
+                      "queries_per_s": round(p.n_queries * args.steps / d2, 2),
+                      "scorer_launch_ms": round(avg2, 5),
+                      "scorer_frac": round(ops_per_launch / (avg2 * 1e-3) / peak, 4) if avg2 > 0 else None}
+        log(f"[bench] {other_name.replace('_', ' ')}: {other_mode['ms_per_step']:.3f} ms/step, "
+            f"{other_mode['queries_per_s']:.0f} q/s, scorer {avg2:.4f} ms per launch")
     stages = stage_breakdown(p)
     log(f"[bench] stage ms per step (one stream, instrumented): {stages}")
     rank = rank_bench(p)
@@ -437,30 +512,31 @@ def main():
 
     others = {}
     if not args.no_others:
-        for name in ["C1", "C3", "C4-q2b", "C4-gqe", "C5"]:
+        for name in ["C1", "C2", "C3", "C4-q2b", "C4-gqe", "C5"]:
             if name == args.workload:
                 continue
             log(f"[bench] other workload {name}")
-            q = Prepared(name, args.streams, merge, args.inflight)
+            q = Prepared(name, args.streams, merge, max(2, args.inflight))
             steps = max(3, min(args.steps, 30))
+            # one step at a time (the scorer's launch interval measures the
+            # kernel alone), then two steps in flight
+            d1, iv2 = time_steps(q, steps, 2, profile_score=True, serial=True)
             d2, _ = time_steps(q, steps, 2, profile_score=False)
-            # the scorer's own launch time from a pass with one step at a
-            # time (in flight, its launches share the GPU with the other
-            # step's kernels)
-            d1, iv2 = time_steps(q, steps, 1, profile_score=True, serial=True)
             ops = OPS_PER_TRIPLE[q.model] * q.triples * steps
             b2 = union_ms(iv2)
             avg2 = float(np.mean(iv2[:, 1] - iv2[:, 0])) if len(iv2) else 0.0
-            others[name] = {"workload": WORKLOAD_DESC[name], "queries_per_s": round(q.n_queries * steps / d2, 1),
-                            "ms_per_step": round(d2 / steps * 1e3, 4),
-                            "steps_in_flight": q.inflight,
-                            "serial_ms_per_step": round(d1 / steps * 1e3, 4),
-                            "entity_scores_per_s": round(q.n_queries * q.w.n_entities * steps / d2, 1),
+            others[name] = {"workload": WORKLOAD_DESC[name], "queries_per_s": round(q.n_queries * steps / d1, 1),
+                            "ms_per_step": round(d1 / steps * 1e3, 4),
+                            "queries_per_s_two_in_flight": round(q.n_queries * steps / d2, 1),
+                            "ms_per_step_two_in_flight": round(d2 / steps * 1e3, 4),
+                            "entity_scores_per_s": round(q.n_queries * q.w.n_entities * steps / d1, 1),
                             "scorer_busy_ms_per_step": round(b2 / steps, 5),
                             "scorer_launch_ms": round(avg2, 5),
                             "scorer_bound": SCORER_PEAK[q.model][1],
                             "scorer_frac": round(ops / len(iv2) / (avg2 * 1e-3) / SCORER_PEAK[q.model][0], 4)
                             if avg2 > 0 else None,
+                            "scorer_frac_of_issue_peak": round(ops / len(iv2) / (avg2 * 1e-3) / PEAK_VALU_OPS, 4)
+                            if avg2 > 0 and q.model != 2 else None,
                             "stage_ms": stage_breakdown(q, reps=2)}
             log(f"[bench]   {name}: {others[name]['queries_per_s']} q/s, scorer frac "
                 f"{others[name]['scorer_frac']} of the {others[name]['scorer_bound']} peak")
@@ -471,8 +547,10 @@ def main():
     cpu = None
     if not args.no_cpu:
         log("[bench] CPU oracle baseline")
-        cpu = cpu_baseline(args.workload, args.cpu_per_structure)
-        log(f"[bench]   oracle {cpu['value']:.1f} q/s on {cpu['cores']} threads ({cpu['seconds']} s)")
+        nq, nq1 = CPU_SAMPLE.get(args.workload, (64, 4))
+        cpu = cpu_baseline(args.workload, args.cpu_queries or nq, nq1)
+        log(f"[bench]   oracle {cpu['value']:.1f} q/s on {cpu['cores']} threads ({cpu['seconds']} s), "
+            f"{cpu['single_thread']['value']:.2f} q/s on 1 thread ({cpu['single_thread']['seconds']} s)")
 
     out = {
         "metric": "queries/sec (score all entities + top-k) and achieved VALU/HBM roofline %",
@@ -489,10 +567,11 @@ def main():
         "data": "synthetic (seeded random tables and queries of the workload's shapes)",
         "config": {"workload": WORKLOAD_DESC[args.workload], "name": args.workload,
                    "queries_per_step": p.n_queries, "scored_rows_per_step": p.rows, "k": p.w.k,
-                   "execute_calls_per_step": len(p.calls), "streams": n_streams, "steps_in_flight": p.inflight},
+                   "execute_calls_per_step": len(p.calls), "streams": n_streams,
+                   "steps_in_flight": in_flight_now},
         "entity_scores_per_s": round(qps * p.w.n_entities, 1),
         "roofline": roofline,
-        "one_step_at_a_time": serial,
+        other_name: other_mode,
         "stage_ms_per_step": stages,
         "ranking_metrics": rank,
         "cpu_baseline": cpu,

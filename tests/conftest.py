@@ -20,3 +20,12 @@ def _oracle_built():
         from oracle import build
         build.build()
     yield
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    """Print what the full-size parity tests compared (also under -q)."""
+    from tests import parity
+    if parity.COVERAGE:
+        terminalreporter.section("parity coverage")
+        for line in parity.COVERAGE:
+            terminalreporter.write_line(line)

@@ -21,6 +21,10 @@ import numpy as np
 
 from oracle import oracle as O
 
+# One line per full-size workload checked: how many score rows and top-k
+# lists were compared (printed in pytest's terminal summary).
+COVERAGE: list = []
+
 
 def tol_of(o: np.ndarray, rtol: float, gamma: float) -> np.ndarray:
     return rtol * np.maximum(np.abs(o), abs(gamma))
