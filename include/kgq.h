@@ -192,6 +192,32 @@ kgq_status kgq_execute_mixed(kgq_handle* h, int32_t batch, const int32_t* struct
                              float* out_scores, int32_t* out_topk_idx, float* out_topk_score,
                              void* stream);
 
+/* Allocation-free variant of kgq_execute_mixed, for callers that cannot
+ * allocate device memory while they run (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation). Same arguments,
+ * outputs, batch limits and errors as kgq_execute_mixed; the difference is
+ * where the call's device scratch lives. kgq_execute_mixed uses the scratch
+ * the handle allocated at create; this call carves every device buffer it
+ * needs (plan image, error flag, state rows, dense-layer rows, packed
+ * queries, the score matrix when out_scores is NULL, top-k candidates, and
+ * the split workspaces of small batches as far as room is left) out of one
+ * static array of KGQ_NOALLOC_SCRATCH_BYTES per GPU, which the library holds
+ * from its first use on that GPU until the process ends. The call itself
+ * allocates nothing, device or pinned; it lowers the plan on the host as
+ * kgq_execute_mixed does and stages it through the handle's pinned slots.
+ * A batch whose buffers exceed the array is INVALID_ARG before anything is
+ * enqueued (passing out_scores, or a smaller batch, reduces the need).
+ * The array is shared by every call on a GPU, from every handle: calls of
+ * this function that overlap on one GPU (on different streams, or from
+ * different handles) race and give unspecified results; calls on one stream
+ * are ordered. The array keeps the previous call's contents; the call clears
+ * what must start at zero (its error flag) itself. */
+#define KGQ_NOALLOC_SCRATCH_BYTES (64 << 20)
+kgq_status kgq_execute_mixed_noalloc(kgq_handle* h, int32_t batch, const int32_t* structure_ids,
+                                     const int32_t* anchors, const int32_t* relations, int32_t k,
+                                     float* out_scores, int32_t* out_topk_idx, float* out_topk_score,
+                                     void* stream);
+
 /* Turn checked mode on (non-zero) or off for this handle. */
 kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
 

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <map>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -71,7 +72,17 @@ struct Lane {
 
 thread_local std::string g_create_error;
 
+std::mutex g_scratch_mu;
+std::map<int, unsigned char*> g_scratch_addr;   // device ordinal -> address of `scratch`
+
 }  // namespace
+
+// Device scratch of kgq_execute_mixed_noalloc: one array per GPU, in the
+// library's code object, held until the process ends. In host code the name
+// `scratch` is only a stand-in; its device address on each GPU comes from
+// hipGetSymbolAddress (taken once per device, with that device current) and
+// is the only form host code passes on.
+static __device__ __align__(256) unsigned char scratch[KGQ_NOALLOC_SCRATCH_BYTES];
 
 struct kgq_handle {
     kgq_config cfg{};
@@ -109,6 +120,10 @@ struct kgq_handle {
     // what one lane holds: state rows, rows of one dense-layer level or
     // intersection stage, groups of one intersection stage, scored rows
     int64_t cap_rows = 0, cap_mlp = 0, cap_groups = 0, cap_score_rows = 0;
+
+    // the device address of the static scratch array on this handle's GPU
+    // (kgq_execute_mixed_noalloc), taken at create
+    unsigned char* noalloc_scratch = nullptr;
 
     std::vector<void*> allocations;
     int64_t bytes_total = 0;      // device bytes allocated by the handle
@@ -477,13 +492,14 @@ kgq_status check_capacity(kgq_handle* h, const Plan& p)
 // an asynchronous copy there goes through a copy engine and costs about
 // 26 us of idle device between the previous execute's kernels and this
 // one's, a copy on a stream of its own still about 15 us of cross-queue wait.
-kgq_status upload_plan(kgq_handle* h, Lane& L, const Plan& p, int slot, hipStream_t s)
+kgq_status upload_plan(kgq_handle* h, Lane& L, const Plan& p, int slot, hipStream_t s, int32_t* dst = nullptr)
 {
     if ((int64_t)p.image.size() > h->plan_words) return fail(h, KGQ_E_DEVICE, "plan image exceeds its slot");
     if (L.slot_event_live[slot]) HIP_TRY(h, hipEventSynchronize(L.slot_event[slot]));
     int32_t* host = L.plan_host + (int64_t)slot * h->plan_words;
     std::memcpy(host, p.image.data(), p.image.size() * sizeof(int32_t));
-    launch_fetch_words(host, L.plan_dev + (int64_t)slot * h->plan_words, (int64_t)p.image.size(), s);
+    if (!dst) dst = L.plan_dev + (int64_t)slot * h->plan_words;
+    launch_fetch_words(host, dst, (int64_t)p.image.size(), s);
     return KGQ_OK;
 }
 
@@ -660,6 +676,101 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
     return KGQ_OK;
 }
 
+// Address of the static scratch array on the handle's device (current at
+// the call): looked up once per device and kept for the process.
+kgq_status noalloc_scratch_address(kgq_handle* h)
+{
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    auto it = g_scratch_addr.find(h->cfg.device);
+    if (it == g_scratch_addr.end()) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(h, KGQ_E_DEVICE, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        it = g_scratch_addr.emplace(h->cfg.device, static_cast<unsigned char*>(p)).first;
+    }
+    h->noalloc_scratch = it->second;
+    return KGQ_OK;
+}
+
+// Lays the device buffers one lowered plan needs out in a region of `cap`
+// bytes at `base` (256-byte aligned pieces), in the roles a lane's buffers
+// play: plan image, error flag, state rows, dense-layer rows, intersection
+// groups, packed queries, the score matrix when the caller does not supply
+// one, and the top-k candidates of long rows. The split-K and split-d
+// workspaces of small batches get what is left, up to a lane's caps (the
+// splitting code takes fewer slices when a workspace is smaller). Returns the
+// bytes the required pieces need; *fits tells whether they fit `cap`.
+int64_t carve_scratch(const kgq_handle* h, const Plan& p, int32_t k, bool need_scores, bool need_topk,
+                      unsigned char* base, int64_t cap, Lane& V, int32_t** plan_dev, bool* fits)
+{
+    const kgq_config& c = h->cfg;
+    const int64_t d = c.dim, N = c.n_entities, B = p.B;
+    const int64_t W = (c.model == KGQ_GQE) ? d : 2 * d;
+    int64_t off = 0;
+    // (with base == nullptr only the sizes are wanted: the addresses formed
+    // here are then never used)
+    auto take = [&](int64_t bytes) -> unsigned char* {
+        off = (off + 255) / 256 * 256;
+        unsigned char* q = reinterpret_cast<unsigned char*>(reinterpret_cast<uintptr_t>(base) + (uintptr_t)off);
+        off += std::max<int64_t>(bytes, 16);
+        return q;
+    };
+    *plan_dev = reinterpret_cast<int32_t*>(take((int64_t)p.image.size() * 4));
+    V.dflag = reinterpret_cast<int*>(take(sizeof(int)));
+    V.states = reinterpret_cast<float*>(take((int64_t)p.n_state_rows * W * 4));
+    const int64_t m = std::max(p.max_level, p.max_and_in), groups = p.max_and_groups;
+    if (c.model == KGQ_BETAE) {
+        V.xbuf = reinterpret_cast<float*>(take(m * 2 * d * 4));
+        V.h1 = reinterpret_cast<float*>(take(m * 4 * d * 4));
+        V.h2 = reinterpret_cast<float*>(take(m * 4 * d * 4));
+    } else {
+        V.h1 = reinterpret_cast<float*>(take(m * d * 4));
+        if (c.model == KGQ_Q2B) {
+            V.zfeat = reinterpret_cast<float*>(take(m * d * 4));
+            V.zmean = reinterpret_cast<float*>(take(groups * d * 4));
+            V.gate = reinterpret_cast<float*>(take(groups * d * 4));
+        }
+    }
+    V.logits = reinterpret_cast<float*>(take(m * d * 4));
+    const int tq = score_row_pad(c.model);
+    const int64_t srows = ((int64_t)(p.n_score_rows + tq - 1) / tq) * tq;
+    V.qpack = reinterpret_cast<float*>(take(srows * 2 * d * 4));
+    V.cq = reinterpret_cast<double*>(take(srows * 8));
+    V.scores = need_scores ? reinterpret_cast<float*>(take(B * N * 4)) : nullptr;
+    const int64_t ncand = need_topk ? topk_scratch_elems(B, N, k) : 0;
+    for (int i = 0; i < 2; ++i) {
+        V.cand_idx[i] = ncand ? reinterpret_cast<int32_t*>(take(ncand * 4)) : nullptr;
+        V.cand_score[i] = ncand ? reinterpret_cast<float*>(take(ncand * 4)) : nullptr;
+    }
+    const int64_t required = off;
+    *fits = required <= cap;
+    V.gemm_ws = nullptr;
+    V.gemm_ws_elems = 0;
+    V.score_ws = nullptr;
+    V.score_ws_elems = 0;
+    if (*fits) {
+        // optional workspaces, each from half of what is left
+        const int64_t n_max = c.model == KGQ_BETAE ? 4 * d : d;
+        int64_t left = (cap - (off + 255) / 256 * 256) / 2 / 4 / 64 * 64;
+        int64_t want = std::min<int64_t>(16 * 3 * B * n_max, (int64_t)16 * 128 * 4096);
+        if (std::min(want, left) >= 64) {
+            V.gemm_ws_elems = std::min(want, left);
+            V.gemm_ws = reinterpret_cast<float*>(take(V.gemm_ws_elems * 4));
+        }
+        if (c.model != KGQ_BETAE) {
+            const int64_t n_pad = h->n_blocks * kEntBlock;
+            left = (cap - (off + 255) / 256 * 256) / 4 / 64 * 64;
+            want = std::min<int64_t>(16 * 2 * (2 * B + 64) * n_pad, (int64_t)8 << 20);
+            if (std::min(want, left) >= 64) {
+                V.score_ws_elems = std::min(want, left);
+                V.score_ws = reinterpret_cast<float*>(take(V.score_ws_elems * 4));
+            }
+        }
+    }
+    return required;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -787,6 +898,7 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out)
         return KGQ_E_NO_DEVICE;
     }
     kgq_status s = allocate_all(h.get());
+    if (s == KGQ_OK) s = noalloc_scratch_address(h.get());
     if (s != KGQ_OK) {
         g_create_error = h->err;
         free_all(h.get());
@@ -841,6 +953,61 @@ kgq_status kgq_destroy(kgq_handle* h)
     free_all(h);
     delete h;
     return KGQ_OK;
+}
+
+kgq_status kgq_execute_mixed_noalloc(kgq_handle* h, int32_t batch, const int32_t* structure_ids,
+                                     const int32_t* anchors, const int32_t* relations, int32_t k, float* out_scores,
+                                     int32_t* out_topk_idx, float* out_topk_score, void* stream)
+{
+    static_assert(KGQ_NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size");
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (!structure_ids) return fail(h, KGQ_E_INVALID_ARG, "structure_ids must not be NULL");
+    kgq_status st = check_outputs(h, batch, anchors, relations, k, out_scores, out_topk_idx, out_topk_score);
+    if (st != KGQ_OK) return st;
+    std::string err;
+    int es = 0;
+    Plan plan;
+    if (!lower(h->cfg.model, batch, structure_ids, 0, 3, 3, true, h->table, plan, err, es))
+        return fail(h, (kgq_status)es, err);
+    st = check_capacity(h, plan);   // the plan is staged through a lane's pinned slots
+    if (st != KGQ_OK) return st;
+    // every device buffer of the call lives in the static array: size check
+    // first (no address needed for it, so a validation-only handle checks it too)
+    Lane V;
+    int32_t* plan_dev = nullptr;
+    bool fits = false;
+    const int64_t need = carve_scratch(h, plan, k, out_scores == nullptr, out_topk_idx != nullptr, nullptr,
+                                       KGQ_NOALLOC_SCRATCH_BYTES, V, &plan_dev, &fits);
+    if (!fits)
+        return fail(h, KGQ_E_INVALID_ARG,
+                    "the batch needs " + std::to_string(need) + " bytes of device scratch, more than the " +
+                        std::to_string((int64_t)KGQ_NOALLOC_SCRATCH_BYTES) +
+                        " of the static array (KGQ_NOALLOC_SCRATCH_BYTES); split it" +
+                        (out_scores ? std::string() : std::string(" or pass out_scores")));
+    if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
+    if (!h->noalloc_scratch) return fail(h, KGQ_E_DEVICE, "no static scratch address for this device");
+    HIP_TRY(h, hipSetDevice(h->cfg.device));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    carve_scratch(h, plan, k, out_scores == nullptr, out_topk_idx != nullptr, h->noalloc_scratch,
+                  KGQ_NOALLOC_SCRATCH_BYTES, V, &plan_dev, &fits);
+    // The lane provides the pinned plan staging, the host flag and the
+    // ordering against the lane's previous call; its device buffers are not
+    // used.
+    Lane* L = nullptr;
+    st = acquire_lane(h, s, &L);
+    if (st != KGQ_OK) return st;
+    V.hflag = L->hflag;
+    // the array keeps the last call's contents: the error flag must start at zero
+    launch_clear_flag(V.dflag, s);
+    const int slot = kNumStructures + L->ring_next;
+    L->ring_next ^= 1;
+    st = upload_plan(h, *L, plan, slot, s, plan_dev);
+    if (st != KGQ_OK) return st;
+    st = run_plan(h, V, plan, plan_dev, anchors, relations, 3, 3, 0, 0, true, k, out_scores, out_topk_idx,
+                  out_topk_score, s);
+    L->slot_event_live[slot] = hipEventRecord(L->slot_event[slot], s) == hipSuccess;
+    L->done_live = hipEventRecord(L->done, s) == hipSuccess;
+    return st;
 }
 
 kgq_status kgq_set_checked(kgq_handle* h, int32_t on)

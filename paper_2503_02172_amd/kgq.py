@@ -74,6 +74,7 @@ def lib() -> ctypes.CDLL:
         "kgq_structure_arity": ([i32, i32p, i32p], i32),
         "kgq_execute": ([vp, i32, i32, vp, vp, i32, vp, vp, vp, vp], i32),
         "kgq_execute_mixed": ([vp, i32, i32p, vp, vp, i32, vp, vp, vp, vp], i32),
+        "kgq_execute_mixed_noalloc": ([vp, i32, i32p, vp, vp, i32, vp, vp, vp, vp], i32),
         "kgq_set_checked": ([vp, i32], i32),
         "kgq_describe_plan": ([vp, i32, i32p, i32p], i32),
         "kgq_parse_structure": ([ctypes.c_char_p, i32p, i32, i32p], i32),
@@ -212,6 +213,16 @@ class Engine:
                                             sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                             _ptr(anchors), _ptr(relations), k, _ptr(out_scores),
                                             _ptr(out_idx), _ptr(out_score), _stream(stream)))
+
+    def execute_mixed_noalloc_into(self, structure_ids: np.ndarray, anchors, relations, k: int,
+                                   out_scores=None, out_idx=None, out_score=None, stream=None):
+        """kgq_execute_mixed_noalloc: as execute_mixed_into, with the call's
+        device scratch in the library's static array (no allocation)."""
+        sid = np.ascontiguousarray(structure_ids, np.int32)
+        self._check(lib().kgq_execute_mixed_noalloc(self.h, sid.shape[0],
+                                                    sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                                    _ptr(anchors), _ptr(relations), k, _ptr(out_scores),
+                                                    _ptr(out_idx), _ptr(out_score), _stream(stream)))
 
     def execute(self, structure, anchors, relations, k: Optional[int] = None, scores: bool = False,
                 stream=None):

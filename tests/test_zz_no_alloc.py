@@ -1,0 +1,97 @@
+"""kgq_execute_mixed_noalloc: the mixed-batch execute whose device scratch is
+carved from the library's static array instead of the handle's lanes.
+
+On the GPU it is compared with kgq_execute_mixed on the same handle and
+inputs (and with the oracle), on two calls in a row, the second with a
+smaller batch, so that the second call runs on an array that still holds the
+first call's contents. The tables have more than 16 Ki entities, so the top-k
+takes two rounds with its candidate lists in the scratch, and the batches are
+small enough for the split-K dense layers and split-dimension scorers, whose
+workspaces come from the array too. On the CPU, a validation-only handle
+checks the size limit."""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2503_02172_amd import synth
+from tests.parity import check_scores, check_topk
+
+
+def _alloc_outputs(B, N, k, scores):
+    import torch
+    out_s = torch.empty((B, N), dtype=torch.float32, device="cuda") if scores else None
+    out_i = torch.empty((B, k), dtype=torch.int32, device="cuda")
+    out_v = torch.empty((B, k), dtype=torch.float32, device="cuda")
+    return out_s, out_i, out_v
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("model", [O.GQE, O.Q2B, O.BETAE], ids=["gqe", "q2b", "betae"])
+def test_gpu_noalloc_matches_execute_mixed(model):
+    import torch
+    from paper_2503_02172_amd import kgq
+
+    N, R, k = 20000, 9, 10
+    w = synth.make_tiny(model, n_ent=N, n_rel=R, dim=32, seed=500 + model)
+    m = O.Model(model, w.params, w.gamma)
+    structs = synth.STRUCTURES if model == O.BETAE else synth.STRUCTURES[:9]
+    with kgq.engine_for(w, max_batch=64) as eng:
+        for call, B in enumerate((40, 13)):
+            qb = synth.draw_mixed(structs, B, N, R, seed=600 + 10 * model + call)
+            a = torch.as_tensor(qb.anchors, dtype=torch.int32, device="cuda")
+            r = torch.as_tensor(qb.relations, dtype=torch.int32, device="cuda")
+            print(f"[noalloc] model={model} call={call} B={B}", flush=True)
+            ref_s, ref_i, ref_v = _alloc_outputs(B, N, k, True)
+            eng.execute_mixed_into(qb.structure_ids, a, r, k, ref_s, ref_i, ref_v)
+            # with the score matrix in the caller's buffer, and with it in the
+            # static array (top-k only)
+            na_s, na_i, na_v = _alloc_outputs(B, N, k, True)
+            eng.execute_mixed_noalloc_into(qb.structure_ids, a, r, k, na_s, na_i, na_v)
+            _, nt_i, nt_v = _alloc_outputs(B, N, k, False)
+            eng.execute_mixed_noalloc_into(qb.structure_ids, a, r, k, None, nt_i, nt_v)
+            torch.cuda.synchronize()
+            ref = ref_s.cpu().numpy().astype(np.float64)
+            what = f"model {model} call {call} B={B}"
+            check_scores(na_s.cpu().numpy(), ref, w.rtol, w.gamma, what + " noalloc vs execute_mixed")
+            check_topk(na_i.cpu().numpy(), na_v.cpu().numpy(), ref, k, w.rtol, w.gamma, what)
+            check_topk(nt_i.cpu().numpy(), nt_v.cpu().numpy(), ref, k, w.rtol, w.gamma, what + " (top-k only)")
+            ora = m.scores(qb.structure_ids, qb.anchors, qb.relations)
+            check_scores(na_s.cpu().numpy(), ora, w.rtol, w.gamma, what + " noalloc vs oracle")
+            check_topk(nt_i.cpu().numpy(), nt_v.cpu().numpy(), ora, k, w.rtol, w.gamma, what + " vs oracle")
+
+
+def test_noalloc_size_limit_on_a_validation_handle():
+    """The scratch a batch needs is checked against the static array before
+    anything else: 64 queries x 2,000,000 entities of score matrix (512 MB) do
+    not fit, so the call is INVALID_ARG unless the caller supplies
+    out_scores; then every argument passes and the validation-only handle
+    answers NO_DEVICE."""
+    from paper_2503_02172_amd import kgq
+
+    L = kgq.lib()
+    cfg = kgq.Config(kgq.GQE, 32, 2_000_000, 9, kgq.F32, 12.0, 0.02, 64, -1, 1)
+    h = ctypes.c_void_p()
+    assert L.kgq_create(ctypes.byref(cfg), ctypes.byref(h)) == 0
+    try:
+        for name, shape in (("entity", (2_000_000, 32)), ("relation", (9, 32)), ("inter.w1", (32, 32)),
+                            ("inter.b1", (32,)), ("inter.w2", (32, 32)), ("inter.b2", (32,))):
+            a = np.zeros(shape, np.float32)
+            assert L.kgq_load_params(h, name.encode(), a.ctypes.data, a.nbytes, 0, 0) == 0
+        sid = np.zeros(64, np.int32)
+        sp = sid.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        fake = 1 << 20   # never dereferenced by a validation-only handle
+        rc = L.kgq_execute_mixed_noalloc(h, 64, sp, fake, fake, 10, None, fake, fake, None)
+        assert rc == -1, rc
+        assert b"static array" in L.kgq_last_error(h)
+        rc = L.kgq_execute_mixed_noalloc(h, 64, sp, fake, fake, 10, fake, fake, fake, None)
+        assert rc == -5, rc
+        # a batch above the handle's max_batch is refused as by kgq_execute_mixed
+        sid2 = np.zeros(65, np.int32)
+        rc = L.kgq_execute_mixed_noalloc(h, 65, sid2.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), fake, fake,
+                                         10, fake, fake, fake, None)
+        assert rc == -1, rc
+    finally:
+        L.kgq_destroy(h)
