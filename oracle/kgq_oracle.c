@@ -39,6 +39,36 @@
  *      BetaE: negation (alpha, beta) -> (1/alpha, 1/beta), no clamp after;
  *             intersection: attention over branches on [alpha; beta];
  *             score gamma - sum_i KL(Beta(entity_i) || Beta(query_i)).
+ *      ConE and LogicE are named as well (Related Work; Experiments,
+ *      Baselines; Table 1) without their operators; the forms used here are
+ *      those of the two models' own papers, read as follows.
+ *      ConE:  a query is a product of d two-dimensional sector cones, axis
+ *             theta in [-pi, pi) and half-aperture psi in [0, pi] per
+ *             dimension (state [theta; psi]); an entity is a cone of
+ *             aperture 0 (its axis). Projection: x = [theta + theta_r;
+ *             psi + psi_r] -> three dense layers (ReLU between) -> theta =
+ *             pi tanh(y_theta), psi = (pi / 2)(tanh(2 y_psi) + 1).
+ *             Intersection: u_j = [theta_j - psi_j; theta_j + psi_j];
+ *             attention logits from an MLP on u_j (2d -> d -> d), softmax
+ *             across branches per dimension, axis = the angle of the
+ *             weighted mean of the unit vectors (cos theta_j, sin theta_j);
+ *             half-aperture = min_j psi_j times a sigmoid gate computed from
+ *             the mean over branches of ReLU(W3 u_j + b3). Negation: the
+ *             complementary cone, axis moved by pi (theta - pi if theta >= 0,
+ *             else theta + pi), half-aperture pi - psi. Score: gamma -
+ *             modulus (sum_i d_out + center_reg sum_i d_in), with
+ *             t = theta_e - theta, d_in = min(|sin(t/2)|, |sin(psi/2)|) and
+ *             d_out = 0 inside the sector (|sin(t/2)| < |sin(psi/2)|), else
+ *             the smaller of |sin((t + psi)/2)| and |sin((t - psi)/2)|.
+ *      LogicE: a query is a vector of truth-value bounds [l; u] in [0, 1]^2d
+ *             with l <= u; an entity is such a vector too. Projection:
+ *             x = [l; u; Rel[r]] (concatenation, width 3d) -> three dense
+ *             layers -> l = sigmoid(y_l), u = l + sigmoid(y_u)(1 - l).
+ *             Intersection: a t-norm applied coordinate-wise to the lower
+ *             bounds and to the upper bounds of the branches, folded from the
+ *             first branch on (product a*b, minimum, or Lukasiewicz
+ *             max(0, a + b - 1)). Negation: [l; u] -> [1 - u; 1 - l].
+ *             Score: gamma - ||e - q||_1 / (2d) over the 2d bounds.
  *  - The 14 query shapes are named in the paper (Introduction; Experiments,
  *    Datasets & Tasks) but drawn only in a figure that is not available;
  *    the shapes below are the standard ones of the BetaE benchmark that the
@@ -60,6 +90,14 @@
 #define KGO_GQE 0
 #define KGO_Q2B 1
 #define KGO_BETAE 2
+#define KGO_CONE 3
+#define KGO_LOGICE 4
+
+#define KGO_TNORM_PRODUCT 0
+#define KGO_TNORM_MIN 1
+#define KGO_TNORM_LUKASIEWICZ 2
+
+#define KGO_PI 3.14159265358979323846
 
 typedef struct {
     int32_t model;
@@ -69,24 +107,51 @@ typedef struct {
     int32_t pad_;
     double gamma;
     double center_reg;
-    const float* entity;     /* GQE/Q2B [N x d]; BetaE [N x 2d], alpha then beta */
-    const float* relation;   /* GQE [R x d]; Q2B centers [R x d]; BetaE [R x 2d] */
+    const float* entity;     /* GQE/Q2B [N x d]; BetaE [N x 2d], alpha then beta;
+                                ConE [N x d] axes; LogicE [N x 2d], l then u */
+    const float* relation;   /* GQE [R x d]; Q2B centers [R x d]; BetaE, ConE [R x 2d];
+                                LogicE [R x d] */
     const float* offset_raw; /* Q2B [R x d], offsets before softplus */
     const float* att_w1;     /* intersection attention layer 1 [h x in] */
     const float* att_b1;
     const float* att_w2;     /* intersection attention layer 2 [d x h] */
     const float* att_b2;
-    const float* off_w1;     /* Q2B offset set-function layers [d x d] */
+    const float* off_w1;     /* Q2B offset set-function layers [d x d];
+                                ConE aperture set function [d x 2d], [d x d] */
     const float* off_b1;
     const float* off_w2;
     const float* off_b2;
-    const float* proj_w1;    /* BetaE projection [4d x 2d], [4d x 4d], [2d x 4d] */
+    const float* proj_w1;    /* projection MLP [4d x in], [4d x 4d], [2d x 4d]; in = 2d (BetaE,
+                                ConE) or 3d (LogicE) */
     const float* proj_b1;
     const float* proj_w2;
     const float* proj_b2;
     const float* proj_w3;
     const float* proj_b3;
+    int32_t tnorm;           /* LogicE intersection t-norm (KGO_TNORM_*) */
+    int32_t pad2_;
+    double modulus;          /* ConE distance scale */
 } kgo_model;
+
+/* Models with a negation operator (the paper: GQE and Query2Box run only
+ * the 9 structures without one; Experiments, Baselines). */
+static int has_negation(const kgo_model* m)
+{
+    return m->model == KGO_BETAE || m->model == KGO_CONE || m->model == KGO_LOGICE;
+}
+
+/* Closest approach, in the query being evaluated, to a point where ConE's
+ * operators are discontinuous: a negated axis at 0 (the complement moves it
+ * by -pi or +pi by its sign) and an intersection axis on the branch cut of
+ * the angle (weighted mean vector on the negative x axis). There a float32
+ * evaluation can land on the other side, with a different but equally
+ * correct result. Reset per query; +inf when no such operator runs. */
+static __thread double g_margin;
+
+static void note_margin(double v)
+{
+    if (v < g_margin) g_margin = v;
+}
 
 /* A query state: GQE uses x[0..d); Q2B holds center x[0..d) and offset
  * x[d..2d); BetaE holds alpha x[0..d) and beta x[d..2d). */
@@ -173,13 +238,27 @@ int kgo_state_width(const kgo_model* m)
     return m->model == KGO_GQE ? m->dim : 2 * m->dim;
 }
 
+static double sigmoid_d(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+/* The three t-norms of LogicE's intersection, as binary operations. */
+static double tnorm2(int kind, double a, double b)
+{
+    if (kind == KGO_TNORM_MIN) return a < b ? a : b;
+    if (kind == KGO_TNORM_LUKASIEWICZ) {
+        double v = a + b - 1.0;
+        return v > 0.0 ? v : 0.0;
+    }
+    return a * b;
+}
+
 /* Anchor entity -> value node (Eq. 2, first rule). */
 void kgo_anchor(const kgo_model* m, int64_t e, double* st)
 {
     int d = m->dim;
     if (m->model == KGO_GQE) {
         for (int i = 0; i < d; ++i) st[i] = m->entity[(size_t)e * d + i];
-    } else if (m->model == KGO_Q2B) {
+    } else if (m->model == KGO_Q2B || m->model == KGO_CONE) {
+        /* Q2B: a point is a box of zero offset; ConE: a cone of zero aperture */
         for (int i = 0; i < d; ++i) { st[i] = m->entity[(size_t)e * d + i]; st[d + i] = 0.0; }
     } else {
         for (int i = 0; i < 2 * d; ++i) st[i] = m->entity[(size_t)e * 2 * d + i];
@@ -201,39 +280,134 @@ void kgo_project(const kgo_model* m, const double* in, int32_t r, double* out)
         }
         return;
     }
-    /* BetaE: x = [alpha; beta] + Rel[r]; three dense layers; regulariser. */
+    /* BetaE, ConE: x = state + Rel[r] (width 2d); LogicE: x = [state; Rel[r]]
+     * (width 3d). Three dense layers with ReLU between, then the model's
+     * output map. */
     int w = 2 * d, h = 4 * d;
-    double* x = (double*)malloc(sizeof(double) * (size_t)(w + h + h + w));
-    double* h1 = x + w;
+    int in_w = m->model == KGO_LOGICE ? 3 * d : w;
+    double* x = (double*)malloc(sizeof(double) * (size_t)(in_w + h + h + w));
+    double* h1 = x + in_w;
     double* h2 = h1 + h;
     double* y = h2 + h;
-    for (int i = 0; i < w; ++i) x[i] = in[i] + (double)m->relation[(size_t)r * w + i];
-    dense(m->proj_w1, m->proj_b1, h, w, x, h1);
+    if (m->model == KGO_LOGICE) {
+        for (int i = 0; i < w; ++i) x[i] = in[i];
+        for (int i = 0; i < d; ++i) x[w + i] = (double)m->relation[(size_t)r * d + i];
+    } else {
+        for (int i = 0; i < w; ++i) x[i] = in[i] + (double)m->relation[(size_t)r * w + i];
+    }
+    dense(m->proj_w1, m->proj_b1, h, in_w, x, h1);
     relu_inplace(h1, h);
     dense(m->proj_w2, m->proj_b2, h, h, h1, h2);
     relu_inplace(h2, h);
     dense(m->proj_w3, m->proj_b3, w, h, h2, y);
-    for (int i = 0; i < w; ++i) {
-        double v = y[i] + 1.0;
-        if (v < 0.05) v = 0.05;
-        if (v > 1e9) v = 1e9;
-        out[i] = v;
+    if (m->model == KGO_BETAE) {
+        for (int i = 0; i < w; ++i) {
+            double v = y[i] + 1.0;
+            if (v < 0.05) v = 0.05;
+            if (v > 1e9) v = 1e9;
+            out[i] = v;
+        }
+    } else if (m->model == KGO_CONE) {
+        for (int i = 0; i < d; ++i) {
+            out[i] = KGO_PI * tanh(y[i]);
+            out[d + i] = 0.5 * KGO_PI * (tanh(2.0 * y[d + i]) + 1.0);
+        }
+    } else {
+        for (int i = 0; i < d; ++i) {
+            double l = sigmoid_d(y[i]);
+            out[i] = l;
+            out[d + i] = l + sigmoid_d(y[d + i]) * (1.0 - l);
+        }
     }
     free(x);
 }
 
-/* Negation (f_not of Eq. 2), defined for BetaE only: reciprocal of both
- * shape parameters. */
+/* Negation (f_not of Eq. 2), for the models that have one. BetaE: the
+ * reciprocal of both shape parameters. ConE: the complementary cone. LogicE:
+ * the complement of the truth bounds. in and out may alias. */
 void kgo_negate(const kgo_model* m, const double* in, double* out)
 {
-    int w = 2 * m->dim;
+    int d = m->dim, w = 2 * d;
+    if (m->model == KGO_CONE) {
+        for (int i = 0; i < d; ++i) {
+            double t = in[i];
+            note_margin(fabs(t));
+            out[i] = t >= 0.0 ? t - KGO_PI : t + KGO_PI;
+            out[d + i] = KGO_PI - in[d + i];
+        }
+        return;
+    }
+    if (m->model == KGO_LOGICE) {
+        for (int i = 0; i < d; ++i) {
+            double l = in[i], u = in[d + i];
+            out[i] = 1.0 - u;
+            out[d + i] = 1.0 - l;
+        }
+        return;
+    }
     for (int i = 0; i < w; ++i) out[i] = 1.0 / in[i];
+}
+
+/* ConE intersection: semantic average of the axes, gated minimum of the
+ * half-apertures. */
+static void cone_intersect(const kgo_model* m, int n, const double* const* br, double* out)
+{
+    int d = m->dim, w = 2 * d;
+    double* u = (double*)malloc(sizeof(double) * (size_t)w);
+    double* hid = (double*)malloc(sizeof(double) * (size_t)d);
+    double* logits = (double*)malloc(sizeof(double) * (size_t)n * d);
+    double* mean = (double*)calloc((size_t)d, sizeof(double));
+    double* g = (double*)malloc(sizeof(double) * (size_t)d);
+    double* wts = (double*)malloc(sizeof(double) * (size_t)n);
+    for (int j = 0; j < n; ++j) {
+        for (int i = 0; i < d; ++i) {
+            u[i] = br[j][i] - br[j][d + i];
+            u[d + i] = br[j][i] + br[j][d + i];
+        }
+        dense(m->att_w1, m->att_b1, d, w, u, hid);
+        relu_inplace(hid, d);
+        dense(m->att_w2, m->att_b2, d, d, hid, logits + (size_t)j * d);
+        dense(m->off_w1, m->off_b1, d, w, u, hid);
+        relu_inplace(hid, d);
+        for (int i = 0; i < d; ++i) mean[i] += hid[i];
+    }
+    for (int i = 0; i < d; ++i) mean[i] /= (double)n;
+    dense(m->off_w2, m->off_b2, d, d, mean, g);
+    for (int i = 0; i < d; ++i) {
+        double mx = logits[i];
+        for (int j = 1; j < n; ++j) if (logits[(size_t)j * d + i] > mx) mx = logits[(size_t)j * d + i];
+        double z = 0.0;
+        for (int j = 0; j < n; ++j) { wts[j] = exp(logits[(size_t)j * d + i] - mx); z += wts[j]; }
+        double cx = 0.0, sy = 0.0, mn = br[0][d + i];
+        for (int j = 0; j < n; ++j) {
+            double wj = wts[j] / z;
+            cx += wj * cos(br[j][i]);
+            sy += wj * sin(br[j][i]);
+            if (br[j][d + i] < mn) mn = br[j][d + i];
+        }
+        if (cx < 0.0) note_margin(fabs(sy));
+        out[i] = atan2(sy, cx);
+        out[d + i] = mn * sigmoid_d(g[i]);
+    }
+    free(u); free(hid); free(logits); free(mean); free(g); free(wts);
 }
 
 /* Intersection (f_and of Eq. 2) of n >= 1 branch states. */
 void kgo_intersect(const kgo_model* m, int n, const double* const* br, double* out)
 {
     int d = m->dim;
+    if (m->model == KGO_CONE) {
+        cone_intersect(m, n, br, out);
+        return;
+    }
+    if (m->model == KGO_LOGICE) {
+        for (int i = 0; i < 2 * d; ++i) {
+            double v = br[0][i];
+            for (int j = 1; j < n; ++j) v = tnorm2(m->tnorm, v, br[j][i]);
+            out[i] = v;
+        }
+        return;
+    }
     int in_w = (m->model == KGO_BETAE) ? 2 * d : d;   /* attention input width */
     int hid = in_w;                                    /* attention hidden width */
     double* hbuf = (double*)malloc(sizeof(double) * (size_t)hid);
@@ -309,6 +483,26 @@ double kgo_score(const kgo_model* m, const double* st, int64_t e)
         }
         return m->gamma - (out + m->center_reg * in);
     }
+    if (m->model == KGO_CONE) {
+        double out = 0.0, in = 0.0;
+        for (int i = 0; i < d; ++i) {
+            double t = (double)m->entity[(size_t)e * d + i] - st[i];
+            double psi = st[d + i];
+            double to_axis = fabs(sin(0.5 * t));
+            double base = fabs(sin(0.5 * psi));
+            if (!(to_axis < base)) {
+                double lo = fabs(sin(0.5 * (t + psi))), hi = fabs(sin(0.5 * (t - psi)));
+                out += lo < hi ? lo : hi;
+            }
+            in += to_axis < base ? to_axis : base;
+        }
+        return m->gamma - m->modulus * (out + m->center_reg * in);
+    }
+    if (m->model == KGO_LOGICE) {
+        double s = 0.0;
+        for (int i = 0; i < 2 * d; ++i) s += fabs(st[i] - (double)m->entity[(size_t)e * 2 * d + i]);
+        return m->gamma - s / (2.0 * d);
+    }
     double kl = 0.0;
     for (int i = 0; i < d; ++i) {
         double ae = m->entity[(size_t)e * 2 * d + i], be = m->entity[(size_t)e * 2 * d + d + i];
@@ -345,8 +539,9 @@ int kgo_arity(int s, int* na, int* nr)
 int kgo_query_states(const kgo_model* m, int s, const int32_t* a, const int32_t* r, double* out)
 {
     int w = kgo_state_width(m);
+    g_margin = INFINITY;
     if (s < 0 || s >= S_COUNT) return -1;
-    if (s >= S_2IN && m->model != KGO_BETAE) return -1;
+    if (s >= S_2IN && !has_negation(m)) return -1;
     double* b0 = (double*)malloc(sizeof(double) * (size_t)w * 3);
     double* b1 = b0 + w;
     double* b2 = b1 + w;
@@ -389,6 +584,10 @@ int kgo_query_states(const kgo_model* m, int s, const int32_t* a, const int32_t*
 
 #undef ANCHOR
 #undef PROJ
+
+/* Margin (see g_margin) of the query last evaluated on this thread by
+ * kgo_query_states or kgo_graph_states. */
+double kgo_last_margin(void) { return g_margin; }
 
 /* ------------------------------------------------------------------ */
 /* Batched scoring and top-k                                           */
@@ -489,7 +688,7 @@ static void score_terms(const kgo_model* m, int32_t B, const double* states, con
  * id outside the tables. */
 int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t* anchors,
                int32_t astride, const int32_t* rels, int32_t rstride, double* scores,
-               int nthreads)
+               double* margin, int nthreads)
 {
     int w = kgo_state_width(m);
     int64_t N = m->n_entities;
@@ -497,7 +696,7 @@ int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t*
     for (int32_t q = 0; q < B; ++q) {
         int na, nr;
         if (kgo_arity(sid[q], &na, &nr)) return -1;
-        if (sid[q] >= S_2IN && m->model != KGO_BETAE) return -1;
+        if (sid[q] >= S_2IN && !has_negation(m)) return -1;
         for (int k = 0; k < na; ++k) {
             int32_t e = anchors[(size_t)q * astride + k];
             if (e < 0 || e >= N) return -1;
@@ -515,6 +714,7 @@ int kgo_scores(const kgo_model* m, int32_t B, const int32_t* sid, const int32_t*
     for (int32_t q = 0; q < B; ++q) {
         nst[q] = kgo_query_states(m, sid[q], anchors + (size_t)q * astride,
                                   rels + (size_t)q * rstride, states + (size_t)q * 2 * w);
+        if (margin) margin[q] = g_margin;
         if (nst[q] < 0) bad = 1;
     }
     if (!bad) score_terms(m, B, states, nst, 2, scores);
@@ -578,7 +778,7 @@ int kgo_graph_check(const kgo_model* m, const int32_t* g, int n, int* n_anchor_s
         switch (nd[0]) {
         case KGO_OP_ANCHOR: if (nd[1] + 1 > na) na = nd[1] + 1; c = 1; break;
         case KGO_OP_PROJECT: if (nd[1] + 1 > nr) nr = nd[1] + 1; c = cnt[nd[2]]; break;
-        case KGO_OP_NOT: if (m->model != KGO_BETAE) ok = 0; c = 1; break;
+        case KGO_OP_NOT: if (!has_negation(m)) ok = 0; c = 1; break;
         case KGO_OP_OR: c = 0; for (int j = 0; j < k; ++j) c += cnt[nd[2 + j]]; break;
         case KGO_OP_AND: c = 1; for (int j = 0; j < k; ++j) c *= cnt[nd[2 + j]]; break;
         }
@@ -612,6 +812,7 @@ int kgo_graph_states(const kgo_model* m, const int32_t* g, int n, const int32_t*
                      double* out)
 {
     int na, nr, nt;
+    g_margin = INFINITY;
     if (kgo_graph_check(m, g, n, &na, &nr, &nt)) return -1;
     int w = kgo_state_width(m);
     int* cnt = (int*)calloc((size_t)n, sizeof(int));
@@ -685,7 +886,8 @@ int kgo_graph_states(const kgo_model* m, const int32_t* g, int n, const int32_t*
  * slots are anchors[q*astride ..], its relation slots rels[q*rstride ..].
  * Returns 0, or -1 for a rejected graph or an id outside the tables. */
 int kgo_graph_scores(const kgo_model* m, const int32_t* g, int n, int32_t B, const int32_t* anchors,
-                     int32_t astride, const int32_t* rels, int32_t rstride, double* scores, int nthreads)
+                     int32_t astride, const int32_t* rels, int32_t rstride, double* scores, double* margin,
+                     int nthreads)
 {
     int na, nr, nt;
     if (m->dim > KGO_MAX_DIM) return -1;
@@ -706,9 +908,11 @@ int kgo_graph_scores(const kgo_model* m, const int32_t* g, int n, int32_t B, con
     double* states = (double*)malloc(sizeof(double) * (size_t)B * nt * w);
     int* nst = (int*)malloc(sizeof(int) * (size_t)B);
 #pragma omp parallel for schedule(dynamic, 1)
-    for (int32_t q = 0; q < B; ++q)
+    for (int32_t q = 0; q < B; ++q) {
         nst[q] = kgo_graph_states(m, g, n, anchors + (size_t)q * astride, rels + (size_t)q * rstride,
                                   states + (size_t)q * nt * w);
+        if (margin) margin[q] = g_margin;
+    }
     score_terms(m, B, states, nst, nt, scores);
     free(states);
     free(nst);

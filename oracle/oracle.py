@@ -18,7 +18,8 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liboracle.so")
 
-GQE, Q2B, BETAE = 0, 1, 2
+GQE, Q2B, BETAE, CONE, LOGICE = 0, 1, 2, 3, 4
+TNORM_PRODUCT, TNORM_MIN, TNORM_LUKASIEWICZ = 0, 1, 2
 
 _fp = ctypes.POINTER(ctypes.c_float)
 
@@ -33,6 +34,7 @@ class _Model(ctypes.Structure):
         ("off_w1", _fp), ("off_b1", _fp), ("off_w2", _fp), ("off_b2", _fp),
         ("proj_w1", _fp), ("proj_b1", _fp), ("proj_w2", _fp), ("proj_b2", _fp),
         ("proj_w3", _fp), ("proj_b3", _fp),
+        ("tnorm", ctypes.c_int32), ("pad2_", ctypes.c_int32), ("modulus", ctypes.c_double),
     ]
 
 
@@ -74,14 +76,16 @@ def lib() -> ctypes.CDLL:
         L.kgo_query_states.argtypes = [mp, ctypes.c_int, ip, ip, dp]
         L.kgo_scores.restype = ctypes.c_int
         L.kgo_scores.argtypes = [mp, ctypes.c_int32, ip, ip, ctypes.c_int32, ip, ctypes.c_int32,
-                                 dp, ctypes.c_int]
+                                 dp, dp, ctypes.c_int]
+        L.kgo_last_margin.restype = ctypes.c_double
+        L.kgo_last_margin.argtypes = []
         L.kgo_graph_check.restype = ctypes.c_int
         L.kgo_graph_check.argtypes = [mp, ip, ctypes.c_int, ip, ip, ip]
         L.kgo_graph_states.restype = ctypes.c_int
         L.kgo_graph_states.argtypes = [mp, ip, ctypes.c_int, ip, ip, dp]
         L.kgo_graph_scores.restype = ctypes.c_int
         L.kgo_graph_scores.argtypes = [mp, ip, ctypes.c_int, ctypes.c_int32, ip, ctypes.c_int32, ip,
-                                       ctypes.c_int32, dp, ctypes.c_int]
+                                       ctypes.c_int32, dp, dp, ctypes.c_int]
         L.kgo_topk.restype = ctypes.c_int
         L.kgo_topk.argtypes = [dp, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ip, dp,
                                ctypes.c_int]
@@ -124,10 +128,28 @@ class Model:
     """
 
     def __init__(self, model: int, params: Dict[str, np.ndarray], gamma: float,
-                 center_reg: float = 0.02, entity_override: Optional[np.ndarray] = None):
+                 center_reg: float = 0.02, entity_override: Optional[np.ndarray] = None,
+                 tnorm: int = TNORM_PRODUCT):
         self.model = model
         keep = {}
-        if model == BETAE:
+        modulus = 0.0
+        if model == CONE:
+            keep["entity"] = _f32(params["entity.axis"] if entity_override is None else entity_override)
+            keep["relation"] = _f32(params["relation"])
+            for k in ("w1", "b1", "w2", "b2"):
+                keep["att_" + k] = _f32(params["inter.axis." + k])
+                keep["off_" + k] = _f32(params["inter.arg." + k])
+            for k in ("w1", "b1", "w2", "b2", "w3", "b3"):
+                keep["proj_" + k] = _f32(params["proj." + k])
+            modulus = float(np.asarray(params["modulus"], np.float32).reshape(-1)[0])
+            dim = keep["entity"].shape[1]
+        elif model == LOGICE:
+            keep["entity"] = _f32(params["entity.bounds"] if entity_override is None else entity_override)
+            keep["relation"] = _f32(params["relation"])
+            for k in ("w1", "b1", "w2", "b2", "w3", "b3"):
+                keep["proj_" + k] = _f32(params["proj." + k])
+            dim = keep["entity"].shape[1] // 2
+        elif model == BETAE:
             ent = params["entity.alpha_beta"] if entity_override is None else entity_override
             keep["entity"] = _f32(ent)
             keep["relation"] = _f32(params["relation"])
@@ -158,6 +180,8 @@ class Model:
         s.n_relations = keep["relation"].shape[0]
         s.gamma = gamma
         s.center_reg = center_reg
+        s.tnorm = tnorm
+        s.modulus = modulus
         for name, _ in _Model._fields_:
             if name in keep:
                 setattr(s, name, _ptr(keep[name]))
@@ -208,6 +232,12 @@ class Model:
             raise ValueError("unsupported structure")
         return out[: n * self.width].reshape(n, self.width)
 
+    @staticmethod
+    def last_margin() -> float:
+        """ConE: closest approach to a discontinuity of the operators in the
+        query last evaluated by query_states / graph_states (inf if none)."""
+        return float(lib().kgo_last_margin())
+
     # -- query computation graphs -------------------------------------------
     def graph_info(self, nodes) -> tuple:
         """(anchor slots, relation slots, answer terms) of a graph given as an
@@ -233,8 +263,10 @@ class Model:
             raise ValueError("oracle rejected the graph")
         return out[: n * self.width].reshape(n, self.width)
 
-    def graph_scores(self, nodes, anchors: np.ndarray, rels: np.ndarray, nthreads: int = 0) -> np.ndarray:
-        """[B x N] float64 scores of B queries sharing one graph."""
+    def graph_scores(self, nodes, anchors: np.ndarray, rels: np.ndarray, nthreads: int = 0,
+                     with_margin: bool = False):
+        """[B x N] float64 scores of B queries sharing one graph (and, with
+        with_margin, each query's ConE discontinuity margin [B])."""
         g = np.ascontiguousarray(nodes, np.int32).reshape(-1, 6)
         a = np.ascontiguousarray(anchors, np.int32)
         r = np.ascontiguousarray(rels, np.int32)
@@ -244,16 +276,18 @@ class Model:
             r = r.reshape(-1, 1)
         B = a.shape[0]
         out = np.empty((B, self.n_entities), np.float64)
+        mg = np.empty(B, np.float64)
         rc = lib().kgo_graph_scores(self.ref, _ip(g), g.shape[0], B, _ip(a), a.shape[1], _ip(r), r.shape[1],
-                                    _dp(out), nthreads)
+                                    _dp(out), _dp(mg), nthreads)
         if rc != 0:
             raise ValueError("oracle rejected the graph or an id")
-        return out
+        return (out, mg) if with_margin else out
 
     # -- batched ------------------------------------------------------------
     def scores(self, structure_ids, anchors: np.ndarray, rels: np.ndarray,
-               nthreads: int = 0) -> np.ndarray:
-        """[B x N] float64 scores. structure_ids: int or int array [B]."""
+               nthreads: int = 0, with_margin: bool = False):
+        """[B x N] float64 scores. structure_ids: int or int array [B]. With
+        with_margin, also each query's ConE discontinuity margin [B]."""
         a = np.ascontiguousarray(anchors, np.int32)
         r = np.ascontiguousarray(rels, np.int32)
         B = a.shape[0]
@@ -262,11 +296,12 @@ class Model:
         else:
             sid = np.ascontiguousarray(structure_ids, np.int32)
         out = np.empty((B, self.n_entities), np.float64)
+        mg = np.empty(B, np.float64)
         rc = lib().kgo_scores(self.ref, B, _ip(sid), _ip(a), a.shape[1], _ip(r), r.shape[1],
-                              _dp(out), nthreads)
+                              _dp(out), _dp(mg), nthreads)
         if rc != 0:
             raise ValueError("oracle rejected the batch (structure, arity or id out of range)")
-        return out
+        return (out, mg) if with_margin else out
 
 
 def topk(scores: np.ndarray, k: int, nthreads: int = 0):

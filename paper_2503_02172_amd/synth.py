@@ -37,8 +37,14 @@ ARITY: Dict[str, tuple] = {
     "2in": (2, 2), "3in": (3, 3), "inp": (2, 3), "pin": (2, 3), "pni": (2, 3),
 }
 
-MODEL_GQE, MODEL_Q2B, MODEL_BETAE = 0, 1, 2
-MODEL_NAMES = {MODEL_GQE: "gqe", MODEL_Q2B: "q2b", MODEL_BETAE: "betae"}
+MODEL_GQE, MODEL_Q2B, MODEL_BETAE, MODEL_CONE, MODEL_LOGICE = 0, 1, 2, 3, 4
+MODEL_NAMES = {MODEL_GQE: "gqe", MODEL_Q2B: "q2b", MODEL_BETAE: "betae", MODEL_CONE: "cone",
+               MODEL_LOGICE: "logice"}
+# LogicE intersection t-norms
+TNORM_PRODUCT, TNORM_MIN, TNORM_LUKASIEWICZ = 0, 1, 2
+TNORM_NAMES = {TNORM_PRODUCT: "product", TNORM_MIN: "min", TNORM_LUKASIEWICZ: "lukasiewicz"}
+# models with a negation operator: they run all 14 structures
+NEGATION_MODELS = (MODEL_BETAE, MODEL_CONE, MODEL_LOGICE)
 
 
 def glorot(rng: np.random.Generator, out_f: int, in_f: int) -> np.ndarray:
@@ -102,6 +108,7 @@ class Workload:
     center_reg: float = 0.02
     entity_bf16: Optional[np.ndarray] = None   # uint16 [N x 2d] when the table is stored as bf16
     extra_models: Dict[str, dict] = dataclasses.field(default_factory=dict)
+    tnorm: int = TNORM_PRODUCT                 # LogicE intersection t-norm
 
 
 def _draw_single(rng, structure: str, n: int, n_ent: int, n_rel: int) -> QueryBatch:
@@ -162,11 +169,56 @@ def _betae_params(rng, n_ent, n_rel, d) -> Dict[str, np.ndarray]:
     return p
 
 
+def _cone_params(rng, n_ent, n_rel, d, gamma) -> Dict[str, np.ndarray]:
+    """ConE: entity axes uniform on the circle; relation axes uniform and
+    relation half-apertures uniform in [0, pi] (both enter the projection
+    input additively); MLP weights per Glorot; the distance scale of the
+    model's score, 0.5 (gamma + 2) / d."""
+    p = {}
+    p["entity.axis"] = rng.uniform(-np.pi, np.pi, size=(n_ent, d)).astype(np.float32)
+    rel_axis = rng.uniform(-np.pi, np.pi, size=(n_rel, d))
+    rel_arg = rng.uniform(0.0, np.pi, size=(n_rel, d))
+    p["relation"] = np.concatenate([rel_axis, rel_arg], axis=1).astype(np.float32)
+    h = 4 * d
+    p["proj.w1"] = glorot(rng, h, 2 * d)
+    p["proj.b1"] = bias(rng, h, 2 * d)
+    p["proj.w2"] = glorot(rng, h, h)
+    p["proj.b2"] = bias(rng, h, h)
+    p["proj.w3"] = glorot(rng, 2 * d, h)
+    p["proj.b3"] = bias(rng, 2 * d, h)
+    for grp in ("inter.axis", "inter.arg"):
+        p[grp + ".w1"] = glorot(rng, d, 2 * d)
+        p[grp + ".b1"] = bias(rng, d, 2 * d)
+        p[grp + ".w2"] = glorot(rng, d, d)
+        p[grp + ".b2"] = bias(rng, d, d)
+    p["modulus"] = np.array([0.5 * (gamma + 2.0) / d], np.float32)
+    return p
+
+
+def _logice_params(rng, n_ent, n_rel, d) -> Dict[str, np.ndarray]:
+    """LogicE: entity bounds l ~ U(0, 1), u = l + U(0, 1) (1 - l); relation
+    vectors ~ U(-1, 1) (concatenated to the projection input); MLP weights
+    per Glorot (the first layer takes 3d inputs)."""
+    p = {}
+    lo = rng.uniform(0.0, 1.0, size=(n_ent, d))
+    hi = lo + rng.uniform(0.0, 1.0, size=(n_ent, d)) * (1.0 - lo)
+    p["entity.bounds"] = np.concatenate([lo, hi], axis=1).astype(np.float32)
+    p["relation"] = rng.uniform(-1.0, 1.0, size=(n_rel, d)).astype(np.float32)
+    h = 4 * d
+    p["proj.w1"] = glorot(rng, h, 3 * d)
+    p["proj.b1"] = bias(rng, h, 3 * d)
+    p["proj.w2"] = glorot(rng, h, h)
+    p["proj.b2"] = bias(rng, h, h)
+    p["proj.w3"] = glorot(rng, 2 * d, h)
+    p["proj.b3"] = bias(rng, 2 * d, h)
+    return p
+
+
 EPFO = ["1p", "2p", "3p", "2i", "3i", "pi", "ip", "2u", "up"]
 
 
 def make_workload(name: str) -> Workload:
-    """Build one of the five named workloads (C1..C5)."""
+    """Build one of the named workloads: C1..C5, and "cone" / "logice"."""
     if name == "C1":
         rng = np.random.Generator(np.random.PCG64(20250301))
         N, R, d = 1000, 20, 32
@@ -215,11 +267,25 @@ def make_workload(name: str) -> Workload:
         w = Workload("C5", MODEL_BETAE, N, R, d, 60.0, 100, 2e-3, p, batches)
         w.entity_bf16 = bf16_rne(p["entity.alpha_beta"])
         return w
+    if name == "cone":
+        # ConE at FB15K-237's shape, every structure
+        rng = np.random.Generator(np.random.PCG64(20250306))
+        N, R, d, g = 14505, 474, 400, 30.0
+        p = _cone_params(rng, N, R, d, g)
+        batches = [_draw_single(rng, s, 256, N, R) for s in STRUCTURES]
+        return Workload("cone", MODEL_CONE, N, R, d, g, 100, 1e-4, p, batches)
+    if name == "logice":
+        # LogicE at FB15K-237's shape, every structure, product t-norm
+        rng = np.random.Generator(np.random.PCG64(20250307))
+        N, R, d, g = 14505, 474, 400, 1.0
+        p = _logice_params(rng, N, R, d)
+        batches = [_draw_single(rng, s, 512, N, R) for s in STRUCTURES]
+        return Workload("logice", MODEL_LOGICE, N, R, d, g, 100, 1e-4, p, batches, tnorm=TNORM_PRODUCT)
     raise ValueError(f"unknown workload {name!r}")
 
 
 def make_tiny(model: int, n_ent: int = 37, n_rel: int = 5, dim: int = 8, seed: int = 7,
-              gamma: Optional[float] = None) -> Workload:
+              gamma: Optional[float] = None, tnorm: int = TNORM_PRODUCT) -> Workload:
     """A small workload of the given model with odd sizes (tile tails)."""
     rng = np.random.Generator(np.random.PCG64(seed))
     if model == MODEL_GQE:
@@ -233,6 +299,14 @@ def make_tiny(model: int, n_ent: int = 37, n_rel: int = 5, dim: int = 8, seed: i
         g = 24.0 if gamma is None else gamma
         p = _q2b_params(rng, n_ent, n_rel, dim, g)
         return Workload("tiny-q2b", model, n_ent, n_rel, dim, g, 5, 1e-4, p, [])
+    if model == MODEL_CONE:
+        g = 30.0 if gamma is None else gamma
+        p = _cone_params(rng, n_ent, n_rel, dim, g)
+        return Workload("tiny-cone", model, n_ent, n_rel, dim, g, 5, 1e-4, p, [])
+    if model == MODEL_LOGICE:
+        g = 1.0 if gamma is None else gamma
+        p = _logice_params(rng, n_ent, n_rel, dim)
+        return Workload("tiny-logice", model, n_ent, n_rel, dim, g, 5, 1e-4, p, [], tnorm=tnorm)
     g = 60.0 if gamma is None else gamma
     p = _betae_params(rng, n_ent, n_rel, dim)
     return Workload("tiny-betae", model, n_ent, n_rel, dim, g, 5, 1e-4, p, [])
