@@ -10,9 +10,11 @@
  * entity against each query embedding (the "entity similarity query" of
  * the Experiments section) and selects the top k.
  *
- * Three embedding models are supported: GQE, Query2Box and BetaE (the paper
- * names them in Related Work and Experiments/Baselines; BetaE's Beta
- * embedding is its Eq. 3 and BetaE's projection the MLP of its Eq. 4).
+ * Five embedding models are supported: GQE, Query2Box, BetaE, ConE and
+ * LogicE (the paper names them in Related Work and Experiments/Baselines and
+ * times them in Table 1; BetaE's Beta embedding is its Eq. 3 and BetaE's
+ * projection the MLP of its Eq. 4; the operators of the others follow the
+ * models' own definitions, as described at kgq_load_params).
  *
  * Conventions
  *  - Every function returns a kgq_status; no C++ exception crosses the ABI.
@@ -62,8 +64,10 @@ typedef enum {
     KGQ_E_DEVICE = -7         /* a HIP runtime call failed */
 } kgq_status;
 
-typedef enum { KGQ_GQE = 0, KGQ_Q2B = 1, KGQ_BETAE = 2 } kgq_model;
+typedef enum { KGQ_GQE = 0, KGQ_Q2B = 1, KGQ_BETAE = 2, KGQ_CONE = 3, KGQ_LOGICE = 4 } kgq_model;
 typedef enum { KGQ_F32 = 0, KGQ_BF16 = 1 } kgq_dtype;
+/* LogicE intersection t-norm: a * b, min(a, b), or max(0, a + b - 1). */
+typedef enum { KGQ_TNORM_PRODUCT = 0, KGQ_TNORM_MIN = 1, KGQ_TNORM_LUKASIEWICZ = 2 } kgq_tnorm;
 
 /* Query structures, in the column order of the paper's Table 1. The shapes
  * (the paper shows them only in its Fig. 1): "p" chains projections, "i"
@@ -77,7 +81,8 @@ typedef enum { KGQ_F32 = 0, KGQ_BF16 = 1 } kgq_dtype;
  *   2u  a0.r0 | a1.r1              up  (a0.r0 | a1.r1).r2 = a0.r0.r2 | a1.r1.r2
  *   2in a0.r0 & !a1.r1             3in a0.r0 & a1.r1 & !a2.r2
  *   inp (a0.r0 & !a1.r1).r2        pin a0.r0.r1 & !a1.r2      pni !(a0.r0.r1) & a1.r2
- * The five structures with negation (ids 9..13) exist for BetaE only. */
+ * The five structures with negation (ids 9..13) exist for BetaE, ConE and
+ * LogicE; GQE and Query2Box define no negation (Experiments, Baselines). */
 typedef enum {
     KGQ_1P = 0, KGQ_2P, KGQ_3P, KGQ_2I, KGQ_3I, KGQ_PI, KGQ_IP, KGQ_2U, KGQ_UP,
     KGQ_2IN, KGQ_3IN, KGQ_INP, KGQ_PIN, KGQ_PNI, KGQ_NUM_STRUCTURES
@@ -92,11 +97,13 @@ typedef struct {
     int32_t n_relations;  /* R >= 1 */
     int32_t entity_dtype; /* kgq_dtype of the entity table as passed to kgq_load_params */
     float gamma;          /* score margin: score = gamma - distance */
-    float center_reg;     /* Query2Box weight of the inside distance (0.02 in the standard model); ignored otherwise */
+    float center_reg;     /* Query2Box and ConE: weight of the inside distance (0.02 in the standard
+                             models); ignored otherwise */
     int32_t max_batch;    /* largest batch any execute call will pass; sizes the scratch space */
     int32_t device;       /* HIP device ordinal, or -1 for a validation-only handle with no GPU */
     int32_t concurrency;  /* scratch sets (1 if 0): executes issued on different streams can run
                              concurrently, up to this many at once */
+    int32_t tnorm;        /* LogicE: kgq_tnorm of the intersection; ignored otherwise */
 } kgq_config;
 
 /* Create a handle for one embedding model on one GPU (GQE, Query2Box or
@@ -107,7 +114,8 @@ typedef struct {
  * structures are compiled into fused programs (once per process, at the
  * first create) and the handle refers to them; parameters arrive with
  * kgq_load_params.
- * Errors: INVALID_ARG (cfg or out null, bad field), NO_DEVICE, OOM, DEVICE.
+ * Errors: INVALID_ARG (cfg or out null, bad field, tnorm outside kgq_tnorm
+ * for LogicE), NO_DEVICE, OOM, DEVICE.
  * A handle with device = -1 validates arguments exactly like a real one;
  * its execute calls return NO_DEVICE once every argument has passed. */
 kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out);
@@ -124,6 +132,26 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out);
  *          "proj.w1" [4d x 2d], "proj.b1" [4d], "proj.w2" [4d x 4d], "proj.b2" [4d],
  *          "proj.w3" [2d x 4d], "proj.b3" [2d],
  *          "inter.w1" [2d x 2d], "inter.b1" [2d], "inter.w2" [d x 2d], "inter.b2" [d]
+ *   ConE:  "entity.axis" [N x d] (entity cone axes in [-pi, pi); an entity is a
+ *          cone of aperture 0), "relation" [R x 2d] (axis | half-aperture, added
+ *          to the source cone before the projection MLP),
+ *          "proj.w1" [4d x 2d], "proj.b1" [4d], "proj.w2" [4d x 4d], "proj.b2" [4d],
+ *          "proj.w3" [2d x 4d], "proj.b3" [2d] (axis = pi tanh(y), half-aperture =
+ *          pi/2 (tanh(2 y') + 1)),
+ *          "inter.axis.{w1 [d x 2d], b1 [d], w2 [d x d], b2 [d]}" (attention over
+ *          [axis - aperture; axis + aperture], softmax across branches, weighted
+ *          mean of the axes' unit vectors),
+ *          "inter.arg.{w1 [d x 2d], b1 [d], w2 [d x d], b2 [d]}" (sigmoid gate on
+ *          the mean of the branches' features, times the minimum half-aperture),
+ *          "modulus" [1] (score = gamma - modulus (outside + center_reg inside
+ *          sector distance)); negation is the complementary cone
+ *   LogicE: "entity.bounds" [N x 2d] (lower bounds in columns 0..d-1, upper in
+ *          d..2d-1, 0 <= lower <= upper <= 1), "relation" [R x d] (concatenated
+ *          to the source bounds before the projection MLP),
+ *          "proj.w1" [4d x 3d], "proj.b1" [4d], "proj.w2" [4d x 4d], "proj.b2" [4d],
+ *          "proj.w3" [2d x 4d], "proj.b3" [2d] (lower = sigmoid(y), upper = lower +
+ *          sigmoid(y') (1 - lower)); intersection by cfg.tnorm, negation
+ *          [l; u] -> [1 - u; 1 - l], score gamma - ||e - q||_1 / (2d)
  * dtype is KGQ_F32 for every array except the entity table, which takes
  * cfg.entity_dtype (KGQ_BF16: bfloat16 bit patterns, decoded to float32 on
  * the device). nbytes must equal the array's size. src is a host pointer,
@@ -131,11 +159,13 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out);
  * call returns (the call synchronises). Loading a name again replaces it.
  * Derived tables are rebuilt here, not in execute: the blocked entity
  * layout for scoring, Query2Box's softplus offsets, BetaE's per-entity
- * digamma / log-Beta tables, and BetaE's first-projection-layer tables
- * (entity alpha|beta . W1^T [N x 4d] and relation . W1^T + b1 [R x 4d]; the
- * layer is linear in its input [alpha; beta] + Rel[r], Eq. 4), which are
- * rebuilt when "entity.alpha_beta", "relation", "proj.w1" or "proj.b1" is
- * loaded and all four are present.
+ * digamma / log-Beta tables, ConE's per-entity half-angle sines and cosines,
+ * ConE's stacked intersection first layer ([inter.axis.w1; inter.arg.w1]),
+ * and the first-projection-layer tables of BetaE, ConE and LogicE (entity
+ * state . W1^T [N x 4d] and relation . W1^T + b1 [R x 4d], where W1 is split
+ * by columns for LogicE's concatenated input; the layer is linear in its
+ * input, Eq. 4), rebuilt when the entity table, "relation", "proj.w1" or
+ * "proj.b1" is loaded and all four are present.
  * Errors: INVALID_ARG (unknown name, wrong nbytes or dtype, null src), OOM, DEVICE. */
 kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, size_t nbytes,
                            int32_t dtype, int32_t src_is_device);
@@ -261,7 +291,7 @@ typedef enum {
     KGQ_OP_PROJECT = 1,   /* projection of in[0] by the relation in relation slot `slot` */
     KGQ_OP_AND = 2,       /* intersection of in[0..] (2 to 4 inputs) */
     KGQ_OP_OR = 3,        /* union of in[0..] (2 to 4 inputs) */
-    KGQ_OP_NOT = 4        /* negation of in[0] (BetaE only) */
+    KGQ_OP_NOT = 4        /* negation of in[0] (BetaE, ConE, LogicE) */
 } kgq_op;
 
 typedef struct {

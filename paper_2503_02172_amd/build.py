@@ -27,7 +27,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I" + os.path.join(ROOT, "include"),
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall", "-Wno-unused-result"]
 EXTRA = {"k_score.hip": ["-fno-honor-nans"]}
-SOURCES = ["kgq_api.cpp", "plan.cpp", "k_embed.hip", "k_gemm.hip", "k_score.hip", "k_score_kl.hip", "k_topk.hip", "k_rank.hip"]
+SOURCES = ["kgq_api.cpp", "plan.cpp", "k_embed.hip", "k_gemm.hip", "k_score.hip", "k_score_kl.hip", "k_topk.hip",
+           "k_rank.hip", "k_cone_logice.hip"]
 
 
 def _compile(src: str, verbose: bool) -> str:

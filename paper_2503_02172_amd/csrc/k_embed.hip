@@ -486,16 +486,19 @@ void launch_betae_proj1(const int32_t* anchor_ref, const int32_t* rel_ref, int M
 }
 
 // ---------------------------------------------------------------------------
-// Query packing for the VALU scorers (GQE, Query2Box): [row_block][k][field][TQ].
+// Query packing for the VALU scorers (GQE, Query2Box, LogicE): [row_block][k][field][TQ].
 // One workgroup per block of TQ rows transposes through LDS, KC dimensions at
 // a time (as many as a 32 KiB tile holds, so that all loads of a chunk are in
 // flight together): the state rows are read along k and the packed block is
 // written in its own order, both contiguous.
 // ---------------------------------------------------------------------------
 
-template <int TQ, int F>
-__global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows, const float* states, int W, int d,
-                                              float* qpack)
+// NEGL (LogicE): a row with neg[j] != 0 is packed complemented, [1 - u; 1 - l]
+// of its state [l; u] (d = 2 * half coordinates): coordinate c reads the
+// state's coordinate (c + half) mod d and packs 1 minus it.
+template <int TQ, int F, bool NEGL>
+__global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, const int32_t* neg, int half, int n_rows,
+                                              const float* states, int W, int d, float* qpack)
 {
     // dimensions per chunk: up to a 32 KiB tile (d = 400: one or two
     // chunks), a multiple of 4 so that no float4 straddles two fields
@@ -503,11 +506,13 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows
     constexpr int RS = F * KC + 1;            // padded LDS row: the transposed reads hit distinct banks
     __shared__ float tile[TQ * RS];
     __shared__ int srcs[TQ];
+    __shared__ int negs[TQ];
     const int qb = blockIdx.x;
     const int t = threadIdx.x;
     if (t < TQ) {
         const int j = qb * TQ + t;
         srcs[t] = j < n_rows ? src_row[j] : -1;
+        negs[t] = (NEGL && j < n_rows && neg) ? neg[j] : 0;
     }
     __syncthreads();
     float* out = qpack + (int64_t)qb * d * F * TQ;
@@ -527,7 +532,9 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows
             const int f = rem / kc, kk = rem - f * kc;
             const int src = srcs[i];
             const bool ok = t + 256 * u < n4 && src >= 0;
-            const int64_t off = ok ? (int64_t)src * W + f * d + k0 + kk : 0;
+            int col = f * d + k0 + kk;
+            if (NEGL && negs[i]) col = col >= half ? col - half : col + half;
+            const int64_t off = ok ? (int64_t)src * W + col : 0;
             v[u] = *reinterpret_cast<const float4*>(states + off);
         }
 #pragma unroll
@@ -540,10 +547,12 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, int n_rows
             const int f = rem / kc, kk = rem - f * kc;
             const bool ok = srcs[i] >= 0;
             float* dst = tile + i * RS + f * KC + kk;
-            dst[0] = ok ? v[u].x : 0.f;
-            dst[1] = ok ? v[u].y : 0.f;
-            dst[2] = ok ? v[u].z : 0.f;
-            dst[3] = ok ? v[u].w : 0.f;
+            float4 x = v[u];
+            if (NEGL && negs[i]) x = make_float4(1.0f - x.x, 1.0f - x.y, 1.0f - x.z, 1.0f - x.w);
+            dst[0] = ok ? x.x : 0.f;
+            dst[1] = ok ? x.y : 0.f;
+            dst[2] = ok ? x.z : 0.f;
+            dst[3] = ok ? x.w : 0.f;
         }
         __syncthreads();
         for (int o = t; o < kc * F * TQ; o += 256) {
@@ -596,20 +605,28 @@ void launch_pack(int model, const int32_t* src_row, const int32_t* neg, int n_ro
                  const float* states, int W, int d, float* qpack, double* cq, hipStream_t s)
 {
     if (n_rows_pad <= 0) return;
-    if (model == 2) {
+    if (model == KGQ_BETAE) {
         hipLaunchKernelGGL(k_pack_rows, dim3(n_rows_pad), dim3(256), 0, s, src_row, neg, n_rows, states, d, qpack,
                            cq);
+        return;
+    }
+    if (model == KGQ_CONE) {
+        launch_pack_cone(src_row, neg, n_rows, n_rows_pad, states, d, qpack, s);
         return;
     }
     const int tq = score_tq(model, n_rows);
     const bool small = score_small(n_rows);
     const dim3 grid(n_rows_pad / tq);          // n_rows_pad is a multiple of score_row_pad, hence of tq
-    if (model == 0) {
-        if (small) hipLaunchKernelGGL((k_pack<kTqGqeSmall, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
-        else hipLaunchKernelGGL((k_pack<kTqGqe, 1>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
+    if (model == KGQ_GQE) {
+        if (small) hipLaunchKernelGGL((k_pack<kTqGqeSmall, 1, false>), grid, dim3(256), 0, s, src_row, nullptr, 0, n_rows, states, W, d, qpack);
+        else hipLaunchKernelGGL((k_pack<kTqGqe, 1, false>), grid, dim3(256), 0, s, src_row, nullptr, 0, n_rows, states, W, d, qpack);
+    } else if (model == KGQ_LOGICE) {
+        // the 2d bound coordinates as one field (d here is the width 2d)
+        if (small) hipLaunchKernelGGL((k_pack<kTqGqeSmall, 1, true>), grid, dim3(256), 0, s, src_row, neg, d / 2, n_rows, states, W, d, qpack);
+        else hipLaunchKernelGGL((k_pack<kTqGqe, 1, true>), grid, dim3(256), 0, s, src_row, neg, d / 2, n_rows, states, W, d, qpack);
     } else {
-        if (small) hipLaunchKernelGGL((k_pack<kTqQ2bSmall, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
-        else hipLaunchKernelGGL((k_pack<kTqQ2b, 2>), grid, dim3(256), 0, s, src_row, n_rows, states, W, d, qpack);
+        if (small) hipLaunchKernelGGL((k_pack<kTqQ2bSmall, 2, false>), grid, dim3(256), 0, s, src_row, nullptr, 0, n_rows, states, W, d, qpack);
+        else hipLaunchKernelGGL((k_pack<kTqQ2b, 2, false>), grid, dim3(256), 0, s, src_row, nullptr, 0, n_rows, states, W, d, qpack);
     }
 }
 

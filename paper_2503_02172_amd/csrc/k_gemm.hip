@@ -1,8 +1,9 @@
 // Dense layers on the FP32 matrix cores of gfx950:  C = epi(A W^T + b).
 //
-// These are the dense contractions of the operators: BetaE's projection MLP
-// (Eq. 4 of the paper: three matmul + bias layers with ReLU between them)
-// and the attention / set-function MLPs of the intersection operators. Both
+// These are the dense contractions of the operators: the projection MLPs of
+// BetaE, ConE and LogicE (Eq. 4 of the paper: three matmul + bias layers with
+// ReLU between them) and the attention / set-function MLPs of the
+// intersection operators. Both
 // operands are K-contiguous (A rows, W rows). The tile loop (mfma_tile.hpp)
 // runs 64 x 64 workgroup tiles: at the path's shapes (M of a few hundred to a
 // few thousand rows, N and K of 400 to 1,600) they give enough workgroups to
@@ -49,9 +50,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, int tm, int tn, int pe
             for (int r = 0; r < 4; ++r) {
                 const int m = m0 + GemmTile::row_of(i) + r;
                 if (m >= g.M) continue;
-                float v = acc[i][j][r] + b;
-                if (g.epi == EPI_RELU) v = v > 0.f ? v : 0.f;
-                else if (g.epi == EPI_BETA_REG) v = fminf(fmaxf(v + 1.0f, 0.05f), 1e9f);
+                const float v = apply_epilogue(g.epi, g.epi_split, n, acc[i][j][r] + b);
                 const int64_t row = g.c_rowmap ? (int64_t)g.c_rowmap[m] : (int64_t)m;
                 g.C[row * g.ldc + n] = v;
             }
@@ -104,8 +103,7 @@ __global__ __launch_bounds__(256) void k_gemm_reduce(GemmArgs g, int splits)
     float v = 0.f;
     for (int z = 0; z < splits; ++z) v += g.ws[(int64_t)z * g.M * g.N + t];
     v += g.bias ? g.bias[n] : 0.f;
-    if (g.epi == EPI_RELU) v = v > 0.f ? v : 0.f;
-    else if (g.epi == EPI_BETA_REG) v = fminf(fmaxf(v + 1.0f, 0.05f), 1e9f);
+    v = apply_epilogue(g.epi, g.epi_split, n, v);
     const int64_t row = g.c_rowmap ? (int64_t)g.c_rowmap[m] : (int64_t)m;
     g.C[row * g.ldc + n] = v;
 }

@@ -1,8 +1,9 @@
-// Entity scoring for GQE and Query2Box: the "entity similarity query" that
-// the paper times together with operator execution (Experiments, Metrics):
-// every query embedding is scored against every entity. (BetaE's regrouped
-// KL score is a dense contraction and runs on the matrix cores,
-// k_score_kl.hip.)
+// Entity scoring for GQE, Query2Box, ConE and LogicE: the "entity similarity
+// query" that the paper times together with operator execution (Experiments,
+// Metrics): every query embedding is scored against every entity. (BetaE's
+// regrouped KL score is a dense contraction and runs on the matrix cores,
+// k_score_kl.hip.) LogicE's score is GQE's L1 distance over its 2d bound
+// coordinates, scaled by 1 / (2d).
 //
 // This is VALU work, not a dense contraction: per (query, entity, dim)
 // triple GQE needs |q - e| accumulated, Query2Box a box distance. The kernel
@@ -25,6 +26,16 @@
 //           score = gamma - acc1 + (1 - center_reg) * acc2, the exact
 //           regrouping of dist_out + center_reg * dist_in
 //           (t <= o: center_reg * t; t > o: (t - o) + center_reg * o)
+//   ConE    with the entity's half-angle sine / cosine (Se, Ce) from the
+//           table and the query's (Ca, Sa) of theta/2 and (Cb, Sb) of psi/2:
+//           s = Se Ca - Ce Sa = sin((theta_e - theta)/2),
+//           c = Ce Ca + Se Sa = cos((theta_e - theta)/2),
+//           t = |s| Cb - |c| Sb;  acc1 += max(t, 0);  acc2 += min(|s|, Sb) (10)
+//           score = gamma - modulus (acc1 + center_reg acc2). This is the
+//           sector distance exactly: min(|sin(a + b)|, |sin(a - b)|) =
+//           ||sin a| cos b - |cos a| sin b| for b = psi/2 in [0, pi/2], and
+//           the bracket is negative exactly when |sin a| < sin b, i.e. inside
+//           the sector, where the outside distance is 0.
 // Union (disjunctive normal form, Eq. 1 of the paper): a query whose answer
 // has 2 conjunctive terms has two adjacent rows (a pair), one with 3 or 4
 // terms a group of four rows; its score is the max over the rows' scores.
@@ -78,23 +89,26 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     const int qb = qg * 4 + wave;
     if (qb * TQ >= a.n_rows) return;
 
-    constexpr int F = (MODEL == 0) ? 1 : 2;      // query fields per row
+    constexpr int F = (MODEL == 0) ? 1 : (MODEL == 1 ? 2 : 4);   // query fields per row
+    constexpr int EF = (MODEL == 3) ? 2 : 1;                       // entity fields per dimension
+    constexpr bool TWO = MODEL != 0;                               // two accumulators per triple
+    constexpr int AF = TWO ? 2 : 1;                                // accumulator fields (split-d partials)
     // Small batches split the dimensions over blockIdx.y: slice z covers
     // [z * kslice, z * kslice + d) (kslice and d multiples of 4) and writes
     // its raw accumulators to a.part instead of scores.
     const int k_begin = blockIdx.y * kslice;
     const int d = min(kslice, a.d - k_begin);
     const float* __restrict__ qp = a.qpack + ((int64_t)qb * a.d + k_begin) * F * TQ;
-    const float* __restrict__ ep = a.ent + ((int64_t)eb * a.d + k_begin) * kEntBlock + lane * 4;
+    const float* __restrict__ ep = a.ent + ((int64_t)eb * a.d + k_begin) * EF * kEntBlock + lane * 4;
 
     float acc[TQ][4];
-    float acc2[(MODEL == 1) ? TQ : 1][4];
+    float acc2[TWO ? TQ : 1][4];
 #pragma unroll
     for (int i = 0; i < TQ; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
 #pragma unroll
-    for (int i = 0; i < ((MODEL == 1) ? TQ : 1); ++i)
+    for (int i = 0; i < (TWO ? TQ : 1); ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc2[i][j] = 0.f;
 
@@ -107,17 +121,37 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     // The packed queries are read-only for the whole kernel; reading them
     // through the constant address space keeps them on scalar loads.
     const __attribute__((address_space(4))) float* qc = (const __attribute__((address_space(4))) float*)qp;
-    auto load_e = [&](int k, float4& u) { u = *reinterpret_cast<const float4*>(ep + (int64_t)k * kEntBlock); };
+    // a step's entity vectors: EF float4 (ConE: sines, then cosines)
+    struct EVec {
+        float4 v[EF];
+    };
+    auto load_e = [&](int k, EVec& u) {
+#pragma unroll
+        for (int f = 0; f < EF; ++f)
+            u.v[f] = *reinterpret_cast<const float4*>(ep + ((int64_t)k * EF + f) * kEntBlock);
+    };
     // rows [R0, R1) of one step
-    auto compute = [&](const float4& eu, const float* qv, auto R0c, auto R1c) {
+    auto compute = [&](const EVec& eu, const float* qv, auto R0c, auto R1c) {
         constexpr int R0 = decltype(R0c)::value, R1 = decltype(R1c)::value;
-        const float e4[4] = {eu.x, eu.y, eu.z, eu.w};
+        const float e4[4] = {eu.v[0].x, eu.v[0].y, eu.v[0].z, eu.v[0].w};
 #pragma unroll
         for (int i = R0; i < R1; ++i) {
             const float c = qv[i];
             if (MODEL == 0) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] += fabsf(e4[j] - c);
+            } else if (MODEL == 3) {
+                const float ce4[4] = {eu.v[EF - 1].x, eu.v[EF - 1].y, eu.v[EF - 1].z, eu.v[EF - 1].w};
+                const float sa = qv[TQ + i], cb = qv[2 * TQ + i], sb = qv[3 * TQ + i];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float sn = fmaf(-ce4[j], sa, e4[j] * c);    // sin((theta_e - theta) / 2)
+                    const float cs = fmaf(e4[j], sa, ce4[j] * c);     // cos((theta_e - theta) / 2)
+                    const float as = fabsf(sn);
+                    const float t = fmaf(-fabsf(cs), sb, as * cb);
+                    acc[i][j] += __builtin_fmaxf(t, 0.f);
+                    acc2[i][j] += __builtin_fminf(as, sb);
+                }
             } else {
                 const float o = qv[TQ + i];
 #pragma unroll
@@ -132,7 +166,7 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
     using H0 = std::integral_constant<int, 0>;
     using H1 = std::integral_constant<int, TQ / 2>;
     using H2 = std::integral_constant<int, TQ>;
-    float4 ua, ub;
+    EVec ua, ub;
     float qa[QN], qb2[QN];
     load_e(0, ua);
 #pragma unroll
@@ -163,12 +197,12 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
         // split-d: raw accumulators of this slice, [slice][field][row][entity]
         // over the padded rows (nqg * 4 * TQ) and entities (n_blocks * 256)
         const int64_t n_pad = a.n_blocks * kEntBlock, rows_pad = (int64_t)nqg * 4 * TQ;
-        float* pz = a.part + (int64_t)blockIdx.y * F * rows_pad * n_pad;
+        float* pz = a.part + (int64_t)blockIdx.y * AF * rows_pad * n_pad;
 #pragma unroll
         for (int i = 0; i < TQ; ++i) {
             const int64_t row = (int64_t)qb * TQ + i;
             *reinterpret_cast<float4*>(pz + row * n_pad + e0) = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
-            if (MODEL == 1)
+            if (TWO)
                 *reinterpret_cast<float4*>(pz + (rows_pad + row) * n_pad + e0) =
                     make_float4(acc2[i][0], acc2[i][1], acc2[i][2], acc2[i][3]);
         }
@@ -184,7 +218,8 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
         for (int u = 0; u < 4; ++u)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                if (MODEL == 0) sc[u][j] = a.gamma - acc[i + u][j];
+                if (MODEL == 0) sc[u][j] = a.gamma - a.dist_scale * acc[i + u][j];
+                else if (MODEL == 3) sc[u][j] = a.gamma - a.dist_scale * fmaf(a.center_reg, acc2[i + u][j], acc[i + u][j]);
                 else sc[u][j] = a.gamma - acc[i + u][j] + (1.0f - a.center_reg) * acc2[i + u][j];
             }
         if (row < a.n_quad) {
@@ -220,7 +255,7 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
 template <int MODEL>
 __global__ __launch_bounds__(256) void k_score_sum(ScoreArgs a, int splits, int64_t rows_pad, int n_out)
 {
-    constexpr int F = (MODEL == 0) ? 1 : 2;
+    constexpr int F = (MODEL == 0) ? 1 : 2;     // accumulator fields of the partials (as AF in k_score)
     const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (t >= (int64_t)n_out * a.N) return;
     const int o = (int)(t / a.N);
@@ -244,9 +279,11 @@ __global__ __launch_bounds__(256) void k_score_sum(ScoreArgs a, int splits, int6
         for (int z = 0; z < splits; ++z) {
             const float* pz = a.part + (int64_t)z * F * rows_pad * n_pad;
             s1 += pz[(int64_t)(r0 + u) * n_pad + e];
-            if (MODEL == 1) s2 += pz[(rows_pad + r0 + u) * n_pad + e];
+            if (MODEL != 0) s2 += pz[(rows_pad + r0 + u) * n_pad + e];
         }
-        const float v = MODEL == 0 ? a.gamma - s1 : a.gamma - s1 + (1.0f - a.center_reg) * s2;
+        const float v = MODEL == 0   ? a.gamma - a.dist_scale * s1
+                        : MODEL == 3 ? a.gamma - a.dist_scale * fmaf(a.center_reg, s2, s1)
+                                     : a.gamma - s1 + (1.0f - a.center_reg) * s2;
         best = u == 0 ? v : fmaxf(best, v);
     }
     a.scores[(int64_t)a.out_dest[o] * a.ld + e] = best;
@@ -255,26 +292,28 @@ __global__ __launch_bounds__(256) void k_score_sum(ScoreArgs a, int splits, int6
 void launch_score(const ScoreArgs& a, hipStream_t s)
 {
     if (a.n_rows <= 0) return;
-    if (a.model == 2) {
+    if (a.model == KGQ_BETAE) {
         launch_score_kl(a, s);
         return;
     }
-    const int tq = score_tq(a.model, a.n_rows);       // the pack's layout for this row count
+    const int form = valu_form(a.model);           // LogicE runs GQE's kernel
+    const int tq = score_tq(a.model, a.n_rows);    // the pack's layout for this row count
     const bool small = score_small(a.n_rows);
     const int nqb = (a.n_rows + tq - 1) / tq;
     const int nqg = (nqb + 3) / 4;
     const int total = (int)(a.n_blocks * nqg);
     const int per_xcd = (total + 7) / 8;
+    const int QF = form == KGQ_GQE ? 1 : (form == KGQ_Q2B ? 2 : 4);   // query fields
     // query chunk: as many query groups as ~2 MiB of packed queries (about
     // half an XCD's L2); the entity table is streamed once per chunk, and the
     // XCDs split the global order evenly whatever the chunk size
-    const int64_t qg_bytes = (int64_t)4 * tq * a.d * (a.model == 0 ? 1 : 2) * 4;   // packed queries of one group
+    const int64_t qg_bytes = (int64_t)4 * tq * a.d * QF * 4;   // packed queries of one group
     const int qc = (int)std::min<int64_t>(nqg, std::max<int64_t>(1, (int64_t)(2 << 20) / qg_bytes));
     // Small batches: with fewer than 128 workgroups the dimension loop is a
     // latency chain on a few compute units, so the dimensions are split over
     // up to 16 slices (each at least 16 dimensions) whose partials fit the
     // lane's workspace; a second kernel sums them.
-    const int F = a.model == 0 ? 1 : 2;
+    const int F = form == KGQ_GQE ? 1 : 2;         // accumulator fields
     const int64_t rows_pad = (int64_t)nqg * 4 * tq, n_pad = a.n_blocks * kEntBlock;
     int splits = 1;
     if (a.part && total < 128 && a.d >= 32) {
@@ -290,21 +329,26 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
         b.part = nullptr;
     }
     dim3 grid(per_xcd * 8, z);
-    if (a.model == 0) {
+    if (form == KGQ_GQE) {
         if (small) hipLaunchKernelGGL((k_score<0, kTqGqeSmall>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
         else hipLaunchKernelGGL((k_score<0, kTqGqe>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
-    } else {
+    } else if (form == KGQ_Q2B) {
         if (small) hipLaunchKernelGGL((k_score<1, kTqQ2bSmall>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
         else hipLaunchKernelGGL((k_score<1, kTqQ2b>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+    } else {
+        if (small) hipLaunchKernelGGL((k_score<3, kTqConeSmall>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
+        else hipLaunchKernelGGL((k_score<3, kTqCone>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
     }
     if (z > 1) {
         const int n_out = (a.n_quad >> 2) + (a.n_pair >> 1) + (a.n_rows - a.n_quad - a.n_pair);
         const int64_t tot = (int64_t)n_out * a.N;
         const dim3 g2((unsigned)((tot + 255) / 256));
-        if (a.model == 0)
+        if (form == KGQ_GQE)
             hipLaunchKernelGGL((k_score_sum<0>), g2, dim3(256), 0, s, b, z, rows_pad, n_out);
-        else
+        else if (form == KGQ_Q2B)
             hipLaunchKernelGGL((k_score_sum<1>), g2, dim3(256), 0, s, b, z, rows_pad, n_out);
+        else
+            hipLaunchKernelGGL((k_score_sum<3>), g2, dim3(256), 0, s, b, z, rows_pad, n_out);
     }
 }
 

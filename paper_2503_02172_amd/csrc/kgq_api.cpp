@@ -96,15 +96,20 @@ struct kgq_handle {
 
     // derived entity tables
     int64_t n_blocks = 0;
-    float* ent_rm = nullptr;      // GQE/Q2B [N x d]; BetaE alpha|beta [N x 2d]
-    float* ent_blk = nullptr;     // scoring table: GQE/Q2B blocked points; BetaE row-major U|V
+    float* ent_rm = nullptr;      // GQE/Q2B [N x d]; BetaE alpha|beta, ConE [axis; 0], LogicE [l; u] [N x 2d]
+    float* ent_blk = nullptr;     // scoring table: GQE/Q2B/LogicE blocked points; BetaE row-major U|V;
+                                  // ConE blocked half-angle sin | cos
     double* ent_const = nullptr;  // BetaE E_e [n_pad]
     float* rel_o_sp = nullptr;    // Q2B softplus(offset_raw) [R x d]
-    // BetaE: the first projection layer is linear in [alpha; beta] + Rel[r],
-    // so for first-hop projections (input = an anchor entity) it splits into
-    // two parameter-only tables, built when their inputs are loaded:
-    float* proj1_ent = nullptr;   // [N x 4d]  entity alpha|beta . W1^T
-    float* proj1_rel = nullptr;   // [R x 4d]  Rel . W1^T + b1
+    float cone_modulus = 0.f;     // ConE distance scale (host copy of "modulus")
+    float* int_cat_w = nullptr;   // ConE [inter.axis.w1; inter.arg.w1] [2d x 2d]
+    float* int_cat_b = nullptr;   // ConE [inter.axis.b1; inter.arg.b1] [2d]
+    // BetaE, ConE, LogicE: the first projection layer is linear in its
+    // input (the source state plus or next to Rel[r]), so for first-hop
+    // projections (input = an anchor entity) it splits into two
+    // parameter-only tables, built when their inputs are loaded:
+    float* proj1_ent = nullptr;   // [N x 4d]  entity state . W1^T (LogicE: its state columns of W1)
+    float* proj1_rel = nullptr;   // [R x 4d]  Rel . W1^T + b1 (LogicE: its relation columns)
     bool proj1_ready = false;
 
     // structure id -> compiled program: the built-ins for this model, then
@@ -178,6 +183,33 @@ void build_specs(kgq_handle* h)
             s[std::string(grp) + "w2"] = {d, d, false};
             s[std::string(grp) + "b2"] = {1, d, false};
         }
+        break;
+    case KGQ_CONE:
+        s["entity.axis"] = {N, d, true};
+        s["relation"] = {R, 2 * d, false};
+        s["proj.w1"] = {4 * d, 2 * d, false};
+        s["proj.b1"] = {1, 4 * d, false};
+        s["proj.w2"] = {4 * d, 4 * d, false};
+        s["proj.b2"] = {1, 4 * d, false};
+        s["proj.w3"] = {2 * d, 4 * d, false};
+        s["proj.b3"] = {1, 2 * d, false};
+        for (const char* grp : {"inter.axis.", "inter.arg."}) {
+            s[std::string(grp) + "w1"] = {d, 2 * d, false};
+            s[std::string(grp) + "b1"] = {1, d, false};
+            s[std::string(grp) + "w2"] = {d, d, false};
+            s[std::string(grp) + "b2"] = {1, d, false};
+        }
+        s["modulus"] = {1, 1, false};
+        break;
+    case KGQ_LOGICE:
+        s["entity.bounds"] = {N, 2 * d, true};
+        s["relation"] = {R, d, false};
+        s["proj.w1"] = {4 * d, 3 * d, false};
+        s["proj.b1"] = {1, 4 * d, false};
+        s["proj.w2"] = {4 * d, 4 * d, false};
+        s["proj.b2"] = {1, 4 * d, false};
+        s["proj.w3"] = {2 * d, 4 * d, false};
+        s["proj.b3"] = {1, 2 * d, false};
         break;
     default:
         s["entity.alpha_beta"] = {N, 2 * d, true};
@@ -284,6 +316,14 @@ void free_all(kgq_handle* h)
     if (h->prof_ref) (void)hipEventDestroy(h->prof_ref);
 }
 
+// Floats of one scored row in the packed query buffer: GQE d; Query2Box
+// (center, offset), BetaE (alpha, beta) and LogicE (l, u) 2d; ConE 4d (the
+// half-angle cosine and sine of axis and aperture).
+int64_t qpack_row_floats(int model, int d)
+{
+    return (int64_t)d * (model == KGQ_GQE ? 1 : model == KGQ_CONE ? 4 : 2);
+}
+
 kgq_status allocate_all(kgq_handle* h)
 {
     const kgq_config& c = h->cfg;
@@ -300,12 +340,16 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(p, kv.second.rows * kv.second.cols);
         h->dparam[kv.first] = p;
     }
-    if (c.model == KGQ_BETAE) {
+    if (mlp_model(c.model)) {
         ALLOC(h->ent_rm, N * 2 * d);
         ALLOC(h->ent_blk, n_pad * 2 * d);
-        ALLOC(h->ent_const, n_pad);
+        if (c.model == KGQ_BETAE) ALLOC(h->ent_const, n_pad);
         ALLOC(h->proj1_ent, N * 4 * d);
         ALLOC(h->proj1_rel, (int64_t)c.n_relations * 4 * d);
+        if (c.model == KGQ_CONE) {
+            ALLOC(h->int_cat_w, 4 * d * d);
+            ALLOC(h->int_cat_b, 2 * d);
+        }
     } else {
         ALLOC(h->ent_rm, N * d);
         ALLOC(h->ent_blk, n_pad * d);
@@ -318,10 +362,14 @@ kgq_status allocate_all(kgq_handle* h)
         Lane& L = *h->lanes.back();
         ALLOC(L.states, h->cap_rows * W);
         const int64_t m_max = h->cap_mlp;   // rows of one MLP level / intersection stage inputs
-        if (c.model == KGQ_BETAE) {
-            ALLOC(L.xbuf, m_max * 2 * d);
+        if (mlp_model(c.model)) {
+            ALLOC(L.xbuf, m_max * (c.model == KGQ_LOGICE ? 3 : 2) * d);
             ALLOC(L.h1, m_max * 4 * d);
             ALLOC(L.h2, m_max * 4 * d);
+            if (c.model == KGQ_CONE) {
+                ALLOC(L.zmean, h->cap_groups * d);
+                ALLOC(L.gate, h->cap_groups * d);
+            }
         } else {
             ALLOC(L.h1, m_max * d);
             if (c.model == KGQ_Q2B) {
@@ -331,13 +379,13 @@ kgq_status allocate_all(kgq_handle* h)
             }
         }
         ALLOC(L.logits, m_max * d);
-        ALLOC(L.qpack, h->cap_score_rows * 2 * d);
+        ALLOC(L.qpack, h->cap_score_rows * qpack_row_floats(c.model, (int)d));
         ALLOC(L.cq, h->cap_score_rows);
         ALLOC(L.scores, Bm * N);
         // split-K runs only while a layer has fewer than 128 output tiles of
         // 64 x 64, so 16 slices of it stay below 16 x 128 x 4096 floats
         {
-            const int64_t n_max = c.model == KGQ_BETAE ? 4 * d : d;
+            const int64_t n_max = mlp_model(c.model) ? 4 * d : d;
             L.gemm_ws_elems = std::min<int64_t>(16 * 3 * Bm * n_max, (int64_t)16 * 128 * 4096);
             ALLOC(L.gemm_ws, L.gemm_ws_elems);
         }
@@ -537,8 +585,10 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
                         N, n_rel, L.dflag, s);
     }
     const bool betae = c.model == KGQ_BETAE, q2b = c.model == KGQ_Q2B;
-    const float* rel_c = betae ? nullptr : q2b ? param("relation.center") : param("relation");
-    const float* rel_ab = betae ? param("relation") : nullptr;
+    const bool cone = c.model == KGQ_CONE, logice = c.model == KGQ_LOGICE;
+    const bool mlp = mlp_model(c.model);
+    const float* rel_c = q2b ? param("relation.center") : c.model == KGQ_GQE ? param("relation") : nullptr;
+    const float* rel_ab = mlp ? param("relation") : nullptr;
     const std::string pre = q2b ? "inter.center." : "inter.";
 
     for (const Stage& st : p.stages) {
@@ -548,9 +598,10 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
             launch_chain(c.model, P + st.a, P + st.b, P + st.c, P + st.d, st.count, anchors, rels, h->ent_rm, rel_c,
                          h->rel_o_sp, N, n_rel, d, L.states, L.dflag, s);
         } else if (st.kind == ST_LEVEL) {
-            // BetaE: one projection MLP pass over every projection at this
-            // stage and hop
+            // BetaE, ConE, LogicE: one projection MLP pass over every
+            // projection at this stage and hop
             const int M = st.count;
+            const int in_w = logice ? 3 * d : 2 * d;   // LogicE concatenates Rel[r] to the state
             if (st.table) {
                 // first hop from the anchors: the first layer is a gather
                 // from the precomputed tables
@@ -560,27 +611,74 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
             } else {
                 {
                     StageTimer t(h, 0, s);
-                    launch_betae_proj_prep(P + st.a, P + st.b, P + st.c, P + st.d, M, anchors, rels, L.states,
-                                           h->ent_rm, rel_ab, N, n_rel, d, L.xbuf, L.dflag, s);
+                    if (betae)
+                        launch_betae_proj_prep(P + st.a, P + st.b, P + st.c, P + st.d, M, anchors, rels, L.states,
+                                               h->ent_rm, rel_ab, N, n_rel, d, L.xbuf, L.dflag, s);
+                    else
+                        launch_mlp_proj_prep(c.model, P + st.a, P + st.b, P + st.c, P + st.d, M, anchors, rels,
+                                             L.states, h->ent_rm, rel_ab, N, n_rel, d, L.xbuf, L.dflag, s);
                 }
                 StageTimer t(h, 1, s);
-                gemm({L.xbuf, 2 * d, param("proj.w1"), 2 * d, param("proj.b1"), L.h1, 4 * d, nullptr, M, 4 * d,
-                      2 * d, EPI_RELU});
+                gemm({L.xbuf, in_w, param("proj.w1"), in_w, param("proj.b1"), L.h1, 4 * d, nullptr, M, 4 * d, in_w,
+                      EPI_RELU});
             }
             {
                 StageTimer t(h, 1, s);
                 gemm({L.h1, 4 * d, param("proj.w2"), 4 * d, param("proj.b2"), L.h2, 4 * d, nullptr, M, 4 * d, 4 * d,
                       EPI_RELU});
             }
-            StageTimer t(h, 1, s);
-            gemm({L.h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), L.states, 2 * d, P + st.e, M, 2 * d,
-                  4 * d, EPI_BETA_REG});
+            // the last layer writes the model's output map through the row map
+            GemmArgs g3{L.h2, 4 * d, param("proj.w3"), 4 * d, param("proj.b3"), L.states, 2 * d, P + st.e, M, 2 * d,
+                        4 * d, betae ? EPI_BETA_REG : cone ? EPI_CONE_ANGLES : EPI_SIGMOID};
+            g3.epi_split = d;
+            {
+                StageTimer t(h, 1, s);
+                gemm(g3);
+            }
+            if (logice) {
+                StageTimer t(h, 0, s);
+                launch_logic_bounds(P + st.e, M, d, L.states, s);
+            }
         } else {
             // every intersection group of one stage; its inputs are the rows
             // in_base .. in_base + n_in - 1 of the state buffer
             GroupArgs g{P + st.a, P + st.b, P + st.c, P + st.d, P + st.e, P + st.f, st.count};
             const float* sin = L.states + (int64_t)st.in_base * W;
             const int n_in = st.n_in;
+            if (logice) {
+                StageTimer t(h, 2, s);
+                launch_logic_combine(c.tnorm, g, sin, d, L.states, s);
+                continue;
+            }
+            if (cone) {
+                {
+                    StageTimer t(h, 2, s);
+                    launch_cone_int_prep(g, sin, d, L.xbuf, s);
+                }
+                {
+                    // both set functions' first layers, stacked: [attention | aperture] hidden
+                    StageTimer t(h, 1, s);
+                    gemm({L.xbuf, 2 * d, h->int_cat_w, 2 * d, h->int_cat_b, L.h1, 2 * d, nullptr, n_in, 2 * d, 2 * d,
+                          EPI_RELU});
+                }
+                {
+                    StageTimer t(h, 1, s);
+                    gemm({L.h1, 2 * d, param("inter.axis.w2"), d, param("inter.axis.b2"), L.logits, d, nullptr, n_in,
+                          d, d, EPI_NONE});
+                }
+                {
+                    StageTimer t(h, 2, s);
+                    launch_cone_combine_axis(g, sin, L.logits, L.h1, d, L.zmean, L.states, s);
+                }
+                {
+                    StageTimer t(h, 1, s);
+                    gemm({L.zmean, d, param("inter.arg.w2"), d, param("inter.arg.b2"), L.gate, d, nullptr, st.count,
+                          d, d, EPI_NONE});
+                }
+                StageTimer t(h, 2, s);
+                launch_cone_combine_arg(g, sin, L.gate, d, L.states, s);
+                continue;
+            }
             if (betae) {
                 {
                     StageTimer t(h, 2, s);
@@ -634,16 +732,18 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
 
     const int tq = score_row_pad(c.model);
     const int n_rows_pad = ((p.n_score_rows + tq - 1) / tq) * tq;
+    const int d_score = logice ? 2 * d : d;    // LogicE scores its 2d bound coordinates as one vector
     {
         StageTimer t(h, 3, s);
-        launch_pack(c.model, P + p.off_score_src, betae ? P + p.off_score_neg : nullptr, p.n_score_rows, n_rows_pad,
-                    L.states, W, d, L.qpack, L.cq, s);
+        launch_pack(c.model, P + p.off_score_src, mlp ? P + p.off_score_neg : nullptr, p.n_score_rows, n_rows_pad,
+                    L.states, W, d_score, L.qpack, L.cq, s);
     }
     float* dst = out_scores ? out_scores : L.scores;
     {
         StageTimer t(h, 4, s);
         ScoreArgs a{c.model, L.qpack, h->ent_blk, L.cq, h->ent_const, P + p.off_out_dest, p.n_score_rows,
-                    p.n_quad_rows, p.n_pair_rows, d, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
+                    p.n_quad_rows, p.n_pair_rows, d_score, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
+        a.dist_scale = logice ? 1.0f / (float)(2 * d) : cone ? h->cone_modulus : 1.0f;
         a.part = L.score_ws;
         a.part_elems = L.score_ws_elems;
         launch_score(a, s);
@@ -720,10 +820,14 @@ int64_t carve_scratch(const kgq_handle* h, const Plan& p, int32_t k, bool need_s
     V.dflag = reinterpret_cast<int*>(take(sizeof(int)));
     V.states = reinterpret_cast<float*>(take((int64_t)p.n_state_rows * W * 4));
     const int64_t m = std::max(p.max_level, p.max_and_in), groups = p.max_and_groups;
-    if (c.model == KGQ_BETAE) {
-        V.xbuf = reinterpret_cast<float*>(take(m * 2 * d * 4));
+    if (mlp_model(c.model)) {
+        V.xbuf = reinterpret_cast<float*>(take(m * (c.model == KGQ_LOGICE ? 3 : 2) * d * 4));
         V.h1 = reinterpret_cast<float*>(take(m * 4 * d * 4));
         V.h2 = reinterpret_cast<float*>(take(m * 4 * d * 4));
+        if (c.model == KGQ_CONE) {
+            V.zmean = reinterpret_cast<float*>(take(groups * d * 4));
+            V.gate = reinterpret_cast<float*>(take(groups * d * 4));
+        }
     } else {
         V.h1 = reinterpret_cast<float*>(take(m * d * 4));
         if (c.model == KGQ_Q2B) {
@@ -735,7 +839,7 @@ int64_t carve_scratch(const kgq_handle* h, const Plan& p, int32_t k, bool need_s
     V.logits = reinterpret_cast<float*>(take(m * d * 4));
     const int tq = score_row_pad(c.model);
     const int64_t srows = ((int64_t)(p.n_score_rows + tq - 1) / tq) * tq;
-    V.qpack = reinterpret_cast<float*>(take(srows * 2 * d * 4));
+    V.qpack = reinterpret_cast<float*>(take(srows * qpack_row_floats(c.model, (int)d) * 4));
     V.cq = reinterpret_cast<double*>(take(srows * 8));
     V.scores = need_scores ? reinterpret_cast<float*>(take(B * N * 4)) : nullptr;
     const int64_t ncand = need_topk ? topk_scratch_elems(B, N, k) : 0;
@@ -751,7 +855,7 @@ int64_t carve_scratch(const kgq_handle* h, const Plan& p, int32_t k, bool need_s
     V.score_ws_elems = 0;
     if (*fits) {
         // optional workspaces, each from half of what is left
-        const int64_t n_max = c.model == KGQ_BETAE ? 4 * d : d;
+        const int64_t n_max = mlp_model(c.model) ? 4 * d : d;
         int64_t left = (cap - (off + 255) / 256 * 256) / 2 / 4 / 64 * 64;
         int64_t want = std::min<int64_t>(16 * 3 * B * n_max, (int64_t)16 * 128 * 4096);
         if (std::min(want, left) >= 64) {
@@ -866,7 +970,11 @@ kgq_status kgq_create(const kgq_config* cfg, kgq_handle** out)
     if (!cfg || !out) return bad("cfg and out must not be NULL");
     *out = nullptr;
     const kgq_config& c = *cfg;
-    if (c.model < KGQ_GQE || c.model > KGQ_BETAE) return bad("unknown model " + std::to_string(c.model));
+    if (c.model < KGQ_GQE || c.model > KGQ_LOGICE) return bad("unknown model " + std::to_string(c.model));
+    if (c.model == KGQ_LOGICE && (c.tnorm < KGQ_TNORM_PRODUCT || c.tnorm > KGQ_TNORM_LUKASIEWICZ))
+        return bad("unknown t-norm " + std::to_string(c.tnorm));
+    if (c.model == KGQ_CONE && c.entity_dtype != KGQ_F32) return bad("ConE takes a float32 entity table");
+    if (c.model == KGQ_CONE && !(c.center_reg >= 0.f && c.center_reg <= 1.f)) return bad("center_reg outside [0, 1]");
     if (c.dim < 4 || c.dim > 4096 || c.dim % 4) return bad("dim must be a multiple of 4 in [4, 4096]");
     if (c.n_entities < 1 || c.n_entities > 0x7fffffffLL) return bad("n_entities outside [1, 2^31-1]");
     if (c.n_relations < 1) return bad("n_relations must be >= 1");
@@ -1019,17 +1127,40 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on)
 
 // BetaE first-layer tables (see proj1_ent / proj1_rel): rebuilt whenever
 // one of their inputs is (re)loaded and all of them are present.
+static const char* entity_param_name(int model)
+{
+    switch (model) {
+    case KGQ_BETAE: return "entity.alpha_beta";
+    case KGQ_CONE: return "entity.axis";
+    case KGQ_LOGICE: return "entity.bounds";
+    default: return "entity";
+    }
+}
+
+// First-layer tables of the projection MLP (BetaE, ConE, LogicE): the layer
+// is linear in its input, so W1 x + b1 for an anchor entity's state splits
+// into an entity table and a relation table. BetaE and ConE add the relation
+// to the state (x = state + Rel[r]: both tables use all of W1); LogicE
+// concatenates it (x = [state; Rel[r]]: the entity table uses W1's first 2d
+// columns, the relation table the last d).
 static kgq_status build_proj1(kgq_handle* h)
 {
     const kgq_config& c = h->cfg;
     h->proj1_ready = false;
-    for (const char* n : {"entity.alpha_beta", "relation", "proj.w1", "proj.b1"})
+    for (const char* n : {entity_param_name(c.model), "relation", "proj.w1", "proj.b1"})
         if (!h->loaded[n]) return KGQ_OK;
     const int d = c.dim;
-    launch_gemm({h->ent_rm, 2 * d, h->dparam.at("proj.w1"), 2 * d, nullptr, h->proj1_ent, 4 * d, nullptr,
-                 (int)c.n_entities, 4 * d, 2 * d, EPI_NONE}, nullptr);
-    launch_gemm({h->dparam.at("relation"), 2 * d, h->dparam.at("proj.w1"), 2 * d, h->dparam.at("proj.b1"),
-                 h->proj1_rel, 4 * d, nullptr, c.n_relations, 4 * d, 2 * d, EPI_NONE}, nullptr);
+    const bool logice = c.model == KGQ_LOGICE;
+    const int in_w = logice ? 3 * d : 2 * d;
+    const float* w1 = h->dparam.at("proj.w1");
+    launch_gemm({h->ent_rm, 2 * d, w1, in_w, nullptr, h->proj1_ent, 4 * d, nullptr, (int)c.n_entities, 4 * d, 2 * d,
+                 EPI_NONE}, nullptr);
+    if (logice)
+        launch_gemm({h->dparam.at("relation"), d, w1 + 2 * d, in_w, h->dparam.at("proj.b1"), h->proj1_rel, 4 * d,
+                     nullptr, c.n_relations, 4 * d, d, EPI_NONE}, nullptr);
+    else
+        launch_gemm({h->dparam.at("relation"), 2 * d, w1, 2 * d, h->dparam.at("proj.b1"), h->proj1_rel, 4 * d,
+                     nullptr, c.n_relations, 4 * d, 2 * d, EPI_NONE}, nullptr);
     HIP_TRY(h, hipGetLastError());
     HIP_TRY(h, hipStreamSynchronize(nullptr));
     h->proj1_ready = true;
@@ -1069,9 +1200,20 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
             HIP_TRY(h, hipGetLastError());
             HIP_TRY(h, hipStreamSynchronize(nullptr));
         }
+        if (c.model == KGQ_CONE) {
+            // the two set functions' first layers, stacked for one GEMM
+            const size_t half_w = (size_t)2 * c.dim * c.dim, half_b = (size_t)c.dim;
+            if (!std::strcmp(name, "inter.axis.w1")) HIP_TRY(h, hipMemcpy(h->int_cat_w, dst, nbytes, hipMemcpyDeviceToDevice));
+            if (!std::strcmp(name, "inter.arg.w1"))
+                HIP_TRY(h, hipMemcpy(h->int_cat_w + half_w, dst, nbytes, hipMemcpyDeviceToDevice));
+            if (!std::strcmp(name, "inter.axis.b1")) HIP_TRY(h, hipMemcpy(h->int_cat_b, dst, nbytes, hipMemcpyDeviceToDevice));
+            if (!std::strcmp(name, "inter.arg.b1"))
+                HIP_TRY(h, hipMemcpy(h->int_cat_b + half_b, dst, nbytes, hipMemcpyDeviceToDevice));
+            if (!std::strcmp(name, "modulus")) HIP_TRY(h, hipMemcpy(&h->cone_modulus, dst, sizeof(float), hipMemcpyDeviceToHost));
+        }
         h->loaded[name] = true;
-        if (c.model == KGQ_BETAE && (!std::strcmp(name, "relation") || !std::strcmp(name, "proj.w1") ||
-                                     !std::strcmp(name, "proj.b1")))
+        if (mlp_model(c.model) && (!std::strcmp(name, "relation") || !std::strcmp(name, "proj.w1") ||
+                                   !std::strcmp(name, "proj.b1")))
             return build_proj1(h);
         return KGQ_OK;
     }
@@ -1085,15 +1227,19 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
         if (c.model == KGQ_BETAE)
             launch_betae_entity_prep(stage, bf16, c.n_entities, c.dim, h->n_blocks, h->ent_rm, h->ent_blk,
                                      h->ent_const, nullptr);
+        else if (c.model == KGQ_CONE)
+            launch_cone_entity_prep(static_cast<const float*>(stage), c.n_entities, c.dim, h->n_blocks, h->ent_rm,
+                                    h->ent_blk, nullptr);
         else
-            launch_relayout_points(stage, bf16, c.n_entities, c.dim, h->n_blocks, h->ent_rm, h->ent_blk, nullptr);
+            launch_relayout_points(stage, bf16, c.n_entities, c.model == KGQ_LOGICE ? 2 * c.dim : c.dim,
+                                   h->n_blocks, h->ent_rm, h->ent_blk, nullptr);
         e = hipGetLastError();
         if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
     }
     (void)hipFree(stage);
     if (e != hipSuccess) return fail(h, KGQ_E_DEVICE, std::string("entity table load: ") + hipGetErrorString(e));
     h->loaded[name] = true;
-    if (c.model == KGQ_BETAE) return build_proj1(h);
+    if (mlp_model(c.model)) return build_proj1(h);
     return KGQ_OK;
 }
 

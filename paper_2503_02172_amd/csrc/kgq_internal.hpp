@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/kgq.h"
+
 namespace kgq {
 
 // ---- data layout constants -------------------------------------------------
@@ -13,8 +15,10 @@ namespace kgq {
 // block, dimension-major inside a block, element (e, k) at
 //   [e / 256][k][e % 256]
 // so that a VALU wavefront (64 lanes x 4 entities) reads 1 KiB contiguous per
-// dimension. BetaE's scoring table is row-major [e][U (d) | V (d)], the B
-// operand of the matrix-core scorer.
+// dimension; LogicE's bounds the same way over its 2d coordinates. ConE
+// keeps two fields per dimension, [e / 256][k][sin | cos of theta/2][e % 256].
+// BetaE's scoring table is row-major [e][U (d) | V (d)], the B operand of the
+// matrix-core scorer.
 constexpr int kEntBlock = 256;
 
 // Largest k of a top-k request (the selection buffer lives in LDS).
@@ -24,12 +28,24 @@ constexpr int kMaxK = 1024;
 // read through the scalar cache). Packed layout [row_block][k][field][kTq].
 constexpr int kTqGqe = 24;
 constexpr int kTqQ2b = 12;
+constexpr int kTqCone = 8;
 // BetaE query rows are packed row-major [row][alpha (d) | beta (d)] and
 // padded to the matrix-core scorer's 128-row tile.
 constexpr int kRowTileBetae = 128;
 
+// LogicE scores with GQE's L1 kernel over its 2d bound coordinates.
+inline int valu_form(int model) { return model == KGQ_LOGICE ? KGQ_GQE : model; }
+
 // Scored rows are padded to a multiple of this per model.
-inline int score_row_pad(int model) { return model == 0 ? kTqGqe : (model == 1 ? kTqQ2b : kRowTileBetae); }
+inline int score_row_pad(int model)
+{
+    switch (valu_form(model)) {
+    case KGQ_GQE: return kTqGqe;
+    case KGQ_Q2B: return kTqQ2b;
+    case KGQ_CONE: return kTqCone;
+    default: return kRowTileBetae;
+    }
+}
 
 // Small batches (at most kSmallScoreRows scored rows) run the GQE / Query2Box
 // pack and scorer with fewer rows per wavefront: there the scorer's dimension
@@ -38,13 +54,22 @@ inline int score_row_pad(int model) { return model == 0 ? kTqGqe : (model == 1 ?
 // layout holds either form; pack and scorer decide from the same row count.
 constexpr int kTqGqeSmall = 8;
 constexpr int kTqQ2bSmall = 4;
+constexpr int kTqConeSmall = 4;
 constexpr int kSmallScoreRows = 1024;
 inline bool score_small(int n_rows) { return n_rows <= kSmallScoreRows; }
 inline int score_tq(int model, int n_rows)
 {
     const bool small = score_small(n_rows);
-    return model == 0 ? (small ? kTqGqeSmall : kTqGqe) : (small ? kTqQ2bSmall : kTqQ2b);
+    switch (valu_form(model)) {
+    case KGQ_GQE: return small ? kTqGqeSmall : kTqGqe;
+    case KGQ_Q2B: return small ? kTqQ2bSmall : kTqQ2b;
+    default: return small ? kTqConeSmall : kTqCone;
+    }
 }
+
+// Models whose projection is an MLP (one dense-layer pass per hop) and that
+// define negation: BetaE, ConE, LogicE.
+inline bool mlp_model(int model) { return model == KGQ_BETAE || model == KGQ_CONE || model == KGQ_LOGICE; }
 
 // Device error flag bits.
 constexpr int kErrRange = 1;    // an anchor or relation id outside its table
@@ -54,7 +79,10 @@ constexpr int kErrAnswers = 4;  // an answer list longer than kMaxAnswers or of 
 // Largest answer list of one query for the ranking metrics (sorted in LDS).
 constexpr int kMaxAnswers = 1024;
 
-enum Epilogue { EPI_NONE = 0, EPI_RELU = 1, EPI_BETA_REG = 2 };
+// Dense-layer epilogues. EPI_CONE_ANGLES maps columns below epi_split to
+// pi tanh(v) (ConE axes) and the others to pi/2 (tanh(2 v) + 1) (ConE
+// half-apertures); EPI_SIGMOID is LogicE's sigmoid before its bound map.
+enum Epilogue { EPI_NONE = 0, EPI_RELU = 1, EPI_BETA_REG = 2, EPI_CONE_ANGLES = 3, EPI_SIGMOID = 4 };
 
 // ---- launchers (each enqueues on `s` and returns) ---------------------------
 
@@ -68,8 +96,20 @@ struct GemmArgs {
     int epi;
     float* ws = nullptr;               // split-K partials for small M (nullptr: never split)
     int64_t ws_elems = 0;
+    int epi_split = 0;                 // EPI_CONE_ANGLES: first column of the second map
 };
 void launch_gemm(const GemmArgs& g, hipStream_t s);
+
+// Epilogue value of output column n.
+__device__ __forceinline__ float apply_epilogue(int epi, int split, int n, float v)
+{
+    if (epi == EPI_RELU) return v > 0.f ? v : 0.f;
+    if (epi == EPI_BETA_REG) return fminf(fmaxf(v + 1.0f, 0.05f), 1e9f);
+    if (epi == EPI_CONE_ANGLES)
+        return n < split ? 3.14159265358979323846f * tanhf(v) : 1.57079632679489661923f * (tanhf(2.0f * v) + 1.0f);
+    if (epi == EPI_SIGMOID) return 1.0f / (1.0f + expf(-v));
+    return v;
+}
 
 // Relayout a row-major [N x d] table (fp32 or bf16 bits) into the blocked
 // scorer layout (fp32), padding with zeros; also writes a row-major fp32 copy.
@@ -149,6 +189,29 @@ void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, c
 void launch_pack(int model, const int32_t* src_row, const int32_t* neg, int n_rows, int n_rows_pad,
                  const float* states, int W, int d, float* qpack, double* cq, hipStream_t s);
 
+// ---- ConE / LogicE (k_cone_logice.hip) ----
+void launch_cone_entity_prep(const float* src, int64_t N, int d, int64_t n_blocks, float* ent_rm, float* blocked,
+                             hipStream_t s);
+// Projection input rows: ConE x = source (complemented where neg[m]) +
+// Rel[r] (width 2d); LogicE x = [source (complemented where neg[m]); Rel[r]]
+// (width 3d). The source is a state row, or the anchor entity when
+// src_row[m] < 0.
+void launch_mlp_proj_prep(int model, const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
+                          const int32_t* neg, int M, const int32_t* anchors, const int32_t* rels,
+                          const float* states, const float* ent_rm, const float* rel, int64_t n_ent, int n_rel,
+                          int d, float* x, int* flag, hipStream_t s);
+// LogicE: u = l + s (1 - l) in the destination rows of a projection level.
+void launch_logic_bounds(const int32_t* rowmap, int M, int d, float* states, hipStream_t s);
+void launch_cone_int_prep(const GroupArgs& g, const float* states, int d, float* x_int, hipStream_t s);
+void launch_cone_combine_axis(const GroupArgs& g, const float* states, const float* logits, const float* hid, int d,
+                              float* zmean, float* out_states, hipStream_t s);
+void launch_cone_combine_arg(const GroupArgs& g, const float* states, const float* gate, int d, float* out_states,
+                             hipStream_t s);
+void launch_logic_combine(int tnorm, const GroupArgs& g, const float* states, int d, float* out_states,
+                          hipStream_t s);
+void launch_pack_cone(const int32_t* src_row, const int32_t* neg, int n_rows, int n_rows_pad, const float* states,
+                      int d, float* qpack, hipStream_t s);
+
 struct ScoreArgs {
     int model;
     const float* qpack; const float* ent; const double* cq; const double* ee;
@@ -160,6 +223,9 @@ struct ScoreArgs {
     int64_t N, n_blocks;
     float gamma, center_reg;
     float* scores; int64_t ld;
+    // distance scale: score = gamma - dist_scale * distance (GQE 1, LogicE
+    // 1 / (2d), ConE its modulus; Query2Box ignores it)
+    float dist_scale = 1.0f;
     float* part = nullptr;             // GQE / Query2Box split-d partials for small batches
     int64_t part_elems = 0;            //   (nullptr: never split)
 };

@@ -9,6 +9,11 @@
 
 namespace kgq {
 
+// Models whose projection is an MLP pass per hop and that define negation
+// (BetaE, ConE, LogicE); GQE and Query2Box translate, and fuse projection
+// runs into chains.
+static bool per_hop_mlp(int model) { return model == KGQ_BETAE || model == KGQ_CONE || model == KGQ_LOGICE; }
+
 // ---------------------------------------------------------------------------
 // Built-in structures
 // ---------------------------------------------------------------------------
@@ -268,9 +273,9 @@ bool compile_graph(int model, const kgq_node* nodes, int n, const std::string& n
     if (nodes[n - 1].op == KGQ_OP_ANCHOR) return bad("the answer must not be an anchor");
     if ((amask & (amask + 1)) || (rmask & (rmask + 1)))
         return bad("anchor and relation slots must be numbered 0, 1, ... without gaps");
-    if (negation && model != KGQ_BETAE) {
+    if (negation && !per_hop_mlp(model)) {
         err = (name.empty() ? std::string() : "structure " + name + ": ") +
-              "negation is defined for BetaE only";
+              "negation is defined for BetaE, ConE and LogicE only";
         st = KGQ_E_UNSUPPORTED;
         return false;
     }
@@ -383,7 +388,7 @@ bool compile_graph(int model, const kgq_node* nodes, int n, const std::string& n
         if (ir[cur].op == KGQ_OP_ANCHOR) anchor = ir[cur].slot;
         else src = emit(cur, src_neg);
         neg = false;
-        if (model != KGQ_BETAE) {
+        if (!per_hop_mlp(model)) {
             if (src < 0) {
                 FusedOp f;
                 f.kind = OP_CHAIN;
@@ -458,10 +463,10 @@ bool compile_graph(int model, const kgq_node* nodes, int n, const std::string& n
 
 const Program* builtin_program(int model, int id)
 {
-    static std::vector<Program> table[3];
+    static std::vector<Program> table[5];
     static std::once_flag once;
     std::call_once(once, [] {
-        for (int m = 0; m < 3; ++m) {
+        for (int m = 0; m < 5; ++m) {
             table[m].resize(kNumStructures);
             for (int s = 0; s < kNumStructures; ++s) {
                 std::vector<kgq_node> nodes;
@@ -484,7 +489,7 @@ const Program* builtin_program(int model, int id)
             }
         }
     });
-    if (model < 0 || model > 2 || id < 0 || id >= kNumStructures) return nullptr;
+    if (model < 0 || model > 4 || id < 0 || id >= kNumStructures) return nullptr;
     return &table[model][id];
 }
 
@@ -492,15 +497,30 @@ const Program* builtin_program(int model, int id)
 // Launch counts
 // ---------------------------------------------------------------------------
 
-static int and_stage_launches(int model) { return model == KGQ_GQE ? 3 : model == KGQ_Q2B ? 6 : 4; }
+// launches per intersection stage: dense layers + combines (LogicE: the
+// t-norm combine only)
+static int and_stage_launches(int model)
+{
+    switch (model) {
+    case KGQ_GQE: return 3;
+    case KGQ_Q2B: return 6;
+    case KGQ_BETAE: return 4;
+    case KGQ_CONE: return 6;
+    default: return 1;
+    }
+}
+
+// launches per projection level: (table gather | prep + layer 1) + layers 2,
+// 3, and LogicE's bound map
+static int level_launches(int model, bool table) { return (table ? 3 : 4) + (model == KGQ_LOGICE ? 1 : 0); }
 
 int plan_launches(const Plan& p, bool topk)
 {
     int n = 0;
     for (const Stage& s : p.stages) {
-        if (s.kind == ST_CHAIN) n += 1;                        // chains
-        else if (s.kind == ST_LEVEL) n += s.table ? 3 : 4;    // (table gather | prep + layer 1) + layers 2, 3
-        else n += and_stage_launches(p.model);                // dense layers + combines
+        if (s.kind == ST_CHAIN) n += 1;                                   // chains
+        else if (s.kind == ST_LEVEL) n += level_launches(p.model, s.table);
+        else n += and_stage_launches(p.model);
     }
     return n + 2 + (topk ? 1 : 0);                            // pack, score, top-k
 }
@@ -508,11 +528,11 @@ int plan_launches(const Plan& p, bool topk)
 int program_launches(int model, const Program& prog, bool topk)
 {
     int n = prog.and_stages * and_stage_launches(model);
-    if (model == KGQ_BETAE) {
+    if (per_hop_mlp(model)) {
         std::map<std::pair<int, int>, int> level;
         for (const FusedOp& f : prog.ops)
             if (f.kind == OP_PROJ) level[{f.stage, f.hop}] = 1;
-        for (auto& kv : level) n += (kv.first.first == 0 && kv.first.second == 1) ? 3 : 4;
+        for (auto& kv : level) n += level_launches(model, kv.first.first == 0 && kv.first.second == 1);
     } else {
         for (const FusedOp& f : prog.ops)
             if (f.kind == OP_CHAIN) {
@@ -597,7 +617,7 @@ bool lower(int model, int B, const int32_t* sid, int fixed_sid, int a_stride, in
     };
 
     // GQE / Query2Box: every chain of the batch in one stage.
-    if (model != KGQ_BETAE) {
+    if (!per_hop_mlp(model)) {
         std::vector<int32_t> aref, roff{0}, rref, dst;
         for (int q = 0; q < B; ++q) {
             const std::vector<FusedOp>& ops = pq[q]->ops;
@@ -622,9 +642,9 @@ bool lower(int model, int B, const int32_t* sid, int fixed_sid, int a_stride, in
         }
     }
 
-    // BetaE projections, bucketed by (stage, hop) in query order.
+    // MLP projections (BetaE, ConE, LogicE), bucketed by (stage, hop) in query order.
     std::map<std::pair<int, int>, std::vector<std::pair<int, int>>> levels;
-    if (model == KGQ_BETAE)
+    if (per_hop_mlp(model))
         for (int q = 0; q < B; ++q) {
             const std::vector<FusedOp>& ops = pq[q]->ops;
             for (int o = 0; o < (int)ops.size(); ++o)
@@ -693,10 +713,10 @@ bool lower(int model, int B, const int32_t* sid, int fixed_sid, int a_stride, in
         p.max_and_in = std::max(p.max_and_in, s.n_in);
         p.max_and_groups = std::max(p.max_and_groups, s.count);
     };
-    if (model == KGQ_BETAE) emit_levels(0);
+    if (per_hop_mlp(model)) emit_levels(0);
     for (int k = 1; k <= K; ++k) {
         emit_and(k);
-        if (model == KGQ_BETAE) emit_levels(k);
+        if (per_hop_mlp(model)) emit_levels(k);
     }
 
     // Scored rows: groups of four, then pairs, then single rows.

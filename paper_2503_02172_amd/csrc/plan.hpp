@@ -25,7 +25,7 @@
 //
 // The result, a Program, is a list of fused operators with their schedule
 // position: its intersection stage (one more than the deepest stage below
-// it) and, for BetaE projections, the position within the run of
+// it) and, for MLP projections (BetaE, ConE, LogicE), the position within the run of
 // projections since the last stage. lower() then builds one plan for a
 // whole batch, in which every fused operator kind at one schedule position
 // runs as one launch across all queries, whatever their structures.
@@ -57,17 +57,17 @@ struct FusedOp {
     int hop = 0;                  // PROJ: 1 + hop of a PROJ source, else 1
     int src = -1;                 // CHAIN / PROJ: producing op, or -1 for an anchor
     int anchor = -1;              //   anchor slot when src < 0
-    bool src_neg = false;         // PROJ: the source is read negated (BetaE)
+    bool src_neg = false;         // PROJ: the source is read negated (BetaE, ConE, LogicE)
     std::vector<int> rels;        // CHAIN: relation slots in hop order; PROJ: one;
                                   // AND: relation slots of a folded post-chain (GQE / Query2Box)
     std::vector<int> in;          // AND: input ops, in the graph's order
-    std::vector<char> in_neg;     // AND: inputs read negated (BetaE)
+    std::vector<char> in_neg;     // AND: inputs read negated (BetaE, ConE, LogicE)
 };
 
 struct Program {
     std::string name;
     int n_anchors = 0, n_relations = 0;
-    bool negation = false;        // uses negation (BetaE only)
+    bool negation = false;        // uses negation (BetaE, ConE, LogicE only)
     bool supported = true;        // false: a built-in structure this model cannot run
     std::vector<FusedOp> ops;     // every op after its inputs
     int n_terms = 1;              // conjunctive terms of the answer (1 .. 4)
@@ -75,7 +75,7 @@ struct Program {
     std::vector<char> answer_neg;
     int and_stages = 0;
     // per-query needs, for capacity checks
-    int max_stage_level = 0;      // BetaE: largest projection level (rows at one stage and hop)
+    int max_stage_level = 0;      // MLP models: largest projection level (rows at one stage and hop)
     int max_stage_inputs = 0;     // largest intersection-stage input count
     int max_stage_groups = 0;     // largest intersection-stage group count
     int image_words = 0;          // plan-image words per query (without per-stage padding)
@@ -125,7 +125,7 @@ struct Plan {
     int n_score_rows = 0, n_quad_rows = 0, n_pair_rows = 0;
     // summary counts
     int n_anchor_chains = 0, n_groups = 0, n_int_in = 0, n_and_stages = 0;
-    int level_rows[4] = {0, 0, 0, 0};   // BetaE: stage-0 hops 1, 2, >= 3; later stages
+    int level_rows[4] = {0, 0, 0, 0};   // MLP models: stage-0 hops 1, 2, >= 3; later stages
     int max_level = 0, max_and_in = 0, max_and_groups = 0;
     // Flattened device image: every list at a fixed, 16-byte aligned offset.
     std::vector<int32_t> image;

@@ -17,8 +17,9 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkgq.so")
 
-GQE, Q2B, BETAE = 0, 1, 2
+GQE, Q2B, BETAE, CONE, LOGICE = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
+TNORM_PRODUCT, TNORM_MIN, TNORM_LUKASIEWICZ = 0, 1, 2
 NUM_STRUCTURES = 14
 MAX_K = 1024
 PLAN_FIELDS = ["chains", "groups", "intersection_inputs", "level1", "level2", "level3", "post",
@@ -47,7 +48,7 @@ class Config(ctypes.Structure):
     _fields_ = [("model", ctypes.c_int32), ("dim", ctypes.c_int32), ("n_entities", ctypes.c_int64),
                 ("n_relations", ctypes.c_int32), ("entity_dtype", ctypes.c_int32), ("gamma", ctypes.c_float),
                 ("center_reg", ctypes.c_float), ("max_batch", ctypes.c_int32), ("device", ctypes.c_int32),
-                ("concurrency", ctypes.c_int32)]
+                ("concurrency", ctypes.c_int32), ("tnorm", ctypes.c_int32)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -144,9 +145,9 @@ class Engine:
 
     def __init__(self, model: int, n_entities: int, n_relations: int, dim: int, gamma: float,
                  max_batch: int, center_reg: float = 0.02, entity_dtype: int = F32, device: int = 0,
-                 concurrency: int = 1):
+                 concurrency: int = 1, tnorm: int = TNORM_PRODUCT):
         self.cfg = Config(model, dim, n_entities, n_relations, entity_dtype, gamma, center_reg,
-                          max_batch, device, concurrency)
+                          max_batch, device, concurrency, tnorm)
         h = ctypes.c_void_p()
         rc = lib().kgq_create(ctypes.byref(self.cfg), ctypes.byref(h))
         if rc != OK:
@@ -376,6 +377,7 @@ def engine_for(workload, max_batch: Optional[int] = None, device: int = 0, model
     bmax = max_batch or max(b.batch for b in workload.batches)
     bf16 = workload.entity_bf16 if (m == BETAE and workload.entity_bf16 is not None) else None
     eng = Engine(m, workload.n_entities, workload.n_relations, workload.dim, workload.gamma, bmax,
-                 workload.center_reg, BF16 if bf16 is not None else F32, device, concurrency)
+                 workload.center_reg, BF16 if bf16 is not None else F32, device, concurrency,
+                 getattr(workload, "tnorm", TNORM_PRODUCT))
     eng.load_all(p, entity_bf16=bf16)
     return eng

@@ -54,14 +54,19 @@ def rc_of(fn):
 
 
 def test_create_validation():
-    bad = [dict(model=3), dict(dim=6), dict(dim=0), dict(n_entities=0), dict(n_relations=0),
-           dict(max_batch=0), dict(device=-2)]
+    bad = [dict(model=5), dict(model=-1), dict(dim=6), dict(dim=0), dict(n_entities=0), dict(n_relations=0),
+           dict(max_batch=0), dict(device=-2), dict(model=kgq.LOGICE, tnorm=3), dict(model=kgq.LOGICE, tnorm=-1),
+           dict(model=kgq.CONE, entity_dtype=kgq.BF16), dict(model=kgq.CONE, center_reg=1.5)]
     for kw in bad:
         args = dict(model=kgq.GQE, n_entities=10, n_relations=2, dim=8, gamma=1.0, max_batch=4, device=-1)
         args.update(kw)
         assert rc_of(lambda: kgq.Engine(**args)) == INVALID, kw
     assert kgq.lib().kgq_create(None, None) == INVALID
     assert kgq.lib().kgq_destroy(None) == 0
+    # the two cone / fuzzy-logic models create, with every t-norm
+    for tn in (kgq.TNORM_PRODUCT, kgq.TNORM_MIN, kgq.TNORM_LUKASIEWICZ):
+        kgq.Engine(kgq.LOGICE, 10, 2, 8, 1.0, 4, device=-1, tnorm=tn).close()
+    kgq.Engine(kgq.CONE, 10, 2, 8, 30.0, 4, device=-1).close()
 
 
 def test_arity_table():
@@ -116,6 +121,9 @@ def test_execute_mixed_validation():
                                               stream=0)) == UNSUP
     assert rc_of(lambda: e.execute_mixed_into(np.array([0, 99], np.int32), a, r, 3, None, idx, val,
                                               stream=0)) == INVALID
+    for model in (kgq.CONE, kgq.LOGICE):
+        ec = dry(model=model)
+        full_load(ec, model)
     eb = dry(model=kgq.BETAE)
     full_load(eb, kgq.BETAE)
     allq = np.arange(14, dtype=np.int32)

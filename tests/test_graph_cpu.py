@@ -74,12 +74,12 @@ def test_compile_rules():
     assert rc_of(lambda: f.compile("p(e0,r0)")) == INVALID
 
 
-@pytest.mark.parametrize("model", [kgq.GQE, kgq.Q2B, kgq.BETAE])
+@pytest.mark.parametrize("model", [kgq.GQE, kgq.Q2B, kgq.BETAE, kgq.CONE, kgq.LOGICE])
 def test_builtins_compile_like_their_text(model):
     """A built-in structure and its text form compiled on the handle lower to
     the same plan, alone and mixed."""
     e = dry(model, max_batch=64)
-    names = [n for n in synth.STRUCTURES if model == kgq.BETAE or n not in NEG]
+    names = [n for n in synth.STRUCTURES if model in synth.NEGATION_MODELS or n not in NEG]
     own = {n: e.compile(synth.STRUCTURE_TEXT[n]) for n in names}
     for n in names:
         assert e.describe_plan([S[n]] * 3) == e.describe_plan([own[n]] * 3), n
@@ -89,7 +89,7 @@ def test_builtins_compile_like_their_text(model):
         assert e.structure_info(S[n]) == info
     mix = [S[n] for n in names] * 2
     assert e.describe_plan(mix) == e.describe_plan([own[synth.STRUCTURES[s]] for s in mix])
-    if model != kgq.BETAE:
+    if model not in synth.NEGATION_MODELS:
         assert rc_of(lambda: e.structure_info(S["2in"])) == UNSUP
 
 
@@ -104,10 +104,15 @@ def test_horizontal_fusion_one_chain_per_path():
                 t = f"p({t},r{h})"
             info = e.structure_info(e.compile(t))
             assert info["fused_ops"] == 1 and info["launches"] == 4, (model, hops, info)
-    e = dry(kgq.BETAE)
+    for model in (kgq.BETAE, kgq.CONE):
+        e = dry(model)
+        info = e.structure_info(e.compile("p(p(p(p(e0,r0),r1),r2),r3)"))
+        assert info["fused_ops"] == 4
+        assert info["launches"] == 3 + 3 * 4 + 3   # table-path first hop, three full hops, pack/score/top-k
+    # LogicE: one more launch per hop (the bound map after the sigmoid layer)
+    e = dry(kgq.LOGICE)
     info = e.structure_info(e.compile("p(p(p(p(e0,r0),r1),r2),r3)"))
-    assert info["fused_ops"] == 4
-    assert info["launches"] == 3 + 3 * 4 + 3   # table-path first hop, three full hops, pack/score/top-k
+    assert info["fused_ops"] == 4 and info["launches"] == 4 + 3 * 5 + 3
 
 
 def test_vertical_and_hybrid_fusion():
@@ -125,13 +130,25 @@ def test_vertical_and_hybrid_fusion():
     p = b.describe_plan([sid, sid])
     assert (p["level1"], p["level2"], p["post"], p["groups"], p["intersection_inputs"]) == (6, 2, 4, 2, 6)
     assert b.structure_info(sid)["fused_ops"] == 4 + 1 + 2
+    # ConE and LogicE plan like BetaE; an intersection stage is 6 launches
+    # for ConE (prep, stacked first layers, attention layer, axis combine,
+    # gate layer, aperture combine) and 1 for LogicE (the t-norm)
+    for model, per_and, per_level in ((kgq.CONE, 6, 4), (kgq.LOGICE, 1, 5)):
+        e = dry(model)
+        sid = e.compile(t)
+        pm = e.describe_plan([sid, sid])
+        assert {k: v for k, v in pm.items() if k != "launches"} == {k: v for k, v in p.items() if k != "launches"}
+        info = e.structure_info(sid)
+        assert info["fused_ops"] == 4 + 1 + 2
+        # levels: first hop (table path), the second hop of the 2p branch, two post hops
+        assert info["launches"] == (per_level - 1) + 3 * per_level + per_and + 3
 
 
 def test_nested_intersections_run_in_stages():
     """An intersection over another intersection's result runs one stage
     later; all intersections of a stage run together across the batch."""
     t = "i(p(i(p(e0,r0),p(e1,r1)),r2),p(e2,r3))"
-    for model in (kgq.GQE, kgq.Q2B, kgq.BETAE):
+    for model in (kgq.GQE, kgq.Q2B, kgq.BETAE, kgq.CONE, kgq.LOGICE):
         e = dry(model, max_batch=32)
         sid = e.compile(t)
         p = e.describe_plan([sid, S["2i"], sid])
