@@ -53,11 +53,16 @@ PEAK_VALU_OPS = 256 * 4 * 32 * 2.4e9
 PEAK_VALU_F32 = 157.3e12
 PEAK_MFMA_F32 = 157.3e12
 HBM_PEAK = 8.0e12
-# algorithmic flops per (query row, entity, dimension) triple, the peak
-# they are counted against, and its unit
-OPS_PER_TRIPLE = {0: 2, 1: 4, 2: 4}
+# algorithmic flops per (query row, entity, scored coordinate) triple, the
+# peak they are counted against, and its unit. ConE's sector distance is 10
+# VALU instructions per triple, 3 of them fused multiply-adds (13 flops);
+# LogicE's triple is one of its 2d bound coordinates scored by GQE's L1 form.
+OPS_PER_TRIPLE = {0: 2, 1: 4, 2: 4, 3: 13, 4: 2}
+# VALU lane-operations per triple (instructions per lane), for the issue-rate fraction
+LANE_OPS_PER_TRIPLE = {0: 2, 1: 4, 3: 10, 4: 2}
 SCORER_PEAK = {0: (PEAK_VALU_F32, "alu", "TFLOP/s"), 1: (PEAK_VALU_F32, "alu", "TFLOP/s"),
-               2: (PEAK_MFMA_F32, "mfma", "TFLOP/s")}
+               2: (PEAK_MFMA_F32, "mfma", "TFLOP/s"), 3: (PEAK_VALU_F32, "alu", "TFLOP/s"),
+               4: (PEAK_VALU_F32, "alu", "TFLOP/s")}
 K_TOP = 100
 
 WORKLOAD_DESC = {
@@ -70,6 +75,10 @@ WORKLOAD_DESC = {
     "C4-gqe": "GQE, 63,361 entities x 400 relations, d=400, fp32; 1,024 mixed 3p/ip/pi/up/3i; top-100",
     "C5": "BetaE, 63,361 entities x 400 relations, d=400, bf16 entity table; 2,048 mixed over all 14 "
           "structures; top-100",
+    "cone": "ConE, 14,505 entities x 474 relations, d=400, fp32; 256 queries per structure over all 14 "
+            "structures (3,584 queries); top-100",
+    "logice": "LogicE (product t-norm), 14,505 entities x 474 relations, d=400, fp32; 512 queries per structure "
+              "over all 14 structures (7,168 queries); top-100",
 }
 
 
@@ -79,7 +88,7 @@ WORKLOAD_DESC = {
 # computed once per pass and shared by the pass's queries, so a pass of very
 # few queries would mostly time that table.
 CPU_SAMPLE = {"C1": (16, 16), "C2": (128, 32), "C3": (64, 32), "C4-q2b": (128, 16), "C4-gqe": (128, 16),
-              "C5": (256, 32)}
+              "C5": (256, 32), "cone": (16, 2), "logice": (64, 8)}
 
 
 def log(*a):
@@ -156,7 +165,9 @@ class Prepared:
             ids = np.full(c[1], c[0]) if np.ndim(c[0]) == 0 else c[0]
             rows += self.eng.describe_plan(ids)["scored_rows"]
         self.rows = rows
-        self.triples = rows * w.n_entities * w.dim
+        # scored coordinates per entity: LogicE scores its 2d bounds
+        self.width = 2 * w.dim if model == kgq.LOGICE else w.dim
+        self.triples = rows * w.n_entities * self.width
         torch.cuda.synchronize()
 
     def step(self, n_streams=None):
@@ -184,9 +195,12 @@ def scorer_derivation(p: "Prepared") -> str:
     per = OPS_PER_TRIPLE[p.model]
     what = {0: "sub, add of |.| (GQE L1 distance)",
             1: "sub, add of |.|, min, add (Query2Box box distance, regrouped exactly)",
-            2: "2 multiply-adds alpha_q*U_e + beta_q*V_e (BetaE KL, regrouped exactly)"}[p.model]
-    return (f"{per} flops per (scored row, entity, dimension) triple [{what}] x {p.rows} scored rows x "
-            f"{w.n_entities} entities x {w.dim} dimensions = {per * p.triples:.4g} flops per launch")
+            2: "2 multiply-adds alpha_q*U_e + beta_q*V_e (BetaE KL, regrouped exactly)",
+            3: "mul, fma, mul, fma, mul, fma, max, add, min, add: half-angle sine and cosine of the angle "
+               "difference, outside and inside distance (ConE sector distance, regrouped exactly)",
+            4: "sub, add of |.| over each of the 2d bound coordinates (LogicE L1 distance)"}[p.model]
+    return (f"{per} flops per (scored row, entity, coordinate) triple [{what}] x {p.rows} scored rows x "
+            f"{w.n_entities} entities x {p.width} coordinates = {per * p.triples:.4g} flops per launch")
 
 
 def union_ms(iv: np.ndarray) -> float:
@@ -484,8 +498,10 @@ def main():
                           f"({in_flight_now} step(s) in flight); achieved = algorithmic ops per launch / average "
                           f"launch duration"}
     roofline["derivation"] = scorer_derivation(p)
-    if p.model != 2:
-        roofline["frac_of_issue_peak"] = round(achieved / PEAK_VALU_OPS, 4)
+    if p.model != 2 and avg_launch_ms > 0:
+        # lane-operations of one launch against the non-packed issue rate
+        lane_ops_per_launch = LANE_OPS_PER_TRIPLE[p.model] * p.triples * args.steps / max(n_launch, 1)
+        roofline["frac_of_issue_peak"] = round(lane_ops_per_launch / (avg_launch_ms * 1e-3) / PEAK_VALU_OPS, 4)
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {qps:.0f} q/s, scorer busy {busy:.2f} ms over "
         f"{n_launch} launches ({avg_launch_ms:.4f} ms each), {roofline['frac']*100:.1f}% of the {bound} peak")
     # The other mode, reported beside the headline: with two steps in flight
@@ -512,7 +528,7 @@ def main():
 
     others = {}
     if not args.no_others:
-        for name in ["C1", "C2", "C3", "C4-q2b", "C4-gqe", "C5"]:
+        for name in ["C1", "C2", "C3", "C4-q2b", "C4-gqe", "C5", "cone", "logice"]:
             if name == args.workload:
                 continue
             log(f"[bench] other workload {name}")
@@ -535,7 +551,8 @@ def main():
                             "scorer_bound": SCORER_PEAK[q.model][1],
                             "scorer_frac": round(ops / len(iv2) / (avg2 * 1e-3) / SCORER_PEAK[q.model][0], 4)
                             if avg2 > 0 else None,
-                            "scorer_frac_of_issue_peak": round(ops / len(iv2) / (avg2 * 1e-3) / PEAK_VALU_OPS, 4)
+                            "scorer_frac_of_issue_peak": round(LANE_OPS_PER_TRIPLE[q.model] * q.triples * steps
+                                                               / len(iv2) / (avg2 * 1e-3) / PEAK_VALU_OPS, 4)
                             if avg2 > 0 and q.model != 2 else None,
                             "stage_ms": stage_breakdown(q, reps=2)}
             log(f"[bench]   {name}: {others[name]['queries_per_s']} q/s, scorer frac "
