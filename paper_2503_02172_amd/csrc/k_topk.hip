@@ -1,42 +1,48 @@
 // Top-k selection over each query's N entity scores (the ranking the paper
 // evaluates with MRR, Experiments/Metrics). Order: score descending, equal
-// scores by entity index ascending.
+// scores by entity index ascending. Scores map to order-preserving 32-bit
+// keys; equal keys are ordered by index through a (key, ~index) composite.
 //
-// One workgroup of NT threads (256, or 1024 for the short candidate lists of
-// later rounds) selects the top k of one segment of at most 16 Ki scores, held
-// in registers (KPT keys per thread, element i = j * NT + tid). Small
-// workgroups keep several rows in flight per compute unit, which hides the
-// latency of the selection's barrier-separated phases. Scores map to
-// order-preserving 32-bit keys; equal keys are ordered by index through a
-// (key, ~index) composite.
+// Two kernels, chosen per round by launch_topk:
 //
-// Common path (k <= 256): each thread's largest key is taken, and the k-th
-// largest of those 256 maxima, L, is a lower bound of the segment's k-th key
-// (k distinct keys, one per thread, are at least L). Only slightly more than
-// k keys usually reach L (about 120 for k = 100 among 14,505 scores), so they
-// are compacted straight into LDS, with ranges per wavefront from ballot
-// counts and no atomics, and one wavefront sorts them in registers; the
-// first k are the answer.
+// Streaming (k <= 256 with enough rows to occupy the chip, the path of large
+// batches): one wavefront per row (or per segment of a row when rows are
+// few), no workgroup barriers. The wavefront streams its scores once and
+// keeps only those at or above a running threshold in an LDS candidate
+// buffer; the threshold starts from the k-th largest of the column maxima
+// of the first 1,536 scores and rises whenever the buffer is pruned. The end is a last prune
+// and a sort of at most 256 candidates inside the wavefront. Its cost per
+// score is a compare and a ballot, so it runs near the rate the scores
+// stream in.
 //
-// Histogram path (k > 256, or more than 256 keys at or above L: masses of
-// equal or nearly equal scores). Bits that every key of the segment shares
-// are found with a block-wide OR / AND and skipped. One histogram pass over
-// the next 11 bits locates the bin that holds the k-th key; every key in that
-// bin or above is compacted and sorted. If that bin is crowded, a second
-// 11-bit histogram over the bin's keys, still in registers, narrows it. If
-// the candidate set would still exceed the LDS buffer, exact radix passes of
-// 8 bits narrow the threshold key T down instead, and the keys above T plus
-// the lowest-index keys equal to T are taken. Sorting runs in registers
-// inside one wavefront for up to 256 candidates, in LDS across the workgroup
-// otherwise.
+// Register-resident (k > 256, or small batches, where latency matters more
+// than throughput): one workgroup of 256 threads selects the top k of one
+// segment of at most 16 Ki scores, held in registers (KPT keys per thread,
+// element i = j * 256 + tid), all loads issued at once.
+//   Common case (k <= 256): each thread's largest key is taken, and the k-th
+//   largest of those 256 maxima, L, is a lower bound of the segment's k-th
+//   key (k distinct keys, one per thread, are at least L). Only slightly
+//   more than k keys usually reach L (about 120 for k = 100 among 14,505
+//   scores); they are compacted into LDS, with ranges per wavefront from
+//   ballot counts and no atomics, and one wavefront sorts them in registers.
+//   Histogram case (k > 256, or more than 256 keys at or above L: masses of
+//   equal or nearly equal scores): bits shared by every key are skipped, one
+//   histogram pass over the next 11 bits locates the bin of the k-th key,
+//   and every key in it or above is compacted and sorted; a second 11-bit
+//   histogram narrows a crowded bin, and exact radix passes of 8 bits handle
+//   what would still overflow LDS (the keys above the threshold T plus the
+//   lowest-index keys equal to T are taken). Sorting runs in registers inside
+//   one wavefront for up to 256 candidates, in LDS across the workgroup
+//   otherwise.
 //
-// Rows longer than one segment take two (or more) launches: each segment of
-// a row yields its top k, then the same kernel selects the top k of those
+// Rows cut into several segments take two (or more) launches: each segment
+// yields its top k, then the next round selects the top k of those
 // candidates through an index map. Segments are contiguous index ranges and
-// each segment's list is ordered by (score desc, index asc), so among equal
-// scores candidate position order is global index order, and the tie rule
-// carries through. A segment shorter than k pads its list with -inf
-// entries, which never outrank a real score.
+// the composite carries the global index, so the tie rule holds across
+// segments. A segment shorter than k pads its list with -inf entries (index
+// 0x7FFFFFFF), which never outrank a real score.
+#include <algorithm>
+
 #include "kgq_internal.hpp"
 
 namespace kgq {
@@ -589,6 +595,390 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(5))) void k_
     }
 }
 
+// ---------------------------------------------------------------------------
+// Streaming selection (k <= kStreamK): one wavefront per segment, no
+// workgroup barriers. The wavefront reads its segment once, four coalesced
+// 256-byte loads per step, with several steps in flight, and compares each
+// score with a running threshold score tf. Scores not below it are appended,
+// as (raw bits, element index) pairs, to the wavefront's candidate buffer in
+// LDS: ballot ranges, no atomics, no branches, a few instructions per 64
+// scores. When fewer free slots remain than one group of steps could fill,
+// the buffer is pruned: its entries become order-preserving keys, and a radix
+// select over them (one bit at a time from their highest differing bit,
+// counting with ballots) raises the threshold T = (key, inverted index) to a
+// bound that at least k of them still reach and at most max(k, kStreamKeep)
+// do; masses of equal keys are narrowed by index, which makes T exact. T
+// never exceeds the k-th largest (key, index) seen so far, so no element of
+// the top k is dropped; the score compare only admits a superset (ties with
+// T, NaN), which the prunes sort out. At the end the buffer is pruned to at
+// most 64, 128 or 256 entries (by k) and sorted inside the wavefront.
+// ---------------------------------------------------------------------------
+constexpr int kStreamK = 256;        // largest k on the streaming path
+constexpr int kStreamKeep = 128;     // a prune leaves at most max(k, this) entries
+constexpr int kStreamWaves = 2;      // wavefronts (segments) per workgroup
+constexpr int kStreamGroup = 1;      // load steps per group
+constexpr int kStreamDepth = 6;      // groups held in registers (depth - 1 in flight)
+constexpr int kStreamCap = 768;      // candidate buffer entries per wavefront
+
+// Smallest buffer (entries per wavefront) for H-step groups: one group of
+// appends on top of what a prune leaves (at most kStreamK, plus fewer than k
+// copies of the padding pair in later rounds, whose lists hold the padding
+// of short segments).
+template <int H, bool IDX>
+constexpr int stream_min_cap() { return kStreamK + (IDX ? kStreamK : 0) + 256 * H; }
+
+__device__ __forceinline__ uint64_t ballot64(bool f) { return __builtin_amdgcn_ballot_w64(f); }
+
+__device__ __forceinline__ int lanes_below(uint64_t m)
+{
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Number of keys at or above x >= 1 (empty slots hold key 0).
+template <int E>
+__device__ __forceinline__ int stream_count_ge(const uint32_t (&key)[E], uint32_t x)
+{
+    int c = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) c += __popcll(ballot64(key[e] >= x));
+    return c;
+}
+
+// Raise the threshold (tk, ti) so that at least k and at most `keep` of the
+// cnt buffered entries reach it (cnt > keep >= k). key[e] holds the key of
+// entry e * 64 + lane (0 past cnt); inv_of(e) gives its inverted index.
+template <int E, bool TIES = true, typename Inv>
+__device__ __forceinline__ void stream_threshold(const uint32_t (&key)[E], Inv inv_of, int cnt, int k, int keep,
+                                                 uint32_t& tk, uint32_t& ti)
+{
+    // common leading bits of the buffered keys (valid keys are >= 1; empty
+    // slots drop out of the maximum, and out of the minimum over key - 1)
+    uint32_t mx = 0u, mn1 = 0xFFFFFFFFu;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        mx = max(mx, key[e]);
+        mn1 = min(mn1, key[e] - 1u);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        mx = max(mx, (uint32_t)__shfl_xor(mx, off, 64));
+        mn1 = min(mn1, (uint32_t)__shfl_xor(mn1, off, 64));
+    }
+    // (the reduced values are uniform: keep them, and all that follows from
+    // them, in scalar registers)
+    mx = __builtin_amdgcn_readfirstlane(mx);
+    mn1 = __builtin_amdgcn_readfirstlane(mn1);
+    const uint32_t diff = mx ^ (mn1 + 1u);
+    const int top = diff ? 31 - __clz(diff) : -1;
+    // p: the k-th largest key with the bits below the current one cleared
+    // (every key >= p until the loop moves it); np = keys >= p
+    uint32_t p = diff ? mx & ~((2u << top) - 1u) : mx;
+    int np = cnt;
+    for (int b = top; b >= 0 && np > keep; --b) {
+        const uint32_t c = p | (1u << b);
+        const int n = stream_count_ge(key, c);
+        if (n >= k) { p = c; np = n; }
+    }
+    uint32_t q = 0u;
+    if (TIES && np > keep) {
+        // p is the k-th largest key and too many keys equal it: select among
+        // those by inverted index, down to k entries (distinct indices)
+        const int above = p == 0xFFFFFFFFu ? 0 : stream_count_ge(key, p + 1u);
+        const int need = k - above;
+        int nq = np - above;
+        for (int b = 31; b >= 0 && above + nq > keep; --b) {
+            const uint32_t c = q | (1u << b);
+            int n = 0;
+#pragma unroll
+            for (int e = 0; e < E; ++e) n += __popcll(ballot64(key[e] == p && inv_of(e) >= c));
+            if (n >= need) { q = c; nq = n; }
+        }
+    }
+    // the threshold only rises
+    if (p > tk || (p == tk && q > ti)) { tk = p; ti = q; }
+}
+
+// Prune while the stream runs (its loads in flight hold registers): keys in
+// registers, indices read from LDS. Entries reaching the new threshold are
+// compacted to the front, in place, as (score bits, index). Copies of one
+// (key, index) pair come only from the padding of short segments' lists
+// (fewer than k per row), so at most keep + k - 1 entries remain.
+template <int E>
+__device__ __forceinline__ void stream_prune(uint2* buf, int& cnt, uint32_t& tk, uint32_t& ti, int k, int keep,
+                                             int lane)
+{
+    uint32_t key[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int p = e * 64 + lane;
+        key[e] = p < cnt ? max(score_key(__uint_as_float(buf[p].x)), 1u) : 0u;
+    }
+    stream_threshold<E>(key, [&](int e) { return ~buf[e * 64 + lane].y; }, cnt, k, keep, tk, ti);
+    // In place: chunk e's entries move to slots below (e + 1) * 64, which
+    // hold entries of chunks up to e, already read (a wavefront's LDS
+    // accesses complete in order).
+    int base = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int p = e * 64 + lane;
+        const uint32_t idx = buf[p].y;
+        const bool f = p < cnt && (key[e] > tk || (key[e] == tk && ~idx >= ti));
+        const uint64_t bc = ballot64(f);
+        if (f) buf[base + lanes_below(bc)] = make_uint2(__float_as_uint(key_score(key[e])), idx);
+        base += __popcll(bc);
+    }
+    cnt = base;
+}
+
+// Final prune (nothing in flight; cnt <= 64 E): keys and indices in
+// registers. Keeps at most `keep` entries, those above the threshold and
+// then copies of the threshold pair (identical, so any copies do), and
+// writes them as (key, inverted index) for the sort.
+template <int E>
+__device__ __forceinline__ void stream_prune_final(uint2* buf, int& cnt, uint32_t& tk, uint32_t& ti, int k, int keep,
+                                                   int lane)
+{
+    uint32_t key[E], inv[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int p = e * 64 + lane;
+        const uint2 b = p < cnt ? buf[p] : make_uint2(0u, 0xFFFFFFFFu);
+        key[e] = p < cnt ? max(score_key(__uint_as_float(b.x)), 1u) : 0u;
+        inv[e] = ~b.y;
+    }
+    if (cnt > keep) stream_threshold<E>(key, [&](int e) { return inv[e]; }, cnt, k, keep, tk, ti);
+    int base = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const bool f = (e * 64 + lane < cnt) && (key[e] > tk || (key[e] == tk && inv[e] > ti));
+        const uint64_t bc = ballot64(f);
+        if (f) buf[base + lanes_below(bc)] = make_uint2(key[e], inv[e]);
+        base += __popcll(bc);
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const bool f = (e * 64 + lane < cnt) && key[e] == tk && inv[e] == ti;
+        const uint64_t bc = ballot64(f);
+        const int slot = base + lanes_below(bc);
+        if (f && slot < keep) buf[slot] = make_uint2(key[e], inv[e]);
+        base = min(base + __popcll(bc), keep);
+    }
+    cnt = base;
+}
+
+// Sort the n (key, inverted index) entries of buf inside one wavefront and
+// write the first k (the network of bitonic_wave).
+template <int E>
+__device__ __forceinline__ void stream_sort(const uint2* buf, int n, int k, int64_t orow, int lane, const TopkArgs& a)
+{
+    constexpr int P = 64 * E;
+    uint64_t v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int p = e * 64 + lane;
+        v[e] = p < n ? (((uint64_t)buf[p].x << 32) | buf[p].y) : 0ull;
+    }
+#pragma unroll
+    for (int size = 2; size <= P; size <<= 1) {
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            if (stride >= 64) {
+                const int es = stride >> 6;
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const int f = e ^ es;
+                    if (f > e) {
+                        const bool desc = ((e * 64 + lane) & size) == 0;
+                        const uint64_t a0 = v[e], a1 = v[f];
+                        const bool sw = desc ? (a0 < a1) : (a0 > a1);
+                        v[e] = sw ? a1 : a0;
+                        v[f] = sw ? a0 : a1;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const uint32_t lo = __shfl_xor((uint32_t)v[e], stride, 64);
+                    const uint32_t hi = __shfl_xor((uint32_t)(v[e] >> 32), stride, 64);
+                    const uint64_t w = ((uint64_t)hi << 32) | lo;
+                    const bool desc = ((e * 64 + lane) & size) == 0;
+                    const bool lower = (lane & stride) == 0;
+                    const uint64_t mx = v[e] > w ? v[e] : w, mn = v[e] > w ? w : v[e];
+                    v[e] = (desc == lower) ? mx : mn;
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int p = e * 64 + lane;
+        if (p < k) store_one(a, orow, p, v[e]);
+    }
+}
+
+// State of one wavefront's stream.
+struct StreamState {
+    uint2* buf;                        // (score bits, element index) pairs
+    int cnt;                           // buffered entries (wave-uniform)
+    uint32_t tk, ti;                   // threshold; (0, 0): everything passes
+    float tf;                          // score of tk (NaN: every score passes)
+};
+
+// Append the scores of step s not below tf (NaN scores included; all of
+// them while tf is NaN). y: the elements' indices when IDX, else position
+// + seg0. CHECK: the step reaches past the segment's end (positions past it
+// read as 0 and are masked). No memory is read here: a load would wait for
+// every load in flight before it (the vector memory counter is in order).
+template <bool IDX, bool CHECK>
+__device__ __forceinline__ void stream_step(StreamState& st, const float (&x)[4], const int32_t (&y)[4], int s, int nn,
+                                            int32_t seg0, int dummy, int lane)
+{
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int i = s * 256 + c * 64 + lane;
+        const bool f = (!CHECK || i < nn) && !(x[c] < st.tf);
+        const uint64_t bc = ballot64(f);
+        if (bc != 0ull) {
+            // every lane writes: those not appending to a slot of their own
+            // past the buffer (no exec-mask changes on this path)
+            const int slot = f ? st.cnt + lanes_below(bc) : dummy + lane;
+            st.buf[slot] = make_uint2(__float_as_uint(x[c]), IDX ? (uint32_t)y[c] : (uint32_t)(seg0 + i));
+            st.cnt += __popcll(bc);
+        }
+    }
+}
+
+// Loads of the H steps from s0 (positions past the segment read as 0), and
+// of the elements' indices when IDX.
+template <int H, bool IDX>
+__device__ __forceinline__ void stream_load(float (&v)[H][4], int32_t (&w)[H][4], __amdgpu_buffer_rsrc_t rsrc,
+                                            __amdgpu_buffer_rsrc_t irsrc, int s0, int lane)
+{
+#pragma unroll
+    for (int h = 0; h < H; ++h)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int off = lane * 4 + ((s0 + h) * 256 + c * 64) * 4;
+            v[h][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, off, 0, 0));
+            if (IDX) w[h][c] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(irsrc, off, 0, 0);
+        }
+}
+
+// One group of H steps (first step s0) held in v / w: room for all of them
+// first, then each step's appends (checked only where the segment ends).
+template <int H, bool IDX, int CAP, int KEEP>
+__device__ __forceinline__ void stream_group(StreamState& st, const float (&v)[H][4], const int32_t (&w)[H][4], int s0,
+                                             int nsteps, int nn, int32_t seg0, int k, int lane)
+{
+    static_assert(CAP % 64 == 0, "the dummy slots follow the buffer");
+    if (st.cnt > CAP - 256 * H) {
+        stream_prune<CAP / 64>(st.buf, st.cnt, st.tk, st.ti, k, k > KEEP ? k : KEEP, lane);
+        st.tf = key_score(st.tk);
+    }
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+        const int s = s0 + h;
+        if ((s + 1) * 256 <= nn) stream_step<IDX, false>(st, v[h], w[h], s, nn, seg0, CAP, lane);
+        else if (s < nsteps) stream_step<IDX, true>(st, v[h], w[h], s, nn, seg0, CAP, lane);
+    }
+}
+
+// H: steps per group; D groups held in registers, D - 1 of them in flight
+// while one is compared. IDX: element indices come from in_idx (later
+// rounds).
+template <int H, int D, bool IDX, int CAP, int KEEP, int W>
+__global__ __launch_bounds__(64 * W) void k_topk_stream(TopkArgs a)
+{
+    static_assert(CAP >= stream_min_cap<H, IDX>() && CAP % 64 == 0 && KEEP <= kStreamK, "stream buffer too small");
+    __shared__ uint2 s_buf[W][CAP + 64];     // + 64 slots for the lanes that append nothing
+    const int lane = threadIdx.x & 63;
+    // (readfirstlane: the wavefront index is uniform, so the segment's
+    // addresses and its buffer resource stay in scalar registers)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nseg = (a.N + a.seg_len - 1) / a.seg_len;
+    const int64_t unit = (int64_t)blockIdx.x * W + wave;   // (row, segment), row-major
+    if (unit >= nseg * a.n_rows) return;
+    const int64_t row = unit / nseg;
+    const int64_t seg = unit - row * nseg;
+    const int64_t seg0 = seg * a.seg_len;
+    int64_t n64 = a.N - seg0;
+    if (n64 > a.seg_len) n64 = a.seg_len;
+    const int nn = (int)n64;
+    const int k = a.k < nn ? a.k : nn;
+    StreamState st{s_buf[wave], 0, 0u, 0u, key_score(0u)};
+
+    // Step s covers positions s * 256 + c * 64 + lane, c = 0 .. 3. All offsets
+    // go in the per-lane offset, which the buffer range check covers: loads
+    // past the segment's end return 0 (and are masked in the append).
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.scores + row * a.ld + seg0), (short)0, nn * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t irsrc = __builtin_amdgcn_make_buffer_rsrc(
+        IDX ? const_cast<int32_t*>(a.in_idx + row * a.ld + seg0) : nullptr, (short)0, IDX ? nn * 4 : 0, 0x00020000);
+    const int nsteps = (nn + 255) >> 8;
+    float v[D][H][4];
+    int32_t w[D][H][4];
+    // (the scheduling barriers keep the groups' loads in order, so that
+    // waiting for the oldest group leaves the others in flight)
+#pragma unroll
+    for (int g = 0; g < D; ++g) {
+        stream_load<H, IDX>(v[g], w[g], rsrc, irsrc, g * H, lane);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // Initial threshold: each (lane, column) takes the largest of its scores
+    // in the first D * H steps, which are all inside the segment and still in
+    // registers, and the threshold is the k-th largest of those 256 maxima
+    // (radix select). Each maximum is a distinct element, so k elements reach
+    // it: it bounds the k-th largest of the segment from below. From there on
+    // few scores reach the threshold and the stream rarely prunes.
+    if (nn >= D * H * 256) {
+        uint32_t key[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            float m = v[0][0][c];
+#pragma unroll
+            for (int t = 1; t < D * H; ++t) m = fmaxf(m, v[t / H][t % H][c]);
+            key[c] = max(score_key(m), 1u);
+        }
+        stream_threshold<4, false>(key, [](int) { return 0u; }, 256, k, k, st.tk, st.ti);
+        st.tf = key_score(st.tk);
+    }
+    // Oldest-first issue would let the first wavefronts of a compute unit
+    // run ahead and leave the last ones to finish alone, with too few loads
+    // in flight to keep memory busy. Instead each wavefront lowers its
+    // priority as it advances (3 .. 0 by quarters of its segment), so the
+    // ones behind issue first and all finish together.
+    const int q1 = nsteps >> 2, q2 = nsteps >> 1, q3 = (3 * nsteps) >> 2;
+    __builtin_amdgcn_s_setprio(3);
+    for (int s0 = 0; s0 < nsteps; s0 += D * H) {
+        if (s0 >= q3) __builtin_amdgcn_s_setprio(0);
+        else if (s0 >= q2) __builtin_amdgcn_s_setprio(1);
+        else if (s0 >= q1) __builtin_amdgcn_s_setprio(2);
+#pragma unroll
+        for (int g = 0; g < D; ++g) {
+            stream_group<H, IDX, CAP, KEEP>(st, v[g], w[g], s0 + g * H, nsteps, nn, (int32_t)seg0, k, lane);
+            __builtin_amdgcn_sched_barrier(0);
+            stream_load<H, IDX>(v[g], w[g], rsrc, irsrc, s0 + (g + D) * H, lane);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    __builtin_amdgcn_s_setprio(0);
+    // Every score of the segment reached the threshold or is below the k-th
+    // largest, so the buffer holds the top k (all nn when nn <= k). The final
+    // prune also turns the entries into keys for the sort.
+    const int fin = k <= 64 ? 64 : k <= 128 ? 128 : 256;     // sort size
+    if (st.cnt <= 256) stream_prune_final<4>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
+    else if (st.cnt <= 512) stream_prune_final<8>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
+    else stream_prune_final<CAP / 64>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
+    const int64_t orow = row * a.out_rows_per_row + seg;
+    for (int p = k + lane; p < a.k; p += 64) {
+        a.out_idx[orow * a.out_ld + p] = 0x7FFFFFFF;
+        a.out_score[orow * a.out_ld + p] = -__builtin_inff();
+    }
+    if (st.cnt <= 64) stream_sort<1>(st.buf, st.cnt, k, orow, lane, a);
+    else if (st.cnt <= 128) stream_sort<2>(st.buf, st.cnt, k, orow, lane, a);
+    else stream_sort<4>(st.buf, st.cnt, k, orow, lane, a);
+}
+
 static void launch_segments(const TopkArgs& a, hipStream_t s)
 {
     // (rows x segments fits 32 bits: the score buffer holds rows x N floats)
@@ -609,35 +999,75 @@ int64_t topk_scratch_elems(int64_t n_rows, int64_t N, int k)
     return segs > 1 ? n_rows * segs * k : 0;
 }
 
-void launch_topk(const TopkArgs& in, hipStream_t s)
+// Streaming rounds want at least kStreamMinUnits (row, segment) wavefronts
+// (8 per compute unit): one per row when the rows alone give that many,
+// however long the rows; otherwise long rows are split until they do, which
+// costs one more (short) round over the per-segment lists. Below that the
+// chip is mostly idle and the register-resident kernel, which issues a whole
+// segment's loads at once, has the lower latency.
+constexpr int64_t kStreamMinUnits = 2048;
+
+static void launch_stream(const TopkArgs& a, hipStream_t s)
 {
-    if (in.n_rows <= 0) return;
+    const int64_t units = ((a.N + a.seg_len - 1) / a.seg_len) * a.n_rows;
+    const dim3 grid((unsigned)((units + kStreamWaves - 1) / kStreamWaves));
+    if (a.in_idx)
+        hipLaunchKernelGGL((k_topk_stream<kStreamGroup, kStreamDepth, true, kStreamCap, kStreamKeep, kStreamWaves>),
+                           grid, dim3(64 * kStreamWaves), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_topk_stream<kStreamGroup, kStreamDepth, false, kStreamCap, kStreamKeep, kStreamWaves>),
+                           grid, dim3(64 * kStreamWaves), 0, s, a);
+}
+
+bool launch_topk(const TopkArgs& in, hipStream_t s)
+{
+    if (in.n_rows <= 0) return true;
     TopkArgs a = in;
     a.in_idx = nullptr;
     a.out_ld = a.k;
     a.out_rows_per_row = 1;
-    // Rounds: segments of kTopkSegment -> per-segment top-k candidates laid
-    // out [row][segment][k] in a scratch buffer, until one segment holds a
-    // row's whole candidate list. Each round's output is smaller than the
-    // first's, so two buffers of topk_scratch_elems() entries suffice.
+    // Rounds: each row is cut into segments, each segment yields its top k
+    // laid out [row][segment][k] in a scratch buffer, and the next round
+    // selects over those lists, until one segment holds a row. A streaming
+    // round cuts rows only as far as kStreamMinUnits asks, a register-
+    // resident round into segments of kTopkSegment; neither makes more
+    // segments than the kTopkSegment cut, so each round's output fits the two
+    // buffers of topk_scratch_elems() entries, used in turn.
     int ping = 0;
-    while (a.N > kTopkSegment) {
-        const int64_t segs = (a.N + kTopkSegment - 1) / kTopkSegment;
+    for (;;) {
+        const int64_t max_segs = (a.N + kTopkSegment - 1) / kTopkSegment;
+        const int64_t fit = a.n_rows >= kStreamMinUnits
+                                ? 1
+                                : std::min<int64_t>(max_segs, (kStreamMinUnits + a.n_rows - 1) / a.n_rows);
+        const bool stream = a.k <= kStreamK && a.n_rows * fit >= kStreamMinUnits;
+        int64_t segs = stream ? fit : max_segs;
+        int64_t seg_len = a.N;
+        if (segs > 1) {
+            seg_len = stream ? ((a.N + segs - 1) / segs + 255) / 256 * 256 : kTopkSegment;
+            segs = (a.N + seg_len - 1) / seg_len;
+        }
+        if (segs == 1) {
+            a.seg_len = a.N;
+            if (stream) launch_stream(a, s);
+            else launch_segments(a, s);
+            return true;
+        }
+        // a round of several segments writes its lists to the scratch buffers
+        if (!in.cand_idx[ping] || !in.cand_score[ping]) return false;
         TopkArgs r = a;
-        r.seg_len = kTopkSegment;
+        r.seg_len = seg_len;
         r.out_idx = in.cand_idx[ping];
         r.out_score = in.cand_score[ping];
         r.out_ld = a.k;
         r.out_rows_per_row = (int)segs;
-        launch_segments(r, s);
+        if (stream) launch_stream(r, s);
+        else launch_segments(r, s);
         a.scores = in.cand_score[ping];
         a.in_idx = in.cand_idx[ping];
         a.ld = segs * a.k;
         a.N = segs * a.k;
         ping ^= 1;
     }
-    a.seg_len = a.N;
-    launch_segments(a, s);
 }
 
 }  // namespace kgq

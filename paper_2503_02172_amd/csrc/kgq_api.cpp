@@ -762,7 +762,7 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
             ta.cand_idx[i] = L.cand_idx[i];
             ta.cand_score[i] = L.cand_score[i];
         }
-        launch_topk(ta, s);
+        if (!launch_topk(ta, s)) return fail(h, KGQ_E_DEVICE, "top-k scratch buffers missing");
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(h, KGQ_E_DEVICE, std::string("kernel launch: ") + hipGetErrorString(e));

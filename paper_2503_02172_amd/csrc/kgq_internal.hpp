@@ -261,7 +261,9 @@ struct TopkArgs {
     int64_t out_ld;
     int out_rows_per_row;
 };
-void launch_topk(const TopkArgs& a, hipStream_t s);
+// Launches every round; false (nothing launched) when a round needs the
+// scratch buffers and they are missing.
+bool launch_topk(const TopkArgs& a, hipStream_t s);
 int64_t topk_scratch_elems(int64_t n_rows, int64_t N, int k);
 
 }  // namespace kgq
