@@ -362,7 +362,7 @@ def rank_bench(p: Prepared, reps: int = 20):
     torch.cuda.synchronize()
     ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
     nbytes = B * w.n_entities * 4 + (B + 1) * 4 + ids.size * (4 + 4 + 4) + B * 4 * 8
-    return {"kernel": "k_rank_answers", "queries": B, "answers": int(ids.size), "avg_launch_ms": round(ms, 5),
+    return {"kernel": "k_rank_stream (lists of up to 32 answers) + k_rank_answers (the rest)", "queries": B, "answers": int(ids.size), "avg_launch_ms": round(ms, 5),
             "bytes_per_launch": nbytes, "achieved_GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
             "frac_of_hbm_peak": round(nbytes / (ms * 1e-3) / HBM_PEAK, 4),
             "queries_per_s": round(B / (ms * 1e-3), 1)}

@@ -75,6 +75,18 @@ def test_gpu_ranks_at_the_63361_entity_shape():
     _check(eng, s, off, ids, hard)
 
 
+@pytest.mark.parametrize("B,N", [(2304, 14505), (520, 63361)], ids=["2304x14505", "520x63361"])
+def test_gpu_ranks_at_batch_scale(B, N):
+    """Batches large enough for the streaming kernel's wide forms: one
+    wavefront per query (two queries a workgroup) on 14,505-entity rows, and
+    rows of 63,361 split over four wavefronts; lists of every length up to 64
+    (the streaming kernel takes up to 32, the workgroup kernel the rest)."""
+    eng = _engine(N, max_batch=8)
+    s = _scores(B, N, seed=B + N)
+    off, ids, hard = synth.draw_answers(B, N, seed=B + N + 1, max_len=64, special={7: 0, 8: 1, 9: 32, 10: 33})
+    _check(eng, s, off, ids, hard)
+
+
 def test_gpu_ranks_agree_with_the_topk_order():
     """On the scores of a real execute: the top-k entries taken as answers are
     each preceded only by answers (rank 1); the k-th entry alone is preceded by
