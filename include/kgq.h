@@ -251,6 +251,23 @@ kgq_status kgq_execute_mixed_noalloc(kgq_handle* h, int32_t batch, const int32_t
 /* Turn checked mode on (non-zero) or off for this handle. */
 kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
 
+/* Which matrix cores the dense layers (the MLPs of Eq. 4 and of the
+ * intersection operators, and kgq_dense) run on. Both paths compute in FP32
+ * precision class:
+ *   KGQ_DENSE_AUTO (the default): layers whose K is a multiple of 32 and that
+ *     have at least 192 output tiles of 64 x 64 run on the bf16 matrix cores,
+ *     each FP32 operand split exactly into three bf16 parts and six of the
+ *     nine part products kept (the dropped ones are below 2^-23 of each
+ *     product); the others on the FP32 matrix cores. Inputs must be finite
+ *     and below 3.39e38 in magnitude on the bf16 path.
+ *   KGQ_DENSE_FP32: every layer on the FP32 matrix cores.
+ *   KGQ_DENSE_BF16X3: every layer whose K is a multiple of 32 on the bf16
+ *     path, whatever its size (for tests).
+ * The weights' bf16 parts are made when the weights are loaded, whatever the
+ * path. Takes effect for calls enqueued after it. Errors: INVALID_ARG. */
+typedef enum { KGQ_DENSE_AUTO = 0, KGQ_DENSE_FP32 = 1, KGQ_DENSE_BF16X3 = 2 } kgq_dense_path;
+kgq_status kgq_set_dense_path(kgq_handle* h, int32_t path);
+
 /* Describe the lowered plan of a batch (host structure ids, built-in or
  * compiled) without running it. counts receives KGQ_PLAN_NCOUNTS values, in
  * this order:
@@ -405,13 +422,15 @@ kgq_status kgq_profile_reset(kgq_handle* h);
  * union of the intervals is the time the stage had work on the GPU. */
 kgq_status kgq_profile_intervals(kgq_handle* h, int32_t stage, double* out, int64_t cap, int64_t* n);
 
-/* One dense layer on the device with the library's FP32 matrix-core GEMM:
+/* One dense layer on the device with the library's GEMM:
  * y[m][n] = act(sum_k x[m][k] * w[n][k] + b[n]) (the matmul + add (+ ReLU)
- * pattern of the paper's Eq. 4).
+ * pattern of the paper's Eq. 4), on the matrix cores kgq_set_dense_path
+ * selects; on the bf16 path, w is split into its bf16 parts on `stream` in
+ * a stream-ordered allocation freed after the layer.
  *   x  device float [M x K], w device float [N x K], b device float [N] or NULL,
  *   y  device float [M x N]; K a multiple of 4, rows 16-byte aligned.
  *   act 0 = none, 1 = ReLU, 2 = BetaE regulariser clamp(v + 1, 0.05, 1e9).
- * Asynchronous on `stream`. Errors: INVALID_ARG, NO_DEVICE, DEVICE. */
+ * Asynchronous on `stream`. Errors: INVALID_ARG, NO_DEVICE, OOM, DEVICE. */
 kgq_status kgq_dense(kgq_handle* h, const float* x, int32_t M, int32_t K, const float* w, const float* b,
                      int32_t N, int32_t act, float* y, void* stream);
 

@@ -111,6 +111,11 @@ struct kgq_handle {
     float* proj1_ent = nullptr;   // [N x 4d]  entity state . W1^T (LogicE: its state columns of W1)
     float* proj1_rel = nullptr;   // [R x 4d]  Rel . W1^T + b1 (LogicE: its relation columns)
     bool proj1_ready = false;
+    // dense-layer weights split into three bf16 planes each (weight -> planes),
+    // for the FP32-accurate bf16 matrix-core GEMM; the split is redone when a
+    // weight is loaded
+    std::map<const float*, uint16_t*> wplanes;
+    int dense_path = KGQ_DENSE_AUTO;
 
     // structure id -> compiled program: the built-ins for this model, then
     // the structures compiled on this handle
@@ -355,6 +360,22 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(h->ent_blk, n_pad * d);
         if (c.model == KGQ_Q2B) ALLOC(h->rel_o_sp, (int64_t)c.n_relations * d);
     }
+    // bf16 planes of every dense-layer weight whose K (its columns) the
+    // bf16 matrix-core GEMM takes
+    for (auto& kv : h->specs) {
+        const std::string& n = kv.first;
+        const bool weight = n.size() > 3 && n[n.size() - 3] == '.' && n[n.size() - 2] == 'w' &&
+                            n.back() >= '1' && n.back() <= '3';
+        if (kv.second.entity || !weight || kv.second.cols % 32 != 0) continue;
+        uint16_t* planes = nullptr;
+        ALLOC(planes, 3 * kv.second.rows * kv.second.cols);
+        h->wplanes[h->dparam.at(n)] = planes;
+    }
+    if (h->int_cat_w && (2 * d) % 32 == 0) {
+        uint16_t* planes = nullptr;
+        ALLOC(planes, 3 * 4 * d * d);
+        h->wplanes[h->int_cat_w] = planes;
+    }
     h->bytes_params = h->bytes_total;   // everything after this is execute scratch
     const int n_lanes = c.concurrency > 0 ? c.concurrency : 1;
     for (int li = 0; li < n_lanes; ++li) {
@@ -576,6 +597,11 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
     auto gemm = [&](GemmArgs g) {
         g.ws = L.gemm_ws;
         g.ws_elems = L.gemm_ws_elems;
+        if (h->dense_path != KGQ_DENSE_FP32) {
+            auto pl = h->wplanes.find(g.W);
+            if (pl != h->wplanes.end()) g.Wp = pl->second;
+            g.bf16x3_always = h->dense_path == KGQ_DENSE_BF16X3;
+        }
         launch_gemm(g, s);
     };
 
@@ -1200,12 +1226,24 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
             HIP_TRY(h, hipGetLastError());
             HIP_TRY(h, hipStreamSynchronize(nullptr));
         }
+        auto split = [&](const float* w, int64_t n) -> kgq_status {
+            auto pl = h->wplanes.find(w);
+            if (pl == h->wplanes.end()) return KGQ_OK;
+            launch_split_planes(w, pl->second, n, nullptr);
+            HIP_TRY(h, hipGetLastError());
+            HIP_TRY(h, hipStreamSynchronize(nullptr));
+            return KGQ_OK;
+        };
+        kgq_status st = split(dst, ps.rows * ps.cols);
+        if (st != KGQ_OK) return st;
         if (c.model == KGQ_CONE) {
             // the two set functions' first layers, stacked for one GEMM
             const size_t half_w = (size_t)2 * c.dim * c.dim, half_b = (size_t)c.dim;
             if (!std::strcmp(name, "inter.axis.w1")) HIP_TRY(h, hipMemcpy(h->int_cat_w, dst, nbytes, hipMemcpyDeviceToDevice));
             if (!std::strcmp(name, "inter.arg.w1"))
                 HIP_TRY(h, hipMemcpy(h->int_cat_w + half_w, dst, nbytes, hipMemcpyDeviceToDevice));
+            if (!std::strcmp(name, "inter.axis.w1") || !std::strcmp(name, "inter.arg.w1"))
+                if ((st = split(h->int_cat_w, 4 * (int64_t)c.dim * c.dim)) != KGQ_OK) return st;
             if (!std::strcmp(name, "inter.axis.b1")) HIP_TRY(h, hipMemcpy(h->int_cat_b, dst, nbytes, hipMemcpyDeviceToDevice));
             if (!std::strcmp(name, "inter.arg.b1"))
                 HIP_TRY(h, hipMemcpy(h->int_cat_b + half_b, dst, nbytes, hipMemcpyDeviceToDevice));
@@ -1376,11 +1414,30 @@ kgq_status kgq_dense(kgq_handle* h, const float* x, int32_t M, int32_t K, const 
     if (h->dry) return fail(h, KGQ_E_NO_DEVICE, "validation-only handle (device = -1)");
     HIP_TRY(h, hipSetDevice(h->cfg.device));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    GemmArgs g{x, K, w, K, b, y, N, nullptr, M, N, K, act};
+    // the bf16 matrix-core path needs w's planes: split into a
+    // stream-ordered buffer that lives until the layer has run
+    uint16_t* planes = nullptr;
+    g.bf16x3_always = h->dense_path == KGQ_DENSE_BF16X3;
+    if (h->dense_path != KGQ_DENSE_FP32 && gemm_shape_takes_bf16x3(M, N, K, K, g.bf16x3_always)) {
+        HIP_TRY(h, hipMallocAsync((void**)&planes, (size_t)3 * N * K * sizeof(uint16_t), s));
+        launch_split_planes(w, planes, (int64_t)N * K, s);
+        g.Wp = planes;
+    }
     {
         StageTimer t(h, 1, s);
-        launch_gemm({x, K, w, K, b, y, N, nullptr, M, N, K, act}, s);
+        launch_gemm(g, s);
     }
+    if (planes) HIP_TRY(h, hipFreeAsync(planes, s));
     HIP_TRY(h, hipGetLastError());
+    return KGQ_OK;
+}
+
+kgq_status kgq_set_dense_path(kgq_handle* h, int32_t path)
+{
+    if (!h) return KGQ_E_INVALID_ARG;
+    if (path < KGQ_DENSE_AUTO || path > KGQ_DENSE_BF16X3) return fail(h, KGQ_E_INVALID_ARG, "unknown dense path");
+    h->dense_path = path;
     return KGQ_OK;
 }
 

@@ -97,8 +97,21 @@ struct GemmArgs {
     float* ws = nullptr;               // split-K partials for small M (nullptr: never split)
     int64_t ws_elems = 0;
     int epi_split = 0;                 // EPI_CONE_ANGLES: first column of the second map
+    // W split into three bf16 planes (launch_split_planes: [3][N][K], row
+    // stride K) or nullptr. With the planes, K a multiple of 32 and enough
+    // output tiles to fill the chip, the layer runs on the bf16 matrix cores
+    // with FP32 accuracy (k_gemm_bf16x3); bf16x3_always takes that path
+    // whenever K allows it.
+    const uint16_t* Wp = nullptr;
+    bool bf16x3_always = false;
 };
 void launch_gemm(const GemmArgs& g, hipStream_t s);
+// Whether launch_gemm, given weight planes, runs a layer of this shape on
+// the bf16 matrix cores.
+bool gemm_shape_takes_bf16x3(int M, int N, int K, int64_t lda, bool always);
+// W [n floats] -> three bf16 planes p[0..n), p[n..2n), p[2n..3n) with
+// w = p0 + p1 + p2 exactly (round to nearest even at each step).
+void launch_split_planes(const float* w, uint16_t* p, int64_t n, hipStream_t s);
 
 // Epilogue value of output column n.
 __device__ __forceinline__ float apply_epilogue(int epi, int split, int n, float v)

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(HERE, "libkgq.so")
 GQE, Q2B, BETAE, CONE, LOGICE = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 TNORM_PRODUCT, TNORM_MIN, TNORM_LUKASIEWICZ = 0, 1, 2
+DENSE_AUTO, DENSE_FP32, DENSE_BF16X3 = 0, 1, 2
 NUM_STRUCTURES = 14
 MAX_K = 1024
 PLAN_FIELDS = ["chains", "groups", "intersection_inputs", "level1", "level2", "level3", "post",
@@ -77,6 +78,7 @@ def lib() -> ctypes.CDLL:
         "kgq_execute_mixed": ([vp, i32, i32p, vp, vp, i32, vp, vp, vp, vp], i32),
         "kgq_execute_mixed_noalloc": ([vp, i32, i32p, vp, vp, i32, vp, vp, vp, vp], i32),
         "kgq_set_checked": ([vp, i32], i32),
+        "kgq_set_dense_path": ([vp, i32], i32),
         "kgq_describe_plan": ([vp, i32, i32p, i32p], i32),
         "kgq_parse_structure": ([ctypes.c_char_p, i32p, i32, i32p], i32),
         "kgq_compile_structure": ([vp, i32p, i32, i32p], i32),
@@ -198,6 +200,11 @@ class Engine:
 
     def set_checked(self, on: bool):
         self._check(lib().kgq_set_checked(self.h, int(bool(on))))
+
+    def set_dense_path(self, path: int):
+        """DENSE_AUTO, DENSE_FP32 or DENSE_BF16X3 (which matrix cores the
+        dense layers run on)."""
+        self._check(lib().kgq_set_dense_path(self.h, int(path)))
 
     # -- execution ------------------------------------------------------------
     def execute_into(self, structure: int, batch: int, anchors, relations, k: int,

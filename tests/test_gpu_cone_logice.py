@@ -85,6 +85,35 @@ def test_gpu_cone_logice_every_structure(model, n_ent, dim, B):
     assert amb <= 2, amb
 
 
+@pytest.mark.parametrize("model", [O.CONE, O.LOGICE], ids=["cone", "logice"])
+def test_gpu_cone_logice_dense_bf16x3(model):
+    """Every dense layer whose K is a multiple of 32 forced onto the bf16
+    matrix-core path (d = 32: all of ConE's, LogicE's second and third
+    projection layers; LogicE's first layer, K = 3d = 96, too): every
+    structure and a mixed batch."""
+    import torch
+    from paper_2503_02172_amd import kgq
+    w = synth.make_tiny(model, n_ent=70, n_rel=7, dim=32, seed=730 + model)
+    m = _oracle(w, model)
+    amb = 0
+    with kgq.engine_for(w, max_batch=64) as eng:
+        eng.set_dense_path(kgq.DENSE_BF16X3)
+        for s in ALL:
+            name = synth.STRUCTURES[s]
+            print(f"[bf16x3] model={model} structure={name}", flush=True)
+            qb = synth.draw_queries(name, 37, 70, 7, seed=1730 + s)
+            out = eng.execute(s, qb.anchors, qb.relations, k=5, scores=True)
+            torch.cuda.synchronize()
+            ora, mg = m.scores(s, qb.anchors, qb.relations, with_margin=True)
+            amb += _compare(out, ora, mg, w, 5, f"model {model} {name} bf16x3")[1]
+        qb = synth.draw_mixed(synth.STRUCTURES, 53, 70, 7, seed=1799)
+        out = eng.execute(qb.structure_ids, qb.anchors, qb.relations, k=10, scores=True)
+        torch.cuda.synchronize()
+        ora, mg = m.scores(qb.structure_ids, qb.anchors, qb.relations, with_margin=True)
+        amb += _compare(out, ora, mg, w, 10, f"model {model} mixed bf16x3")[1]
+    assert amb <= 2, amb
+
+
 @pytest.mark.parametrize("tnorm", [O.TNORM_PRODUCT, O.TNORM_MIN, O.TNORM_LUKASIEWICZ],
                          ids=["product", "min", "lukasiewicz"])
 def test_gpu_logice_tnorms_mixed(tnorm):

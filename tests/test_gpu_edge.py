@@ -162,13 +162,20 @@ def test_gpu_deterministic_and_stream():
     eng.close()
 
 
+@pytest.mark.parametrize("path", [0, 1, 2], ids=["auto", "fp32", "bf16x3"])
 @pytest.mark.parametrize("M,N,K,act", [(1, 1, 4, 0), (37, 50, 12, 1), (130, 1600, 800, 1), (700, 800, 1600, 2),
                                        (64, 64, 64, 0), (1029, 400, 400, 0),
                                        # direct-to-LDS loop: one half stage, stages fewer than / equal to
                                        # the ring, a half last stage after full ones, ragged M and N
                                        (65, 70, 16, 1), (200, 33, 48, 0), (129, 127, 80, 2), (66, 190, 96, 1),
-                                       (3, 400, 400, 1)])
-def test_gpu_dense_matches_fp64(M, N, K, act):
+                                       (3, 400, 400, 1),
+                                       # bf16 path: one or two stages, ragged tiles, 64 x 128 tiles
+                                       (65, 70, 32, 1), (200, 33, 64, 0), (129, 127, 96, 2),
+                                       (1100, 800, 800, 1), (4100, 1100, 160, 0), (4097, 1030, 1600, 1)])
+def test_gpu_dense_matches_fp64(M, N, K, act, path):
+    """One dense layer against an fp64 matmul on each path: automatic choice,
+    FP32 matrix cores only, and the bf16 path wherever K is a multiple of 32
+    (x split into three bf16 parts in registers, w when the layer is set up)."""
     import torch
     from paper_2503_02172_amd import kgq
     rng = np.random.default_rng(M * 7 + N)
@@ -176,6 +183,7 @@ def test_gpu_dense_matches_fp64(M, N, K, act):
     wt = (rng.uniform(-1, 1, (N, K)) / np.sqrt(K)).astype(np.float32)
     b = rng.uniform(-0.5, 0.5, N).astype(np.float32)
     eng = kgq.Engine(kgq.GQE, 10, 2, 4, 1.0, 1, device=0)
+    eng.set_dense_path(path)
     y = eng.dense(torch.tensor(x, device="cuda"), torch.tensor(wt, device="cuda"),
                   torch.tensor(b, device="cuda"), act)
     torch.cuda.synchronize()

@@ -99,3 +99,25 @@ def test_gpu_small_form_switch(model, B):
     print(f"[small-switch] model={model} B={B} d=48", flush=True)
     _run_and_check(eng, w, m, 0, qb.anchors, qb.relations, 10)
     eng.close()
+
+
+@pytest.mark.parametrize("model", [O.GQE, O.Q2B, O.BETAE], ids=["gqe", "q2b", "betae"])
+def test_gpu_tiny_dense_bf16x3(model):
+    """Every dense layer forced onto the bf16 matrix-core path (weights and
+    inputs split into three bf16 parts, six part products): every structure,
+    then a mixed batch, at d = 32 so that every layer's K is a multiple of 32,
+    with 70 entities (a ragged entity tile) and 37 queries (ragged row tiles)."""
+    from paper_2503_02172_amd import kgq
+    w = synth.make_tiny(model, n_ent=70, n_rel=7, dim=32, seed=130 + model)
+    m = O.Model(model, w.params, w.gamma)
+    eng = _engine(w)
+    eng.set_dense_path(kgq.DENSE_BF16X3)
+    structures = EPFO if model != O.BETAE else ALL
+    for s in structures:
+        name = synth.STRUCTURES[s]
+        print(f"[bf16x3] model={model} structure={name}", flush=True)
+        qb = synth.draw_queries(name, 37, 70, 7, seed=1300 + s)
+        _run_and_check(eng, w, m, s, qb.anchors, qb.relations, 5)
+    qb = synth.draw_mixed([synth.STRUCTURES[s] for s in structures], 53, 70, 7, seed=1399)
+    _run_and_check(eng, w, m, qb.structure_ids, qb.anchors, qb.relations, 10, mixed=True)
+    eng.close()
