@@ -14,8 +14,9 @@ Prints one JSON line. `value` is queries/s over the timed steps.
 `roofline` describes the dominant kernel (the entity scorer): the
 algorithmic operations of one launch divided by the launch's average
 duration (HIP events around each launch on the stream it runs on), against
-the chip's published peak for the units it runs on (FP32 matrix cores for
-BetaE; FP32 vector units for GQE / Query2Box). `cpu_baseline` times the CPU
+the chip's published peak for the units it runs on (for BetaE the bf16
+matrix cores at six bf16 products per FP32-accurate product, or the FP32
+matrix cores with --matrix-path fp32; FP32 vector units for the others). `cpu_baseline` times the CPU
 oracle on a bounded sample of the same workload, on every host thread and on
 one. `others` reports the other workloads (throughput and scorer fraction).
 """
@@ -35,9 +36,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 # Scorer rooflines.
-# BetaE scores on the matrix cores: the published dense FP32 MFMA peak,
-# 157.3 TFLOP/s; each (row, entity, dimension) triple is 2 multiply-adds
-# (alpha * U + beta * V), 4 flops.
+# BetaE scores on the matrix cores; each (row, entity, dimension) triple is 2
+# multiply-adds (alpha * U + beta * V), 4 flops. By default the contraction
+# runs on the bf16 matrix cores with each FP32 operand split exactly into
+# three bf16 parts and six part products kept (FP32 accuracy), so its ceiling
+# is the published dense bf16 MFMA peak, 2.5 PFLOP/s, over 6: 416.7 TFLOP/s of
+# FP32-accurate flops. On the FP32 matrix cores (--matrix-path fp32) it is the
+# published dense FP32 MFMA peak, 157.3 TFLOP/s; that fraction is reported
+# beside the other as `frac_of_fp32_mfma_peak`.
 # GQE and Query2Box score on the vector units. Each sub / add / min of the
 # scorer is one flop and one lane-operation (the library is compiled without
 # packed FP32 instructions, so an instruction does one operation per lane).
@@ -52,6 +58,8 @@ sys.path.insert(0, ROOT)
 PEAK_VALU_OPS = 256 * 4 * 32 * 2.4e9
 PEAK_VALU_F32 = 157.3e12
 PEAK_MFMA_F32 = 157.3e12
+PEAK_MFMA_BF16 = 2.5e15
+BF16X3_PRODUCTS = 6
 HBM_PEAK = 8.0e12
 # algorithmic flops per (query row, entity, scored coordinate) triple, the
 # peak they are counted against, and its unit. ConE's sector distance is 10
@@ -64,6 +72,16 @@ SCORER_PEAK = {0: (PEAK_VALU_F32, "alu", "TFLOP/s"), 1: (PEAK_VALU_F32, "alu", "
                2: (PEAK_MFMA_F32, "mfma", "TFLOP/s"), 3: (PEAK_VALU_F32, "alu", "TFLOP/s"),
                4: (PEAK_VALU_F32, "alu", "TFLOP/s")}
 K_TOP = 100
+
+
+def scorer_peak(model: int, matrix_path: str):
+    """(peak, bound, unit, basis) of a model's scorer on the given matrix path."""
+    if model == 2 and matrix_path != "fp32":
+        return (PEAK_MFMA_BF16 / BF16X3_PRODUCTS, "mfma", "TFLOP/s",
+                "dense bf16 MFMA peak 2.5 PFLOP/s / 6 bf16 products per FP32-accurate product")
+    peak, bound, unit = SCORER_PEAK[model]
+    basis = "dense FP32 MFMA peak" if model == 2 else "FP32 vector peak (packed FMA, 4 flops per lane per clock)"
+    return peak, bound, unit, basis
 
 WORKLOAD_DESC = {
     "C1": "GQE, 1,000 entities x 20 relations, d=32, fp32; 16 x 1p + 16 x 2i; top-10",
@@ -103,7 +121,8 @@ class Prepared:
     order); otherwise one call per batch, round-robin over n_streams streams.
     """
 
-    def __init__(self, name: str, n_streams: int = 1, merge: bool = True, inflight: int = 1):
+    def __init__(self, name: str, n_streams: int = 1, merge: bool = True, inflight: int = 1,
+                 matrix_path: str = "auto"):
         import torch
         from paper_2503_02172_amd import kgq, synth
 
@@ -142,6 +161,8 @@ class Prepared:
             n_streams = self.inflight
         self.eng = kgq.engine_for(w, max_batch=max(g[1] for g in groups), model=model, params=params,
                                   concurrency=n_streams)
+        self.matrix_path = matrix_path
+        self.eng.set_dense_path(kgq.DENSE_FP32 if matrix_path == "fp32" else kgq.DENSE_AUTO)
         self.streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
         dev = torch.device("cuda", 0)
         self.calls = []
@@ -449,6 +470,10 @@ def main():
                          "time; 2 or more alternate consecutive steps over that many streams (one scratch lane "
                          "and output buffer each), so that one step's small kernels overlap another's scorer. "
                          "The other mode is timed after the headline and reported beside it")
+    ap.add_argument("--matrix-path", choices=["auto", "fp32"], default="auto",
+                    help="dense contractions (MLP layers, BetaE scorer) on the bf16 matrix cores with the exact "
+                         "three-part split where it pays (auto, the library default) or on the FP32 matrix "
+                         "cores only (fp32)")
     ap.add_argument("--sweep", default=None, metavar="SIZES",
                     help="instead of the benchmark: per-query time and device memory against batch size, per "
                          "structure, on --workload's tables (comma-separated batch sizes, e.g. 1,16,256,1024)")
@@ -469,7 +494,7 @@ def main():
     # The engine always has two scratch lanes and two output buffers, so the
     # same prepared workload can be timed one step at a time and with two
     # steps in flight.
-    p = Prepared(args.workload, args.streams, merge, max(2, args.inflight))
+    p = Prepared(args.workload, args.streams, merge, max(2, args.inflight), args.matrix_path)
     headline_serial = args.inflight == 1
     n_streams = 1 if headline_serial else len(p.streams)
     log(f"[bench] warmup {args.warmup}, timing {args.steps} steps: {len(p.calls)} execute call(s) per "
@@ -485,11 +510,11 @@ def main():
     achieved = ops_per_launch / (avg_launch_ms * 1e-3) if avg_launch_ms > 0 else 0.0
     achieved_busy = total_ops / (busy * 1e-3) if busy > 0 else 0.0
     traffic, traffic_req = traffic_for(p.model, f"score:{args.workload}")
-    peak, bound, unit = SCORER_PEAK[p.model]
+    peak, bound, unit, basis = scorer_peak(p.model, args.matrix_path)
     in_flight_now = 1 if headline_serial else p.inflight
     roofline = {"bound": bound, "kernel": "k_score (entity scorer)" if p.model != 2 else "k_score_kl (entity scorer)",
                 "achieved": round(achieved / 1e12, 3), "peak": round(peak / 1e12, 2),
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+                "unit": unit, "frac": round(achieved / peak, 4), "peak_basis": basis, "traffic": traffic,
                 "traffic_by_request_size": traffic_req,
                 "ops_per_launch": ops_per_launch, "avg_launch_ms": round(avg_launch_ms, 5),
                 "launches": n_launch, "scorer_busy_ms": round(busy, 4),
@@ -498,6 +523,9 @@ def main():
                           f"({in_flight_now} step(s) in flight); achieved = algorithmic ops per launch / average "
                           f"launch duration"}
     roofline["derivation"] = scorer_derivation(p)
+    if p.model == 2:
+        roofline["matrix_path"] = args.matrix_path
+        roofline["frac_of_fp32_mfma_peak"] = round(achieved / PEAK_MFMA_F32, 4)
     if p.model != 2 and avg_launch_ms > 0:
         # lane-operations of one launch against the non-packed issue rate
         lane_ops_per_launch = LANE_OPS_PER_TRIPLE[p.model] * p.triples * args.steps / max(n_launch, 1)
@@ -532,7 +560,7 @@ def main():
             if name == args.workload:
                 continue
             log(f"[bench] other workload {name}")
-            q = Prepared(name, args.streams, merge, max(2, args.inflight))
+            q = Prepared(name, args.streams, merge, max(2, args.inflight), args.matrix_path)
             steps = max(3, min(args.steps, 30))
             # one step at a time (the scorer's launch interval measures the
             # kernel alone), then two steps in flight
@@ -548,9 +576,12 @@ def main():
                             "entity_scores_per_s": round(q.n_queries * q.w.n_entities * steps / d1, 1),
                             "scorer_busy_ms_per_step": round(b2 / steps, 5),
                             "scorer_launch_ms": round(avg2, 5),
-                            "scorer_bound": SCORER_PEAK[q.model][1],
-                            "scorer_frac": round(ops / len(iv2) / (avg2 * 1e-3) / SCORER_PEAK[q.model][0], 4)
+                            "scorer_bound": scorer_peak(q.model, args.matrix_path)[1],
+                            "scorer_frac": round(ops / len(iv2) / (avg2 * 1e-3)
+                                                 / scorer_peak(q.model, args.matrix_path)[0], 4)
                             if avg2 > 0 else None,
+                            "scorer_frac_of_fp32_mfma_peak": round(ops / len(iv2) / (avg2 * 1e-3) / PEAK_MFMA_F32, 4)
+                            if avg2 > 0 and q.model == 2 else None,
                             "scorer_frac_of_issue_peak": round(LANE_OPS_PER_TRIPLE[q.model] * q.triples * steps
                                                                / len(iv2) / (avg2 * 1e-3) / PEAK_VALU_OPS, 4)
                             if avg2 > 0 and q.model != 2 else None,

@@ -251,20 +251,23 @@ kgq_status kgq_execute_mixed_noalloc(kgq_handle* h, int32_t batch, const int32_t
 /* Turn checked mode on (non-zero) or off for this handle. */
 kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
 
-/* Which matrix cores the dense layers (the MLPs of Eq. 4 and of the
- * intersection operators, and kgq_dense) run on. Both paths compute in FP32
- * precision class:
+/* Which matrix cores the dense contractions run on: the dense layers (the
+ * MLPs of Eq. 4 and of the intersection operators, and kgq_dense) and
+ * BetaE's scoring contraction (the regrouped KL of Eq. 3's embeddings). Both
+ * paths compute in FP32 precision class:
  *   KGQ_DENSE_AUTO (the default): layers whose K is a multiple of 32 and that
  *     have at least 192 output tiles of 64 x 64 run on the bf16 matrix cores,
  *     each FP32 operand split exactly into three bf16 parts and six of the
  *     nine part products kept (the dropped ones are below 2^-23 of each
  *     product); the others on the FP32 matrix cores. Inputs must be finite
  *     and below 3.39e38 in magnitude on the bf16 path.
- *   KGQ_DENSE_FP32: every layer on the FP32 matrix cores.
+ *     BetaE scores on the bf16 path when 2d is a multiple of 32.
+ *   KGQ_DENSE_FP32: every layer and the BetaE scorer on the FP32 matrix cores.
  *   KGQ_DENSE_BF16X3: every layer whose K is a multiple of 32 on the bf16
  *     path, whatever its size (for tests).
- * The weights' bf16 parts are made when the weights are loaded, whatever the
- * path. Takes effect for calls enqueued after it. Errors: INVALID_ARG. */
+ * The bf16 parts of the weights and of BetaE's entity-side scoring rows are
+ * made when they are loaded, whatever the path. Takes effect for calls
+ * enqueued after it. Errors: INVALID_ARG. */
 typedef enum { KGQ_DENSE_AUTO = 0, KGQ_DENSE_FP32 = 1, KGQ_DENSE_BF16X3 = 2 } kgq_dense_path;
 kgq_status kgq_set_dense_path(kgq_handle* h, int32_t path);
 

@@ -1,4 +1,4 @@
-// BetaE entity scoring on the FP32 matrix cores of gfx950.
+// BetaE entity scoring on the matrix cores of gfx950.
 //
 // The score of query row q against entity e is gamma minus the KL divergence
 // of the entity's Beta embedding from the query's, summed over dimensions
@@ -9,14 +9,21 @@
 // constant E_e built at load time, the per-query constant C_q built by the
 // pack kernel. The sum is a dense [rows x 2d] . [2d x N] contraction of the
 // packed query rows [alpha | beta] with the entity rows [U | V], so it runs
-// on v_mfma_f32_16x16x4_f32 (full FP32 inputs and accumulation); the VALU
-// form is bound by the half-rate FMA issue of the vector units.
+// on the matrix cores; the VALU form is bound by the half-rate FMA issue of
+// the vector units.
 //
 // Tiling (mfma_tile.hpp): 64-row x 64-entity workgroup tiles, 2 x 2 MFMA
-// tiles of 16 x 16 per wavefront, through the direct-to-LDS ring of three
-// stages when 2d is a multiple of 16 (measured faster, epilogue included,
-// than 128 x 64, 64 x 128 or 128 x 128 tiles and than two or four stages);
-// otherwise the register-staged loop with 128 x 128 tiles. The epilogue adds
+// tiles of 16 x 16 per wavefront. When 2d is a multiple of 32 and the [U | V]
+// rows have been split into three bf16 planes at load, the contraction runs
+// on v_mfma_f32_16x16x32_bf16 with the query rows split in registers and six
+// part products kept: FP32 accuracy at 0.375 of the FP32 matrix-core time per
+// k range (MfmaTileBf16x3; 1.36x faster than the FP32 loop at the
+// 63,361-entity workload, and 64 x 64 tiles ran faster there than 64 x 128).
+// Otherwise v_mfma_f32_16x16x4_f32 with full FP32 inputs: through the
+// direct-to-LDS ring of three stages when 2d is a multiple of 16 (measured
+// faster, epilogue included, than 128 x 64, 64 x 128 or 128 x 128 tiles and
+// than two or four stages), else the register-staged loop with 128 x 128
+// tiles. The epilogue adds
 // C_q + E_e in double precision, stages the output tile in LDS, takes the
 // max over union groups of four and pairs of rows and writes each output
 // row with 16-byte non-temporal stores.
@@ -39,7 +46,7 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
                                                      int per_xcd)
 {
     constexpr int KL_BM = KlTile::kBM, KL_BN = KlTile::kBN;
-    __shared__ float sm[KlTile::SMEM];
+    __shared__ __align__(16) float sm[KlTile::SMEM];
 
     // XCD-aware order (workgroup b runs on XCD b % 8): chunks of qchunk row
     // tiles, then entity tiles, then the chunk's row tiles.
@@ -57,8 +64,13 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     // Query rows are padded (with zeros) to a multiple of 128 and entity
     // rows to a multiple of 256, so the whole tile is inside both buffers.
     const int K = 2 * a.d;
+    const int n_ent_pad = (int)(a.n_blocks * kEntBlock);
     v4f acc[KlTile::TM][KlTile::TN];
-    KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent, K, (int)(a.n_blocks * kEntBlock), K, m0, n0, sm, acc);
+    if constexpr (KlTile::kBf16x3)
+        KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent_planes, (int64_t)n_ent_pad * K, K, n_ent_pad, K, m0, n0, sm,
+                    acc);
+    else
+        KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent, K, n_ent_pad, K, m0, n0, sm, acc);
 
     // Epilogue, staged through LDS (the ring is free after the K loop):
     //   1. each lane adds C_q + E_e in double precision to its accumulators
@@ -152,7 +164,10 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
     if (a.n_rows <= 0) return;
     using LdsTile = MfmaTileLds<64, 64, 3>;
     using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
-    if (LdsTile::supports(2 * a.d)) {
+    using SplitTile = MfmaTileBf16x3<64, 64>;
+    if (a.ent_planes && SplitTile::supports(2 * a.d)) {
+        launch_tiles<SplitTile>(a, s);
+    } else if (LdsTile::supports(2 * a.d)) {
         launch_tiles<LdsTile>(a, s);
     } else if (LdsTileHalf::supports(2 * a.d)) {
         launch_tiles<LdsTileHalf>(a, s);

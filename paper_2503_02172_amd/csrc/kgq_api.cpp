@@ -100,6 +100,7 @@ struct kgq_handle {
     float* ent_blk = nullptr;     // scoring table: GQE/Q2B/LogicE blocked points; BetaE row-major U|V;
                                   // ConE blocked half-angle sin | cos
     double* ent_const = nullptr;  // BetaE E_e [n_pad]
+    uint16_t* ent_planes = nullptr;   // BetaE [U | V] rows of ent_blk as three bf16 planes (when 2d % 32 == 0)
     float* rel_o_sp = nullptr;    // Q2B softplus(offset_raw) [R x d]
     float cone_modulus = 0.f;     // ConE distance scale (host copy of "modulus")
     float* int_cat_w = nullptr;   // ConE [inter.axis.w1; inter.arg.w1] [2d x 2d]
@@ -349,6 +350,7 @@ kgq_status allocate_all(kgq_handle* h)
         ALLOC(h->ent_rm, N * 2 * d);
         ALLOC(h->ent_blk, n_pad * 2 * d);
         if (c.model == KGQ_BETAE) ALLOC(h->ent_const, n_pad);
+        if (c.model == KGQ_BETAE && (2 * d) % 32 == 0) ALLOC(h->ent_planes, 3 * n_pad * 2 * d);
         ALLOC(h->proj1_ent, N * 4 * d);
         ALLOC(h->proj1_rel, (int64_t)c.n_relations * 4 * d);
         if (c.model == KGQ_CONE) {
@@ -770,6 +772,7 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
         ScoreArgs a{c.model, L.qpack, h->ent_blk, L.cq, h->ent_const, P + p.off_out_dest, p.n_score_rows,
                     p.n_quad_rows, p.n_pair_rows, d_score, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
         a.dist_scale = logice ? 1.0f / (float)(2 * d) : cone ? h->cone_modulus : 1.0f;
+        if (betae && h->dense_path != KGQ_DENSE_FP32) a.ent_planes = h->ent_planes;
         a.part = L.score_ws;
         a.part_elems = L.score_ws_elems;
         launch_score(a, s);
@@ -1262,9 +1265,12 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
     e = hipMemcpy(stage, src, nbytes, kind);
     if (e == hipSuccess) {
         const int bf16 = dtype == KGQ_BF16;
-        if (c.model == KGQ_BETAE)
+        if (c.model == KGQ_BETAE) {
             launch_betae_entity_prep(stage, bf16, c.n_entities, c.dim, h->n_blocks, h->ent_rm, h->ent_blk,
                                      h->ent_const, nullptr);
+            if (h->ent_planes)
+                launch_split_planes(h->ent_blk, h->ent_planes, h->n_blocks * kEntBlock * 2 * c.dim, nullptr);
+        }
         else if (c.model == KGQ_CONE)
             launch_cone_entity_prep(static_cast<const float*>(stage), c.n_entities, c.dim, h->n_blocks, h->ent_rm,
                                     h->ent_blk, nullptr);

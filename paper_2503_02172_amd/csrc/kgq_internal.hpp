@@ -241,6 +241,10 @@ struct ScoreArgs {
     float dist_scale = 1.0f;
     float* part = nullptr;             // GQE / Query2Box split-d partials for small batches
     int64_t part_elems = 0;            //   (nullptr: never split)
+    // BetaE: the [U | V] rows of `ent` split into three bf16 planes (plane
+    // stride n_blocks * 256 * 2d) for the bf16 matrix-core contraction, or
+    // nullptr for the FP32 one
+    const uint16_t* ent_planes = nullptr;
 };
 // Filtered answer ranks and per-query [MRR, Hits@1, @3, @10] (k_rank.hip).
 void launch_rank_answers(const float* scores, int64_t ld, int64_t N, int batch, const int32_t* off,

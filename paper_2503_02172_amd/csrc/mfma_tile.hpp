@@ -1,4 +1,4 @@
-// Device-side FP32 matrix-core tile loops shared by the dense layers and the
+// Device-side matrix-core tile loops shared by the dense layers and the
 // BetaE scorer: acc = A[m0 : m0 + BM, :K] . B[n0 : n0 + BN, :K]^T, both
 // operands row-major with K contiguous (A rows: inputs or query rows; B rows:
 // weight rows or entity rows).
@@ -28,6 +28,10 @@
 // MfmaTileReg (any K multiple of 4): double-buffered LDS, the next stage's
 //   global loads held in registers while the current stage computes, padded
 //   LDS rows; the K tail reads as zero.
+// MfmaTileBf16x3 (K a multiple of 32): FP32 accuracy on the bf16 matrix
+//   cores. B comes as three bf16 planes (split beforehand), A as FP32 and is
+//   split in registers; six of the nine part products per k range, on
+//   v_mfma_f32_16x16x32_bf16 with FP32 accumulation (details at the struct).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -42,6 +46,7 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 template <int BM, int BN>
 struct MfmaTileReg {
     static constexpr int kBM = BM, kBN = BN;
+    static constexpr bool kBf16x3 = false;
     static constexpr int BK = 32;
     static constexpr int LD = BK + 4;                  // padded LDS row (floats)
     static constexpr int TM = BM / 32, TN = BN / 32;   // MFMA tiles per wavefront
@@ -152,6 +157,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 template <int BM, int BN, int S, bool HALF = false>
 struct MfmaTileLds {
     static constexpr int kBM = BM, kBN = BN;
+    static constexpr bool kBf16x3 = false;
     static constexpr int BK = 32;
     static constexpr int CH = BK / 4;                  // 16-byte chunks per row per stage
     static constexpr int RPI = 64 / CH;                // rows written by one wave instruction
@@ -293,6 +299,222 @@ struct MfmaTileLds {
         }
         // the half stage: its first half-stage fragments are in buffer 0
         if constexpr (HALF) mma(0);
+    }
+
+    __device__ static int row_of(int i) { return ((threadIdx.x >> 6) >> 1) * (BM / 2) + i * 16 + ((threadIdx.x & 63) >> 4) * 4; }
+    __device__ static int col_of(int j) { return ((threadIdx.x >> 6) & 1) * (BN / 2) + j * 16 + (threadIdx.x & 15); }
+};
+
+// ---- FP32 accuracy on the bf16 matrix cores ---------------------------------
+//
+// Split. Every FP32 value x is written exactly as x = h + m + l with h, m, l
+// bf16: h = bf16(x), m = bf16(x - h), l = x - h - m (round to nearest even at
+// each step). Both subtractions are exact in FP32, and l has at most 8
+// significant bits, so it is a bf16 value and the sum is exact; |m| <= 2^-8 |x|
+// and |l| <= 2^-16 |x|, up to rounding. Values must be finite and below the
+// largest bf16 (3.39e38), above which h would round to infinity.
+// Products. x y = hh' + hm' + mh' + mm' + hl' + lh' + (ml' + lm' + ll'): the
+// first six are kept, the dropped three are below 2^-23 |x y| together. A
+// bf16 x bf16 product is exact in FP32 and the matrix core accumulates in
+// FP32, so a contraction has the error class of an FP32 one. Per 32 of K, six
+// 16x16x32 bf16 MFMAs (16 cycles each) replace eight 16x16x4 FP32 MFMAs (32
+// cycles each).
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+struct Bf16x3 {
+    v4u h, m, l;   // 8 bf16 each, element e in half e % 2 of word e / 2
+};
+
+__device__ __forceinline__ uint32_t pack_bf16_rne(float a, float b)
+{
+    typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+    typedef float v2f __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f){a, b}, v2bf));
+}
+
+// 8 FP32 values (lo: elements 0..3, hi: 4..7) -> their three bf16 parts
+__device__ __forceinline__ Bf16x3 split_bf16x3(const v4u& lo, const v4u& hi)
+{
+    const float x[8] = {__uint_as_float(lo.x), __uint_as_float(lo.y), __uint_as_float(lo.z), __uint_as_float(lo.w),
+                        __uint_as_float(hi.x), __uint_as_float(hi.y), __uint_as_float(hi.z), __uint_as_float(hi.w)};
+    Bf16x3 f;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const float a = x[2 * p], b = x[2 * p + 1];
+        const uint32_t H = pack_bf16_rne(a, b);
+        const float ra = a - __uint_as_float(H << 16), rb = b - __uint_as_float(H & 0xffff0000u);
+        const uint32_t Mm = pack_bf16_rne(ra, rb);
+        const float sa = ra - __uint_as_float(Mm << 16), sb = rb - __uint_as_float(Mm & 0xffff0000u);
+        f.h[p] = H;
+        f.m[p] = Mm;
+        f.l[p] = pack_bf16_rne(sa, sb);
+    }
+    return f;
+}
+
+__device__ __forceinline__ v4f mfma_bf16(const v4u& a, const v4u& b, v4f c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a), __builtin_bit_cast(v8bf, b), c, 0, 0,
+                                                   0);
+}
+
+// Tiles. A workgroup of 4 wavefronts (2 x 2) owns a BM x BN tile, each
+// wavefront (BM/32) x (BN/32) 16x16 blocks. Stages of 32 of K go through a
+// two-slot LDS ring by direct-to-LDS loads: A as FP32 rows (128 bytes, 16-byte
+// chunks XOR-swizzled by row), B as three planes of bf16 rows (64 bytes,
+// chunks swizzled by row / 2), so that the fragment reads of 16 rows at one
+// chunk fall in distinct banks. Lane l supplies row l % 16 of a block at
+// k = 8 (l / 16) .. + 7 (the builtin's operand layout) and holds the output
+// rows 4 (l / 16) .. + 3 of column l % 16, as in the FP32 loops. Stage kt + 1's
+// fragments are read while stage kt's products run; stage kt + 2 is loaded
+// into the slot stage kt leaves. Rows of A at or past M and of B at or past N
+// are read from the last valid row.
+template <int BM, int BN>
+struct MfmaTileBf16x3 {
+    static constexpr int kBM = BM, kBN = BN;
+    static constexpr bool kBf16x3 = true;
+    static constexpr int BK = 32;
+    static constexpr int AROW = BK * 4;                // bytes of one A row per stage (FP32)
+    static constexpr int BROW = BK * 2;                // bytes of one B row per stage and plane (bf16)
+    static constexpr int ABYTES = BM * AROW;
+    static constexpr int STAGE = ABYTES + 3 * BN * BROW;
+    static constexpr int SMEM = 2 * STAGE / 4;         // floats
+    static constexpr int TM = BM / 32, TN = BN / 32;   // 16x16 blocks per wavefront
+    static constexpr int AI = BM / 32;                 // A load instructions per wavefront and stage (8 rows each)
+    static constexpr int BI = 3 * BN / 64;             // B load instructions per wavefront and stage (16 rows each)
+    static constexpr int LPS = AI + BI;
+    static_assert(BM % 32 == 0 && BN % 64 == 0 && LPS < 64, "tile shape");
+    static_assert(2 * STAGE <= 65536, "LDS");
+
+    static bool supports(int K) { return K >= BK && K % BK == 0; }
+    __device__ static int aswz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+    __device__ static int bswz(int row) { return (row >> 1) & 3; }
+
+    // acc = A[m0 : m0 + BM, :K] . B[n0 : n0 + BN, :K]^T; B's planes are
+    // Bp, Bp + plane, Bp + 2 plane (row stride ldb elements).
+    __device__ static void run(const float* __restrict__ A, int64_t lda, int M, const uint16_t* __restrict__ Bp,
+                               int64_t plane, int64_t ldb, int N, int K, int m0, int n0, float* sm_f,
+                               v4f (&acc)[TM][TN])
+    {
+        char* sm = reinterpret_cast<char*>(sm_f);
+        const int nk = K / BK;
+        const int tid = threadIdx.x, lane = tid & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+        const int wm = wave >> 1, wn = wave & 1;
+        const int grp = lane >> 4, li = lane & 15;
+
+        // A: load instruction t = h * 4 + wave writes rows 8t .. 8t + 7
+        // (1 KiB); lane l lands at row 8t + l / 8, chunk position l % 8
+        const float* ag[AI];
+#pragma unroll
+        for (int h = 0; h < AI; ++h) {
+            const int row = (h * 4 + wave) * 8 + (lane >> 3);
+            ag[h] = A + (int64_t)min(m0 + row, M - 1) * lda + ((lane & 7) ^ aswz(row)) * 4;
+        }
+        // B: load instruction u = h * 4 + wave writes plane u / (BN / 16),
+        // rows 16 (u % (BN / 16)) .. + 15; lane l lands at row + l / 4,
+        // chunk position l % 4
+        const uint16_t* bg[BI];
+        int bdst[BI];
+#pragma unroll
+        for (int h = 0; h < BI; ++h) {
+            const int u = h * 4 + wave;
+            const int p = u / (BN / 16), rb = u % (BN / 16);
+            const int row = rb * 16 + (lane >> 2);
+            bg[h] = Bp + p * plane + (int64_t)min(n0 + row, N - 1) * ldb + ((lane & 3) ^ bswz(row)) * 8;
+            bdst[h] = ABYTES + (p * BN + rb * 16) * BROW;
+        }
+        auto issue = [&](int kt, int slot) {
+            char* st = sm + slot * STAGE;
+#pragma unroll
+            for (int h = 0; h < AI; ++h)
+                __builtin_amdgcn_global_load_lds((const void*)(ag[h] + kt * BK),
+                                                 (lds_void*)(st + (h * 4 + wave) * 8 * AROW), 16, 0, 0);
+#pragma unroll
+            for (int h = 0; h < BI; ++h)
+                __builtin_amdgcn_global_load_lds((const void*)(bg[h] + kt * BK), (lds_void*)(st + bdst[h]), 16, 0,
+                                                 0);
+        };
+
+        // fragment offsets in a stage: A block i at k = 8 grp .. + 7
+        // (chunks 2 grp, 2 grp + 1), B block j at chunk grp
+        int aoff[TM][2], boff[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wm * (BM / 2) + i * 16 + li;
+#pragma unroll
+            for (int q = 0; q < 2; ++q) aoff[i][q] = row * AROW + ((2 * grp + q) ^ aswz(row)) * 16;
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int row = wn * (BN / 2) + j * 16 + li;
+            boff[j] = ABYTES + row * BROW + (grp ^ bswz(row)) * 16;
+        }
+
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+        Bf16x3 fa[TM];          // stage kt, split
+        v4u fb[3][TN];
+        v4u ra[TM][2];          // stage kt + 1, as read
+        v4u rb[3][TN];
+        auto read = [&](int slot) {
+            const char* st = sm + slot * STAGE;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                ra[i][0] = *reinterpret_cast<const v4u*>(st + aoff[i][0]);
+                ra[i][1] = *reinterpret_cast<const v4u*>(st + aoff[i][1]);
+            }
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) rb[p][j] = *reinterpret_cast<const v4u*>(st + boff[j] + p * BN * BROW);
+        };
+        auto take = [&]() {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[i] = split_bf16x3(ra[i][0], ra[i][1]);
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) fb[p][j] = rb[p][j];
+        };
+        // the six kept products, largest first; consecutive MFMAs update
+        // different accumulators
+        auto products = [&]() {
+#pragma unroll
+            for (int q = 0; q < 6; ++q)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        const v4u& a = (q == 0 || q == 1 || q == 4) ? fa[i].h : (q == 5 ? fa[i].l : fa[i].m);
+                        const v4u& b = (q == 0 || q == 2 || q == 5) ? fb[0][j] : (q == 4 ? fb[2][j] : fb[1][j]);
+                        acc[i][j] = mfma_bf16(a, b, acc[i][j]);
+                    }
+        };
+
+        // The vmcnt counts below are this loop's loads only: the caller has
+        // no vector-memory load outstanding on entry.
+        issue(0, 0);
+        if (nk > 1) issue(1, 1);
+        if (nk > 1) wait_vm_barrier<LPS>();   // stage 0 landed
+        else wait_vm_barrier<0>();
+        read(0);
+        take();
+        for (int kt = 0; kt < nk; ++kt) {
+            if (kt + 1 < nk) {
+                // stage kt + 1 landed (stage kt + 2 is not issued yet), and
+                // every wavefront holds stage kt's fragments, so its slot is free
+                wait_vm_barrier<0>();
+                if (kt + 2 < nk) issue(kt + 2, kt & 1);
+                read((kt + 1) & 1);
+            }
+            products();
+            if (kt + 1 < nk) take();
+        }
     }
 
     __device__ static int row_of(int i) { return ((threadIdx.x >> 6) >> 1) * (BM / 2) + i * 16 + ((threadIdx.x & 63) >> 4) * 4; }
