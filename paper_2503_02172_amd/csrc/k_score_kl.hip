@@ -12,14 +12,14 @@
 // on the matrix cores; the VALU form is bound by the half-rate FMA issue of
 // the vector units.
 //
-// Tiling (mfma_tile.hpp): 64-row x 64-entity workgroup tiles, 2 x 2 MFMA
-// tiles of 16 x 16 per wavefront. When 2d is a multiple of 32 and the [U | V]
-// rows have been split into three bf16 planes at load, the contraction runs
-// on v_mfma_f32_16x16x32_bf16 with the query rows split in registers and six
+// Tiling (mfma_tile.hpp). When 2d is a multiple of 32 and the [U | V] rows
+// have been split into three bf16 planes at load, the contraction runs on
+// v_mfma_f32_16x16x32_bf16 with the query rows split in registers and six
 // part products kept: FP32 accuracy at 0.375 of the FP32 matrix-core time per
-// k range (MfmaTileBf16x3; 1.36x faster than the FP32 loop at the
-// 63,361-entity workload, and 64 x 64 tiles ran faster there than 64 x 128).
-// Otherwise v_mfma_f32_16x16x4_f32 with full FP32 inputs: through the
+// k range (MfmaTileBf16x3 with 128-row x 64-entity tiles and 4 x 1
+// wavefronts; 1.5x faster than the FP32 loop at the 63,361-entity workload).
+// Otherwise 64-row x 64-entity tiles, 2 x 2 MFMA tiles of 16 x 16 per
+// wavefront, on v_mfma_f32_16x16x4_f32 with full FP32 inputs: through the
 // direct-to-LDS ring of three stages when 2d is a multiple of 16 (measured
 // faster, epilogue included, than 128 x 64, 64 x 128 or 128 x 128 tiles and
 // than two or four stages), else the register-staged loop with 128 x 128
@@ -164,7 +164,7 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
     if (a.n_rows <= 0) return;
     using LdsTile = MfmaTileLds<64, 64, 3>;
     using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
-    using SplitTile = MfmaTileBf16x3<64, 64>;
+    using SplitTile = MfmaTileBf16x3<128, 64>;
     if (a.ent_planes && SplitTile::supports(2 * a.d)) {
         launch_tiles<SplitTile>(a, s);
     } else if (LdsTile::supports(2 * a.d)) {

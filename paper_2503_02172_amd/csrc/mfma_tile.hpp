@@ -359,32 +359,39 @@ __device__ __forceinline__ v4f mfma_bf16(const v4u& a, const v4u& b, v4f c)
                                                    0);
 }
 
-// Tiles. A workgroup of 4 wavefronts (2 x 2) owns a BM x BN tile, each
-// wavefront (BM/32) x (BN/32) 16x16 blocks. Stages of 32 of K go through a
-// two-slot LDS ring by direct-to-LDS loads: A as FP32 rows (128 bytes, 16-byte
-// chunks XOR-swizzled by row), B as three planes of bf16 rows (64 bytes,
-// chunks swizzled by row / 2), so that the fragment reads of 16 rows at one
-// chunk fall in distinct banks. Lane l supplies row l % 16 of a block at
-// k = 8 (l / 16) .. + 7 (the builtin's operand layout) and holds the output
-// rows 4 (l / 16) .. + 3 of column l % 16, as in the FP32 loops. Stage kt + 1's
-// fragments are read while stage kt's products run; stage kt + 2 is loaded
-// into the slot stage kt leaves. Rows of A at or past M and of B at or past N
-// are read from the last valid row.
-template <int BM, int BN>
+// Tiles. A workgroup of 4 wavefronts owns a BM x BN tile; the wavefronts
+// are stacked WM x (4 / WM) (4 x 1 by default: each splits a different part
+// of A, so no A fragment is split twice in a workgroup), each with
+// (BM / WM / 16) x (BN / (4 / WM) / 16) 16x16 blocks. Stages of 32 of K go
+// through a two-slot LDS ring by direct-to-LDS loads: A as FP32 rows (128
+// bytes, 16-byte chunks XOR-swizzled by row), B as three planes of bf16 rows
+// (64 bytes, chunks swizzled by row / 2), so that the fragment reads of 16
+// rows at one chunk fall in distinct banks. Lane l supplies row l % 16 of a
+// block at k = 8 (l / 16) .. + 7 (the builtin's operand layout) and holds the
+// output rows 4 (l / 16) .. + 3 of column l % 16, as in the FP32 loops. Rows
+// of A at or past M and of B at or past N are read from the last valid row.
+// Measured on the BetaE scorer (63,361 entities): 128 x 64 tiles with 4 x 1
+// wavefronts and fragments read when their stage is multiplied ran 1.31 ms,
+// against 1.37 ms with the next stage's fragments read ahead (which needs a
+// second register set), 1.42-1.50 ms with 2 x 2 wavefronts, and 1.48 ms for
+// 64 x 64 tiles with 2 x 2 wavefronts.
+template <int BM, int BN, int WM = 4>
 struct MfmaTileBf16x3 {
     static constexpr int kBM = BM, kBN = BN;
     static constexpr bool kBf16x3 = true;
     static constexpr int BK = 32;
+    static constexpr int WN = 4 / WM;                  // wavefronts along N
     static constexpr int AROW = BK * 4;                // bytes of one A row per stage (FP32)
     static constexpr int BROW = BK * 2;                // bytes of one B row per stage and plane (bf16)
     static constexpr int ABYTES = BM * AROW;
     static constexpr int STAGE = ABYTES + 3 * BN * BROW;
     static constexpr int SMEM = 2 * STAGE / 4;         // floats
-    static constexpr int TM = BM / 32, TN = BN / 32;   // 16x16 blocks per wavefront
+    static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;   // 16x16 blocks per wavefront
     static constexpr int AI = BM / 32;                 // A load instructions per wavefront and stage (8 rows each)
     static constexpr int BI = 3 * BN / 64;             // B load instructions per wavefront and stage (16 rows each)
     static constexpr int LPS = AI + BI;
-    static_assert(BM % 32 == 0 && BN % 64 == 0 && LPS < 64, "tile shape");
+    static_assert((WM == 2 || WM == 4) && TM >= 1 && TN >= 1 && BM % 32 == 0 && BN % 64 == 0 && LPS < 64,
+                  "tile shape");
     static_assert(2 * STAGE <= 65536, "LDS");
 
     static bool supports(int K) { return K >= BK && K % BK == 0; }
@@ -401,7 +408,7 @@ struct MfmaTileBf16x3 {
         const int nk = K / BK;
         const int tid = threadIdx.x, lane = tid & 63;
         const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-        const int wm = wave >> 1, wn = wave & 1;
+        const int wm = wave / WN, wn = wave % WN;
         const int grp = lane >> 4, li = lane & 15;
 
         // A: load instruction t = h * 4 + wave writes rows 8t .. 8t + 7
@@ -442,13 +449,13 @@ struct MfmaTileBf16x3 {
         int aoff[TM][2], boff[TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
-            const int row = wm * (BM / 2) + i * 16 + li;
+            const int row = wm * (BM / WM) + i * 16 + li;
 #pragma unroll
             for (int q = 0; q < 2; ++q) aoff[i][q] = row * AROW + ((2 * grp + q) ^ aswz(row)) * 16;
         }
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const int row = wn * (BN / 2) + j * 16 + li;
+            const int row = wn * (BN / WN) + j * 16 + li;
             boff[j] = ABYTES + row * BROW + (grp ^ bswz(row)) * 16;
         }
 
@@ -457,12 +464,11 @@ struct MfmaTileBf16x3 {
 #pragma unroll
             for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-        Bf16x3 fa[TM];          // stage kt, split
+        Bf16x3 fa[TM];          // the stage being multiplied: A split, B as read
         v4u fb[3][TN];
-        v4u ra[TM][2];          // stage kt + 1, as read
-        v4u rb[3][TN];
-        auto read = [&](int slot) {
+        auto read_split = [&](int slot) {
             const char* st = sm + slot * STAGE;
+            v4u ra[TM][2];
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 ra[i][0] = *reinterpret_cast<const v4u*>(st + aoff[i][0]);
@@ -471,15 +477,9 @@ struct MfmaTileBf16x3 {
 #pragma unroll
             for (int p = 0; p < 3; ++p)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) rb[p][j] = *reinterpret_cast<const v4u*>(st + boff[j] + p * BN * BROW);
-        };
-        auto take = [&]() {
+                for (int j = 0; j < TN; ++j) fb[p][j] = *reinterpret_cast<const v4u*>(st + boff[j] + p * BN * BROW);
 #pragma unroll
             for (int i = 0; i < TM; ++i) fa[i] = split_bf16x3(ra[i][0], ra[i][1]);
-#pragma unroll
-            for (int p = 0; p < 3; ++p)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) fb[p][j] = rb[p][j];
         };
         // the six kept products, largest first; consecutive MFMAs update
         // different accumulators
@@ -497,28 +497,28 @@ struct MfmaTileBf16x3 {
         };
 
         // The vmcnt counts below are this loop's loads only: the caller has
-        // no vector-memory load outstanding on entry.
+        // no vector-memory load outstanding on entry. A stage's fragments
+        // are read when it is multiplied (the other workgroups on the
+        // compute unit cover the LDS latency); the stage two ahead is loaded
+        // into its slot once every wavefront has read it.
         issue(0, 0);
         if (nk > 1) issue(1, 1);
-        if (nk > 1) wait_vm_barrier<LPS>();   // stage 0 landed
-        else wait_vm_barrier<0>();
-        read(0);
-        take();
         for (int kt = 0; kt < nk; ++kt) {
-            if (kt + 1 < nk) {
-                // stage kt + 1 landed (stage kt + 2 is not issued yet), and
-                // every wavefront holds stage kt's fragments, so its slot is free
-                wait_vm_barrier<0>();
-                if (kt + 2 < nk) issue(kt + 2, kt & 1);
-                read((kt + 1) & 1);
-            }
+            // stage kt landed (stage kt + 1 may stay in flight)
+            if (kt + 1 < nk) wait_vm_barrier<LPS>();
+            else wait_vm_barrier<0>();
+            read_split(kt & 1);
             products();
-            if (kt + 1 < nk) take();
+            if (kt + 2 < nk) {
+                wait_vm_barrier<LPS>();   // every wavefront has read stage kt
+                issue(kt + 2, kt & 1);
+            }
         }
     }
 
-    __device__ static int row_of(int i) { return ((threadIdx.x >> 6) >> 1) * (BM / 2) + i * 16 + ((threadIdx.x & 63) >> 4) * 4; }
-    __device__ static int col_of(int j) { return ((threadIdx.x >> 6) & 1) * (BN / 2) + j * 16 + (threadIdx.x & 15); }
+    // Output position of acc[i][j][r] within the workgroup tile.
+    __device__ static int row_of(int i) { return ((threadIdx.x >> 6) / WN) * (BM / WM) + i * 16 + ((threadIdx.x & 63) >> 4) * 4; }
+    __device__ static int col_of(int j) { return ((threadIdx.x >> 6) % WN) * (BN / WN) + j * 16 + (threadIdx.x & 15); }
 };
 
 }  // namespace kgq
