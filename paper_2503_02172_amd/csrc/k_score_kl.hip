@@ -16,8 +16,9 @@
 // have been split into three bf16 planes at load, the contraction runs on
 // v_mfma_f32_16x16x32_bf16 with the query rows split in registers and six
 // part products kept: FP32 accuracy at 0.375 of the FP32 matrix-core time per
-// k range (MfmaTileBf16x3 with 128-row x 64-entity tiles and 4 x 1
-// wavefronts; 1.5x faster than the FP32 loop at the 63,361-entity workload).
+// k range (MfmaTileBf16x3 with 128-row x 128-entity tiles and 4 x 1
+// wavefronts, an 80 KiB LDS ring; 1.66x faster than the FP32 loop at the
+// 63,361-entity workload, and 6% faster than 128 x 64 tiles).
 // Otherwise 64-row x 64-entity tiles, 2 x 2 MFMA tiles of 16 x 16 per
 // wavefront, on v_mfma_f32_16x16x4_f32 with full FP32 inputs: through the
 // direct-to-LDS ring of three stages when 2d is a multiple of 16 (measured
@@ -46,7 +47,7 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
                                                      int per_xcd)
 {
     constexpr int KL_BM = KlTile::kBM, KL_BN = KlTile::kBN;
-    __shared__ __align__(16) float sm[KlTile::SMEM];
+    extern __shared__ __align__(16) float sm[];   // KlTile::SMEM floats, set at launch
 
     // XCD-aware order (workgroup b runs on XCD b % 8): chunks of qchunk row
     // tiles, then entity tiles, then the chunk's row tiles.
@@ -155,7 +156,19 @@ static void launch_tiles(const ScoreArgs& a, hipStream_t s)
     // chunks cost no balance.
     const int64_t tile_bytes = (int64_t)BM * 2 * a.d * 4;
     const int qchunk = (int)std::min<int64_t>(n_mt, std::max<int64_t>(1, (int64_t)(2 << 20) / tile_bytes));
-    hipLaunchKernelGGL((k_score_kl<Tile>), dim3(per_xcd * 8), dim3(256), 0, s, a, n_mt, n_nt, qchunk, total,
+    // LDS is dynamic so that rings above the 64 KiB static limit fit; the
+    // limit is raised once per device and tile
+    constexpr int lds = Tile::SMEM * 4;
+    if (lds > 65536) {
+        static bool raised[64] = {};
+        int dev = 0;
+        if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !raised[dev]) {
+            if (hipFuncSetAttribute((const void*)k_score_kl<Tile>, hipFuncAttributeMaxDynamicSharedMemorySize, lds) ==
+                hipSuccess)
+                raised[dev] = true;
+        }
+    }
+    hipLaunchKernelGGL((k_score_kl<Tile>), dim3(per_xcd * 8), dim3(256), lds, s, a, n_mt, n_nt, qchunk, total,
                        per_xcd);
 }
 
@@ -164,7 +177,7 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
     if (a.n_rows <= 0) return;
     using LdsTile = MfmaTileLds<64, 64, 3>;
     using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
-    using SplitTile = MfmaTileBf16x3<128, 64>;
+    using SplitTile = MfmaTileBf16x3<128, 128>;
     if (a.ent_planes && SplitTile::supports(2 * a.d)) {
         launch_tiles<SplitTile>(a, s);
     } else if (LdsTile::supports(2 * a.d)) {

@@ -370,11 +370,11 @@ __device__ __forceinline__ v4f mfma_bf16(const v4u& a, const v4u& b, v4f c)
 // block at k = 8 (l / 16) .. + 7 (the builtin's operand layout) and holds the
 // output rows 4 (l / 16) .. + 3 of column l % 16, as in the FP32 loops. Rows
 // of A at or past M and of B at or past N are read from the last valid row.
-// Measured on the BetaE scorer (63,361 entities): 128 x 64 tiles with 4 x 1
-// wavefronts and fragments read when their stage is multiplied ran 1.31 ms,
-// against 1.37 ms with the next stage's fragments read ahead (which needs a
-// second register set), 1.42-1.50 ms with 2 x 2 wavefronts, and 1.48 ms for
-// 64 x 64 tiles with 2 x 2 wavefronts.
+// Measured on the BetaE scorer (63,361 entities): 128 x 128 tiles with 4 x 1
+// wavefronts and fragments read when their stage is multiplied ran 1.21 ms,
+// 128 x 64 tiles 1.28-1.31 ms, against 1.37 ms with the next stage's
+// fragments read ahead (which needs a second register set), 1.42-1.50 ms
+// with 2 x 2 wavefronts, and 1.48 ms for 64 x 64 tiles with 2 x 2 wavefronts.
 template <int BM, int BN, int WM = 4>
 struct MfmaTileBf16x3 {
     static constexpr int kBM = BM, kBN = BN;
@@ -392,7 +392,7 @@ struct MfmaTileBf16x3 {
     static constexpr int LPS = AI + BI;
     static_assert((WM == 2 || WM == 4) && TM >= 1 && TN >= 1 && BM % 32 == 0 && BN % 64 == 0 && LPS < 64,
                   "tile shape");
-    static_assert(2 * STAGE <= 65536, "LDS");
+    static_assert(2 * STAGE <= 160 * 1024, "LDS");   // above 64 KiB only as dynamic LDS
 
     static bool supports(int K) { return K >= BK && K % BK == 0; }
     __device__ static int aswz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
