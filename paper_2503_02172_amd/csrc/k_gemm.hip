@@ -199,8 +199,9 @@ static void launch_gemm_bf16x3(const GemmArgs& g, hipStream_t s)
     // Measured on the 14,505-entity BetaE step: dense stage 0.576 ms, against
     // 0.597 ms with 64 x 128 tiles for the largest layers, 0.594 ms with
     // 128 x 64 tiles for every layer of 4,096 rows or more, 0.628 ms with
-    // 64 x 64 tiles throughout.
-    if (g.M >= 4096 && g.N >= 1024) {
+    // 64 x 64 tiles throughout; on the 63,361-entity step, 128 x 64 tiles from
+    // 2,048 rows (its 3,947-row layers) took the stage from 0.534 to 0.516 ms.
+    if (g.M >= 2048 && g.N >= 1024) {
         const int tm = (g.M + 127) / 128, tn = (g.N + 63) / 64, per_xcd = (tm * tn + 7) / 8;
         hipLaunchKernelGGL((k_gemm_bf16x3<128, 64>), dim3(per_xcd * 8), dim3(256), 0, s, g, tm, tn, per_xcd);
     } else {
