@@ -496,23 +496,19 @@ struct MfmaTileBf16x3 {
                     }
         };
 
-        // The vmcnt counts below are this loop's loads only: the caller has
-        // no vector-memory load outstanding on entry. A stage's fragments
-        // are read when it is multiplied (the other workgroups on the
-        // compute unit cover the LDS latency); the stage two ahead is loaded
-        // into its slot once every wavefront has read it.
+        // A stage's fragments are read when it is multiplied (the other
+        // workgroups on the compute unit cover the LDS latency). One barrier
+        // per stage: past it, stage kt has landed for every wavefront and
+        // every wavefront has read stage kt - 1, whose slot then takes stage
+        // kt + 1 while stage kt is multiplied. The wait counts this loop's
+        // loads only: the caller has no vector-memory load outstanding on
+        // entry, and at the wait stage kt's are the only ones in flight.
         issue(0, 0);
-        if (nk > 1) issue(1, 1);
         for (int kt = 0; kt < nk; ++kt) {
-            // stage kt landed (stage kt + 1 may stay in flight)
-            if (kt + 1 < nk) wait_vm_barrier<LPS>();
-            else wait_vm_barrier<0>();
+            wait_vm_barrier<0>();
+            if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
             read_split(kt & 1);
             products();
-            if (kt + 2 < nk) {
-                wait_vm_barrier<LPS>();   // every wavefront has read stage kt
-                issue(kt + 2, kt & 1);
-            }
         }
     }
 
