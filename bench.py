@@ -612,6 +612,10 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "arithmetic": ("dense contractions (BetaE scorer, MLP layers of 256+ output tiles) on the bf16 matrix cores: "
+                       "each FP32 operand split exactly into three bf16 parts, six part products accumulated in FP32 "
+                       "(FP32 error class); the rest FP32"
+                       if args.matrix_path == "auto" else "FP32 throughout (FP32 matrix cores and vector units)"),
         "data": "synthetic (seeded random tables and queries of the workload's shapes)",
         "config": {"workload": WORKLOAD_DESC[args.workload], "name": args.workload,
                    "queries_per_step": p.n_queries, "scored_rows_per_step": p.rows, "k": p.w.k,

@@ -141,6 +141,21 @@ def test_dense_validation():
         kgq.lib().kgq_dense(e.h, x.ctypes.data, 4, 8, x.ctypes.data, 0, 4, 1, x.ctypes.data, 0))) == NO_DEV
 
 
+def test_dense_path_selection():
+    """kgq_set_dense_path takes the three paths and refuses others; a layer on
+    a validation-only handle still reports that there is no device."""
+    e = dry()
+    for path in (kgq.DENSE_AUTO, kgq.DENSE_FP32, kgq.DENSE_BF16X3):
+        e.set_dense_path(path)
+    for bad in (-1, 3, 1 << 20):
+        assert rc_of(lambda: e.set_dense_path(bad)) == INVALID
+    assert rc_of(lambda: e._check(kgq.lib().kgq_set_dense_path(None, 0))) == INVALID
+    x = np.zeros(64, np.float32)
+    e.set_dense_path(kgq.DENSE_BF16X3)
+    assert rc_of(lambda: e._check(
+        kgq.lib().kgq_dense(e.h, x.ctypes.data, 4, 32, x.ctypes.data, 0, 4, 1, x.ctypes.data, 0))) == NO_DEV
+
+
 def plan(model, sids):
     e = dry(model=model, max_batch=max(16, len(sids)))
     return e.describe_plan(sids)
