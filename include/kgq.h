@@ -259,8 +259,10 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
  *     least 1,024 rows and 192 output tiles of 64 x 64, run on the bf16 matrix cores,
  *     each FP32 operand split exactly into three bf16 parts and six of the
  *     nine part products kept (the dropped ones are below 2^-23 of each
- *     product); the others on the FP32 matrix cores. Inputs must be finite
- *     and below 3.39e38 in magnitude on the bf16 path.
+ *     product); smaller layers of an execute whose K is a multiple of 32
+ *     split K there; the others (K not a multiple of 32, and kgq_dense
+ *     layers below the bounds) on the FP32 matrix cores. Inputs must be
+ *     finite and below 3.39e38 in magnitude on the bf16 path.
  *     BetaE scores on the bf16 path when 2d is a multiple of 32.
  *   KGQ_DENSE_FP32: every layer and the BetaE scorer on the FP32 matrix cores.
  *   KGQ_DENSE_BF16X3: every layer whose K is a multiple of 32 on the bf16

@@ -175,6 +175,34 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn,
     }
 }
 
+// Split K on the bf16 matrix cores: each of S workgroups per 64 x 64 tile
+// multiplies a K slice (a multiple of 32) and writes its partial tile;
+// k_gemm_reduce then adds the S partials in slice order (deterministic), the
+// bias and the activation, and stores through the row map.
+__global__ __launch_bounds__(256) void k_gemm_bf16x3_part(GemmArgs g, int kc)
+{
+    using Tile = MfmaTileBf16x3<64, 64>;
+    __shared__ float sm[Tile::SMEM];
+    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+    const int k0 = blockIdx.z * kc;
+    const int kn = min(kc, g.K - k0);
+    v4f acc[Tile::TM][Tile::TN];
+    Tile::run(g.A + k0, g.lda, g.M, g.Wp + k0, (int64_t)g.N * g.K, g.K, g.N, kn, m0, n0, sm, acc);
+    float* part = g.ws + (int64_t)blockIdx.z * g.M * g.N;
+#pragma unroll
+    for (int j = 0; j < Tile::TN; ++j) {
+        const int n = n0 + Tile::col_of(j);
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int i = 0; i < Tile::TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + Tile::row_of(i) + r;
+                if (m < g.M) part[(int64_t)m * g.N + n] = acc[i][j][r];
+            }
+    }
+}
+
 // Whether a layer of this shape runs on the bf16 matrix cores (given the
 // weight planes): K is a multiple of the 32-wide stage, A's rows are 16-byte
 // aligned, and (unless forced) the layer has at least 1,024 rows and 192
@@ -220,6 +248,21 @@ void launch_gemm(const GemmArgs& g, hipStream_t s)
     }
     const int tn = (g.N + 63) / 64, tm = (g.M + 63) / 64;
     const int tiles = tn * tm;
+    // smaller layers with the weight planes: split K on the bf16 matrix
+    // cores, about 1.5 workgroups per compute unit, slices of at least two
+    // 32-wide stages
+    if (g.Wp && g.ws && g.K >= 64 && g.K % 32 == 0 && g.lda % 4 == 0) {
+        int sb = std::min({16, (384 + tiles - 1) / tiles, g.K / 64});
+        while (sb > 1 && (int64_t)sb * g.M * g.N > g.ws_elems) --sb;
+        if (sb > 1) {
+            const int kc = (((g.K + sb - 1) / sb) + 31) / 32 * 32;
+            const int z = (g.K + kc - 1) / kc;
+            hipLaunchKernelGGL(k_gemm_bf16x3_part, dim3(tn, tm, z), dim3(256), 0, s, g, kc);
+            const int64_t total = (int64_t)g.M * g.N;
+            hipLaunchKernelGGL(k_gemm_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, g, z);
+            return;
+        }
+    }
     // split K when the tiles alone leave most of the chip idle, keeping at
     // least two stages (64 of K) per slice
     int splits = 1;
