@@ -256,7 +256,8 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
  * BetaE's scoring contraction (the regrouped KL of Eq. 3's embeddings). Both
  * paths compute in FP32 precision class:
  *   KGQ_DENSE_AUTO (the default): layers whose K is a multiple of 32, with at
- *     least 1,024 rows and 192 output tiles of 64 x 64, run on the bf16 matrix cores,
+ *     least 384 output tiles of 64 x 64, or 1,024 rows and 192 such tiles, run
+ *     on the bf16 matrix cores,
  *     each FP32 operand split exactly into three bf16 parts and six of the
  *     nine part products kept (the dropped ones are below 2^-23 of each
  *     product); smaller layers of an execute whose K is a multiple of 32

@@ -205,15 +205,17 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3_part(GemmArgs g, int kc)
 
 // Whether a layer of this shape runs on the bf16 matrix cores (given the
 // weight planes): K is a multiple of the 32-wide stage, A's rows are 16-byte
-// aligned, and (unless forced) the layer has at least 1,024 rows and 192
-// output tiles of 64 x 64. Below that the FP32 path, with its split-K mode,
-// measured as fast or faster (512 x 1,600 layers, 200 tiles: 21.5 and
-// 36.3 us against 22.4 and 40.2 us; 1,024 x 800 x 1,600, 208 tiles: bf16
-// 34.2 us against 37.5 us).
+// aligned, and (unless forced) the layer has at least 384 output tiles of
+// 64 x 64 (1.5 per compute unit), or 1,024 rows and 192 tiles. Fewer rows on
+// fewer tiles lost to the FP32 loop as a whole-K tile loop (512 x 1,600
+// layers, 200 tiles: 21.5 and 36.3 us against 22.4 and 40.2 us; 1,024 x
+// 800 x 1,600, 208 tiles: bf16 34.2 us against 37.5 us); launch_gemm splits
+// their K on the bf16 path when it has a workspace.
 bool gemm_shape_takes_bf16x3(int M, int N, int K, int64_t lda, bool always)
 {
     if (M <= 0 || N <= 0 || K < 32 || K % 32 != 0 || lda % 4 != 0) return false;
-    return always || (M >= 1024 && (int64_t)((M + 63) / 64) * ((N + 63) / 64) >= 192);
+    const int64_t tiles = (int64_t)((M + 63) / 64) * ((N + 63) / 64);
+    return always || tiles >= 384 || (M >= 1024 && tiles >= 192);
 }
 
 static bool use_bf16x3(const GemmArgs& g)
