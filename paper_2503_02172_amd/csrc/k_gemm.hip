@@ -155,7 +155,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn,
     const int mt = L / tn, nt = L - mt * tn;
     const int m0 = mt * BM, n0 = nt * BN;
     v4f acc[Tile::TM][Tile::TN];
-    Tile::run(g.A, g.lda, g.M, g.Wp, (int64_t)g.N * g.K, g.K, g.N, g.K, m0, n0, sm, acc);
+    Tile::run(g.A, g.lda, g.M, g.M, g.Wp, (int64_t)g.N * g.K, g.K, g.N, g.K, m0, n0, sm, acc);
 
 #pragma unroll
     for (int j = 0; j < Tile::TN; ++j) {
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3_part(GemmArgs g, int kc)
     const int k0 = blockIdx.z * kc;
     const int kn = min(kc, g.K - k0);
     v4f acc[Tile::TM][Tile::TN];
-    Tile::run(g.A + k0, g.lda, g.M, g.Wp + k0, (int64_t)g.N * g.K, g.K, g.N, kn, m0, n0, sm, acc);
+    Tile::run(g.A + k0, g.lda, g.M, g.M, g.Wp + k0, (int64_t)g.N * g.K, g.K, g.N, kn, m0, n0, sm, acc);
     float* part = g.ws + (int64_t)blockIdx.z * g.M * g.N;
 #pragma unroll
     for (int j = 0; j < Tile::TN; ++j) {

@@ -68,8 +68,8 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     const int n_ent_pad = (int)(a.n_blocks * kEntBlock);
     v4f acc[KlTile::TM][KlTile::TN];
     if constexpr (KlTile::kBf16x3)
-        KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent_planes, (int64_t)n_ent_pad * K, K, n_ent_pad, K, m0, n0, sm,
-                    acc);
+        KlTile::run(a.qpack, K, n_mt * KL_BM, a.n_rows, a.ent_planes, (int64_t)n_ent_pad * K, K, n_ent_pad, K, m0,
+                    n0, sm, acc);
     else
         KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent, K, n_ent_pad, K, m0, n0, sm, acc);
 

@@ -399,10 +399,13 @@ struct MfmaTileBf16x3 {
     __device__ static int bswz(int row) { return (row >> 1) & 3; }
 
     // acc = A[m0 : m0 + BM, :K] . B[n0 : n0 + BN, :K]^T; B's planes are
-    // Bp, Bp + plane, Bp + 2 plane (row stride ldb elements).
-    __device__ static void run(const float* __restrict__ A, int64_t lda, int M, const uint16_t* __restrict__ Bp,
-                               int64_t plane, int64_t ldb, int N, int K, int m0, int n0, float* sm_f,
-                               v4f (&acc)[TM][TN])
+    // Bp, Bp + plane, Bp + 2 plane (row stride ldb elements). A's rows are
+    // read up to M - 1; a wavefront whose rows all lie at or past live_rows
+    // (output rows the caller drops) takes its share of the loads and the
+    // barriers but no products, and its acc stays zero.
+    __device__ static void run(const float* __restrict__ A, int64_t lda, int M, int live_rows,
+                               const uint16_t* __restrict__ Bp, int64_t plane, int64_t ldb, int N, int K, int m0,
+                               int n0, float* sm_f, v4f (&acc)[TM][TN])
     {
         char* sm = reinterpret_cast<char*>(sm_f);
         const int nk = K / BK;
@@ -504,11 +507,18 @@ struct MfmaTileBf16x3 {
         // loads only: the caller has no vector-memory load outstanding on
         // entry, and at the wait stage kt's are the only ones in flight.
         issue(0, 0);
-        for (int kt = 0; kt < nk; ++kt) {
-            wait_vm_barrier<0>();
-            if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
-            read_split(kt & 1);
-            products();
+        if (m0 + wm * (BM / WM) < live_rows) {
+            for (int kt = 0; kt < nk; ++kt) {
+                wait_vm_barrier<0>();
+                if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+                read_split(kt & 1);
+                products();
+            }
+        } else {
+            for (int kt = 0; kt < nk; ++kt) {
+                wait_vm_barrier<0>();
+                if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+            }
         }
     }
 
