@@ -612,7 +612,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
-        "arithmetic": ("dense contractions (BetaE scorer, MLP layers of 256+ output tiles) on the bf16 matrix cores: "
+        "arithmetic": ("dense contractions (BetaE scorer, MLP layers) on the bf16 matrix cores: "
                        "each FP32 operand split exactly into three bf16 parts, six part products accumulated in FP32 "
                        "(FP32 error class); the rest FP32"
                        if args.matrix_path == "auto" else "FP32 throughout (FP32 matrix cores and vector units)"),

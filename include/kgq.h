@@ -255,19 +255,19 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
  * MLPs of Eq. 4 and of the intersection operators, and kgq_dense) and
  * BetaE's scoring contraction (the regrouped KL of Eq. 3's embeddings). Both
  * paths compute in FP32 precision class:
- *   KGQ_DENSE_AUTO (the default): layers whose K is a multiple of 32, with at
- *     least 384 output tiles of 64 x 64, or 1,024 rows and 192 such tiles, run
- *     on the bf16 matrix cores,
- *     each FP32 operand split exactly into three bf16 parts and six of the
- *     nine part products kept (the dropped ones are below 2^-23 of each
- *     product); smaller layers of an execute whose K is a multiple of 32
- *     split K there; the others (K not a multiple of 32, and kgq_dense
- *     layers below the bounds) on the FP32 matrix cores. Inputs must be
- *     finite and below 3.39e38 in magnitude on the bf16 path.
+ *   KGQ_DENSE_AUTO (the default): layers with K >= 32 (K is a multiple of 4
+ *     on every path) and at least 384 output tiles of 64 x 64, or 1,024 rows
+ *     and 192 such tiles, run on the bf16 matrix cores, each FP32 operand
+ *     split exactly into three bf16 parts and six of the nine part products
+ *     kept (the dropped ones are below 2^-23 of each product; the weight
+ *     parts are zero-padded to a multiple of 32 columns); smaller layers of
+ *     an execute with K >= 64 split K there; the others (K < 32, and
+ *     kgq_dense layers below the bounds) on the FP32 matrix cores. Inputs
+ *     must be finite and below 3.39e38 in magnitude on the bf16 path.
  *     BetaE scores on the bf16 path when 2d is a multiple of 32.
  *   KGQ_DENSE_FP32: every layer and the BetaE scorer on the FP32 matrix cores.
- *   KGQ_DENSE_BF16X3: every layer whose K is a multiple of 32 on the bf16
- *     path, whatever its size (for tests).
+ *   KGQ_DENSE_BF16X3: every layer with K >= 32 on the bf16 path, whatever
+ *     its size (for tests).
  * The bf16 parts of the weights and of BetaE's entity-side scoring rows are
  * made when they are loaded, whatever the path. Takes effect for calls
  * enqueued after it. Errors: INVALID_ARG. */

@@ -124,11 +124,13 @@ __global__ __launch_bounds__(256) void k_gemm_reduce(GemmArgs g, int splits)
 // loaded (launch_split_planes); the inputs A are split in registers as their
 // fragments are read from LDS, so A keeps its FP32 layout and the producers
 // of the layer inputs are unchanged. Epilogue and tile order as in k_gemm.
-__global__ __launch_bounds__(256) void k_split_planes(const float* __restrict__ w, uint16_t* __restrict__ p, int64_t n)
+__global__ __launch_bounds__(256) void k_split_planes(const float* __restrict__ w, uint16_t* __restrict__ p,
+                                                      int64_t cols, int64_t ld, int64_t n)
 {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
-    const float x = w[i];
+    const int64_t row = i / ld, c = i - row * ld;
+    const float x = c < cols ? w[row * cols + c] : 0.f;
     const uint32_t H = pack_bf16_rne(x, 0.f);
     const float r = x - __uint_as_float(H << 16);
     const uint32_t Mm = pack_bf16_rne(r, 0.f);
@@ -138,10 +140,11 @@ __global__ __launch_bounds__(256) void k_split_planes(const float* __restrict__ 
     p[2 * n + i] = (uint16_t)pack_bf16_rne(t, 0.f);
 }
 
-void launch_split_planes(const float* w, uint16_t* p, int64_t n, hipStream_t s)
+void launch_split_planes(const float* w, uint16_t* p, int64_t rows, int64_t cols, hipStream_t s)
 {
+    const int64_t ld = plane_ld(cols), n = rows * ld;
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_split_planes, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, w, p, n);
+    hipLaunchKernelGGL(k_split_planes, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, w, p, cols, ld, n);
 }
 
 template <int BM, int BN>
@@ -155,7 +158,8 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn,
     const int mt = L / tn, nt = L - mt * tn;
     const int m0 = mt * BM, n0 = nt * BN;
     v4f acc[Tile::TM][Tile::TN];
-    Tile::run(g.A, g.lda, g.M, g.M, g.Wp, (int64_t)g.N * g.K, g.K, g.N, g.K, m0, n0, sm, acc);
+    const int64_t ldp = plane_ld(g.K);
+    Tile::run(g.A, g.lda, g.M, g.M, g.Wp, (int64_t)g.N * ldp, ldp, g.N, g.K, m0, n0, sm, acc);
 
 #pragma unroll
     for (int j = 0; j < Tile::TN; ++j) {
@@ -187,7 +191,8 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3_part(GemmArgs g, int kc)
     const int k0 = blockIdx.z * kc;
     const int kn = min(kc, g.K - k0);
     v4f acc[Tile::TM][Tile::TN];
-    Tile::run(g.A + k0, g.lda, g.M, g.M, g.Wp + k0, (int64_t)g.N * g.K, g.K, g.N, kn, m0, n0, sm, acc);
+    const int64_t ldp = plane_ld(g.K);
+    Tile::run(g.A + k0, g.lda, g.M, g.M, g.Wp + k0, (int64_t)g.N * ldp, ldp, g.N, kn, m0, n0, sm, acc);
     float* part = g.ws + (int64_t)blockIdx.z * g.M * g.N;
 #pragma unroll
     for (int j = 0; j < Tile::TN; ++j) {
@@ -204,8 +209,9 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3_part(GemmArgs g, int kc)
 }
 
 // Whether a layer of this shape runs on the bf16 matrix cores (given the
-// weight planes): K is a multiple of the 32-wide stage, A's rows are 16-byte
-// aligned, and (unless forced) the layer has at least 384 output tiles of
+// weight planes): K is a multiple of 4 and at least one 32-wide stage (the
+// planes are zero-padded to a whole stage), A's rows are 16-byte aligned,
+// and (unless forced) the layer has at least 384 output tiles of
 // 64 x 64 (1.5 per compute unit), or 1,024 rows and 192 tiles. Fewer rows on
 // fewer tiles lost to the FP32 loop as a whole-K tile loop (512 x 1,600
 // layers, 200 tiles: 21.5 and 36.3 us against 22.4 and 40.2 us; 1,024 x
@@ -213,7 +219,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3_part(GemmArgs g, int kc)
 // their K on the bf16 path when it has a workspace.
 bool gemm_shape_takes_bf16x3(int M, int N, int K, int64_t lda, bool always)
 {
-    if (M <= 0 || N <= 0 || K < 32 || K % 32 != 0 || lda % 4 != 0) return false;
+    if (M <= 0 || N <= 0 || K < 32 || K % 4 != 0 || lda % 4 != 0) return false;
     const int64_t tiles = (int64_t)((M + 63) / 64) * ((N + 63) / 64);
     return always || tiles >= 384 || (M >= 1024 && tiles >= 192);
 }
@@ -253,7 +259,7 @@ void launch_gemm(const GemmArgs& g, hipStream_t s)
     // smaller layers with the weight planes: split K on the bf16 matrix
     // cores, about 1.5 workgroups per compute unit, slices of at least two
     // 32-wide stages
-    if (g.Wp && g.ws && g.K >= 64 && g.K % 32 == 0 && g.lda % 4 == 0) {
+    if (g.Wp && g.ws && g.K >= 64 && g.K % 4 == 0 && g.lda % 4 == 0) {
         int sb = std::min({16, (384 + tiles - 1) / tiles, g.K / 64});
         while (sb > 1 && (int64_t)sb * g.M * g.N > g.ws_elems) --sb;
         if (sb > 1) {

@@ -178,7 +178,7 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
     using LdsTile = MfmaTileLds<64, 64, 3>;
     using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
     using SplitTile = MfmaTileBf16x3<128, 128>;
-    if (a.ent_planes && SplitTile::supports(2 * a.d)) {
+    if (a.ent_planes && (2 * a.d) % 32 == 0) {   // planes of row stride 2d, whole stages
         launch_tiles<SplitTile>(a, s);
     } else if (LdsTile::supports(2 * a.d)) {
         launch_tiles<LdsTile>(a, s);

@@ -363,19 +363,19 @@ kgq_status allocate_all(kgq_handle* h)
         if (c.model == KGQ_Q2B) ALLOC(h->rel_o_sp, (int64_t)c.n_relations * d);
     }
     // bf16 planes of every dense-layer weight whose K (its columns) the
-    // bf16 matrix-core GEMM takes
+    // bf16 matrix-core GEMM takes, rows padded to whole 32-wide stages
     for (auto& kv : h->specs) {
         const std::string& n = kv.first;
         const bool weight = n.size() > 3 && n[n.size() - 3] == '.' && n[n.size() - 2] == 'w' &&
                             n.back() >= '1' && n.back() <= '3';
-        if (kv.second.entity || !weight || kv.second.cols % 32 != 0) continue;
+        if (kv.second.entity || !weight || kv.second.cols % 4 != 0 || kv.second.cols < 32) continue;
         uint16_t* planes = nullptr;
-        ALLOC(planes, 3 * kv.second.rows * kv.second.cols);
+        ALLOC(planes, 3 * kv.second.rows * plane_ld(kv.second.cols));
         h->wplanes[h->dparam.at(n)] = planes;
     }
-    if (h->int_cat_w && (2 * d) % 32 == 0) {
+    if (h->int_cat_w && (2 * d) % 4 == 0 && 2 * d >= 32) {
         uint16_t* planes = nullptr;
-        ALLOC(planes, 3 * 4 * d * d);
+        ALLOC(planes, 3 * 2 * d * plane_ld(2 * d));
         h->wplanes[h->int_cat_w] = planes;
     }
     h->bytes_params = h->bytes_total;   // everything after this is execute scratch
@@ -1229,15 +1229,15 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
             HIP_TRY(h, hipGetLastError());
             HIP_TRY(h, hipStreamSynchronize(nullptr));
         }
-        auto split = [&](const float* w, int64_t n) -> kgq_status {
+        auto split = [&](const float* w, int64_t rows, int64_t cols) -> kgq_status {
             auto pl = h->wplanes.find(w);
             if (pl == h->wplanes.end()) return KGQ_OK;
-            launch_split_planes(w, pl->second, n, nullptr);
+            launch_split_planes(w, pl->second, rows, cols, nullptr);
             HIP_TRY(h, hipGetLastError());
             HIP_TRY(h, hipStreamSynchronize(nullptr));
             return KGQ_OK;
         };
-        kgq_status st = split(dst, ps.rows * ps.cols);
+        kgq_status st = split(dst, ps.rows, ps.cols);
         if (st != KGQ_OK) return st;
         if (c.model == KGQ_CONE) {
             // the two set functions' first layers, stacked for one GEMM
@@ -1246,7 +1246,7 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
             if (!std::strcmp(name, "inter.arg.w1"))
                 HIP_TRY(h, hipMemcpy(h->int_cat_w + half_w, dst, nbytes, hipMemcpyDeviceToDevice));
             if (!std::strcmp(name, "inter.axis.w1") || !std::strcmp(name, "inter.arg.w1"))
-                if ((st = split(h->int_cat_w, 4 * (int64_t)c.dim * c.dim)) != KGQ_OK) return st;
+                if ((st = split(h->int_cat_w, 2 * (int64_t)c.dim, 2 * (int64_t)c.dim)) != KGQ_OK) return st;
             if (!std::strcmp(name, "inter.axis.b1")) HIP_TRY(h, hipMemcpy(h->int_cat_b, dst, nbytes, hipMemcpyDeviceToDevice));
             if (!std::strcmp(name, "inter.arg.b1"))
                 HIP_TRY(h, hipMemcpy(h->int_cat_b + half_b, dst, nbytes, hipMemcpyDeviceToDevice));
@@ -1269,7 +1269,7 @@ kgq_status kgq_load_params(kgq_handle* h, const char* name, const void* src, siz
             launch_betae_entity_prep(stage, bf16, c.n_entities, c.dim, h->n_blocks, h->ent_rm, h->ent_blk,
                                      h->ent_const, nullptr);
             if (h->ent_planes)
-                launch_split_planes(h->ent_blk, h->ent_planes, h->n_blocks * kEntBlock * 2 * c.dim, nullptr);
+                launch_split_planes(h->ent_blk, h->ent_planes, h->n_blocks * kEntBlock, 2 * (int64_t)c.dim, nullptr);
         }
         else if (c.model == KGQ_CONE)
             launch_cone_entity_prep(static_cast<const float*>(stage), c.n_entities, c.dim, h->n_blocks, h->ent_rm,
@@ -1426,8 +1426,8 @@ kgq_status kgq_dense(kgq_handle* h, const float* x, int32_t M, int32_t K, const 
     uint16_t* planes = nullptr;
     g.bf16x3_always = h->dense_path == KGQ_DENSE_BF16X3;
     if (h->dense_path != KGQ_DENSE_FP32 && gemm_shape_takes_bf16x3(M, N, K, K, g.bf16x3_always)) {
-        HIP_TRY(h, hipMallocAsync((void**)&planes, (size_t)3 * N * K * sizeof(uint16_t), s));
-        launch_split_planes(w, planes, (int64_t)N * K, s);
+        HIP_TRY(h, hipMallocAsync((void**)&planes, (size_t)3 * N * plane_ld(K) * sizeof(uint16_t), s));
+        launch_split_planes(w, planes, N, K, s);
         g.Wp = planes;
     }
     {

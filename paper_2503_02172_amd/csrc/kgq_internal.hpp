@@ -97,11 +97,11 @@ struct GemmArgs {
     float* ws = nullptr;               // split-K partials for small M (nullptr: never split)
     int64_t ws_elems = 0;
     int epi_split = 0;                 // EPI_CONE_ANGLES: first column of the second map
-    // W split into three bf16 planes (launch_split_planes: [3][N][K], row
-    // stride K) or nullptr. With the planes, K a multiple of 32 and enough
-    // output tiles to fill the chip, the layer runs on the bf16 matrix cores
-    // with FP32 accuracy (k_gemm_bf16x3); bf16x3_always takes that path
-    // whenever K allows it.
+    // W split into three bf16 planes (launch_split_planes: [3][N][plane_ld(K)],
+    // zero past K) or nullptr. With the planes, K >= 32 and enough output
+    // tiles to fill the chip, the layer runs on the bf16 matrix cores with
+    // FP32 accuracy (k_gemm_bf16x3); bf16x3_always takes that path whenever
+    // K allows it.
     const uint16_t* Wp = nullptr;
     bool bf16x3_always = false;
 };
@@ -109,9 +109,13 @@ void launch_gemm(const GemmArgs& g, hipStream_t s);
 // Whether launch_gemm, given weight planes, runs a layer of this shape on
 // the bf16 matrix cores.
 bool gemm_shape_takes_bf16x3(int M, int N, int K, int64_t lda, bool always);
-// W [n floats] -> three bf16 planes p[0..n), p[n..2n), p[2n..3n) with
+// Row stride of the bf16 planes of a [rows x cols] matrix: cols rounded up
+// to the 32-wide stage of the bf16 tile loop.
+__host__ __device__ inline int64_t plane_ld(int64_t cols) { return (cols + 31) / 32 * 32; }
+// W [rows x cols] -> three bf16 planes, plane q at p + q * rows * ld with
+// ld = plane_ld(cols), row r at r * ld, zeros in columns cols .. ld - 1;
 // w = p0 + p1 + p2 exactly (round to nearest even at each step).
-void launch_split_planes(const float* w, uint16_t* p, int64_t n, hipStream_t s);
+void launch_split_planes(const float* w, uint16_t* p, int64_t rows, int64_t cols, hipStream_t s);
 
 // Epilogue value of output column n.
 __device__ __forceinline__ float apply_epilogue(int epi, int split, int n, float v)

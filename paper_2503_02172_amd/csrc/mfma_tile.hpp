@@ -394,33 +394,45 @@ struct MfmaTileBf16x3 {
                   "tile shape");
     static_assert(2 * STAGE <= 160 * 1024, "LDS");   // above 64 KiB only as dynamic LDS
 
-    static bool supports(int K) { return K >= BK && K % BK == 0; }
+    // K a multiple of 4 of at least one stage; when K is not a multiple of 32
+    // the B planes must hold zeros from K to the next multiple of 32 (their
+    // rows padded to it), and the last stage's A chunks past K re-read the
+    // previous stage's (finite values, multiplied by those zeros)
+    static bool supports(int K) { return K >= BK && K % 4 == 0; }
     __device__ static int aswz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
     __device__ static int bswz(int row) { return (row >> 1) & 3; }
 
     // acc = A[m0 : m0 + BM, :K] . B[n0 : n0 + BN, :K]^T; B's planes are
-    // Bp, Bp + plane, Bp + 2 plane (row stride ldb elements). A's rows are
-    // read up to M - 1; a wavefront whose rows all lie at or past live_rows
-    // (output rows the caller drops) takes its share of the loads and the
-    // barriers but no products, and its acc stays zero.
+    // Bp, Bp + plane, Bp + 2 plane (row stride ldb elements, zero-padded
+    // past K as above). A's rows are read up to M - 1; a wavefront whose rows
+    // all lie at or past live_rows (output rows the caller drops) takes its
+    // share of the loads and the barriers but no products, and its acc stays
+    // zero.
     __device__ static void run(const float* __restrict__ A, int64_t lda, int M, int live_rows,
                                const uint16_t* __restrict__ Bp, int64_t plane, int64_t ldb, int N, int K, int m0,
                                int n0, float* sm_f, v4f (&acc)[TM][TN])
     {
         char* sm = reinterpret_cast<char*>(sm_f);
-        const int nk = K / BK;
+        const int nk = (K + BK - 1) / BK;
         const int tid = threadIdx.x, lane = tid & 63;
         const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
         const int wm = wave / WN, wn = wave % WN;
         const int grp = lane >> 4, li = lane & 15;
 
         // A: load instruction t = h * 4 + wave writes rows 8t .. 8t + 7
-        // (1 KiB); lane l lands at row 8t + l / 8, chunk position l % 8
+        // (1 KiB); lane l lands at row 8t + l / 8, chunk position l % 8.
+        // With K not a multiple of 32, a lane whose chunk of the last stage
+        // starts at or past K reads the chunk one stage back: inside the row,
+        // since K >= 32, or the caller's A starts at least a stage into it.
         const float* ag[AI];
+        bool past[AI];
+        const int k_last = (nk - 1) * BK;
 #pragma unroll
         for (int h = 0; h < AI; ++h) {
             const int row = (h * 4 + wave) * 8 + (lane >> 3);
-            ag[h] = A + (int64_t)min(m0 + row, M - 1) * lda + ((lane & 7) ^ aswz(row)) * 4;
+            const int chunk = (lane & 7) ^ aswz(row);
+            ag[h] = A + (int64_t)min(m0 + row, M - 1) * lda + chunk * 4;
+            past[h] = k_last + chunk * 4 >= K;
         }
         // B: load instruction u = h * 4 + wave writes plane u / (BN / 16),
         // rows 16 (u % (BN / 16)) .. + 15; lane l lands at row + l / 4,
@@ -437,9 +449,10 @@ struct MfmaTileBf16x3 {
         }
         auto issue = [&](int kt, int slot) {
             char* st = sm + slot * STAGE;
+            const bool tail = kt == nk - 1 && (K % BK) != 0;
 #pragma unroll
             for (int h = 0; h < AI; ++h)
-                __builtin_amdgcn_global_load_lds((const void*)(ag[h] + kt * BK),
+                __builtin_amdgcn_global_load_lds((const void*)(ag[h] + (kt - (tail && past[h] ? 1 : 0)) * BK),
                                                  (lds_void*)(st + (h * 4 + wave) * 8 * AROW), 16, 0, 0);
 #pragma unroll
             for (int h = 0; h < BI; ++h)

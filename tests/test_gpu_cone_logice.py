@@ -85,22 +85,24 @@ def test_gpu_cone_logice_every_structure(model, n_ent, dim, B):
     assert amb <= 2, amb
 
 
+@pytest.mark.parametrize("dim", [32, 40])
 @pytest.mark.parametrize("model", [O.CONE, O.LOGICE], ids=["cone", "logice"])
-def test_gpu_cone_logice_dense_bf16x3(model):
-    """Every dense layer whose K is a multiple of 32 forced onto the bf16
-    matrix-core path (d = 32: all of ConE's, LogicE's second and third
-    projection layers; LogicE's first layer, K = 3d = 96, too): every
-    structure and a mixed batch."""
+def test_gpu_cone_logice_dense_bf16x3(model, dim):
+    """Every dense layer forced onto the bf16 matrix-core path: every
+    structure and a mixed batch. d = 32: every K a multiple of 32. d = 40:
+    ConE's set-function layers (K = 80, 40) and LogicE's first projection
+    layer (K = 3d = 120) end in a partial stage against zero-padded weight
+    planes."""
     import torch
     from paper_2503_02172_amd import kgq
-    w = synth.make_tiny(model, n_ent=70, n_rel=7, dim=32, seed=730 + model)
+    w = synth.make_tiny(model, n_ent=70, n_rel=7, dim=dim, seed=730 + model)
     m = _oracle(w, model)
     amb = 0
     with kgq.engine_for(w, max_batch=64) as eng:
         eng.set_dense_path(kgq.DENSE_BF16X3)
         for s in ALL:
             name = synth.STRUCTURES[s]
-            print(f"[bf16x3] model={model} structure={name}", flush=True)
+            print(f"[bf16x3] model={model} d={dim} structure={name}", flush=True)
             qb = synth.draw_queries(name, 37, 70, 7, seed=1730 + s)
             out = eng.execute(s, qb.anchors, qb.relations, k=5, scores=True)
             torch.cuda.synchronize()

@@ -171,11 +171,17 @@ def test_gpu_deterministic_and_stream():
                                        (3, 400, 400, 1),
                                        # bf16 path: one or two stages, ragged tiles, 64 x 128 tiles
                                        (65, 70, 32, 1), (200, 33, 64, 0), (129, 127, 96, 2),
-                                       (1100, 800, 800, 1), (4100, 1100, 160, 0), (4097, 1030, 1600, 1)])
+                                       (1100, 800, 800, 1), (4100, 1100, 160, 0), (4097, 1030, 1600, 1),
+                                       # bf16 path, K not a multiple of 32: a last stage of 4, 16 or 8
+                                       # columns against zero-padded weight planes (64 x 64 and
+                                       # 128 x 64 tiles)
+                                       (65, 70, 36, 1), (129, 127, 48, 0), (1100, 800, 400, 1),
+                                       (300, 1600, 1200, 1), (4100, 1100, 400, 0), (2050, 1030, 1000, 2)])
 def test_gpu_dense_matches_fp64(M, N, K, act, path):
     """One dense layer against an fp64 matmul on each path: automatic choice,
-    FP32 matrix cores only, and the bf16 path wherever K is a multiple of 32
-    (x split into three bf16 parts in registers, w when the layer is set up)."""
+    FP32 matrix cores only, and the bf16 path wherever K allows it (a
+    multiple of 4, at least 32; x split into three bf16 parts in registers,
+    w into zero-padded planes when the layer is set up)."""
     import torch
     from paper_2503_02172_amd import kgq
     rng = np.random.default_rng(M * 7 + N)

@@ -101,21 +101,24 @@ def test_gpu_small_form_switch(model, B):
     eng.close()
 
 
+@pytest.mark.parametrize("dim", [32, 40])
 @pytest.mark.parametrize("model", [O.GQE, O.Q2B, O.BETAE], ids=["gqe", "q2b", "betae"])
-def test_gpu_tiny_dense_bf16x3(model):
+def test_gpu_tiny_dense_bf16x3(model, dim):
     """Every dense layer forced onto the bf16 matrix-core path (weights and
     inputs split into three bf16 parts, six part products): every structure,
-    then a mixed batch, at d = 32 so that every layer's K is a multiple of 32,
-    with 70 entities (a ragged entity tile) and 37 queries (ragged row tiles)."""
+    then a mixed batch, at d = 32 (every layer's K a multiple of 32) and
+    d = 40 (K = 40 or 80: a last stage of 8 or 16 columns against
+    zero-padded weight planes), with 70 entities (a ragged entity tile) and
+    37 queries (ragged row tiles)."""
     from paper_2503_02172_amd import kgq
-    w = synth.make_tiny(model, n_ent=70, n_rel=7, dim=32, seed=130 + model)
+    w = synth.make_tiny(model, n_ent=70, n_rel=7, dim=dim, seed=130 + model)
     m = O.Model(model, w.params, w.gamma)
     eng = _engine(w)
     eng.set_dense_path(kgq.DENSE_BF16X3)
     structures = EPFO if model != O.BETAE else ALL
     for s in structures:
         name = synth.STRUCTURES[s]
-        print(f"[bf16x3] model={model} structure={name}", flush=True)
+        print(f"[bf16x3] model={model} d={dim} structure={name}", flush=True)
         qb = synth.draw_queries(name, 37, 70, 7, seed=1300 + s)
         _run_and_check(eng, w, m, s, qb.anchors, qb.relations, 5)
     qb = synth.draw_mixed([synth.STRUCTURES[s] for s in structures], 53, 70, 7, seed=1399)
