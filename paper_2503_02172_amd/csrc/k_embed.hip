@@ -93,20 +93,28 @@ __device__ __forceinline__ double lngamma_stirling(double x)
 }
 
 // ln B(a, b) = ln Gamma(a) + ln Gamma(b) - ln Gamma(a + b) in double
-// precision. Each argument below 8 is shifted up with
+// precision for a, b > 0. Each argument below 8 is shifted up with
 // ln Gamma(x) = ln Gamma(x + 1) - ln x, and the three products of the shifted
 // factors share one logarithm (at most 8 factors each, all in (0, 8), so the
-// products of fp32-sourced arguments stay within double range). Arguments
-// that are not positive (never produced by the BetaE regulariser) take the
-// library lgamma.
-__device__ __forceinline__ double lnbeta_d(double a, double b)
+// products of fp32-sourced arguments stay within double range). Other
+// arguments give NaN: the Beta distribution needs positive shape parameters.
+__device__ __forceinline__ double lnbeta_pos(double a, double b)
 {
-    if (!(a > 0.0 && b > 0.0)) return lgamma(a) + lgamma(b) - lgamma(a + b);
+    if (!(a > 0.0 && b > 0.0)) return __builtin_nan("");
     double c = a + b, pa = 1.0, pb = 1.0, pc = 1.0;
     while (a < 8.0) { pa *= a; a += 1.0; }
     while (b < 8.0) { pb *= b; b += 1.0; }
     while (c < 8.0) { pc *= c; c += 1.0; }
     return lngamma_stirling(a) + lngamma_stirling(b) - lngamma_stirling(c) - log((pa / pc) * pb);
+}
+
+// The same for any arguments: those that are not positive take the library
+// lgamma (for the entity table as loaded; the scored query states are
+// regulariser outputs or their reciprocals, always positive).
+__device__ __forceinline__ double lnbeta_d(double a, double b)
+{
+    if (!(a > 0.0 && b > 0.0)) return lgamma(a) + lgamma(b) - lgamma(a + b);
+    return lnbeta_pos(a, b);
 }
 
 // BetaE entity tables: alpha|beta decoded to fp32 (row-major, for anchor
@@ -565,7 +573,9 @@ __global__ __launch_bounds__(256) void k_pack(const int32_t* src_row, const int3
 
 // BetaE: the query rows row-major, [row][alpha (d) | beta (d)], the A operand
 // of the matrix-core scorer, and C_q = sum_i lnB(alpha_i, beta_i) per row in
-// double precision. A negated answer row (neg[j] != 0) is packed as the
+// double precision (rows are regulariser outputs or their reciprocals, so
+// positive; lnbeta_pos keeps the kernel at 45 VGPRs where the library lgamma
+// fallback took 176). A negated answer row (neg[j] != 0) is packed as the
 // reciprocals of its shape parameters. One workgroup per row; padding rows
 // are zero with C_q = 0.
 __global__ __launch_bounds__(256) void k_pack_rows(const int32_t* src_row, const int32_t* neg, int n_rows,
@@ -592,7 +602,7 @@ __global__ __launch_bounds__(256) void k_pack_rows(const int32_t* src_row, const
                 bf = 1.0f / bf;
             }
             const double a = af, b = bf;
-            lnb += lnbeta_d(a, b);
+            lnb += lnbeta_pos(a, b);
         }
     }
     for (int off = 32; off > 0; off >>= 1) lnb += __shfl_xor(lnb, off, 64);
