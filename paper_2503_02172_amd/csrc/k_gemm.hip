@@ -150,7 +150,7 @@ void launch_split_planes(const float* w, uint16_t* p, int64_t rows, int64_t cols
 template <int BM, int BN>
 __global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn, int per_xcd)
 {
-    using Tile = MfmaTileBf16x3<BM, BN>;
+    using Tile = MfmaTileBf16x3<BM, BN, 4, BM == 64>;   // raised read priority: see the tile
     __shared__ float sm[Tile::SMEM];
     const int b = blockIdx.x;
     const int L = (b & 7) * per_xcd + (b >> 3);
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn,
 // bias and the activation, and stores through the row map.
 __global__ __launch_bounds__(256) void k_gemm_bf16x3_part(GemmArgs g, int kc)
 {
-    using Tile = MfmaTileBf16x3<64, 64>;
+    using Tile = MfmaTileBf16x3<64, 64, 4, true>;
     __shared__ float sm[Tile::SMEM];
     const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
     const int k0 = blockIdx.z * kc;

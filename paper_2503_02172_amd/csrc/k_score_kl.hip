@@ -16,9 +16,10 @@
 // have been split into three bf16 planes at load, the contraction runs on
 // v_mfma_f32_16x16x32_bf16 with the query rows split in registers and six
 // part products kept: FP32 accuracy at 0.375 of the FP32 matrix-core time per
-// k range (MfmaTileBf16x3 with 128-row x 128-entity tiles and 4 x 1
-// wavefronts, an 80 KiB LDS ring; 1.66x faster than the FP32 loop at the
-// 63,361-entity workload, and 6% faster than 128 x 64 tiles).
+// k range (MfmaTileBf16x3 with 128-row x 128-entity tiles, 4 x 1
+// wavefronts and raised issue priority while fragments are read and split,
+// an 80 KiB LDS ring; 1.7x faster than the FP32 loop at the 63,361-entity
+// workload, and 6% faster than 128 x 64 tiles).
 // Otherwise 64-row x 64-entity tiles, 2 x 2 MFMA tiles of 16 x 16 per
 // wavefront, on v_mfma_f32_16x16x4_f32 with full FP32 inputs: through the
 // direct-to-LDS ring of three stages when 2d is a multiple of 16 (measured
@@ -177,7 +178,7 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
     if (a.n_rows <= 0) return;
     using LdsTile = MfmaTileLds<64, 64, 3>;
     using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
-    using SplitTile = MfmaTileBf16x3<128, 128>;
+    using SplitTile = MfmaTileBf16x3<128, 128, 4, true>;
     if (a.ent_planes && (2 * a.d) % 32 == 0) {   // planes of row stride 2d, whole stages
         launch_tiles<SplitTile>(a, s);
     } else if (LdsTile::supports(2 * a.d)) {
