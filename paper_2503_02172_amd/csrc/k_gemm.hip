@@ -257,8 +257,8 @@ void launch_gemm(const GemmArgs& g, hipStream_t s)
     const int tn = (g.N + 63) / 64, tm = (g.M + 63) / 64;
     const int tiles = tn * tm;
     // smaller layers with the weight planes: split K on the bf16 matrix
-    // cores, about 1.5 workgroups per compute unit, slices of at least two
-    // 32-wide stages
+    // cores, about 1.5 workgroups per compute unit, slices of whole 32-wide
+    // stages, at least two (the last slice ends at K, which may cut it short)
     if (g.Wp && g.ws && g.K >= 64 && g.K % 4 == 0 && g.lda % 4 == 0) {
         int sb = std::min({16, (384 + tiles - 1) / tiles, g.K / 64});
         while (sb > 1 && (int64_t)sb * g.M * g.N > g.ws_elems) --sb;
