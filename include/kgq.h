@@ -264,10 +264,14 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
  *     an execute with K >= 64 split K there; the others (K < 32, and
  *     kgq_dense layers below the bounds) on the FP32 matrix cores. Inputs
  *     must be finite and below 3.39e38 in magnitude on the bf16 path.
- *     BetaE scores on the bf16 path when 2d is a multiple of 32.
+ *     BetaE scores on the bf16 path when 2d is a multiple of 32 and the call
+ *     scores more than 64 rows (more than 128 when 128-row tiles would give
+ *     fewer than 256 workgroups); smaller calls score on the FP32 matrix
+ *     cores.
  *   KGQ_DENSE_FP32: every layer and the BetaE scorer on the FP32 matrix cores.
- *   KGQ_DENSE_BF16X3: every layer with K >= 32 on the bf16 path, whatever
- *     its size (for tests).
+ *   KGQ_DENSE_BF16X3: every layer with K >= 32, and the BetaE scorer when
+ *     2d is a multiple of 32, on the bf16 path, whatever the size (for
+ *     tests).
  * The bf16 parts of the weights and of BetaE's entity-side scoring rows are
  * made when they are loaded, whatever the path. Takes effect for calls
  * enqueued after it. Errors: INVALID_ARG. */

@@ -173,13 +173,26 @@ static void launch_tiles(const ScoreArgs& a, hipStream_t s)
                        per_xcd);
 }
 
+constexpr int kScoreKlFp32Rows = 64;   // scored rows up to which the FP32 tile runs
+
 void launch_score_kl(const ScoreArgs& a, hipStream_t s)
 {
     if (a.n_rows <= 0) return;
     using LdsTile = MfmaTileLds<64, 64, 3>;
     using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
     using SplitTile = MfmaTileBf16x3<128, 128, 4, true>;
-    if (a.ent_planes && (2 * a.d) % 32 == 0) {   // planes of row stride 2d, whole stages
+    // The bf16 split tile pays from 65 scored rows on: at fewer, its
+    // 128-row tile is mostly padding and its entity-tile grid too small to
+    // fill the chip (B = 1: 142 us per 1p query at 63,361 entities, 92 us at
+    // 14,505, against 131 and 77 us on the FP32 64 x 64 tile). Up to 128
+    // rows it also needs a workgroup per compute unit (96 rows at 14,505
+    // entities, 114 tiles: 1.12 against 1.04 us per query); from 129 rows
+    // it wins with fewer (160 and 240 rows at 14,505: 0.71 and 0.50 against
+    // 0.74 and 0.57 us per query).
+    const int64_t split_tiles = (int64_t)((a.n_rows + 127) / 128) * ((a.N + 127) / 128);
+    const bool split_pays =
+        a.split_always || (a.n_rows > kScoreKlFp32Rows && (a.n_rows > 128 || split_tiles >= 256));
+    if (a.ent_planes && (2 * a.d) % 32 == 0 && split_pays) {   // planes: row stride 2d
         launch_tiles<SplitTile>(a, s);
     } else if (LdsTile::supports(2 * a.d)) {
         launch_tiles<LdsTile>(a, s);

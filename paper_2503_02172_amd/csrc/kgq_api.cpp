@@ -773,6 +773,7 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
                     p.n_quad_rows, p.n_pair_rows, d_score, N, h->n_blocks, c.gamma, c.center_reg, dst, N};
         a.dist_scale = logice ? 1.0f / (float)(2 * d) : cone ? h->cone_modulus : 1.0f;
         if (betae && h->dense_path != KGQ_DENSE_FP32) a.ent_planes = h->ent_planes;
+        a.split_always = h->dense_path == KGQ_DENSE_BF16X3;
         a.part = L.score_ws;
         a.part_elems = L.score_ws_elems;
         launch_score(a, s);

@@ -249,6 +249,7 @@ struct ScoreArgs {
     // stride n_blocks * 256 * 2d) for the bf16 matrix-core contraction, or
     // nullptr for the FP32 one
     const uint16_t* ent_planes = nullptr;
+    bool split_always = false;         // the bf16 contraction at any row count (tests)
 };
 // Filtered answer ranks and per-query [MRR, Hits@1, @3, @10] (k_rank.hip).
 void launch_rank_answers(const float* scores, int64_t ld, int64_t N, int batch, const int32_t* off,
