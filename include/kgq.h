@@ -261,8 +261,9 @@ kgq_status kgq_set_checked(kgq_handle* h, int32_t on);
  *     split exactly into three bf16 parts and six of the nine part products
  *     kept (the dropped ones are below 2^-23 of each product; the weight
  *     parts are zero-padded to a multiple of 32 columns); smaller layers of
- *     an execute with K >= 64 split K there; the others (K < 32, and
- *     kgq_dense layers below the bounds) on the FP32 matrix cores. Inputs
+ *     an execute with more than 64 rows and K >= 64 split K there; the
+ *     others (K < 32, layers of at most 64 rows, and kgq_dense layers below
+ *     the bounds) on the FP32 matrix cores. Inputs
  *     must be finite and below 3.39e38 in magnitude on the bf16 path.
  *     BetaE scores on the bf16 path when 2d is a multiple of 32 and the call
  *     scores more than 64 rows (more than 128 when 128-row tiles would give
