@@ -30,7 +30,8 @@
 //           table and the query's (Ca, Sa) of theta/2 and (Cb, Sb) of psi/2:
 //           s = Se Ca - Ce Sa = sin((theta_e - theta)/2),
 //           c = Ce Ca + Se Sa = cos((theta_e - theta)/2),
-//           t = |s| Cb - |c| Sb;  acc1 += max(t, 0);  acc2 += min(|s|, Sb) (10)
+//           t = |s| Cb - |c| Sb;  acc1 += max(t, 0);  acc2 += min(|s|, Sb) (10,
+//           plus Cb and Sb moved to vector registers once per row and step)
 //           score = gamma - modulus (acc1 + center_reg acc2). This is the
 //           sector distance exactly: min(|sin(a + b)|, |sin(a - b)|) =
 //           ||sin a| cos b - |cos a| sin b| for b = psi/2 in [0, pi/2], and
@@ -142,7 +143,16 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
                 for (int j = 0; j < 4; ++j) acc[i][j] += fabsf(e4[j] - c);
             } else if (MODEL == 3) {
                 const float ce4[4] = {eu.v[EF - 1].x, eu.v[EF - 1].y, eu.v[EF - 1].z, eu.v[EF - 1].w};
-                const float sa = qv[TQ + i], cb = qv[2 * TQ + i], sb = qv[3 * TQ + i];
+                const float sa = qv[TQ + i];
+                // the aperture's cosine and sine as vector operands: the VALU
+                // takes a scalar operand on at most every other issue cycle,
+                // and with them in SGPRs 7 of the triple's 10 instructions
+                // would read one (2 moves per row and step, per 4 triples:
+                // the scorer at the 14,505-entity ConE workload went from
+                // 4.75 to 4.00 ms)
+                float cb, sb;
+                asm("v_mov_b32 %0, %1" : "=v"(cb) : "s"(qv[2 * TQ + i]));
+                asm("v_mov_b32 %0, %1" : "=v"(sb) : "s"(qv[3 * TQ + i]));
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const float sn = fmaf(-ce4[j], sa, e4[j] * c);    // sin((theta_e - theta) / 2)
