@@ -61,3 +61,14 @@ def test_gpu_small_batch_mixed_matches_large_batch():
         torch.cuda.synchronize()
         check_scores(one["scores"].cpu().numpy(), big["scores"].cpu().numpy()[q:q + 1].astype(np.float64),
                      w.rtol, w.gamma, f"query {q}")
+
+
+@pytest.mark.parametrize("n_ent,batches", [(33000, [64, 65, 128, 129]), (20000, [65, 129])])
+def test_gpu_betae_scorer_path_boundary(n_ent, batches):
+    """The BetaE scorer takes the FP32 64 x 64 tile up to 64 scored rows, or up
+    to 128 when 128-row tiles would give fewer than 256 workgroups, and the
+    bf16 split tile above (2d = 64). 33,000 entities give 258 entity tiles of
+    128: 64 rows on the FP32 tile, 65, 128 and 129 on the bf16 one; 20,000
+    give 157: 65 rows on the FP32 tile, 129 on the bf16 one. Both sides of
+    each boundary against the oracle."""
+    _run(O.BETAE, ["1p"], batches, n_ent=n_ent, n_rel=7, dim=32, seed=57)
