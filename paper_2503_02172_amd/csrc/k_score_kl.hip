@@ -75,7 +75,8 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
         KlTile::run(a.qpack, K, n_mt * KL_BM, a.ent, K, n_ent_pad, K, m0, n0, sm, acc);
 
     // Epilogue, staged through LDS (the ring is free after the K loop):
-    //   1. each lane adds C_q + E_e in double precision to its accumulators
+    //   1. each lane subtracts E_e and its accumulators from gamma - C_q (one
+    //      per row, hoisted) in double precision
     //      and writes the scores of its 4 rows x 1 column per MFMA tile into
     //      a BM x BN tile (rows padded by 4 floats: the 16 lanes of a column
     //      group and the 4 row groups hit distinct banks, and rows stay
@@ -94,6 +95,11 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     static_assert(KL_BN % 4 == 0 && 256 % (KL_BN / 4) == 0, "output row pieces");
     __syncthreads();                                  // every wavefront is done with the ring
     float* T = sm;
+    double gq[KlTile::TM][4];                         // gamma - C_q of the lane's rows, once per tile
+#pragma unroll
+    for (int i = 0; i < KlTile::TM; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gq[i][q] = (double)a.gamma - a.cq[m0 + KlTile::row_of(i) + q];
 #pragma unroll
     for (int j = 0; j < KlTile::TN; ++j) {
         const int cj = KlTile::col_of(j);
@@ -102,8 +108,7 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
         for (int i = 0; i < KlTile::TM; ++i) {
             const int rb = KlTile::row_of(i);
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                T[(rb + q) * TLD + cj] = (float)((double)a.gamma - (a.cq[m0 + rb + q] + ee + (double)acc[i][j][q]));
+            for (int q = 0; q < 4; ++q) T[(rb + q) * TLD + cj] = (float)((gq[i][q] - ee) - (double)acc[i][j][q]);
         }
     }
     __syncthreads();
