@@ -147,11 +147,10 @@ void launch_split_planes(const float* w, uint16_t* p, int64_t rows, int64_t cols
     hipLaunchKernelGGL(k_split_planes, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, w, p, cols, ld, n);
 }
 
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn, int per_xcd)
+template <int BM, int BN, bool PRIO>
+__device__ __forceinline__ void gemm_bf16x3_tile(const GemmArgs& g, int tm, int tn, int per_xcd, float* sm)
 {
-    using Tile = MfmaTileBf16x3<BM, BN, 4, BM == 64>;   // raised read priority: see the tile
-    __shared__ float sm[Tile::SMEM];
+    using Tile = MfmaTileBf16x3<BM, BN, 4, PRIO>;
     const int b = blockIdx.x;
     const int L = (b & 7) * per_xcd + (b >> 3);
     if (L >= tm * tn) return;
@@ -177,6 +176,21 @@ __global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn,
                 g.C[row * g.ldc + n] = v;
             }
     }
+}
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void k_gemm_bf16x3(GemmArgs g, int tm, int tn, int per_xcd)
+{
+    __shared__ float sm[MfmaTileBf16x3<BM, BN, 4, BM == 64>::SMEM];
+    gemm_bf16x3_tile<BM, BN, BM == 64>(g, tm, tn, per_xcd, sm);   // raised read priority: see the tile
+}
+
+// 128 x 128 tiles (the BetaE scorer's): an 80 KiB ring, above the static LDS
+// limit, two workgroups per compute unit, raised read priority
+__global__ __launch_bounds__(256, 2) void k_gemm_bf16x3_128(GemmArgs g, int tm, int tn, int per_xcd)
+{
+    extern __shared__ __align__(16) float sm_dyn[];
+    gemm_bf16x3_tile<128, 128, true>(g, tm, tn, per_xcd, sm_dyn);
 }
 
 // Split K on the bf16 matrix cores: each of S workgroups per 64 x 64 tile
@@ -238,7 +252,23 @@ static void launch_gemm_bf16x3(const GemmArgs& g, hipStream_t s)
     // 128 x 64 tiles for every layer of 4,096 rows or more, 0.628 ms with
     // 64 x 64 tiles throughout; on the 63,361-entity step, 128 x 64 tiles from
     // 2,048 rows (its 3,947-row layers) took the stage from 0.534 to 0.516 ms.
-    if (g.M >= 2048 && g.N >= 1024) {
+    // A layer whose 128 x 64 tiles need a second round of the 512 resident
+    // workgroups while 128 x 128 tiles fit one takes those (3,947 x 1,600 x
+    // 1,600: 775 tiles of 128 x 64 in 142 us, 403 of 128 x 128 in 125 us).
+    const int64_t t128 = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
+    const int64_t t64 = (int64_t)((g.M + 127) / 128) * ((g.N + 63) / 64);
+    if (g.M >= 2048 && g.N >= 1024 && t128 <= 512 && t64 > 512) {
+        constexpr int lds = MfmaTileBf16x3<128, 128, 4, true>::SMEM * 4;
+        static bool raised[64] = {};
+        int dev = 0;
+        if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !raised[dev]) {
+            if (hipFuncSetAttribute((const void*)k_gemm_bf16x3_128, hipFuncAttributeMaxDynamicSharedMemorySize, lds) ==
+                hipSuccess)
+                raised[dev] = true;
+        }
+        const int tm = (g.M + 127) / 128, tn = (g.N + 127) / 128, per_xcd = (tm * tn + 7) / 8;
+        hipLaunchKernelGGL(k_gemm_bf16x3_128, dim3(per_xcd * 8), dim3(256), lds, s, g, tm, tn, per_xcd);
+    } else if (g.M >= 2048 && g.N >= 1024) {
         const int tm = (g.M + 127) / 128, tn = (g.N + 63) / 64, per_xcd = (tm * tn + 7) / 8;
         hipLaunchKernelGGL((k_gemm_bf16x3<128, 64>), dim3(per_xcd * 8), dim3(256), 0, s, g, tm, tn, per_xcd);
     } else {
