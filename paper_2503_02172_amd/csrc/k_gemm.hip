@@ -255,6 +255,8 @@ static void launch_gemm_bf16x3(const GemmArgs& g, hipStream_t s)
     // A layer whose 128 x 64 tiles need a second round of the 512 resident
     // workgroups while 128 x 128 tiles fit one takes those (3,947 x 1,600 x
     // 1,600: 775 tiles of 128 x 64 in 142 us, 403 of 128 x 128 in 125 us).
+    // 128 x 128 for every layer of 2,048 rows or more with 192-512 such
+    // tiles (the N = 800 layers too) made both BetaE dense stages slower.
     const int64_t t128 = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
     const int64_t t64 = (int64_t)((g.M + 127) / 128) * ((g.N + 63) / 64);
     if (g.M >= 2048 && g.N >= 1024 && t128 <= 512 && t64 > 512) {
