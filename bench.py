@@ -7,7 +7,7 @@ uniformly over all 14 structures, executed as one mixed-structure call (the
 plan lowering groups the operators of every structure, one scorer launch
 covers every scored row), every query scored against all entities, top-100.
 Inputs are resident in HBM before the timed region starts. --workload picks
-another of the five workloads; --per-structure issues one execute call per
+another of the eight workloads; --per-structure issues one execute call per
 structure batch instead, spread round-robin over --streams streams.
 
 Prints one JSON line. `value` is queries/s over the timed steps.
@@ -16,9 +16,10 @@ algorithmic operations of one launch divided by the launch's average
 duration (HIP events around each launch on the stream it runs on), against
 the chip's published peak for the units it runs on (for BetaE the bf16
 matrix cores at six bf16 products per FP32-accurate product, or the FP32
-matrix cores with --matrix-path fp32; FP32 vector units for the others). `cpu_baseline` times the CPU
-oracle on a bounded sample of the same workload, on every host thread and on
-one. `others` reports the other workloads (throughput and scorer fraction).
+matrix cores with --matrix-path fp32; FP32 vector units for the others).
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload,
+on every host thread and on one. `others` reports the other workloads
+(throughput and scorer fraction).
 """
 
 from __future__ import annotations
@@ -454,7 +455,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="C5")
-    ap.add_argument("--no-others", action="store_true", help="skip the other four workloads")
+    ap.add_argument("--no-others", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-other-mode", action="store_true",
                     help="skip the second timing of the headline workload in the other in-flight mode (so that "
