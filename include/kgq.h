@@ -106,8 +106,9 @@ typedef struct {
     int32_t tnorm;        /* LogicE: kgq_tnorm of the intersection; ignored otherwise */
 } kgq_config;
 
-/* Create a handle for one embedding model on one GPU (GQE, Query2Box or
- * BetaE: Related Work; Experiments, Baselines). Validates cfg, selects the
+/* Create a handle for one embedding model on one GPU (GQE, Query2Box,
+ * BetaE, ConE or LogicE: Related Work; Experiments, Baselines; Table 1).
+ * Validates cfg, selects the
  * device, and allocates all scratch space for max_batch queries (execute
  * allocates nothing). The handle is the compiled form of the paper's
  * pipeline for that model (Methodology, Fig. 2): the 14 benchmark
