@@ -7,8 +7,9 @@
  * structure fixes a computation graph of projection, intersection, union
  * and negation operators over anchor entities and relations, and the
  * library executes that graph for a batch of queries, then scores every
- * entity against each query embedding (the "entity similarity query" of
- * the Experiments section) and selects the top k.
+ * entity against each query embedding (the entity-similarity step that the
+ * Experiments section times together with the operators) and selects the
+ * top k.
  *
  * Five embedding models are supported: GQE, Query2Box, BetaE, ConE and
  * LogicE (the paper names them in Related Work and Experiments/Baselines and

@@ -1,5 +1,5 @@
-// Entity scoring for GQE, Query2Box, ConE and LogicE: the "entity similarity
-// query" that the paper times together with operator execution (Experiments,
+// Entity scoring for GQE, Query2Box, ConE and LogicE: the entity-similarity
+// step that the paper times together with operator execution (Experiments,
 // Metrics): every query embedding is scored against every entity. (BetaE's
 // regrouped KL score is a dense contraction and runs on the matrix cores,
 // k_score_kl.hip.) LogicE's score is GQE's L1 distance over its 2d bound
