@@ -231,8 +231,9 @@ kgq_status kgq_execute_mixed(kgq_handle* h, int32_t batch, const int32_t* struct
  * where the call's device scratch lives. kgq_execute_mixed uses the scratch
  * the handle allocated at create; this call carves every device buffer it
  * needs (plan image, error flag, state rows, dense-layer rows, packed
- * queries, the score matrix when out_scores is NULL, top-k candidates, and
- * the split workspaces of small batches as far as room is left) out of one
+ * queries, the score matrix when out_scores is NULL, top-k candidates, and,
+ * as far as room is left, BetaE's chunk keys for top-k and the split
+ * workspaces of small batches) out of one
  * static array of KGQ_NOALLOC_SCRATCH_BYTES per GPU, which the library holds
  * from its first use on that GPU until the process ends. The call itself
  * allocates nothing, device or pinned; it lowers the plan on the host as

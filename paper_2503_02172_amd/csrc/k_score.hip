@@ -299,13 +299,10 @@ __global__ __launch_bounds__(256) void k_score_sum(ScoreArgs a, int splits, int6
     a.scores[(int64_t)a.out_dest[o] * a.ld + e] = best;
 }
 
-void launch_score(const ScoreArgs& a, hipStream_t s)
+bool launch_score(const ScoreArgs& a, hipStream_t s)
 {
-    if (a.n_rows <= 0) return;
-    if (a.model == KGQ_BETAE) {
-        launch_score_kl(a, s);
-        return;
-    }
+    if (a.n_rows <= 0) return false;
+    if (a.model == KGQ_BETAE) return launch_score_kl(a, s);
     const int form = valu_form(a.model);           // LogicE runs GQE's kernel
     const int tq = score_tq(a.model, a.n_rows);    // the pack's layout for this row count
     const bool small = score_small(a.n_rows);
@@ -360,6 +357,7 @@ void launch_score(const ScoreArgs& a, hipStream_t s)
         else
             hipLaunchKernelGGL((k_score_sum<3>), g2, dim3(256), 0, s, b, z, rows_pad, n_out);
     }
+    return false;
 }
 
 }  // namespace kgq

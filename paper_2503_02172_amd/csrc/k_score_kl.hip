@@ -28,7 +28,10 @@
 // tiles. The epilogue adds
 // C_q + E_e in double precision, stages the output tile in LDS, takes the
 // max over union groups of four and pairs of rows and writes each output
-// row with 16-byte non-temporal stores.
+// row with 16-byte non-temporal stores. On the 128-entity bf16 tiles it also
+// writes, per output row and chunk of 64 entities, the largest key of the
+// chunk's scores, from which top-k skips the chunks that cannot hold an
+// answer.
 // Workgroups are ordered in chunks of row tiles (about 2 MiB of query rows),
 // each swept against every entity tile: the chunk's rows stay in L2 while
 // the entity table streams past.
@@ -43,6 +46,21 @@ namespace kgq {
 // loop 128 x 128, or 64 x 64 for small batches, where the larger tile leaves
 // the chip underfilled and each workgroup's K loop is a latency chain. Query
 // rows are padded to 128 (kRowTileBetae), a multiple of every tile's rows.
+// s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15)
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Largest x over each DPP row of 16 lanes (all of them active): swaps of
+// neighbours and of pairs inside quads, then the half-row and the row
+// mirrored.
+__device__ __forceinline__ uint32_t chunk16_max(uint32_t x)
+{
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));    // quad_perm 1,0,3,2
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));    // quad_perm 2,3,0,1
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x141, 0xF, 0xF, false));   // row_half_mirror
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x140, 0xF, 0xF, false));   // row_mirror
+    return x;
+}
+
 template <class KlTile>
 __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int n_nt, int qchunk, int total,
                                                      int per_xcd)
@@ -93,6 +111,19 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
     constexpr int TLD = KL_BN + 4;
     static_assert(KL_BM * TLD <= KlTile::SMEM, "output tile fits the LDS ring");
     static_assert(KL_BN % 4 == 0 && 256 % (KL_BN / 4) == 0, "output row pieces");
+    // The output rows of the thread's rows in step 2, loaded now and waited
+    // for once before it: a load inside its loop would wait (vmcnt) for the
+    // stores issued before it as well. (Rows past the last are clamped to
+    // it: no branch, so the loads issue back to back.)
+    constexpr int C4 = KL_BN / 4, RPP = 256 / C4;     // 16-byte pieces per row, rows per pass
+    constexpr int NIT = KL_BM / RPP;
+    const int r0 = threadIdx.x / C4;
+    int32_t od[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int m = min(m0 + r0 + it * RPP, a.n_rows - 1);
+        od[it] = a.out_dest[score_out_index(m, a.n_quad, a.n_pair)];
+    }
     __syncthreads();                                  // every wavefront is done with the ring
     float* T = sm;
     double gq[KlTile::TM][4];                         // gamma - C_q of the lane's rows, once per tile
@@ -111,13 +142,21 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
             for (int q = 0; q < 4; ++q) T[(rb + q) * TLD + cj] = (float)((gq[i][q] - ee) - (double)acc[i][j][q]);
         }
     }
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);          // the output rows
     __syncthreads();
-    constexpr int C4 = KL_BN / 4, RPP = 256 / C4;     // 16-byte pieces per row, rows per pass
     const int c4 = threadIdx.x % C4;
     const int64_t n = n0 + 4 * c4;
-    if (n >= a.N) return;
+    // Chunk keys (128-entity tiles only): the 16 lanes of a chunk are one DPP
+    // row, and every lane of a row stays in the loop below (the row-uniform
+    // branches keep its DPP rows whole); lanes past N add key 0.
+    constexpr bool KEYS = KlTile::kBf16x3 && KL_BN == 2 * kKeyChunk;
+    const bool keys = KEYS && a.chunk_key != nullptr;
+    const bool tail = n0 + KL_BN > a.N;               // the last entity tile
+    if (!keys && n >= a.N) return;
     const int n_grouped = a.n_quad + a.n_pair;
-    for (int r = threadIdx.x / C4; r < KL_BM; r += RPP) {
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int r = r0 + it * RPP;
         const int m = m0 + r;
         if (m >= a.n_rows) break;                     // rows only grow along the loop
         int cnt = 1;
@@ -134,7 +173,27 @@ __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int 
             const float4 w = *reinterpret_cast<const float4*>(t + u * TLD);
             v = make_float4(fmaxf(v.x, w.x), fmaxf(v.y, w.y), fmaxf(v.z, w.z), fmaxf(v.w, w.w));
         }
-        float* dst = a.scores + (int64_t)a.out_dest[score_out_index(m, a.n_quad, a.n_pair)] * a.ld + n;
+        const int64_t orow = od[it];
+        if constexpr (KEYS) {
+            if (keys) {
+                // An upper bound of the keys of the lane's scores: the key of
+                // their float maximum (the scores order as their keys, NaN
+                // aside), or the largest key when one is NaN; columns past N
+                // count as -inf (in the last entity tile only).
+                float4 kv = v;
+                if (tail) {
+                    const float ninf = -__builtin_inff();
+                    kv = make_float4(n < a.N ? kv.x : ninf, n + 1 < a.N ? kv.y : ninf, n + 2 < a.N ? kv.z : ninf,
+                                     n + 3 < a.N ? kv.w : ninf);
+                }
+                const float mx = fmaxf(fmaxf(kv.x, kv.y), fmaxf(kv.z, kv.w));
+                const bool nan = __builtin_isunordered(kv.x, kv.y) || __builtin_isunordered(kv.z, kv.w);
+                const uint32_t u = __float_as_uint(mx == 0.0f ? 0.0f : mx);
+                const uint32_t kx = chunk16_max(nan ? 0xFFFFFFFFu : u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u));
+                if ((c4 & 15) == 0 && n < a.N) a.chunk_key[orow * a.key_ld + n / kKeyChunk] = max(kx, 1u);
+            }
+        }
+        float* dst = a.scores + orow * a.ld + n;
         if (n + 3 < a.N) {
             // rows start only 4-byte aligned; gfx950 takes dword-aligned
             // multi-dword global stores
@@ -180,9 +239,9 @@ static void launch_tiles(const ScoreArgs& a, hipStream_t s)
 
 constexpr int kScoreKlFp32Rows = 64;   // scored rows up to which the FP32 tile runs
 
-void launch_score_kl(const ScoreArgs& a, hipStream_t s)
+bool launch_score_kl(const ScoreArgs& a, hipStream_t s)
 {
-    if (a.n_rows <= 0) return;
+    if (a.n_rows <= 0) return false;
     using LdsTile = MfmaTileLds<64, 64, 3>;
     using LdsTileHalf = MfmaTileLds<64, 64, 3, true>;
     using SplitTile = MfmaTileBf16x3<128, 128, 4, true>;
@@ -199,7 +258,9 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
         a.split_always || (a.n_rows > kScoreKlFp32Rows && (a.n_rows > 128 || split_tiles >= 256));
     if (a.ent_planes && (2 * a.d) % 32 == 0 && split_pays) {   // planes: row stride 2d
         launch_tiles<SplitTile>(a, s);
-    } else if (LdsTile::supports(2 * a.d)) {
+        return a.chunk_key != nullptr;
+    }
+    if (LdsTile::supports(2 * a.d)) {
         launch_tiles<LdsTile>(a, s);
     } else if (LdsTileHalf::supports(2 * a.d)) {
         launch_tiles<LdsTileHalf>(a, s);
@@ -208,6 +269,7 @@ void launch_score_kl(const ScoreArgs& a, hipStream_t s)
         if (big_tiles < 512) launch_tiles<MfmaTileReg<64, 64>>(a, s);
         else launch_tiles<MfmaTileReg<kRowTileBetae, 128>>(a, s);
     }
+    return false;
 }
 
 }  // namespace kgq

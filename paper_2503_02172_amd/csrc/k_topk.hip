@@ -48,13 +48,6 @@
 namespace kgq {
 
 
-__device__ __forceinline__ uint32_t score_key(float f)
-{
-    if (f == 0.0f) f = 0.0f;   // -0 and +0 rank equal
-    const uint32_t u = __float_as_uint(f);
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
 __device__ __forceinline__ float key_score(uint32_t key)
 {
     return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
@@ -612,8 +605,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(5))) void k_
 // the top k is dropped; the score compare only admits a superset (ties with
 // T, NaN), which the prunes sort out. At the end the buffer is pruned to at
 // most 64, 128 or 256 entries (by k) and sorted inside the wavefront.
+// Over a score matrix whose scorer also wrote chunk keys (the largest key of
+// every kKeyChunk scores of a row), the first round reads only the chunks
+// whose key reaches the k-th largest chunk key (k_topk_listed).
 // ---------------------------------------------------------------------------
 constexpr int kStreamK = 256;        // largest k on the streaming path
+constexpr int kPruneChunks = 1024;   // chunk keys per segment on the listed stream (65,536 scores)
 constexpr int kStreamKeep = 128;     // a prune leaves at most max(k, this) entries
 constexpr int kStreamWaves = 2;      // wavefronts (segments) per workgroup
 constexpr int kStreamGroup = 1;      // load steps per group
@@ -883,6 +880,25 @@ __device__ __forceinline__ void stream_group(StreamState& st, const float (&v)[H
     }
 }
 
+// Final prune of the buffer to at most 64, 128 or 256 entries (by k), which
+// also turns them into keys, then the sort, written to output row orow (and
+// padding past k).
+template <int CAP>
+__device__ __forceinline__ void stream_finish(StreamState& st, int k, int64_t orow, int lane, const TopkArgs& a)
+{
+    const int fin = k <= 64 ? 64 : k <= 128 ? 128 : 256;     // sort size
+    if (st.cnt <= 256) stream_prune_final<4>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
+    else if (st.cnt <= 512) stream_prune_final<8>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
+    else stream_prune_final<CAP / 64>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
+    for (int p = k + lane; p < a.k; p += 64) {
+        a.out_idx[orow * a.out_ld + p] = 0x7FFFFFFF;
+        a.out_score[orow * a.out_ld + p] = -__builtin_inff();
+    }
+    if (st.cnt <= 64) stream_sort<1>(st.buf, st.cnt, k, orow, lane, a);
+    else if (st.cnt <= 128) stream_sort<2>(st.buf, st.cnt, k, orow, lane, a);
+    else stream_sort<4>(st.buf, st.cnt, k, orow, lane, a);
+}
+
 // H: steps per group; D groups held in registers, D - 1 of them in flight
 // while one is compared. IDX: element indices come from in_idx (later
 // rounds).
@@ -963,20 +979,129 @@ __global__ __launch_bounds__(64 * W) void k_topk_stream(TopkArgs a)
     }
     __builtin_amdgcn_s_setprio(0);
     // Every score of the segment reached the threshold or is below the k-th
-    // largest, so the buffer holds the top k (all nn when nn <= k). The final
-    // prune also turns the entries into keys for the sort.
-    const int fin = k <= 64 ? 64 : k <= 128 ? 128 : 256;     // sort size
-    if (st.cnt <= 256) stream_prune_final<4>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
-    else if (st.cnt <= 512) stream_prune_final<8>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
-    else stream_prune_final<CAP / 64>(st.buf, st.cnt, st.tk, st.ti, k, fin, lane);
-    const int64_t orow = row * a.out_rows_per_row + seg;
-    for (int p = k + lane; p < a.k; p += 64) {
-        a.out_idx[orow * a.out_ld + p] = 0x7FFFFFFF;
-        a.out_score[orow * a.out_ld + p] = -__builtin_inff();
+    // largest, so the buffer holds the top k (all nn when nn <= k).
+    stream_finish<CAP>(st, k, row * a.out_rows_per_row + seg, lane, a);
+}
+
+// Pruned first round over a score matrix with chunk keys (at most
+// kPruneChunks per segment). The threshold starts at the k-th largest chunk
+// key of the segment (the chunks are disjoint, so at least k elements reach
+// it), the chunks whose key reaches it are listed in LDS, and the wavefront
+// streams that list alone, G chunks (one load each) per group, D groups in
+// flight, appending and pruning as the full stream does. A chunk left out
+// holds only elements below the threshold, none of them among the k largest,
+// so the result is the full stream's. At most about k chunks of a row hold
+// an element of its top k: the rest of the row is never read.
+template <int E>
+__device__ __forceinline__ int list_chunks(const uint32_t* src, uint32_t* list, int nchunk, int k, StreamState& st,
+                                           int lane)
+{
+    uint32_t key[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = e * 64 + lane;
+        key[e] = j < nchunk ? src[j] : 0u;
     }
-    if (st.cnt <= 64) stream_sort<1>(st.buf, st.cnt, k, orow, lane, a);
-    else if (st.cnt <= 128) stream_sort<2>(st.buf, st.cnt, k, orow, lane, a);
-    else stream_sort<4>(st.buf, st.cnt, k, orow, lane, a);
+    if (nchunk > k) {
+        stream_threshold<E, false>(key, [](int) { return 0u; }, nchunk, k, k, st.tk, st.ti);
+        st.tf = key_score(st.tk);
+    }
+    int n = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = e * 64 + lane;
+        const bool f = j < nchunk && key[e] >= st.tk;
+        const uint64_t bc = ballot64(f);
+        if (f) list[n + lanes_below(bc)] = (uint32_t)j;
+        n += __popcll(bc);
+    }
+    return n;
+}
+
+template <int G, int D, int CAP, int KEEP, int W>
+__global__ __launch_bounds__(64 * W) void k_topk_listed(TopkArgs a)
+{
+    static_assert(CAP >= kStreamK + 64 * G && CAP % 64 == 0 && KEEP <= kStreamK && G == 4, "listed stream shape");
+    __shared__ uint2 s_buf[W][CAP + 64];     // + 64 slots for the lanes that append nothing
+    __shared__ __align__(16) uint32_t s_list[W][kPruneChunks];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nseg = (a.N + a.seg_len - 1) / a.seg_len;
+    const int64_t unit = (int64_t)blockIdx.x * W + wave;   // (row, segment), row-major
+    if (unit >= nseg * a.n_rows) return;
+    const int64_t row = unit / nseg;
+    const int64_t seg = unit - row * nseg;
+    const int64_t seg0 = seg * a.seg_len;                    // a multiple of 256
+    int64_t n64 = a.N - seg0;
+    if (n64 > a.seg_len) n64 = a.seg_len;
+    const int nn = (int)n64;
+    const int k = a.k < nn ? a.k : nn;
+    StreamState st{s_buf[wave], 0, 0u, 0u, key_score(0u)};
+    uint32_t* list = s_list[wave];
+    const uint32_t* src = a.chunk_key + row * a.key_ld + seg0 / kKeyChunk;
+    const int nchunk = (nn + kKeyChunk - 1) / kKeyChunk;
+    int nlist;
+    if (nchunk <= 256) nlist = list_chunks<4>(src, list, nchunk, k, st, lane);
+    else if (nchunk <= 512) nlist = list_chunks<8>(src, list, nchunk, k, st, lane);
+    else nlist = list_chunks<kPruneChunks / 64>(src, list, nchunk, k, st, lane);
+    nlist = __builtin_amdgcn_readfirstlane(nlist);
+
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.scores + row * a.ld + seg0), (short)0, nn * 4, 0x00020000);
+    // Group q holds list entries q * G .. q * G + G - 1; an entry past the
+    // list (chunk -1) loads at offset nn * 4, past the segment: the buffer
+    // range check returns 0 without a memory access, and nothing is appended.
+    const int ngroups = (nlist + G - 1) / G;
+    float v[D][G];
+    int ch[D][G];
+    auto issue = [&](int g, int q) {
+        int c4[G] = {-1, -1, -1, -1};
+        if (q * G < nlist) {
+            const uint4 l = *reinterpret_cast<const uint4*>(list + q * G);
+            const int idx[G] = {(int)l.x, (int)l.y, (int)l.z, (int)l.w};
+#pragma unroll
+            for (int c = 0; c < G; ++c)
+                c4[c] = q * G + c < nlist ? __builtin_amdgcn_readfirstlane(idx[c]) : -1;
+        }
+#pragma unroll
+        for (int c = 0; c < G; ++c) {
+            ch[g][c] = c4[c];
+            const int off = c4[c] >= 0 ? (c4[c] * kKeyChunk + lane) * 4 : nn * 4;
+            v[g][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, off, 0, 0));
+        }
+    };
+#pragma unroll
+    for (int g = 0; g < D; ++g) {
+        issue(g, g);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int q0 = 0; q0 < ngroups; q0 += D) {
+#pragma unroll
+        for (int g = 0; g < D; ++g) {
+            if (st.cnt > CAP - 64 * G) {
+                stream_prune<CAP / 64>(st.buf, st.cnt, st.tk, st.ti, k, k > KEEP ? k : KEEP, lane);
+                st.tf = key_score(st.tk);
+            }
+#pragma unroll
+            for (int c = 0; c < G; ++c) {
+                if (ch[g][c] < 0) continue;
+                const int pos = ch[g][c] * kKeyChunk + lane;
+                const bool f = pos < nn && !(v[g][c] < st.tf);
+                const uint64_t bc = ballot64(f);
+                if (bc != 0ull) {
+                    // every lane writes: those not appending to a slot of
+                    // their own past the buffer
+                    const int slot = f ? st.cnt + lanes_below(bc) : CAP + lane;
+                    st.buf[slot] = make_uint2(__float_as_uint(v[g][c]), (uint32_t)(seg0 + pos));
+                    st.cnt += __popcll(bc);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            issue(g, q0 + g + D);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    stream_finish<CAP>(st, k, row * a.out_rows_per_row + seg, lane, a);
 }
 
 static void launch_segments(const TopkArgs& a, hipStream_t s)
@@ -1011,7 +1136,10 @@ static void launch_stream(const TopkArgs& a, hipStream_t s)
 {
     const int64_t units = ((a.N + a.seg_len - 1) / a.seg_len) * a.n_rows;
     const dim3 grid((unsigned)((units + kStreamWaves - 1) / kStreamWaves));
-    if (a.in_idx)
+    if (!a.in_idx && a.chunk_key && (a.seg_len + kKeyChunk - 1) / kKeyChunk <= kPruneChunks)
+        hipLaunchKernelGGL((k_topk_listed<4, kStreamDepth, kStreamCap, kStreamKeep, kStreamWaves>), grid,
+                           dim3(64 * kStreamWaves), 0, s, a);
+    else if (a.in_idx)
         hipLaunchKernelGGL((k_topk_stream<kStreamGroup, kStreamDepth, true, kStreamCap, kStreamKeep, kStreamWaves>),
                            grid, dim3(64 * kStreamWaves), 0, s, a);
     else

@@ -55,6 +55,7 @@ struct Lane {
     int64_t score_ws_elems = 0;
     int32_t* cand_idx[2] = {nullptr, nullptr};   // top-k candidates of long rows
     float* cand_score[2] = {nullptr, nullptr};
+    uint32_t* chunk_key = nullptr;   // BetaE: the scorer's chunk keys for top-k [rows x ceil(N / 64)]
     int* dflag = nullptr;
     int* hflag = nullptr;         // pinned
     // plan images: per-structure cache slots + a ring of two for mixed batches
@@ -423,6 +424,7 @@ kgq_status allocate_all(kgq_handle* h)
             ALLOC(L.cand_idx[i], ncand);
             ALLOC(L.cand_score[i], ncand);
         }
+        if (c.model == KGQ_BETAE) ALLOC(L.chunk_key, Bm * ((N + kKeyChunk - 1) / kKeyChunk));
         ALLOC(L.dflag, 1);
         ALLOC(L.plan_dev, (int64_t)(kNumStructures + 2) * h->plan_words);
         hipError_t e = hipHostMalloc((void**)&L.hflag, sizeof(int), hipHostMallocDefault);
@@ -767,6 +769,7 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
                     L.states, W, d_score, L.qpack, L.cq, s);
     }
     float* dst = out_scores ? out_scores : L.scores;
+    bool keyed = false;   // the scorer wrote chunk keys for top-k
     {
         StageTimer t(h, 4, s);
         ScoreArgs a{c.model, L.qpack, h->ent_blk, L.cq, h->ent_const, P + p.off_out_dest, p.n_score_rows,
@@ -776,7 +779,11 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
         a.split_always = h->dense_path == KGQ_DENSE_BF16X3;
         a.part = L.score_ws;
         a.part_elems = L.score_ws_elems;
-        launch_score(a, s);
+        if (out_idx) {
+            a.chunk_key = L.chunk_key;
+            a.key_ld = (N + kKeyChunk - 1) / kKeyChunk;
+        }
+        keyed = launch_score(a, s);
     }
     if (out_idx) {
         StageTimer t(h, 5, s);
@@ -791,6 +798,10 @@ kgq_status run_plan(kgq_handle* h, Lane& L, const Plan& p, const int32_t* P, con
         for (int i = 0; i < 2; ++i) {
             ta.cand_idx[i] = L.cand_idx[i];
             ta.cand_score[i] = L.cand_score[i];
+        }
+        if (keyed) {
+            ta.chunk_key = L.chunk_key;
+            ta.key_ld = (N + kKeyChunk - 1) / kKeyChunk;
         }
         if (!launch_topk(ta, s)) return fail(h, KGQ_E_DEVICE, "top-k scratch buffers missing");
     }
@@ -827,9 +838,11 @@ kgq_status noalloc_scratch_address(kgq_handle* h)
 // bytes at `base` (256-byte aligned pieces), in the roles a lane's buffers
 // play: plan image, error flag, state rows, dense-layer rows, intersection
 // groups, packed queries, the score matrix when the caller does not supply
-// one, and the top-k candidates of long rows. The split-K and split-d
-// workspaces of small batches get what is left, up to a lane's caps (the
-// splitting code takes fewer slices when a workspace is smaller). Returns the
+// one, and the top-k candidates of long rows. BetaE's chunk keys for top-k
+// (which then reads only the chunks that can hold its answers), then the
+// split-K and split-d workspaces of small batches get what is left, up to a
+// lane's caps (the splitting code takes fewer slices when a workspace is
+// smaller). Returns the
 // bytes the required pieces need; *fits tells whether they fit `cap`.
 int64_t carve_scratch(const kgq_handle* h, const Plan& p, int32_t k, bool need_scores, bool need_topk,
                       unsigned char* base, int64_t cap, Lane& V, int32_t** plan_dev, bool* fits)
@@ -883,7 +896,12 @@ int64_t carve_scratch(const kgq_handle* h, const Plan& p, int32_t k, bool need_s
     V.gemm_ws_elems = 0;
     V.score_ws = nullptr;
     V.score_ws_elems = 0;
+    V.chunk_key = nullptr;
     if (*fits) {
+        // BetaE's chunk keys for top-k first, when they fit whole
+        const int64_t key_bytes = B * ((N + kKeyChunk - 1) / kKeyChunk) * 4;
+        if (c.model == KGQ_BETAE && need_topk && (off + 255) / 256 * 256 + key_bytes <= cap)
+            V.chunk_key = reinterpret_cast<uint32_t*>(take(key_bytes));
         // optional workspaces, each from half of what is left
         const int64_t n_max = mlp_model(c.model) ? 4 * d : d;
         int64_t left = (cap - (off + 255) / 256 * 256) / 2 / 4 / 64 * 64;

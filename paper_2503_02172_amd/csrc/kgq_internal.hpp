@@ -229,6 +229,18 @@ void launch_logic_combine(int tnorm, const GroupArgs& g, const float* states, in
 void launch_pack_cone(const int32_t* src_row, const int32_t* neg, int n_rows, int n_rows_pad, const float* states,
                       int d, float* qpack, hipStream_t s);
 
+// Order-preserving key of a score: unsigned comparison of keys orders the
+// scores as floats, -0 and +0 equal (NaNs sort by their bits, above +inf or
+// below -inf by sign). Top-k selection and the chunk keys share it.
+__device__ __forceinline__ uint32_t score_key(float f)
+{
+    if (f == 0.0f) f = 0.0f;   // -0 and +0 rank equal
+    const uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+constexpr int kKeyChunk = 64;   // entities per chunk key
+
 struct ScoreArgs {
     int model;
     const float* qpack; const float* ent; const double* cq; const double* ee;
@@ -250,6 +262,12 @@ struct ScoreArgs {
     // nullptr for the FP32 one
     const uint16_t* ent_planes = nullptr;
     bool split_always = false;         // the bf16 contraction at any row count (tests)
+    // BetaE on the bf16 contraction: per output row and chunk of kKeyChunk
+    // entities, the largest score_key of the row's scores in the chunk
+    // (at least 1), [rows x key_ld] with key_ld >= ceil(N / kKeyChunk);
+    // nullptr: not written
+    uint32_t* chunk_key = nullptr;
+    int64_t key_ld = 0;
 };
 // Filtered answer ranks and per-query [MRR, Hits@1, @3, @10] (k_rank.hip).
 void launch_rank_answers(const float* scores, int64_t ld, int64_t N, int batch, const int32_t* off,
@@ -264,8 +282,10 @@ __host__ __device__ inline int score_out_index(int r, int n_quad, int n_pair)
     return (n_quad >> 2) + (n_pair >> 1) + (r - n_quad - n_pair);
 }
 
-void launch_score(const ScoreArgs& a, hipStream_t s);      // GQE, Query2Box: VALU
-void launch_score_kl(const ScoreArgs& a, hipStream_t s);   // BetaE: matrix cores
+// Both return whether the chunk keys were written (only the bf16 BetaE
+// contraction writes them, and only when a.chunk_key is set).
+bool launch_score(const ScoreArgs& a, hipStream_t s);      // GQE, Query2Box: VALU
+bool launch_score_kl(const ScoreArgs& a, hipStream_t s);   // BetaE: matrix cores
 
 // Top-k works on segments of at most kTopkSegment scores per workgroup;
 // longer rows take extra rounds over per-segment candidates.
@@ -282,6 +302,11 @@ struct TopkArgs {
     int64_t seg_len;
     int64_t out_ld;
     int out_rows_per_row;
+    // the scorer's chunk keys for rows 0 .. n_rows-1 (ScoreArgs::chunk_key),
+    // or nullptr; the first round skips chunks whose key is below its
+    // running threshold
+    const uint32_t* chunk_key = nullptr;
+    int64_t key_ld = 0;
 };
 // Launches every round; false (nothing launched) when a round needs the
 // scratch buffers and they are missing.

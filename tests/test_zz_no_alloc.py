@@ -63,6 +63,39 @@ def test_gpu_noalloc_matches_execute_mixed(model):
             check_topk(nt_i.cpu().numpy(), nt_v.cpu().numpy(), ora, k, w.rtol, w.gamma, what + " vs oracle")
 
 
+@pytest.mark.gpu
+def test_gpu_noalloc_betae_chunk_keys():
+    """BetaE at streaming batch sizes with the score matrix in the caller's
+    buffer: the static array also holds the scorer's chunk keys, so top-k
+    reads only the chunks that can hold its answers. Two calls in a row (the
+    second smaller, on keys the first left behind) must give the top-k of
+    kgq_execute_mixed bit for bit, and that of a plain sort of the scores."""
+    import torch
+    from paper_2503_02172_amd import kgq
+
+    N, R, k = 9001, 9, 100
+    w = synth.make_tiny(O.BETAE, n_ent=N, n_rel=R, dim=16, seed=530)
+    with kgq.engine_for(w, max_batch=2400) as eng:
+        for call, B in enumerate((2400, 2100)):
+            qb = synth.draw_mixed(["1p", "2p", "2i", "2u", "pin"], B, N, R, seed=630 + call)
+            a = torch.as_tensor(qb.anchors, dtype=torch.int32, device="cuda")
+            r = torch.as_tensor(qb.relations, dtype=torch.int32, device="cuda")
+            print(f"[noalloc] betae chunk keys call={call} B={B}", flush=True)
+            ref_s, ref_i, ref_v = _alloc_outputs(B, N, k, True)
+            eng.execute_mixed_into(qb.structure_ids, a, r, k, ref_s, ref_i, ref_v)
+            na_s, na_i, na_v = _alloc_outputs(B, N, k, True)
+            eng.execute_mixed_noalloc_into(qb.structure_ids, a, r, k, na_s, na_i, na_v)
+            torch.cuda.synchronize()
+            sc = na_s.cpu().numpy()
+            assert np.array_equal(sc.view(np.uint32), ref_s.cpu().numpy().view(np.uint32))
+            gi = na_i.cpu().numpy()
+            assert np.array_equal(gi, ref_i.cpu().numpy())
+            assert np.array_equal(na_v.cpu().numpy().view(np.uint32), ref_v.cpu().numpy().view(np.uint32))
+            for q in range(0, B, 37):
+                o = np.lexsort((np.arange(N), -sc[q].astype(np.float64)))[:k]
+                assert np.array_equal(gi[q], o), (call, q)
+
+
 def test_noalloc_size_limit_on_a_validation_handle():
     """The scratch a batch needs is checked against the static array before
     anything else: 64 queries x 2,000,000 entities of score matrix (512 MB) do
