@@ -31,6 +31,44 @@ using GemmTileLds = MfmaTileLds<64, 64, 3>;
 using GemmTileLdsHalf = MfmaTileLds<64, 64, 3, true>;
 using GemmTileReg = MfmaTileReg<64, 64>;
 
+// s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15)
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Epilogue of a tile: bias, activation, row map, stores. The bias of the
+// lane's columns and the row map of its rows are loaded first (indices
+// clamped, so the loads issue back to back) and waited for once: a load
+// issued between the stores would wait (vmcnt) for the stores before it as
+// well, and the stores would go out one acknowledgement at a time.
+template <class Tile>
+__device__ __forceinline__ void store_tile(const GemmArgs& g, int m0, int n0, const v4f (&acc)[Tile::TM][Tile::TN])
+{
+    float bias[Tile::TN];
+    int64_t row[Tile::TM][4];
+#pragma unroll
+    for (int j = 0; j < Tile::TN; ++j) bias[j] = g.bias ? g.bias[min(n0 + Tile::col_of(j), g.N - 1)] : 0.f;
+#pragma unroll
+    for (int i = 0; i < Tile::TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = m0 + Tile::row_of(i) + r;
+            row[i][r] = g.c_rowmap ? (int64_t)g.c_rowmap[min(m, g.M - 1)] : (int64_t)m;
+        }
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+#pragma unroll
+    for (int j = 0; j < Tile::TN; ++j) {
+        const int n = n0 + Tile::col_of(j);
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int i = 0; i < Tile::TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + Tile::row_of(i) + r;
+                if (m >= g.M) continue;
+                g.C[row[i][r] * g.ldc + n] = apply_epilogue(g.epi, g.epi_split, n, acc[i][j][r] + bias[j]);
+            }
+    }
+}
+
 template <class GemmTile>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, int tm, int tn, int per_xcd)
 {
@@ -45,23 +83,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, int tm, int tn, int pe
     v4f acc[GemmTile::TM][GemmTile::TN];
     GemmTile::run(g.A, g.lda, g.M, g.W, g.ldw, g.N, g.K, m0, n0, sm, acc);
 
-#pragma unroll
-    for (int j = 0; j < GemmTile::TN; ++j) {
-        const int n = n0 + GemmTile::col_of(j);
-        if (n >= g.N) continue;
-        const float b = g.bias ? g.bias[n] : 0.f;
-#pragma unroll
-        for (int i = 0; i < GemmTile::TM; ++i) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = m0 + GemmTile::row_of(i) + r;
-                if (m >= g.M) continue;
-                const float v = apply_epilogue(g.epi, g.epi_split, n, acc[i][j][r] + b);
-                const int64_t row = g.c_rowmap ? (int64_t)g.c_rowmap[m] : (int64_t)m;
-                g.C[row * g.ldc + n] = v;
-            }
-        }
-    }
+    store_tile<GemmTile>(g, m0, n0, acc);
 }
 
 // Split-K for small M: with few 64 x 64 output tiles the K loop is a latency
@@ -160,22 +182,7 @@ __device__ __forceinline__ void gemm_bf16x3_tile(const GemmArgs& g, int tm, int 
     const int64_t ldp = plane_ld(g.K);
     Tile::run(g.A, g.lda, g.M, g.M, g.Wp, (int64_t)g.N * ldp, ldp, g.N, g.K, m0, n0, sm, acc);
 
-#pragma unroll
-    for (int j = 0; j < Tile::TN; ++j) {
-        const int n = n0 + Tile::col_of(j);
-        if (n >= g.N) continue;
-        const float bb = g.bias ? g.bias[n] : 0.f;
-#pragma unroll
-        for (int i = 0; i < Tile::TM; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = m0 + Tile::row_of(i) + r;
-                if (m >= g.M) continue;
-                const float v = apply_epilogue(g.epi, g.epi_split, n, acc[i][j][r] + bb);
-                const int64_t row = g.c_rowmap ? (int64_t)g.c_rowmap[m] : (int64_t)m;
-                g.C[row * g.ldc + n] = v;
-            }
-    }
+    store_tile<Tile>(g, m0, n0, acc);
 }
 
 template <int BM, int BN>

@@ -49,6 +49,9 @@
 
 namespace kgq {
 
+// s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15)
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 // A lane's four consecutive scores of one output row: one 16-byte
 // non-temporal store (rows start only 4-byte aligned; gfx950 takes
 // dword-aligned multi-dword global stores), element stores at the ragged end
@@ -219,6 +222,18 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
         return;
     }
     const int n_grouped = a.n_quad + a.n_pair;
+    // Output row of each of the wavefront's rows (a group's or pair's rows
+    // share theirs), loaded before the first store and waited for once: a
+    // load issued between the stores would wait (vmcnt) for the stores before
+    // it as well. Lane i loads row i's (rows past the last clamped to it),
+    // and each is then read from its lane.
+    static_assert(TQ <= 64, "one row per lane");
+    const int32_t od_lane =
+        a.out_dest[score_out_index(min(qb * TQ + min(lane, TQ - 1), a.n_rows - 1), a.n_quad, a.n_pair)];
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    int32_t od[TQ];
+#pragma unroll
+    for (int i = 0; i < TQ; ++i) od[i] = __builtin_amdgcn_readlane(od_lane, i);
 #pragma unroll
     for (int i = 0; i < TQ; i += 4) {
         const int row = qb * TQ + i;
@@ -233,7 +248,7 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
                 else sc[u][j] = a.gamma - acc[i + u][j] + (1.0f - a.center_reg) * acc2[i + u][j];
             }
         if (row < a.n_quad) {
-            float* dst = a.scores + (int64_t)a.out_dest[row >> 2] * a.ld;
+            float* dst = a.scores + (int64_t)od[i] * a.ld;
             float v[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) v[j] = fmaxf(fmaxf(sc[0][j], sc[1][j]), fmaxf(sc[2][j], sc[3][j]));
@@ -244,16 +259,15 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
         for (int h = 0; h < 2; ++h) {
             const int r = row + 2 * h;
             if (r >= a.n_rows) break;
-            const int o = score_out_index(r, a.n_quad, a.n_pair);
             if (r < n_grouped) {
-                float* dst = a.scores + (int64_t)a.out_dest[o] * a.ld;
+                float* dst = a.scores + (int64_t)od[i + 2 * h] * a.ld;
                 float v[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) v[j] = fmaxf(sc[2 * h][j], sc[2 * h + 1][j]);
                 store_scores4(dst, e0, a.N, v);
             } else {
-                store_scores4(a.scores + (int64_t)a.out_dest[o] * a.ld, e0, a.N, sc[2 * h]);
-                if (r + 1 < a.n_rows) store_scores4(a.scores + (int64_t)a.out_dest[o + 1] * a.ld, e0, a.N, sc[2 * h + 1]);
+                store_scores4(a.scores + (int64_t)od[i + 2 * h] * a.ld, e0, a.N, sc[2 * h]);
+                if (r + 1 < a.n_rows) store_scores4(a.scores + (int64_t)od[i + 2 * h + 1] * a.ld, e0, a.N, sc[2 * h + 1]);
             }
         }
     }
