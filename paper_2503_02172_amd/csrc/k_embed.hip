@@ -379,21 +379,30 @@ __global__ void k_betae_int_prep(GroupArgs g, const float* states, int d, float*
     const int n = g.n_in[gi];
     const int neg = g.neg_mask[gi];
     const int W = 2 * d;
-    for (int j = 0; j < n; ++j) {
-        const bool inv = (neg >> j) & 1;
-        const float* src = states + (int64_t)(i0 + j) * W;
-        float* dst = x_int + (int64_t)(i0 + j) * W;
-        for (int k = threadIdx.x; k < W; k += blockDim.x) {
-            const float v = src[k];
-            dst[k] = inv ? 1.0f / v : v;
-        }
+    // every input's value read before any is stored: a load issued after a
+    // store waits (vmcnt) for that store too
+    for (int k = threadIdx.x; k < W; k += blockDim.x) {
+        float v[kGroupInputs];
+#pragma unroll
+        for (int j = 0; j < kGroupInputs; ++j)
+            if (j < n) {
+                const float x = states[(int64_t)(i0 + j) * W + k];
+                v[j] = ((neg >> j) & 1) ? 1.0f / x : x;
+            }
+#pragma unroll
+        for (int j = 0; j < kGroupInputs; ++j)
+            if (j < n) x_int[(int64_t)(i0 + j) * W + k] = v[j];
     }
 }
+
+// Threads per workgroup for a row of `width` floats: one element per thread
+// (up to 1,024), so that no thread loads after it has stored.
+static inline int row_threads(int width) { return std::min(1024, std::max(64, (width + 63) / 64 * 64)); }
 
 void launch_betae_int_prep(const GroupArgs& g, const float* states, int d, float* x_int, hipStream_t s)
 {
     if (g.n_groups <= 0) return;
-    hipLaunchKernelGGL(k_betae_int_prep, dim3(g.n_groups), dim3(256), 0, s, g, states, d, x_int);
+    hipLaunchKernelGGL(k_betae_int_prep, dim3(g.n_groups), dim3(row_threads(2 * d)), 0, s, g, states, d, x_int);
 }
 
 __global__ void k_betae_combine(GroupArgs g, const float* x_int, const float* logits, int d, float* states)
@@ -420,7 +429,7 @@ void launch_betae_combine(const GroupArgs& g, const float* x_int, const float* l
                           float* states, hipStream_t s)
 {
     if (g.n_groups <= 0) return;
-    hipLaunchKernelGGL(k_betae_combine, dim3(g.n_groups), dim3(128), 0, s, g, x_int, logits, d, states);
+    hipLaunchKernelGGL(k_betae_combine, dim3(g.n_groups), dim3(row_threads(d)), 0, s, g, x_int, logits, d, states);
 }
 
 __global__ void k_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, const int32_t* rel_ref,
@@ -454,7 +463,7 @@ void launch_betae_proj_prep(const int32_t* src_row, const int32_t* anchor_ref, c
                             int64_t n_ent, int n_rel, int d, float* x, int* flag, hipStream_t s)
 {
     if (M <= 0) return;
-    hipLaunchKernelGGL(k_betae_proj_prep, dim3(M), dim3(256), 0, s, src_row, anchor_ref, rel_ref, neg, anchors,
+    hipLaunchKernelGGL(k_betae_proj_prep, dim3(M), dim3(row_threads(2 * d)), 0, s, src_row, anchor_ref, rel_ref, neg, anchors,
                        rels, states, ent_ab, rel, n_ent, n_rel, d, x, flag);
 }
 
