@@ -59,6 +59,7 @@ constexpr int kWaitVmcnt0 = 0x0F70;
 // evicting the packed queries that the other entity blocks still read, and
 // a wavefront writes whole lines.
 typedef float f4u_t __attribute__((ext_vector_type(4), aligned(4)));
+
 __device__ __forceinline__ void store_scores4(float* dst, int64_t e0, int64_t N, const float (&v)[4])
 {
     if (e0 + 3 < N) {
@@ -68,6 +69,32 @@ __device__ __forceinline__ void store_scores4(float* dst, int64_t e0, int64_t N,
         for (int j = 0; j < 4; ++j)
             if (e0 + j < N) __builtin_nontemporal_store(v[j], dst + e0 + j);
     }
+}
+
+// score_key in integer operations only (this file is built without NaN
+// semantics, so no float compare decides it): -0 becomes +0, then the sign
+// flips the other bits or sets the top one.
+__device__ __forceinline__ uint32_t score_key_bits(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u = u == 0x80000000u ? 0u : u;
+    return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+}
+
+// One output row's four scores of the lane (entities e0 .. e0 + 3): stored,
+// and, when keys are wanted, folded into the row's chunk key (the 16 lanes of
+// a 64-entity chunk are one DPP row; entities past N count as key 0). Called
+// by the whole wavefront.
+__device__ __forceinline__ void store_row(const ScoreArgs& a, int64_t orow, int64_t e0, int lane, const float (&v)[4])
+{
+    if (a.chunk_key) {
+        uint32_t kx = 0u;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) kx = max(kx, e0 + j < a.N ? score_key_bits(v[j]) : 0u);
+        kx = chunk16_max(kx);
+        if ((lane & 15) == 0 && e0 < a.N) a.chunk_key[orow * a.key_ld + e0 / kKeyChunk] = max(kx, 1u);
+    }
+    store_scores4(a.scores + orow * a.ld, e0, a.N, v);
 }
 
 template <int MODEL, int TQ>
@@ -248,11 +275,10 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
                 else sc[u][j] = a.gamma - acc[i + u][j] + (1.0f - a.center_reg) * acc2[i + u][j];
             }
         if (row < a.n_quad) {
-            float* dst = a.scores + (int64_t)od[i] * a.ld;
             float v[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) v[j] = fmaxf(fmaxf(sc[0][j], sc[1][j]), fmaxf(sc[2][j], sc[3][j]));
-            store_scores4(dst, e0, a.N, v);
+            store_row(a, od[i], e0, lane, v);
             continue;
         }
 #pragma unroll
@@ -260,14 +286,13 @@ __global__ __launch_bounds__(256) void k_score(ScoreArgs a, int nqg, int qchunk,
             const int r = row + 2 * h;
             if (r >= a.n_rows) break;
             if (r < n_grouped) {
-                float* dst = a.scores + (int64_t)od[i + 2 * h] * a.ld;
                 float v[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) v[j] = fmaxf(sc[2 * h][j], sc[2 * h + 1][j]);
-                store_scores4(dst, e0, a.N, v);
+                store_row(a, od[i + 2 * h], e0, lane, v);
             } else {
-                store_scores4(a.scores + (int64_t)od[i + 2 * h] * a.ld, e0, a.N, sc[2 * h]);
-                if (r + 1 < a.n_rows) store_scores4(a.scores + (int64_t)od[i + 2 * h + 1] * a.ld, e0, a.N, sc[2 * h + 1]);
+                store_row(a, od[i + 2 * h], e0, lane, sc[2 * h]);
+                if (r + 1 < a.n_rows) store_row(a, od[i + 2 * h + 1], e0, lane, sc[2 * h + 1]);
             }
         }
     }
@@ -349,6 +374,7 @@ bool launch_score(const ScoreArgs& a, hipStream_t s)
     } else {
         b.part = nullptr;
     }
+    if (splits > 1) b.chunk_key = nullptr;   // the split-d sum writes no keys
     dim3 grid(per_xcd * 8, z);
     if (form == KGQ_GQE) {
         if (small) hipLaunchKernelGGL((k_score<0, kTqGqeSmall>), grid, dim3(256), 0, s, b, nqg, qc, total, per_xcd, kslice);
@@ -371,7 +397,7 @@ bool launch_score(const ScoreArgs& a, hipStream_t s)
         else
             hipLaunchKernelGGL((k_score_sum<3>), g2, dim3(256), 0, s, b, z, rows_pad, n_out);
     }
-    return false;
+    return b.chunk_key != nullptr;
 }
 
 }  // namespace kgq

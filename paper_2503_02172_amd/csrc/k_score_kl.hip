@@ -49,18 +49,6 @@ namespace kgq {
 // s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15)
 constexpr int kWaitVmcnt0 = 0x0F70;
 
-// Largest x over each DPP row of 16 lanes (all of them active): swaps of
-// neighbours and of pairs inside quads, then the half-row and the row
-// mirrored.
-__device__ __forceinline__ uint32_t chunk16_max(uint32_t x)
-{
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));    // quad_perm 1,0,3,2
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));    // quad_perm 2,3,0,1
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x141, 0xF, 0xF, false));   // row_half_mirror
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x140, 0xF, 0xF, false));   // row_mirror
-    return x;
-}
-
 template <class KlTile>
 __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int n_nt, int qchunk, int total,
                                                      int per_xcd)

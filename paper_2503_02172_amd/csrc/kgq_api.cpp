@@ -55,7 +55,7 @@ struct Lane {
     int64_t score_ws_elems = 0;
     int32_t* cand_idx[2] = {nullptr, nullptr};   // top-k candidates of long rows
     float* cand_score[2] = {nullptr, nullptr};
-    uint32_t* chunk_key = nullptr;   // BetaE: the scorer's chunk keys for top-k [rows x ceil(N / 64)]
+    uint32_t* chunk_key = nullptr;   // the scorer's chunk keys for top-k [rows x ceil(N / 64)]
     int* dflag = nullptr;
     int* hflag = nullptr;         // pinned
     // plan images: per-structure cache slots + a ring of two for mixed batches
@@ -424,7 +424,7 @@ kgq_status allocate_all(kgq_handle* h)
             ALLOC(L.cand_idx[i], ncand);
             ALLOC(L.cand_score[i], ncand);
         }
-        if (c.model == KGQ_BETAE) ALLOC(L.chunk_key, Bm * ((N + kKeyChunk - 1) / kKeyChunk));
+        ALLOC(L.chunk_key, Bm * ((N + kKeyChunk - 1) / kKeyChunk));
         ALLOC(L.dflag, 1);
         ALLOC(L.plan_dev, (int64_t)(kNumStructures + 2) * h->plan_words);
         hipError_t e = hipHostMalloc((void**)&L.hflag, sizeof(int), hipHostMallocDefault);
@@ -838,7 +838,7 @@ kgq_status noalloc_scratch_address(kgq_handle* h)
 // bytes at `base` (256-byte aligned pieces), in the roles a lane's buffers
 // play: plan image, error flag, state rows, dense-layer rows, intersection
 // groups, packed queries, the score matrix when the caller does not supply
-// one, and the top-k candidates of long rows. BetaE's chunk keys for top-k
+// one, and the top-k candidates of long rows. The scorers' chunk keys for top-k
 // (which then reads only the chunks that can hold its answers), then the
 // split-K and split-d workspaces of small batches get what is left, up to a
 // lane's caps (the splitting code takes fewer slices when a workspace is
@@ -898,9 +898,9 @@ int64_t carve_scratch(const kgq_handle* h, const Plan& p, int32_t k, bool need_s
     V.score_ws_elems = 0;
     V.chunk_key = nullptr;
     if (*fits) {
-        // BetaE's chunk keys for top-k first, when they fit whole
+        // the scorers' chunk keys for top-k first, when they fit whole
         const int64_t key_bytes = B * ((N + kKeyChunk - 1) / kKeyChunk) * 4;
-        if (c.model == KGQ_BETAE && need_topk && (off + 255) / 256 * 256 + key_bytes <= cap)
+        if (need_topk && (off + 255) / 256 * 256 + key_bytes <= cap)
             V.chunk_key = reinterpret_cast<uint32_t*>(take(key_bytes));
         // optional workspaces, each from half of what is left
         const int64_t n_max = mlp_model(c.model) ? 4 * d : d;

@@ -241,6 +241,19 @@ __device__ __forceinline__ uint32_t score_key(float f)
 
 constexpr int kKeyChunk = 64;   // entities per chunk key
 
+// Largest x over each DPP row of 16 lanes (all of them active): swaps of
+// neighbours and of pairs inside quads, then the half-row and the row
+// mirrored. The scorers' 16 lanes that hold a chunk's 64 scores form one
+// DPP row.
+__device__ __forceinline__ uint32_t chunk16_max(uint32_t x)
+{
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));    // quad_perm 1,0,3,2
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));    // quad_perm 2,3,0,1
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x141, 0xF, 0xF, false));   // row_half_mirror
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x140, 0xF, 0xF, false));   // row_mirror
+    return x;
+}
+
 struct ScoreArgs {
     int model;
     const float* qpack; const float* ent; const double* cq; const double* ee;
@@ -262,10 +275,10 @@ struct ScoreArgs {
     // nullptr for the FP32 one
     const uint16_t* ent_planes = nullptr;
     bool split_always = false;         // the bf16 contraction at any row count (tests)
-    // BetaE on the bf16 contraction: per output row and chunk of kKeyChunk
-    // entities, the largest score_key of the row's scores in the chunk
-    // (at least 1), [rows x key_ld] with key_ld >= ceil(N / kKeyChunk);
-    // nullptr: not written
+    // Per output row and chunk of kKeyChunk entities, the largest score_key
+    // of the row's scores in the chunk (at least 1), [rows x key_ld] with
+    // key_ld >= ceil(N / kKeyChunk), written by the BetaE bf16 contraction
+    // and the VALU scorers' unsplit form; nullptr: not written
     uint32_t* chunk_key = nullptr;
     int64_t key_ld = 0;
 };
