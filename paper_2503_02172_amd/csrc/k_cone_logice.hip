@@ -38,6 +38,10 @@
 
 namespace kgq {
 
+// Threads per workgroup for a row of `width` floats: one element per thread
+// (up to 1,024), so that no thread loads after it has stored.
+static inline int row_threads(int width) { return std::min(1024, std::max(64, (width + 63) / 64 * 64)); }
+
 constexpr float kPi = 3.14159265358979323846f;
 
 // ConE complement of one dimension's cone.
@@ -101,7 +105,7 @@ void launch_cone_entity_prep(const float* src, int64_t N, int d, int64_t n_block
 // x row m: ConE (width 2d) the source state (complemented where neg[m]) plus
 // Rel[r]; LogicE (width 3d) [source (complemented where neg[m]); Rel[r]].
 template <int MODEL>
-__global__ __launch_bounds__(256) void k_mlp_proj_prep(const int32_t* src_row, const int32_t* anchor_ref,
+__global__ __launch_bounds__(1024) void k_mlp_proj_prep(const int32_t* src_row, const int32_t* anchor_ref,
                                                        const int32_t* rel_ref, const int32_t* neg,
                                                        const int32_t* anchors, const int32_t* rels,
                                                        const float* states, const float* ent_rm, const float* rel,
@@ -147,10 +151,10 @@ void launch_mlp_proj_prep(int model, const int32_t* src_row, const int32_t* anch
 {
     if (M <= 0) return;
     if (model == KGQ_CONE)
-        hipLaunchKernelGGL(k_mlp_proj_prep<KGQ_CONE>, dim3(M), dim3(256), 0, s, src_row, anchor_ref, rel_ref, neg,
+        hipLaunchKernelGGL(k_mlp_proj_prep<KGQ_CONE>, dim3(M), dim3(row_threads(d)), 0, s, src_row, anchor_ref, rel_ref, neg,
                            anchors, rels, states, ent_rm, rel, n_ent, n_rel, d, x, flag);
     else
-        hipLaunchKernelGGL(k_mlp_proj_prep<KGQ_LOGICE>, dim3(M), dim3(256), 0, s, src_row, anchor_ref, rel_ref, neg,
+        hipLaunchKernelGGL(k_mlp_proj_prep<KGQ_LOGICE>, dim3(M), dim3(row_threads(d)), 0, s, src_row, anchor_ref, rel_ref, neg,
                            anchors, rels, states, ent_rm, rel, n_ent, n_rel, d, x, flag);
 }
 
@@ -206,7 +210,7 @@ void launch_cone_int_prep(const GroupArgs& g, const float* states, int d, float*
 // ConE axis: attention-weighted mean of the branch axes' unit vectors; and
 // the mean over branches of the aperture set function's hidden features
 // (columns d .. 2d-1 of the stacked first layer's output).
-__global__ __launch_bounds__(128) void k_cone_combine_axis(GroupArgs g, const float* states, const float* logits,
+__global__ __launch_bounds__(1024) void k_cone_combine_axis(GroupArgs g, const float* states, const float* logits,
                                                            const float* hid, int d, float* zmean, float* out_states)
 {
     const int gi = blockIdx.x;
@@ -239,13 +243,13 @@ void launch_cone_combine_axis(const GroupArgs& g, const float* states, const flo
                               float* zmean, float* out_states, hipStream_t s)
 {
     if (g.n_groups <= 0) return;
-    hipLaunchKernelGGL(k_cone_combine_axis, dim3(g.n_groups), dim3(128), 0, s, g, states, logits, hid, d, zmean,
+    hipLaunchKernelGGL(k_cone_combine_axis, dim3(g.n_groups), dim3(row_threads(d)), 0, s, g, states, logits, hid, d, zmean,
                        out_states);
 }
 
 // ConE half-aperture: min over branches (complemented where negated) times
 // the sigmoid gate.
-__global__ __launch_bounds__(128) void k_cone_combine_arg(GroupArgs g, const float* states, const float* gate, int d,
+__global__ __launch_bounds__(1024) void k_cone_combine_arg(GroupArgs g, const float* states, const float* gate, int d,
                                                           float* out_states)
 {
     const int gi = blockIdx.x;
@@ -268,12 +272,12 @@ void launch_cone_combine_arg(const GroupArgs& g, const float* states, const floa
                              hipStream_t s)
 {
     if (g.n_groups <= 0) return;
-    hipLaunchKernelGGL(k_cone_combine_arg, dim3(g.n_groups), dim3(128), 0, s, g, states, gate, d, out_states);
+    hipLaunchKernelGGL(k_cone_combine_arg, dim3(g.n_groups), dim3(row_threads(d)), 0, s, g, states, gate, d, out_states);
 }
 
 // LogicE: the t-norm over the branches of each group, coordinate-wise.
 template <int TNORM>
-__global__ __launch_bounds__(128) void k_logic_combine(GroupArgs g, const float* states, int d, float* out_states)
+__global__ __launch_bounds__(1024) void k_logic_combine(GroupArgs g, const float* states, int d, float* out_states)
 {
     const int gi = blockIdx.x;
     const int i0 = g.in_start[gi];
@@ -314,13 +318,13 @@ void launch_logic_combine(int tnorm, const GroupArgs& g, const float* states, in
 {
     if (g.n_groups <= 0) return;
     if (tnorm == KGQ_TNORM_MIN)
-        hipLaunchKernelGGL(k_logic_combine<KGQ_TNORM_MIN>, dim3(g.n_groups), dim3(128), 0, s, g, states, d,
+        hipLaunchKernelGGL(k_logic_combine<KGQ_TNORM_MIN>, dim3(g.n_groups), dim3(row_threads(d)), 0, s, g, states, d,
                            out_states);
     else if (tnorm == KGQ_TNORM_LUKASIEWICZ)
-        hipLaunchKernelGGL(k_logic_combine<KGQ_TNORM_LUKASIEWICZ>, dim3(g.n_groups), dim3(128), 0, s, g, states, d,
+        hipLaunchKernelGGL(k_logic_combine<KGQ_TNORM_LUKASIEWICZ>, dim3(g.n_groups), dim3(row_threads(d)), 0, s, g, states, d,
                            out_states);
     else
-        hipLaunchKernelGGL(k_logic_combine<KGQ_TNORM_PRODUCT>, dim3(g.n_groups), dim3(128), 0, s, g, states, d,
+        hipLaunchKernelGGL(k_logic_combine<KGQ_TNORM_PRODUCT>, dim3(g.n_groups), dim3(row_threads(d)), 0, s, g, states, d,
                            out_states);
 }
 

@@ -22,6 +22,10 @@
 
 namespace kgq {
 
+// Threads per workgroup for a row of `width` floats: one element per thread
+// (up to 1,024), so that no thread loads after it has stored.
+static inline int row_threads(int width) { return std::min(1024, std::max(64, (width + 63) / 64 * 64)); }
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h)
 {
     return __uint_as_float(((uint32_t)h) << 16);
@@ -338,7 +342,7 @@ void launch_combine_center(int model, const GroupArgs& g, const float* states, i
                            float* out_states, int* flag, hipStream_t s)
 {
     if (g.n_groups <= 0) return;
-    hipLaunchKernelGGL(k_combine_center, dim3(g.n_groups), dim3(128), 0, s, model, g, states, W, logits,
+    hipLaunchKernelGGL(k_combine_center, dim3(g.n_groups), dim3(row_threads(d)), 0, s, model, g, states, W, logits,
                        zfeat, zmean, rels, rel_c, n_rel, d, out_states, flag);
 }
 
@@ -366,7 +370,7 @@ void launch_combine_offset(const GroupArgs& g, const float* states, int W, const
                            float* out_states, int* flag, hipStream_t s)
 {
     if (g.n_groups <= 0) return;
-    hipLaunchKernelGGL(k_combine_offset, dim3(g.n_groups), dim3(128), 0, s, g, states, W, gate, rels,
+    hipLaunchKernelGGL(k_combine_offset, dim3(g.n_groups), dim3(row_threads(d)), 0, s, g, states, W, gate, rels,
                        rel_o, n_rel, d, out_states, flag);
 }
 
@@ -395,9 +399,6 @@ __global__ void k_betae_int_prep(GroupArgs g, const float* states, int d, float*
     }
 }
 
-// Threads per workgroup for a row of `width` floats: one element per thread
-// (up to 1,024), so that no thread loads after it has stored.
-static inline int row_threads(int width) { return std::min(1024, std::max(64, (width + 63) / 64 * 64)); }
 
 void launch_betae_int_prep(const GroupArgs& g, const float* states, int d, float* x_int, hipStream_t s)
 {
