@@ -38,10 +38,6 @@
 
 namespace kgq {
 
-// Threads per workgroup for a row of `width` floats: one element per thread
-// (up to 1,024), so that no thread loads after it has stored.
-static inline int row_threads(int width) { return std::min(1024, std::max(64, (width + 63) / 64 * 64)); }
-
 constexpr float kPi = 3.14159265358979323846f;
 
 // ConE complement of one dimension's cone.

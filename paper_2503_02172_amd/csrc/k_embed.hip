@@ -22,10 +22,6 @@
 
 namespace kgq {
 
-// Threads per workgroup for a row of `width` floats: one element per thread
-// (up to 1,024), so that no thread loads after it has stored.
-static inline int row_threads(int width) { return std::min(1024, std::max(64, (width + 63) / 64 * 64)); }
-
 __device__ __forceinline__ float bf16_to_f32(uint16_t h)
 {
     return __uint_as_float(((uint32_t)h) << 16);

@@ -31,9 +31,6 @@ using GemmTileLds = MfmaTileLds<64, 64, 3>;
 using GemmTileLdsHalf = MfmaTileLds<64, 64, 3, true>;
 using GemmTileReg = MfmaTileReg<64, 64>;
 
-// s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15)
-constexpr int kWaitVmcnt0 = 0x0F70;
-
 // Epilogue of a tile: bias, activation, row map, stores. The bias of the
 // lane's columns and the row map of its rows are loaded first (indices
 // clamped, so the loads issue back to back) and waited for once: a load

@@ -49,9 +49,6 @@
 
 namespace kgq {
 
-// s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15)
-constexpr int kWaitVmcnt0 = 0x0F70;
-
 // A lane's four consecutive scores of one output row: one 16-byte
 // non-temporal store (rows start only 4-byte aligned; gfx950 takes
 // dword-aligned multi-dword global stores), element stores at the ragged end

@@ -46,9 +46,6 @@ namespace kgq {
 // loop 128 x 128, or 64 x 64 for small batches, where the larger tile leaves
 // the chip underfilled and each workgroup's K loop is a latency chain. Query
 // rows are padded to 128 (kRowTileBetae), a multiple of every tile's rows.
-// s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15)
-constexpr int kWaitVmcnt0 = 0x0F70;
-
 template <class KlTile>
 __global__ __launch_bounds__(256, 2) void k_score_kl(ScoreArgs a, int n_mt, int n_nt, int qchunk, int total,
                                                      int per_xcd)

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "../../include/kgq.h"
 
 namespace kgq {
@@ -240,6 +242,16 @@ __device__ __forceinline__ uint32_t score_key(float f)
 }
 
 constexpr int kKeyChunk = 64;   // entities per chunk key
+
+// s_waitcnt vmcnt(0), other counters not waited for (expcnt 7, lgkmcnt 15).
+// A vector load issued after a store waits (vmcnt) for that store too, since
+// the counter counts stores as well, in issue order; kernels that store in a
+// loop load what the loop needs first and wait for it once with this.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Threads per workgroup for a row of `width` floats: one element per thread
+// (up to 1,024), so that no thread loads after it has stored.
+inline int row_threads(int width) { return std::min(1024, std::max(64, (width + 63) / 64 * 64)); }
 
 // Largest x over each DPP row of 16 lanes (all of them active): swaps of
 // neighbours and of pairs inside quads, then the half-row and the row
